@@ -1,0 +1,246 @@
+/*
+ * tpstage.h -- C ABI of one pipeline stage of GPT pre-LN decoder layers on
+ * one MI355X (gfx950), with per-tensor keep / recompute / offload policies.
+ *
+ * Method (paper: "Enhancing Memory Efficiency in LLM Training Through
+ * Chronos-aware Pipeline Parallelism", arXiv 2503.03182):
+ *   - a pipeline stage runs forward tasks F(mb) and backward tasks B(mb) per
+ *     micro-batch; one activation tensor enters/leaves per task (Section 2.1);
+ *   - recomputation keeps checkpoints and regenerates the other activations
+ *     before they are needed in the backward pass (Section 2.2); T-Recomp
+ *     replays the whole recomputed block as a separate step that runs before
+ *     the dependent backward (Section 4.2, "Addressing the Concerns"),
+ *     while the conventional layer-grouped form replays one group just in
+ *     time (Section 4.2, "Concerns Regarding T-Recomp");
+ *   - offloading parks tensors in host DRAM and brings them back (Section
+ *     2.2); T-Offload moves model state between host and device around the
+ *     compute (Section 5); CPU activation offloading composes with it
+ *     (Section 5, "Compatibility of T-Offload").
+ *
+ * Conventions
+ *   T = micro_batch * seq tokens; activations are token-major row-major
+ *   [T, width] (row r = batch_index * seq + position); weights are [out, in]
+ *   row-major (y = x W^T + b); the packed qkv tensor is [T, 3h] with q, k, v
+ *   in column blocks [0,h), [h,2h), [2h,3h) and head n at columns n*d..n*d+d-1
+ *   of each block.  Storage dtype is f32 or bf16; weight gradients, LN
+ *   statistics and the attention log-sum-exp are always f32.
+ *
+ * Ownership: the caller owns every device and host buffer it passes (device
+ * arena, pinned host arena, parameters, gradients, x / y / dy / dx).  The
+ * library keeps non-owning pointers and owns only HIP events and host
+ * metadata.  Calls are asynchronous on the caller's streams; x, y, dy, dx
+ * must stay valid until the compute stream has passed the call.
+ *
+ * Errors: every call returns TPS_OK (0) or a negative TPS_E* code and sets a
+ * thread-local message readable with tps_last_error().  No C++ exception
+ * crosses the ABI.  Asynchronous kernel and copy faults surface at
+ * tps_stage_sync().
+ */
+#ifndef TPSTAGE_H
+#define TPSTAGE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TPS_ABI_VERSION 1
+#define TPS_MAX_MICRO 64
+
+/* return codes */
+enum {
+  TPS_OK = 0,
+  TPS_EINVAL = -1,   /* bad configuration or argument                        */
+  TPS_ENOMEM = -2,   /* arena smaller than the plan needs                    */
+  TPS_EORDER = -3,   /* call out of the planned F/B order, mb out of range   */
+  TPS_EHIP = -4,     /* HIP runtime error (message in tps_last_error)        */
+  TPS_ETIMEOUT = -5, /* a bounded wait expired                               */
+  TPS_ESTATE = -6    /* call not valid in the stage's current state          */
+};
+
+/* storage dtypes */
+enum { TPS_F32 = 0, TPS_BF16 = 1 };
+
+/* per-tensor policy */
+enum { TPS_KEEP = 0, TPS_RECOMPUTE = 1, TPS_OFFLOAD = 2 };
+
+/* per-(layer, micro-batch) tensors read by the backward pass */
+enum {
+  TPS_T_X = 0,   /* layer input                         [T, h]            */
+  TPS_T_A,       /* LN1 output                          [T, h]            */
+  TPS_T_QKV,     /* packed projections                  [T, 3h]           */
+  TPS_T_O,       /* attention output                    [T, h]            */
+  TPS_T_LSE,     /* attention log-sum-exp, f32          [b, heads, seq]   */
+  TPS_T_X1,      /* residual after attention            [T, h]            */
+  TPS_T_C,       /* LN2 output                          [T, h]            */
+  TPS_T_U,       /* FC1 pre-activation                  [T, f]            */
+  TPS_T_G,       /* GeLU output                         [T, f]            */
+  TPS_T_LN1,     /* LN1 mean and rstd, f32              [2, T]            */
+  TPS_T_LN2,     /* LN2 mean and rstd, f32              [2, T]            */
+  TPS_T_COUNT
+};
+
+/* weights placement */
+enum { TPS_W_RESIDENT = 0, TPS_W_STREAM = 1 };
+
+/* recompute granularity: LAYER replays one layer just before its backward
+ * (layer-grouped); SEGMENT replays every recomputed tensor of the stage for
+ * the micro-batch before its backward starts (block-wise T-Recomp). */
+enum { TPS_GRAN_LAYER = 0, TPS_GRAN_SEGMENT = 1 };
+
+/* op kinds in the planned order */
+enum { TPS_OP_F = 0, TPS_OP_B = 1 };
+
+/* parameter order inside one layer's packed parameter / gradient block */
+enum {
+  TPS_P_W_QKV = 0, TPS_P_B_QKV, TPS_P_W_O, TPS_P_B_O, TPS_P_W_1, TPS_P_B_1,
+  TPS_P_W_2, TPS_P_B_2, TPS_P_G1, TPS_P_BE1, TPS_P_G2, TPS_P_BE2, TPS_P_COUNT
+};
+
+typedef struct tps_config {
+  int32_t abi_version;          /* TPS_ABI_VERSION                              */
+  int32_t n_layers;             /* L >= 1                                       */
+  int32_t hidden;               /* h, multiple of 8                             */
+  int32_t n_heads;              /* h / n_heads must be 64 or 128                */
+  int32_t mlp;                  /* f, multiple of 8                             */
+  int32_t seq;                  /* s >= 1 (any value)                           */
+  int32_t micro_batch;          /* b >= 1                                       */
+  int32_t n_micro;              /* M, 1..TPS_MAX_MICRO                          */
+  int32_t dtype;                /* TPS_F32 or TPS_BF16                          */
+  float ln_eps;                 /* LayerNorm epsilon (biased variance)          */
+  const uint8_t* policy;        /* [n_layers][TPS_T_COUNT] TPS_KEEP/RECOMPUTE/OFFLOAD;
+                                   NULL = keep everything.  X of layer 0 cannot
+                                   be RECOMPUTE.  With TPS_GRAN_LAYER, X of every
+                                   layer must be KEEP or OFFLOAD.               */
+  uint64_t offload_mb_mask;     /* bit mb set: OFFLOAD entries apply to mb; for
+                                   other micro-batches OFFLOAD acts as KEEP.    */
+  int32_t offload_auto;         /* 1: ignore offload_mb_mask and pick victims
+                                   by slack (see tps_plan)                     */
+  int32_t weights;              /* TPS_W_RESIDENT or TPS_W_STREAM               */
+  int32_t window;               /* streamed layers resident at once (>= 2)      */
+  int32_t recompute_granularity;/* TPS_GRAN_LAYER or TPS_GRAN_SEGMENT           */
+  int32_t n_ops;                /* 0: default order from `inflight`             */
+  const int32_t* ops;           /* n_ops pairs (TPS_OP_F|TPS_OP_B, mb)          */
+  int32_t inflight;             /* default order: W forwards, then B(i), F(i+W)
+                                   alternately, then the remaining backwards;
+                                   0 means W = n_micro                          */
+  float link_gbps_hint;         /* host-link GB/s per direction for victim choice */
+  float tflops_hint;            /* sustained TFLOP/s for victim choice          */
+  int32_t lookahead;            /* prefetch an offloaded mb this many ops before
+                                   its backward (>= 1)                          */
+} tps_config;
+
+typedef struct tps_plan_info {
+  uint64_t device_arena_bytes;  /* size of tps_memory.device_arena to allocate   */
+  uint64_t host_arena_bytes;    /* size of the pinned host arena                 */
+  uint64_t slot_bytes;          /* one micro-batch's resident checkpoints (KEEP) */
+  int32_t n_slots;              /* resident checkpoint slots held at the peak    */
+  uint64_t offload_slot_bytes;  /* one micro-batch's OFFLOAD tensors (device
+                                   staging slot and host slot share the layout) */
+  int32_t n_offload_slots;      /* device staging slots held at the peak         */
+  int32_t n_host_slots;         /* pinned host slots held at the peak            */
+  int32_t max_inflight;         /* micro-batches between F and B at the peak     */
+  uint64_t replay_bytes;        /* recompute (replay) buffer                     */
+  uint64_t work_bytes;          /* backward working buffers                      */
+  uint64_t weight_window_bytes; /* streamed weight + grad window (STREAM)        */
+  uint64_t param_bytes;         /* one layer's packed parameter block            */
+  uint64_t grad_bytes;          /* one layer's packed f32 gradient block         */
+  uint64_t keep_all_bytes;      /* activations if every tensor were kept, at the
+                                   same in-flight peak (comparison)              */
+  uint64_t predicted_peak_bytes;/* device arena + resident params + grads        */
+  uint64_t offload_mb_mask;     /* effective mask (after auto selection)         */
+  int32_t n_offload_mbs;
+  int32_t n_replay_layers;      /* layers with at least one recomputed tensor    */
+  double fwd_flops;             /* algorithmic flops per iteration               */
+  double bwd_flops;
+  double recompute_flops;       /* extra forward work the policy implies         */
+  uint64_t h2d_bytes;           /* host-link traffic per iteration               */
+  uint64_t d2h_bytes;
+} tps_plan_info;
+
+typedef struct tps_params {
+  /* [n_layers] pointers to packed parameter blocks in storage dtype, laid out
+   * by tps_param_layout().  RESIDENT: device pointers.  STREAM: pinned host
+   * pointers (the library streams them in). */
+  void* const* layer_params;
+  /* [n_layers] pointers to packed f32 gradient blocks (same order, f32).
+   * RESIDENT: device pointers.  STREAM: pinned host pointers. */
+  float* const* layer_grads;
+} tps_params;
+
+typedef struct tps_memory {
+  void* device_arena;           /* >= plan.device_arena_bytes, 256-byte aligned */
+  uint64_t device_bytes;
+  void* host_arena;             /* pinned, >= plan.host_arena_bytes (may be NULL
+                                   when that is 0)                              */
+  uint64_t host_bytes;
+  void* compute_stream;         /* hipStream_t for kernels                      */
+  void* copy_stream;            /* hipStream_t for host-link copies             */
+} tps_memory;
+
+typedef struct tps_stats {
+  uint64_t h2d_bytes, d2h_bytes;/* issued this iteration                        */
+  uint64_t kernels;             /* kernel launches this iteration               */
+  uint64_t replays;             /* recompute replays (layers) this iteration    */
+  int32_t ops_done;             /* position in the planned order                */
+} tps_stats;
+
+typedef struct tps_stage tps_stage;
+
+/* Layout of one layer's packed parameter block (storage dtype) and gradient
+ * block (f32): byte offsets of the TPS_P_COUNT tensors, each 256-byte aligned.
+ * Shapes: W_qkv[3h,h] b_qkv[3h] W_o[h,h] b_o[h] W_1[f,h] b_1[f] W_2[h,f] b_2[h]
+ * g1[h] be1[h] g2[h] be2[h]. */
+int tps_param_layout(const tps_config* cfg, uint64_t param_offsets[TPS_P_COUNT],
+                     uint64_t* param_bytes, uint64_t grad_offsets[TPS_P_COUNT],
+                     uint64_t* grad_bytes);
+
+/* Host only, no GPU needed.  Validates the config, resolves the op order and
+ * the policy closure, assigns checkpoint slots over the order, lays out the
+ * arenas and predicts the peak.  With offload_auto, victims are picked in
+ * decreasing order of slack between F(mb) and B(mb) (the poorest temporal
+ * locality first, Section 3 and Section 4.2) while the simulated round trip
+ * at link_gbps_hint stays hidden behind compute at tflops_hint. */
+int tps_plan(const tps_config* cfg, tps_plan_info* out);
+
+/* Create a stage.  Copies the config and policy; keeps the pointers of
+ * params and mem.  Launches nothing. */
+int tps_stage_init(const tps_config* cfg, const tps_params* params,
+                   const tps_memory* mem, tps_stage** out);
+
+/* Start an iteration: resets the order cursor; zero_grads != 0 enqueues a
+ * zero fill of every gradient block on the compute stream. */
+int tps_stage_begin_iteration(tps_stage* st, int zero_grads);
+
+/* F(mb): x, y are [b, s, h] device buffers in storage dtype. */
+int tps_stage_forward(tps_stage* st, int mb, const void* x, void* y);
+
+/* B(mb): dy, dx are [b, s, h] device buffers in storage dtype.  Adds the
+ * micro-batch's parameter gradients into the f32 gradient blocks. */
+int tps_stage_backward(tps_stage* st, int mb, const void* dy, void* dx);
+
+/* Layer-major groups: F(mb0..mb0+n-1) (resp. B) run layer by layer, so a
+ * streamed layer is brought in once for the whole group.  x[i], y[i] (resp.
+ * dy[i], dx[i]) belong to micro-batch mb0 + i. */
+int tps_stage_forward_group(tps_stage* st, int mb0, int n, const void* const* x,
+                            void* const* y);
+int tps_stage_backward_group(tps_stage* st, int mb0, int n, const void* const* dy,
+                             void* const* dx);
+
+/* Wait for both streams; reports asynchronous faults as TPS_EHIP. */
+int tps_stage_sync(tps_stage* st);
+
+int tps_stage_stats(const tps_stage* st, tps_stats* out);
+
+/* Releases events and host metadata (caller buffers are untouched). */
+int tps_stage_destroy(tps_stage* st);
+
+/* Thread-local message of the last failing call ("" if none). */
+const char* tps_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TPSTAGE_H */

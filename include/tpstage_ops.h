@@ -1,0 +1,98 @@
+/*
+ * tpstage_ops.h -- op-level C ABI: the individual gfx950 kernels the stage
+ * runs, exposed for per-kernel parity tests and microbenchmarks.
+ *
+ * All pointers are device pointers; `stream` is a hipStream_t (NULL = the
+ * null stream).  Storage dtype is TPS_F32 or TPS_BF16 (tpstage.h); every
+ * kernel computes in f32 and rounds once to the storage dtype on store
+ * (round to nearest even).  All reductions run in a fixed order: results are
+ * bitwise reproducible for a given shape.  Calls are asynchronous; argument
+ * errors return TPS_EINVAL before anything is launched.
+ */
+#ifndef TPSTAGE_OPS_H
+#define TPSTAGE_OPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "tpstage.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* GEMM operand layouts (row-major storage):
+ *   NT: C[M,N] = A[M,K] * B[N,K]^T   (forward linears: x W^T)
+ *   NN: C[M,N] = A[M,K] * B[K,N]     (input gradients: dy W)
+ *   TN: C[M,N] = A[K,M]^T * B[K,N]   (weight gradients: dy^T x, K = tokens)
+ * The contiguous extent of each operand and every leading dimension must be
+ * a multiple of 8 elements (bf16) or 4 elements (f32); the other extents are
+ * free (ragged tiles are masked). */
+enum { TPS_GEMM_NT = 0, TPS_GEMM_NN = 1, TPS_GEMM_TN = 2 };
+
+/* Epilogues (acc = the f32 product, m = row, n = column):
+ *   STORE       C = acc
+ *   BIAS        C = acc + bias[n]
+ *   BIAS_RESID  C = acc + bias[n] + resid[m, n]
+ *   BIAS_GELU   u = round(acc + bias[n]); aux[m, n] = u (if aux != NULL);
+ *               C = round(GeLU(u)), GeLU(u) = u/2 (1 + erf(u / sqrt 2))
+ *   GELU_GRAD   C = acc * GeLU'(aux[m, n]),  GeLU'(u) = Phi(u) + u phi(u)
+ *   ACC_F32     C (f32) += acc  (C is float*, read-modify-write) */
+enum {
+  TPS_EPI_STORE = 0, TPS_EPI_BIAS = 1, TPS_EPI_BIAS_RESID = 2,
+  TPS_EPI_BIAS_GELU = 3, TPS_EPI_GELU_GRAD = 4, TPS_EPI_ACC_F32 = 5
+};
+
+int tps_op_gemm(int dtype, int layout, int epilogue, int M, int N, int K,
+                const void* A, int64_t lda, const void* B, int64_t ldb,
+                void* C, int64_t ldc, const void* bias, const void* resid,
+                int64_t ldr, void* aux, int64_t ldaux, void* stream);
+
+/* LayerNorm over rows of x[rows, cols]: out = (x - mean) * rstd * gamma + beta
+ * with mean, biased variance and rstd = 1/sqrt(var + eps) in f32.  mean and
+ * rstd ([rows] f32) are written when non-NULL.  cols <= 16384. */
+int tps_op_layernorm_fwd(int dtype, int rows, int cols, const void* x,
+                         const void* gamma, const void* beta, float eps,
+                         void* out, float* mean, float* rstd, void* stream);
+
+/* LayerNorm backward: with zhat = (x - mean) rstd and g = dout * gamma,
+ *   dx = resid_grad + rstd (g - mean(g) - zhat mean(g zhat))
+ * (resid_grad may be NULL), and, when dgamma / dbeta are non-NULL,
+ *   dgamma += sum_rows dout * zhat,  dbeta += sum_rows dout  (f32, fixed order).
+ * workspace: tps_op_workspace_bytes(TPS_WS_COLSUM, rows, 2 * cols) bytes. */
+int tps_op_layernorm_bwd(int dtype, int rows, int cols, const void* dout,
+                         const void* x, const float* mean, const float* rstd,
+                         const void* gamma, const void* resid_grad, void* dx,
+                         float* dgamma, float* dbeta, float* workspace,
+                         void* stream);
+
+/* Causal attention forward over packed qkv[b*s, 3*heads*d]:
+ *   o = softmax(q k^T / sqrt(d), keys j <= query i of the same sequence) v,
+ *   lse[b, heads, s] = log sum_{j <= i} exp(q_i . k_j / sqrt(d)) (may be NULL).
+ * d = 64 or 128.  o is [b*s, heads*d]. */
+int tps_op_attention_fwd(int dtype, int b, int s, int n_heads, int head_dim,
+                         const void* qkv, void* o, float* lse, void* stream);
+
+/* Causal attention backward: dqkv[b*s, 3*heads*d] from qkv, o, lse and do.
+ * Deterministic (no atomics).  workspace: tps_op_workspace_bytes(
+ * TPS_WS_ATTN_BWD, b * s, n_heads) bytes. */
+int tps_op_attention_bwd(int dtype, int b, int s, int n_heads, int head_dim,
+                         const void* qkv, const void* o, const float* lse,
+                         const void* d_o, void* dqkv, float* workspace,
+                         void* stream);
+
+/* out[c] += sum_r x[r, c] over x[rows, cols] (leading dimension ldx), f32,
+ * fixed order.  workspace: tps_op_workspace_bytes(TPS_WS_COLSUM, rows, cols). */
+int tps_op_colsum(int dtype, int rows, int cols, const void* x, int64_t ldx,
+                  float* out, float* workspace, void* stream);
+
+/* g[i] = round(GeLU(u[i])) for n elements. */
+int tps_op_gelu(int dtype, int64_t n, const void* u, void* g, void* stream);
+
+enum { TPS_WS_COLSUM = 0, TPS_WS_ATTN_BWD = 1 };
+uint64_t tps_op_workspace_bytes(int kind, int64_t rows, int64_t cols);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TPSTAGE_OPS_H */

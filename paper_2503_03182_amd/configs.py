@@ -1,0 +1,83 @@
+"""The stage workloads (shapes and policies) used by tests and the bench.
+
+Every workload is one pipeline stage of GPT pre-LN decoder layers run
+micro-batch by micro-batch; names say what the workload is.
+"""
+from __future__ import annotations
+
+from .tpstage import (GRAN_LAYER, GRAN_SEGMENT, KEEP, OFFLOAD, RECOMPUTE, TENSORS, W_RESIDENT,
+                      W_STREAM, StageConfig)
+
+
+def policy_all(L: int, mode: int, keep_inputs: bool = False) -> list:
+    pol = [{t: mode for t in TENSORS} for _ in range(L)]
+    if keep_inputs or mode == RECOMPUTE:
+        for l in range(L):
+            if keep_inputs or l == 0:
+                pol[l]["x"] = KEEP
+    return pol
+
+
+def policy_selective(L: int) -> list:
+    """Operator-level recompute: attention output and GeLU output dropped."""
+    return [{t: (RECOMPUTE if t in ("o", "g") else KEEP) for t in TENSORS} for _ in range(L)]
+
+
+def policy_layer_inputs(L: int) -> list:
+    """Full-layer recompute: only each layer's input stays resident."""
+    return [{t: (KEEP if t == "x" else RECOMPUTE) for t in TENSORS} for _ in range(L)]
+
+
+def tiny(policy: str = "keep") -> StageConfig:
+    """2 layers, hidden 256, 4 heads, MLP 1024, causal seq 128, micro-batch 2,
+    4 micro-batches, f32.  policy: keep | recompute | offload."""
+    L, M = 2, 4
+    cfg = StageConfig(n_layers=L, hidden=256, n_heads=4, mlp=1024, seq=128, micro_batch=2, n_micro=M,
+                      dtype="f32")
+    if policy == "recompute":
+        cfg.policy = policy_all(L, RECOMPUTE)
+    elif policy == "offload":
+        cfg.policy = policy_all(L, OFFLOAD)
+        cfg.offload_mb_mask = (1 << M) - 1
+    return cfg
+
+
+def stage4_h2048() -> StageConfig:
+    """4 layers, hidden 2048, 16 heads, MLP 8192, causal seq 2048, micro-batch 1,
+    8 micro-batches, bf16; selective recompute of attention and GeLU outputs."""
+    return StageConfig(n_layers=4, hidden=2048, n_heads=16, mlp=8192, seq=2048, micro_batch=1, n_micro=8,
+                       dtype="bf16", policy=policy_selective(4), granularity=GRAN_SEGMENT)
+
+
+def stage5_h5120_offload() -> StageConfig:
+    """5 layers, hidden 5120, 40 heads, MLP 20480, causal seq 2048, micro-batch 1,
+    16 micro-batches in flight, bf16; activations of the micro-batches with the
+    most slack offloaded to pinned host and prefetched before their backward."""
+    return StageConfig(n_layers=5, hidden=5120, n_heads=40, mlp=20480, seq=2048, micro_batch=1, n_micro=16,
+                       dtype="bf16", policy=policy_all(5, OFFLOAD), offload_auto=True, lookahead=4,
+                       link_gbps_hint=50.0, tflops_hint=1000.0)
+
+
+def stage4_seq8192_recompute() -> StageConfig:
+    """4 layers, hidden 4096, 32 heads, MLP 16384, causal seq 8192, micro-batch 1,
+    8 micro-batches, bf16; full-layer recompute keeping only layer inputs."""
+    return StageConfig(n_layers=4, hidden=4096, n_heads=32, mlp=16384, seq=8192, micro_batch=1, n_micro=8,
+                       dtype="bf16", policy=policy_layer_inputs(4), granularity=GRAN_SEGMENT)
+
+
+def stage12_h8192_stream(n_micro: int = 8) -> StageConfig:
+    """12 layers, hidden 8192, 64 heads, MLP 32768, causal seq 4096, micro-batch 1,
+    8 micro-batches, bf16 weights and f32 grads streamed from pinned host per
+    layer (layer-major groups), activations recomputed from layer inputs."""
+    return StageConfig(n_layers=12, hidden=8192, n_heads=64, mlp=32768, seq=4096, micro_batch=1,
+                       n_micro=n_micro, dtype="bf16", policy=policy_layer_inputs(12), granularity=GRAN_LAYER,
+                       weights=W_STREAM, window=3)
+
+
+WORKLOADS = {
+    "tiny": tiny,
+    "stage4_h2048": stage4_h2048,
+    "stage5_h5120_offload": stage5_h5120_offload,
+    "stage4_seq8192_recompute": stage4_seq8192_recompute,
+    "stage12_h8192_stream": stage12_h8192_stream,
+}

@@ -1,0 +1,55 @@
+// Internal launchers of the gfx950 kernels (host side).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/tpstage_ops.h"
+
+namespace tps {
+
+struct GemmArgs {
+  int M, N, K;
+  const void* A; int64_t lda;
+  const void* B; int64_t ldb;
+  void* C; int64_t ldc;
+  const void* bias;
+  const void* resid; int64_t ldr;
+  void* aux; int64_t ldaux;
+  int epi;
+  int tiles_m, tiles_n;
+};
+
+hipError_t gemm_launch_nt(int dtype, GemmArgs g, hipStream_t stream);
+hipError_t gemm_launch_nn(int dtype, GemmArgs g, hipStream_t stream);
+hipError_t gemm_launch_tn(int dtype, GemmArgs g, hipStream_t stream);
+
+
+hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, const void* A,
+                       int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
+                       const void* bias, const void* resid, int64_t ldr, void* aux, int64_t ldaux,
+                       hipStream_t stream);
+
+hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, void* o,
+                                float* lse, hipStream_t st);
+// dvec: [b, nh, s] f32 scratch
+hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, const void* o,
+                                const float* lse, const void* dout, void* dqkv, float* dvec,
+                                hipStream_t st);
+
+hipError_t layernorm_fwd_launch(int dtype, int rows, int cols, const void* x, const void* gamma,
+                                const void* beta, float eps, void* out, float* mean, float* rstd,
+                                hipStream_t st);
+// dx = resid + LN^T(dout); when dgamma/dbeta are set, partial column sums go
+// to ws ([2 * cols * parts] f32) and are added to dgamma/dbeta in fixed order.
+hipError_t layernorm_bwd_launch(int dtype, int rows, int cols, const void* dout, const void* x,
+                                const float* mean, const float* rstd, const void* gamma,
+                                const void* resid, void* dx, float* dgamma, float* dbeta,
+                                float* ws, hipStream_t st);
+// out[c] += sum_r x[r, c]  (two passes through ws, fixed order)
+hipError_t colsum_launch(int dtype, int rows, int cols, const void* x, int64_t ldx, float* out,
+                         float* ws, hipStream_t st);
+uint64_t colsum_ws_bytes(int64_t rows, int64_t cols);
+hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st);
+hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st);
+
+}  // namespace tps

@@ -1,0 +1,312 @@
+// HBM-bound kernels of the stage: LayerNorm forward/backward, fixed-order
+// column reductions (bias, gain and shift gradients), GeLU recompute and a
+// zero fill.  16-byte vector accesses; one 256-thread workgroup per row for
+// the row-wise kernels, reductions butterfly-within-wave then in wave order.
+#include "kernels.h"
+#include "tps_device.h"
+#include "ws.h"
+
+namespace tps {
+
+namespace {
+
+constexpr int kRowsPerPart = kColsumRowsPerPart;
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int wave = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[wave] = v;
+  __syncthreads();
+  return ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+template <typename T, int NC>
+__global__ __launch_bounds__(256) void ln_fwd_kernel(const T* __restrict__ x, const T* __restrict__ gamma,
+                                                     const T* __restrict__ beta, float eps, T* __restrict__ out,
+                                                     float* __restrict__ mean, float* __restrict__ rstd,
+                                                     int rows, int cols) {
+  constexpr int VEC = 16 / sizeof(T);
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  const T* xr = x + (int64_t)row * cols;
+  float v[NC][VEC];
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int col = (threadIdx.x + c * 256) * VEC;
+    if (col < cols) {
+      const Vec16<T> t = load16(xr + col);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) v[c][i] = to_f32(t.get(i));
+    } else {
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) v[c][i] = 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) s += v[c][i];
+  }
+  const float mu = block_sum(s, red) / (float)cols;
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int col = (threadIdx.x + c * 256) * VEC;
+    if (col < cols) {
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const float d = v[c][i] - mu;
+        ss += d * d;
+      }
+    }
+  }
+  const float var = block_sum(ss, red) / (float)cols;
+  const float rs = 1.0f / sqrtf(var + eps);
+  T* orow = out + (int64_t)row * cols;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int col = (threadIdx.x + c * 256) * VEC;
+    if (col < cols) {
+      const Vec16<T> g = load16(gamma + col), b = load16(beta + col);
+      Vec16<T> o;
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) o.set(i, from_f32<T>((v[c][i] - mu) * rs * to_f32(g.get(i)) + to_f32(b.get(i))));
+      store16(orow + col, o);
+    }
+  }
+  if (threadIdx.x == 0) {
+    if (mean) mean[row] = mu;
+    if (rstd) rstd[row] = rs;
+  }
+}
+
+template <typename T, int NC>
+__global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dout, const T* __restrict__ x,
+                                                     const float* __restrict__ mean, const float* __restrict__ rstd,
+                                                     const T* __restrict__ gamma, const T* __restrict__ resid,
+                                                     T* __restrict__ dx, int rows, int cols) {
+  constexpr int VEC = 16 / sizeof(T);
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  const float mu = mean[row], rs = rstd[row];
+  const T* xr = x + (int64_t)row * cols;
+  const T* dr = dout + (int64_t)row * cols;
+  float zh[NC][VEC], gv[NC][VEC];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int col = (threadIdx.x + c * 256) * VEC;
+    if (col < cols) {
+      const Vec16<T> xv = load16(xr + col), dv = load16(dr + col), g = load16(gamma + col);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        zh[c][i] = (to_f32(xv.get(i)) - mu) * rs;
+        gv[c][i] = to_f32(dv.get(i)) * to_f32(g.get(i));
+        s1 += gv[c][i];
+        s2 += gv[c][i] * zh[c][i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) zh[c][i] = gv[c][i] = 0.f;
+    }
+  }
+  const float m1 = block_sum(s1, red) / (float)cols;
+  const float m2 = block_sum(s2, red) / (float)cols;
+  T* o = dx + (int64_t)row * cols;
+  const T* rr = resid ? resid + (int64_t)row * cols : nullptr;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int col = (threadIdx.x + c * 256) * VEC;
+    if (col < cols) {
+      Vec16<T> r;
+      if (rr) r = load16(rr + col);
+      Vec16<T> w;
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        float val = rs * (gv[c][i] - m1 - zh[c][i] * m2);
+        if (rr) val += to_f32(r.get(i));
+        w.set(i, from_f32<T>(val));
+      }
+      store16(o + col, w);
+    }
+  }
+}
+
+// Pass 1 of a column reduction: ws[part][k][c] = sum over the part's rows.
+// k = 0: sum x (or dout); k = 1 (LN mode): sum dout * zhat.
+template <typename T, bool LN>
+__global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ x, int64_t ldx,
+                                                          const T* __restrict__ xin, const float* __restrict__ mean,
+                                                          const float* __restrict__ rstd, float* __restrict__ ws,
+                                                          int rows, int cols) {
+  constexpr int VEC = 16 / sizeof(T);
+  const int col = (blockIdx.x * 256 + threadIdx.x) * VEC;
+  if (col >= cols) return;
+  const int part = blockIdx.y;
+  const int r0 = part * kRowsPerPart, r1 = min(rows, r0 + kRowsPerPart);
+  float a[VEC], z[VEC];
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) a[i] = z[i] = 0.f;
+  for (int r = r0; r < r1; ++r) {
+    const Vec16<T> v = load16(x + (int64_t)r * ldx + col);
+    if constexpr (LN) {
+      const Vec16<T> xv = load16(xin + (int64_t)r * cols + col);
+      const float mu = mean[r], rs = rstd[r];
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) {
+        const float d = to_f32(v.get(i));
+        a[i] += d;
+        z[i] += d * ((to_f32(xv.get(i)) - mu) * rs);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) a[i] += to_f32(v.get(i));
+    }
+  }
+  const int nk = LN ? 2 : 1;
+  float* w = ws + (int64_t)part * nk * cols;
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) w[col + i] = a[i];
+  if constexpr (LN) {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) w[cols + col + i] = z[i];
+  }
+}
+
+// Pass 2: out_k[c] += sum over parts in ascending order.
+__global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ ws, int parts, int nk,
+                                                           int cols, float* __restrict__ out0,
+                                                           float* __restrict__ out1) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  float s0 = 0.f, s1 = 0.f;
+  for (int p = 0; p < parts; ++p) {
+    s0 += ws[((int64_t)p * nk) * cols + c];
+    if (nk == 2) s1 += ws[((int64_t)p * nk + 1) * cols + c];
+  }
+  if (out0) out0[c] += s0;
+  if (nk == 2 && out1) out1[c] += s1;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gelu_kernel(const T* __restrict__ u, T* __restrict__ g, int64_t n) {
+  constexpr int VEC = 16 / sizeof(T);
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * VEC;
+  if (i + VEC <= n) {
+    const Vec16<T> v = load16(u + i);
+    Vec16<T> w;
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) w.set(k, from_f32<T>(gelu_f(to_f32(v.get(k)))));
+    store16(g + i, w);
+  } else {
+    for (int64_t k = i; k < n; ++k) g[k] = from_f32<T>(gelu_f(to_f32(u[k])));
+  }
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(u32x4* p, uint64_t n16, uint8_t* tail, uint32_t ntail) {
+  const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  for (uint64_t k = i; k < n16; k += stride) p[k] = u32x4{0u, 0u, 0u, 0u};
+  if (i < ntail) tail[i] = 0;
+}
+
+// Per-row kernels are instantiated for NC 16-byte chunks per thread.
+#define TPS_ROW_DISPATCH(KERNEL, T, rows, cols, st, ...)                                        \
+  do {                                                                                           \
+    constexpr int VEC_ = 16 / sizeof(T);                                                         \
+    const int nc_ = (cols + 256 * VEC_ - 1) / (256 * VEC_);                                      \
+    dim3 grid_(rows), block_(256);                                                               \
+    if (nc_ <= 1) hipLaunchKernelGGL((KERNEL<T, 1>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);       \
+    else if (nc_ <= 2) hipLaunchKernelGGL((KERNEL<T, 2>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
+    else if (nc_ <= 4) hipLaunchKernelGGL((KERNEL<T, 4>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
+    else if (nc_ <= 8) hipLaunchKernelGGL((KERNEL<T, 8>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
+    else hipLaunchKernelGGL((KERNEL<T, 16>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);               \
+  } while (0)
+
+template <typename T>
+hipError_t colsum_typed(int rows, int cols, const void* x, int64_t ldx, const void* xin, const float* mean,
+                        const float* rstd, float* out0, float* out1, float* ws, bool ln, hipStream_t st) {
+  constexpr int VEC = 16 / sizeof(T);
+  const int parts = (rows + kRowsPerPart - 1) / kRowsPerPart;
+  dim3 grid((cols / VEC + 255) / 256, parts);
+  if (ln)
+    hipLaunchKernelGGL((colsum_part_kernel<T, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
+                       static_cast<const T*>(xin), mean, rstd, ws, rows, cols);
+  else
+    hipLaunchKernelGGL((colsum_part_kernel<T, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
+                       static_cast<const T*>(nullptr), mean, rstd, ws, rows, cols);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, ws, parts, ln ? 2 : 1,
+                     cols, out0, out1);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+uint64_t colsum_ws_bytes(int64_t rows, int64_t cols) { return colsum_ws_elems(rows, cols) * 4; }
+
+hipError_t layernorm_fwd_launch(int dtype, int rows, int cols, const void* x, const void* gamma,
+                                const void* beta, float eps, void* out, float* mean, float* rstd,
+                                hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  if (dtype == TPS_BF16)
+    TPS_ROW_DISPATCH(ln_fwd_kernel, bf16, rows, cols, st, (const bf16*)x, (const bf16*)gamma, (const bf16*)beta,
+                     eps, (bf16*)out, mean, rstd);
+  else
+    TPS_ROW_DISPATCH(ln_fwd_kernel, float, rows, cols, st, (const float*)x, (const float*)gamma,
+                     (const float*)beta, eps, (float*)out, mean, rstd);
+  return hipGetLastError();
+}
+
+hipError_t layernorm_bwd_launch(int dtype, int rows, int cols, const void* dout, const void* x,
+                                const float* mean, const float* rstd, const void* gamma,
+                                const void* resid, void* dx, float* dgamma, float* dbeta,
+                                float* ws, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  if (dtype == TPS_BF16)
+    TPS_ROW_DISPATCH(ln_bwd_kernel, bf16, rows, cols, st, (const bf16*)dout, (const bf16*)x, mean, rstd,
+                     (const bf16*)gamma, (const bf16*)resid, (bf16*)dx);
+  else
+    TPS_ROW_DISPATCH(ln_bwd_kernel, float, rows, cols, st, (const float*)dout, (const float*)x, mean, rstd,
+                     (const float*)gamma, (const float*)resid, (float*)dx);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || (dgamma == nullptr && dbeta == nullptr)) return e;
+  // dbeta = sum dout (k = 0), dgamma = sum dout * zhat (k = 1)
+  if (dtype == TPS_BF16)
+    return colsum_typed<bf16>(rows, cols, dout, cols, x, mean, rstd, dbeta, dgamma, ws, true, st);
+  return colsum_typed<float>(rows, cols, dout, cols, x, mean, rstd, dbeta, dgamma, ws, true, st);
+}
+
+hipError_t colsum_launch(int dtype, int rows, int cols, const void* x, int64_t ldx, float* out,
+                         float* ws, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  if (dtype == TPS_BF16)
+    return colsum_typed<bf16>(rows, cols, x, ldx, nullptr, nullptr, nullptr, out, nullptr, ws, false, st);
+  return colsum_typed<float>(rows, cols, x, ldx, nullptr, nullptr, nullptr, out, nullptr, ws, false, st);
+}
+
+hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  if (dtype == TPS_BF16) {
+    const int64_t blocks = (n / 8 + 255) / 256 + 1;
+    hipLaunchKernelGGL((gelu_kernel<bf16>), dim3((unsigned)blocks), dim3(256), 0, st, (const bf16*)u, (bf16*)g, n);
+  } else {
+    const int64_t blocks = (n / 4 + 255) / 256 + 1;
+    hipLaunchKernelGGL((gelu_kernel<float>), dim3((unsigned)blocks), dim3(256), 0, st, (const float*)u, (float*)g, n);
+  }
+  return hipGetLastError();
+}
+
+hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st) {
+  if (bytes == 0) return hipSuccess;
+  const uint64_t n16 = bytes / 16;
+  const uint32_t ntail = (uint32_t)(bytes % 16);
+  uint64_t blocks = (n16 + 255) / 256;
+  if (blocks < 1) blocks = 1;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st, (u32x4*)p, n16,
+                     (uint8_t*)p + n16 * 16, ntail);
+  return hipGetLastError();
+}
+
+}  // namespace tps

@@ -1,0 +1,139 @@
+// Op-level C ABI (tpstage_ops.h): argument checks, then one kernel launch
+// sequence on the caller's stream.
+#include <string>
+
+#include "errors.h"
+#include "kernels.h"
+
+using namespace tps;
+
+namespace {
+
+int vec_of(int dtype) { return dtype == TPS_BF16 ? 8 : 4; }
+bool dtype_ok(int dtype) { return dtype == TPS_F32 || dtype == TPS_BF16; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int bad(const std::string& m) { return set_error(TPS_EINVAL, m); }
+
+}  // namespace
+
+extern "C" int tps_op_gemm(int dtype, int layout, int epilogue, int M, int N, int K, const void* A,
+                           int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
+                           const void* bias, const void* resid, int64_t ldr, void* aux,
+                           int64_t ldaux, void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype)) return bad("gemm: dtype");
+  if (layout < TPS_GEMM_NT || layout > TPS_GEMM_TN) return bad("gemm: layout");
+  if (epilogue < TPS_EPI_STORE || epilogue > TPS_EPI_ACC_F32) return bad("gemm: epilogue");
+  if (M < 0 || N < 0 || K < 0) return bad("gemm: negative extent");
+  if (M == 0 || N == 0) return TPS_OK;
+  if (!A || !B || !C) return bad("gemm: null operand");
+  const int v = vec_of(dtype);
+  // contiguous extent of each operand, and leading dimensions
+  const int64_t a_contig = (layout == TPS_GEMM_TN) ? M : K;
+  const int64_t b_contig = (layout == TPS_GEMM_NT) ? K : N;
+  if (a_contig % v || b_contig % v || lda % v || ldb % v)
+    return bad("gemm: contiguous extents and lda/ldb must be multiples of 8 (bf16) / 4 (f32)");
+  if (lda < a_contig || ldb < b_contig || ldc < N) return bad("gemm: leading dimension too small");
+  if (!aligned16(A) || !aligned16(B)) return bad("gemm: A and B must be 16-byte aligned");
+  const bool needs_bias = epilogue == TPS_EPI_BIAS || epilogue == TPS_EPI_BIAS_RESID || epilogue == TPS_EPI_BIAS_GELU;
+  if (needs_bias && !bias) return bad("gemm: epilogue needs bias");
+  if (epilogue == TPS_EPI_BIAS_RESID && (!resid || ldr < N)) return bad("gemm: epilogue needs resid");
+  if (epilogue == TPS_EPI_GELU_GRAD && (!aux || ldaux < N)) return bad("gemm: GELU_GRAD needs aux (u)");
+  if (epilogue == TPS_EPI_BIAS_GELU && aux && ldaux < N) return bad("gemm: ldaux too small");
+  return check_hip(gemm_launch(dtype, layout, epilogue, M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr,
+                               aux, ldaux, (hipStream_t)stream),
+                   "gemm launch");
+}
+
+extern "C" int tps_op_layernorm_fwd(int dtype, int rows, int cols, const void* x, const void* gamma,
+                                    const void* beta, float eps, void* out, float* mean, float* rstd,
+                                    void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype)) return bad("layernorm: dtype");
+  if (rows < 0 || cols <= 0 || cols > 16384 || cols % vec_of(dtype)) return bad("layernorm: cols");
+  if (!x || !gamma || !beta || !out) return bad("layernorm: null pointer");
+  return check_hip(layernorm_fwd_launch(dtype, rows, cols, x, gamma, beta, eps, out, mean, rstd,
+                                        (hipStream_t)stream),
+                   "layernorm_fwd launch");
+}
+
+extern "C" int tps_op_layernorm_bwd(int dtype, int rows, int cols, const void* dout, const void* x,
+                                    const float* mean, const float* rstd, const void* gamma,
+                                    const void* resid_grad, void* dx, float* dgamma, float* dbeta,
+                                    float* workspace, void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype)) return bad("layernorm_bwd: dtype");
+  if (rows < 0 || cols <= 0 || cols > 16384 || cols % vec_of(dtype)) return bad("layernorm_bwd: cols");
+  if (!dout || !x || !mean || !rstd || !gamma || !dx) return bad("layernorm_bwd: null pointer");
+  if ((dgamma || dbeta) && !workspace) return bad("layernorm_bwd: workspace needed for dgamma/dbeta");
+  return check_hip(layernorm_bwd_launch(dtype, rows, cols, dout, x, mean, rstd, gamma, resid_grad, dx,
+                                        dgamma, dbeta, workspace, (hipStream_t)stream),
+                   "layernorm_bwd launch");
+}
+
+extern "C" int tps_op_attention_fwd(int dtype, int b, int s, int n_heads, int head_dim, const void* qkv,
+                                    void* o, float* lse, void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype)) return bad("attention: dtype");
+  if (head_dim != 64 && head_dim != 128) return bad("attention: head_dim must be 64 or 128");
+  if (b < 0 || s < 0 || n_heads <= 0) return bad("attention: shape");
+  if (b == 0 || s == 0) return TPS_OK;
+  if (!qkv || !o || !aligned16(qkv)) return bad("attention: qkv/o");
+  return check_hip(attention_fwd_launch(dtype, b, s, n_heads, head_dim, qkv, o, lse, (hipStream_t)stream),
+                   "attention_fwd launch");
+}
+
+extern "C" int tps_op_attention_bwd(int dtype, int b, int s, int n_heads, int head_dim, const void* qkv,
+                                    const void* o, const float* lse, const void* d_o, void* dqkv,
+                                    float* workspace, void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype)) return bad("attention_bwd: dtype");
+  if (head_dim != 64 && head_dim != 128) return bad("attention_bwd: head_dim must be 64 or 128");
+  if (b < 0 || s < 0 || n_heads <= 0) return bad("attention_bwd: shape");
+  if (b == 0 || s == 0) return TPS_OK;
+  if (!qkv || !o || !lse || !d_o || !dqkv || !workspace) return bad("attention_bwd: null pointer");
+  if (!aligned16(qkv) || !aligned16(o) || !aligned16(d_o)) return bad("attention_bwd: alignment");
+  return check_hip(attention_bwd_launch(dtype, b, s, n_heads, head_dim, qkv, o, lse, d_o, dqkv, workspace,
+                                        (hipStream_t)stream),
+                   "attention_bwd launch");
+}
+
+extern "C" int tps_op_colsum(int dtype, int rows, int cols, const void* x, int64_t ldx, float* out,
+                             float* workspace, void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype)) return bad("colsum: dtype");
+  if (rows < 0 || cols <= 0 || cols % vec_of(dtype) || ldx % vec_of(dtype) || ldx < cols)
+    return bad("colsum: shape");
+  if (!x || !out || !workspace) return bad("colsum: null pointer");
+  return check_hip(colsum_launch(dtype, rows, cols, x, ldx, out, workspace, (hipStream_t)stream),
+                   "colsum launch");
+}
+
+extern "C" int tps_op_gelu(int dtype, int64_t n, const void* u, void* g, void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype) || n < 0) return bad("gelu: args");
+  if (n == 0) return TPS_OK;
+  if (!u || !g || !aligned16(u) || !aligned16(g)) return bad("gelu: pointers");
+  return check_hip(gelu_launch(dtype, n, u, g, (hipStream_t)stream), "gelu launch");
+}
+
+extern "C" uint64_t tps_op_workspace_bytes(int kind, int64_t rows, int64_t cols) {
+  if (kind == TPS_WS_COLSUM) return colsum_ws_bytes(rows, cols);
+  if (kind == TPS_WS_ATTN_BWD) return (uint64_t)(rows * cols * 4);  // rows = b*s, cols = heads
+  return 0;
+}
+
+namespace tps {
+
+hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, const void* A, int64_t lda,
+                       const void* B, int64_t ldb, void* C, int64_t ldc, const void* bias, const void* resid,
+                       int64_t ldr, void* aux, int64_t ldaux, hipStream_t stream) {
+  if (M == 0 || N == 0) return hipSuccess;
+  GemmArgs g{M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux, ldaux, epi, 0, 0};
+  if (layout == TPS_GEMM_NT) return gemm_launch_nt(dtype, g, stream);
+  if (layout == TPS_GEMM_NN) return gemm_launch_nn(dtype, g, stream);
+  return gemm_launch_tn(dtype, g, stream);
+}
+
+}  // namespace tps

@@ -1,0 +1,97 @@
+// Stage planner: host-only (no HIP calls), so tps_plan() runs without a GPU.
+#pragma once
+
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/tpstage.h"
+
+namespace tps {
+
+// Forward operators of one layer, in execution order.
+enum FwdOp { OP_LN1 = 0, OP_QKV, OP_ATTN, OP_OPROJ, OP_LN2, OP_FC1, OP_GELU, OP_FC2, OP_COUNT };
+
+constexpr uint64_t kNone = ~0ull;
+
+struct Plan {
+  // shape
+  int L = 0, h = 0, nh = 0, d = 0, f = 0, s = 0, b = 0, M = 0, T = 0;
+  int dtype = TPS_BF16, esize = 2;
+  float eps = 1e-5f;
+  int weights = TPS_W_RESIDENT, window = 2, granularity = TPS_GRAN_SEGMENT, lookahead = 1;
+  std::vector<uint8_t> policy;        // [L][TPS_T_COUNT]
+  uint64_t offload_mask = 0;
+
+  // order
+  std::vector<int> op_kind, op_mb;    // planned F/B order
+  std::vector<int> pos_f, pos_b;      // op index of F(mb), B(mb)
+
+  // sizes
+  uint64_t tbytes[TPS_T_COUNT] = {};  // bytes of each tensor of one (layer, mb)
+  uint64_t poff[TPS_P_COUNT] = {}, pbytes = 0;   // packed parameter block
+  uint64_t goff[TPS_P_COUNT] = {}, gbytes = 0;   // packed f32 gradient block
+
+  // Checkpoint slots of one micro-batch, in two parts:
+  //  - resident part: KEEP tensors of every layer, held from F(mb) to B(mb);
+  //  - offload part: OFFLOAD tensors of every layer.  Held from F(mb) to B(mb)
+  //    for micro-batches that are not offloaded; for offloaded ones held
+  //    during F(mb) (until the copies to host finish) and again from the
+  //    prefetch to the end of B(mb).  Host slots use the same layout.
+  std::vector<uint64_t> kslot_off;    // [L][T_COUNT], kNone if not KEEP
+  uint64_t kslot_bytes = 0;
+  int n_kslots = 0;
+  std::vector<int> kslot;             // [M]
+  std::vector<uint64_t> oslot_off;    // [L][T_COUNT], kNone if not OFFLOAD
+  uint64_t oslot_bytes = 0;
+  int n_oslots = 0;
+  std::vector<int> oslot_f, oslot_b;  // [M]
+  int max_inflight = 0;
+  int n_host_slots = 0;
+  std::vector<int> host_slot;         // [M], -1 if the mb is not offloaded
+  std::vector<std::vector<int>> prefetch_at;  // [n_ops]: mbs brought back before op p
+
+  // recompute: replay buffer and per-layer replay program
+  std::vector<uint64_t> replay_off;   // [L][T_COUNT], kNone if not recomputed
+  uint64_t replay_bytes = 0;
+  std::vector<uint32_t> replay_ops;   // [L] bit mask over FwdOp
+  int n_replay_layers = 0;
+
+  // backward working buffers (offsets inside the work region)
+  struct Work {
+    uint64_t gA, gB, dx1, t1, du, dqkv, dvec, ws;
+  } work{};
+  uint64_t work_bytes = 0;
+  uint64_t ws_bytes = 0;
+
+  // streamed weights window
+  uint64_t wwin_bytes = 0;
+
+  // arena
+  uint64_t off_kslots = 0, off_oslots = 0, off_replay = 0, off_work = 0, off_wwin = 0;
+  uint64_t arena_bytes = 0, host_bytes = 0;
+
+  // accounting
+  double fwd_flops = 0, bwd_flops = 0, recompute_flops = 0;
+  uint64_t h2d_bytes = 0, d2h_bytes = 0;
+  uint64_t keep_all_bytes = 0, predicted_peak = 0;
+
+  int mode(int layer, int t, int mb) const {
+    const int p = policy[layer * TPS_T_COUNT + t];
+    if (p == TPS_OFFLOAD && !((offload_mask >> mb) & 1ull)) return TPS_KEEP;
+    return p;
+  }
+  int pol(int layer, int t) const { return policy[layer * TPS_T_COUNT + t]; }
+  bool offloaded(int mb) const { return host_slot[mb] >= 0; }
+};
+
+// Builds the plan; returns TPS_OK or an error code (message via set_error).
+int make_plan(const tps_config* cfg, Plan* out);
+
+// Algorithmic flops of one forward operator for one (layer, mb).
+double op_flops(const Plan& p, int op);
+
+void fill_plan_info(const Plan& p, tps_plan_info* info);
+
+}  // namespace tps

@@ -1,0 +1,731 @@
+// Stage executor: runs F(mb) and B(mb) in the planned order on the caller's
+// compute stream, with
+//  - the recompute engine: the replay program of each layer re-runs the same
+//    forward kernels with the same launch shapes, so regenerated tensors are
+//    bit-identical to the ones the forward produced; SEGMENT granularity
+//    replays every layer of the micro-batch before its backward starts
+//    (block-wise T-Recomp), LAYER granularity replays one layer just before
+//    that layer's backward;
+//  - the offload engine: OFFLOAD tensors of offloaded micro-batches go to
+//    pinned host slots on the copy stream after each layer's forward and come
+//    back `lookahead` ops before the backward; cross-stream hazards on the
+//    staging slots are ordered by events recorded at every release and waited
+//    on at every acquire;
+//  - streamed weights: a window of layer parameter blocks (and f32 gradient
+//    blocks) in the arena, brought in on the copy stream ahead of use.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "errors.h"
+#include "kernels.h"
+#include "planner.h"
+
+using namespace tps;
+
+namespace {
+
+#define TPS_HIP(expr)                                      \
+  do {                                                     \
+    hipError_t _e = (expr);                                \
+    if (_e != hipSuccess) return check_hip(_e, #expr);     \
+  } while (0)
+
+#define TPS_TRY(expr)              \
+  do {                             \
+    int _rc = (expr);              \
+    if (_rc != TPS_OK) return _rc; \
+  } while (0)
+
+struct SlotEvent {
+  hipEvent_t ev = nullptr;
+  bool valid = false;
+};
+
+// Streamed-weight window entry.
+struct WinEntry {
+  int layer = -1;
+  bool grads_live = false;     // the device grad block holds this layer's sums
+  SlotEvent param_ready;       // H2D of the parameters finished (copy stream)
+  SlotEvent last_use;          // last kernel reading the entry (compute stream)
+  SlotEvent grads_out;         // D2H of the grads finished (copy stream)
+  uint64_t tick = 0;
+};
+
+}  // namespace
+
+struct tps_stage {
+  Plan p;
+  std::vector<char*> lp;     // per-layer parameter block (device, or pinned host when streamed)
+  std::vector<float*> lg;    // per-layer f32 gradient block (device, or pinned host when streamed)
+  char* arena = nullptr;
+  char* host = nullptr;
+  hipStream_t cs = nullptr, xs = nullptr;
+  int device = 0;
+
+  std::vector<SlotEvent> oslot_ev;               // last release of each offload slot
+  std::vector<std::vector<hipEvent_t>> ready_ev; // [M][L] H2D of (mb, layer) done
+  std::vector<char> prefetched;
+  hipEvent_t ev_tmp = nullptr;
+
+  // streamed weights
+  std::vector<WinEntry> win;
+  std::vector<char> grads_touched;  // [L] this iteration
+  uint64_t tick = 0;
+
+  int cursor = 0;
+  std::vector<char> f_done, b_done;
+  bool in_iteration = false;
+  tps_stats stats{};
+
+  // --- pointers -----------------------------------------------------------
+  char* kslot_base(int mb) const { return arena + p.off_kslots + (uint64_t)p.kslot[mb] * p.kslot_bytes; }
+  char* oslot_base(int slot) const { return arena + p.off_oslots + (uint64_t)slot * p.oslot_bytes; }
+  char* host_base(int mb) const { return host + (uint64_t)p.host_slot[mb] * p.oslot_bytes; }
+
+  // device address of tensor t of (layer l, mb) for the phase (fwd or bwd)
+  void* tensor(int l, int t, int mb, bool bwd) const {
+    const size_t k = (size_t)l * TPS_T_COUNT + t;
+    switch (p.policy[k]) {
+      case TPS_RECOMPUTE: return arena + p.off_replay + p.replay_off[k];
+      case TPS_KEEP: return kslot_base(mb) + p.kslot_off[k];
+      default: return oslot_base(bwd ? p.oslot_b[mb] : p.oslot_f[mb]) + p.oslot_off[k];
+    }
+  }
+  char* work(uint64_t off) const { return arena + p.off_work + off; }
+
+  // --- events ---------------------------------------------------------------
+  int release_oslot(int slot, hipStream_t on) {
+    TPS_HIP(hipEventRecord(oslot_ev[slot].ev, on));
+    oslot_ev[slot].valid = true;
+    return TPS_OK;
+  }
+  int acquire_oslot(int slot, hipStream_t on) {
+    if (oslot_ev[slot].valid) TPS_HIP(hipStreamWaitEvent(on, oslot_ev[slot].ev, 0));
+    return TPS_OK;
+  }
+
+  // --- parameters (resident or streamed window) ------------------------------
+  const char* params_of(int l, int* entry);
+  float* grads_of(int l, int entry);
+  int ensure_layer(int l, bool for_backward, int* entry);
+  int prefetch_layer(int l);
+  int flush_grads(int entry);
+  int flush_all_grads();
+
+  // --- compute ----------------------------------------------------------------
+  int gemm(int layout, int epi, int M, int N, int K, const void* A, int64_t lda, const void* B, int64_t ldb,
+           void* C, int64_t ldc, const void* bias = nullptr, const void* resid = nullptr, int64_t ldr = 0,
+           void* aux = nullptr, int64_t ldaux = 0) {
+    ++stats.kernels;
+    return check_hip(gemm_launch(p.dtype, layout, epi, M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux,
+                                 ldaux, cs),
+                     "gemm");
+  }
+  int fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots);
+  int bwd_layer(int l, int mb, const char* W, float* G, const void* dy, void* dx);
+  int forward_one(int mb, const void* x, void* y);
+  int backward_one(int mb, const void* dy, void* dx);
+  int prefetch_mb(int mb);
+  int run_prefetches(int pos);
+  int d2h_layer(int l, int mb);
+  int check_op(int kind, int mb);
+};
+
+// ---------------------------------------------------------------------------
+// Streamed weights.  Window entries hold a layer's parameter block and its
+// f32 gradient block.  Eviction waits (on the copy stream) for the entry's
+// last compute use; gradients leave with a D2H into the caller's host block
+// and come back with an H2D if the layer is touched again in the iteration.
+// ---------------------------------------------------------------------------
+const char* tps_stage::params_of(int l, int* entry) {
+  if (p.weights == TPS_W_RESIDENT) return lp[l];
+  return arena + p.off_wwin + (uint64_t)(*entry) * (p.pbytes + p.gbytes);
+}
+
+float* tps_stage::grads_of(int l, int entry) {
+  if (p.weights == TPS_W_RESIDENT) return lg[l];
+  return reinterpret_cast<float*>(arena + p.off_wwin + (uint64_t)entry * (p.pbytes + p.gbytes) + p.pbytes);
+}
+
+int tps_stage::flush_grads(int e) {
+  WinEntry& w = win[e];
+  if (w.layer < 0 || !w.grads_live) return TPS_OK;
+  TPS_HIP(hipEventRecord(ev_tmp, cs));
+  TPS_HIP(hipStreamWaitEvent(xs, ev_tmp, 0));
+  TPS_HIP(hipMemcpyAsync(lg[w.layer], grads_of(w.layer, e), p.gbytes, hipMemcpyDeviceToHost, xs));
+  stats.d2h_bytes += p.gbytes;
+  TPS_HIP(hipEventRecord(w.grads_out.ev, xs));
+  w.grads_out.valid = true;
+  w.grads_live = false;
+  return TPS_OK;
+}
+
+int tps_stage::flush_all_grads() {
+  if (p.weights != TPS_W_STREAM) return TPS_OK;
+  for (size_t e = 0; e < win.size(); ++e) TPS_TRY(flush_grads((int)e));
+  return TPS_OK;
+}
+
+// Make layer l's parameters resident (streamed mode); issues the H2D on the
+// copy stream if needed.  Does not make the compute stream wait.
+int tps_stage::prefetch_layer(int l) {
+  if (p.weights != TPS_W_STREAM || l < 0 || l >= p.L) return TPS_OK;
+  for (auto& w : win)
+    if (w.layer == l) return TPS_OK;
+  // evict the least recently used entry
+  int victim = 0;
+  for (size_t e = 1; e < win.size(); ++e)
+    if (win[e].tick < win[victim].tick) victim = (int)e;
+  WinEntry& w = win[victim];
+  TPS_TRY(flush_grads(victim));
+  if (w.last_use.valid) TPS_HIP(hipStreamWaitEvent(xs, w.last_use.ev, 0));
+  w.layer = l;
+  w.tick = ++tick;
+  int e = victim;
+  TPS_HIP(hipMemcpyAsync(const_cast<char*>(params_of(l, &e)), lp[l], p.pbytes, hipMemcpyHostToDevice, xs));
+  stats.h2d_bytes += p.pbytes;
+  TPS_HIP(hipEventRecord(w.param_ready.ev, xs));
+  w.param_ready.valid = true;
+  w.grads_live = false;
+  return TPS_OK;
+}
+
+int tps_stage::ensure_layer(int l, bool for_backward, int* entry) {
+  *entry = -1;
+  if (p.weights != TPS_W_STREAM) return TPS_OK;
+  TPS_TRY(prefetch_layer(l));
+  int e = 0;
+  while (win[e].layer != l) ++e;
+  WinEntry& w = win[e];
+  w.tick = ++tick;
+  TPS_HIP(hipStreamWaitEvent(cs, w.param_ready.ev, 0));
+  if (for_backward && !w.grads_live) {
+    // the grad block of this entry may still be leaving for another layer
+    if (w.grads_out.valid) TPS_HIP(hipStreamWaitEvent(cs, w.grads_out.ev, 0));
+    if (grads_touched[l]) {
+      TPS_HIP(hipEventRecord(ev_tmp, cs));
+      TPS_HIP(hipStreamWaitEvent(xs, ev_tmp, 0));
+      TPS_HIP(hipMemcpyAsync(grads_of(l, e), lg[l], p.gbytes, hipMemcpyHostToDevice, xs));
+      stats.h2d_bytes += p.gbytes;
+      TPS_HIP(hipEventRecord(ev_tmp, xs));
+      TPS_HIP(hipStreamWaitEvent(cs, ev_tmp, 0));
+    } else {
+      TPS_HIP(fill_zero_launch(grads_of(l, e), p.gbytes, cs));
+      ++stats.kernels;
+      grads_touched[l] = 1;
+    }
+    w.grads_live = true;
+  }
+  *entry = e;
+  return TPS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// One layer forward (or a replay of part of it).
+// ---------------------------------------------------------------------------
+int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots) {
+  const int T = p.T, h = p.h, f = p.f;
+  auto ptr = [&](int t) { return tensor(l, t, mb, bwd_slots); };
+  // optional outputs: in the forward written unless dropped; in a replay
+  // written only when they are the tensors being regenerated
+  auto opt = [&](int t) -> bool {
+    const bool rec = p.pol(l, t) == TPS_RECOMPUTE;
+    return replay ? rec : !rec;
+  };
+  const char* P = W;
+  auto par = [&](int i) { return P + p.poff[i]; };
+  void *x = ptr(TPS_T_X), *a = ptr(TPS_T_A), *qkv = ptr(TPS_T_QKV), *o = ptr(TPS_T_O);
+  void *x1 = ptr(TPS_T_X1), *c = ptr(TPS_T_C), *u = ptr(TPS_T_U), *g = ptr(TPS_T_G);
+  float* lse = static_cast<float*>(ptr(TPS_T_LSE));
+  float* ln1 = static_cast<float*>(ptr(TPS_T_LN1));
+  float* ln2 = static_cast<float*>(ptr(TPS_T_LN2));
+
+  if (ops & (1u << OP_LN1)) {
+    ++stats.kernels;
+    TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, x, par(TPS_P_G1), par(TPS_P_BE1), p.eps, a,
+                                 opt(TPS_T_LN1) ? ln1 : nullptr, opt(TPS_T_LN1) ? ln1 + T : nullptr, cs));
+  }
+  if (ops & (1u << OP_QKV))
+    TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS, T, 3 * h, h, a, h, par(TPS_P_W_QKV), h, qkv, 3 * h, par(TPS_P_B_QKV)));
+  if (ops & (1u << OP_ATTN)) {
+    ++stats.kernels;
+    TPS_HIP(attention_fwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, opt(TPS_T_LSE) ? lse : nullptr, cs));
+  }
+  if (ops & (1u << OP_OPROJ))
+    TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_RESID, T, h, h, o, h, par(TPS_P_W_O), h, x1, h, par(TPS_P_B_O), x, h));
+  if (ops & (1u << OP_LN2)) {
+    ++stats.kernels;
+    TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, x1, par(TPS_P_G2), par(TPS_P_BE2), p.eps, c,
+                                 opt(TPS_T_LN2) ? ln2 : nullptr, opt(TPS_T_LN2) ? ln2 + T : nullptr, cs));
+  }
+  if (ops & (1u << OP_FC1))
+    TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_GELU, T, f, h, c, h, par(TPS_P_W_1), h, g, f, par(TPS_P_B_1), nullptr, 0,
+                 opt(TPS_T_U) ? u : nullptr, f));
+  if (ops & (1u << OP_GELU)) {
+    ++stats.kernels;
+    TPS_HIP(gelu_launch(p.dtype, (int64_t)T * f, u, g, cs));
+  }
+  if (ops & (1u << OP_FC2))
+    TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_RESID, T, h, f, g, f, par(TPS_P_W_2), f, y, h, par(TPS_P_B_2), x1, h));
+  return TPS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// One layer backward; parameter gradients accumulate into G (f32).
+// ---------------------------------------------------------------------------
+int tps_stage::bwd_layer(int l, int mb, const char* W, float* G, const void* dy, void* dx) {
+  const int T = p.T, h = p.h, f = p.f;
+  auto ptr = [&](int t) { return tensor(l, t, mb, true); };
+  auto par = [&](int i) { return W + p.poff[i]; };
+  auto grd = [&](int i) { return reinterpret_cast<float*>(reinterpret_cast<char*>(G) + p.goff[i]); };
+  void *x = ptr(TPS_T_X), *a = ptr(TPS_T_A), *qkv = ptr(TPS_T_QKV), *o = ptr(TPS_T_O);
+  void *x1 = ptr(TPS_T_X1), *c = ptr(TPS_T_C), *u = ptr(TPS_T_U), *g = ptr(TPS_T_G);
+  const float* lse = static_cast<const float*>(ptr(TPS_T_LSE));
+  const float* ln1 = static_cast<const float*>(ptr(TPS_T_LN1));
+  const float* ln2 = static_cast<const float*>(ptr(TPS_T_LN2));
+  void* dx1 = work(p.work.dx1);
+  void* t1 = work(p.work.t1);
+  void* du = work(p.work.du);
+  void* dqkv = work(p.work.dqkv);
+  float* dvec = reinterpret_cast<float*>(work(p.work.dvec));
+  float* ws = reinterpret_cast<float*>(work(p.work.ws));
+
+  // MLP: y = x1 + GeLU(c W1^T + b1) W2^T + b2
+  TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_GELU_GRAD, T, f, h, dy, h, par(TPS_P_W_2), f, du, f, nullptr, nullptr, 0, u, f));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f));
+  ++stats.kernels;
+  TPS_HIP(colsum_launch(p.dtype, T, h, dy, h, grd(TPS_P_B_2), ws, cs));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h));
+  ++stats.kernels;
+  TPS_HIP(colsum_launch(p.dtype, T, f, du, f, grd(TPS_P_B_1), ws, cs));
+  TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, f, du, f, par(TPS_P_W_1), h, t1, h));
+  ++stats.kernels;
+  TPS_HIP(layernorm_bwd_launch(p.dtype, T, h, t1, x1, ln2, ln2 + T, par(TPS_P_G2), dy, dx1, grd(TPS_P_G2),
+                               grd(TPS_P_BE2), ws, cs));
+  // attention block: x1 = x + o Wo^T + bo
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h));
+  ++stats.kernels;
+  TPS_HIP(colsum_launch(p.dtype, T, h, dx1, h, grd(TPS_P_B_O), ws, cs));
+  TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, h, dx1, h, par(TPS_P_W_O), h, t1, h));
+  ++stats.kernels;
+  TPS_HIP(attention_bwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, lse, t1, dqkv, dvec, cs));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h));
+  ++stats.kernels;
+  TPS_HIP(colsum_launch(p.dtype, T, 3 * h, dqkv, 3 * h, grd(TPS_P_B_QKV), ws, cs));
+  TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, 3 * h, dqkv, 3 * h, par(TPS_P_W_QKV), h, t1, h));
+  ++stats.kernels;
+  TPS_HIP(layernorm_bwd_launch(p.dtype, T, h, t1, x, ln1, ln1 + T, par(TPS_P_G1), dx1, dx, grd(TPS_P_G1),
+                               grd(TPS_P_BE1), ws, cs));
+  return TPS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Offload engine
+// ---------------------------------------------------------------------------
+int tps_stage::d2h_layer(int l, int mb) {
+  bool any = false;
+  for (int t = 0; t < TPS_T_COUNT; ++t) any |= p.oslot_off[(size_t)l * TPS_T_COUNT + t] != kNone;
+  if (!any) return TPS_OK;
+  TPS_HIP(hipEventRecord(ev_tmp, cs));
+  TPS_HIP(hipStreamWaitEvent(xs, ev_tmp, 0));
+  for (int t = 0; t < TPS_T_COUNT; ++t) {
+    const size_t k = (size_t)l * TPS_T_COUNT + t;
+    if (p.oslot_off[k] == kNone) continue;
+    TPS_HIP(hipMemcpyAsync(host_base(mb) + p.oslot_off[k], oslot_base(p.oslot_f[mb]) + p.oslot_off[k], p.tbytes[t],
+                           hipMemcpyDeviceToHost, xs));
+    stats.d2h_bytes += p.tbytes[t];
+  }
+  return TPS_OK;
+}
+
+// Bring an offloaded micro-batch back into its staging slot, deepest layer
+// first (the backward starts there); one ready event per layer.
+int tps_stage::prefetch_mb(int mb) {
+  if (prefetched[mb]) return TPS_OK;
+  const int slot = p.oslot_b[mb];
+  TPS_TRY(acquire_oslot(slot, xs));
+  for (int l = p.L - 1; l >= 0; --l) {
+    for (int t = 0; t < TPS_T_COUNT; ++t) {
+      const size_t k = (size_t)l * TPS_T_COUNT + t;
+      if (p.oslot_off[k] == kNone) continue;
+      TPS_HIP(hipMemcpyAsync(oslot_base(slot) + p.oslot_off[k], host_base(mb) + p.oslot_off[k], p.tbytes[t],
+                             hipMemcpyHostToDevice, xs));
+      stats.h2d_bytes += p.tbytes[t];
+    }
+    TPS_HIP(hipEventRecord(ready_ev[mb][l], xs));
+  }
+  prefetched[mb] = 1;
+  return TPS_OK;
+}
+
+int tps_stage::run_prefetches(int pos) {
+  for (int mb : p.prefetch_at[pos]) TPS_TRY(prefetch_mb(mb));
+  return TPS_OK;
+}
+
+int tps_stage::check_op(int kind, int mb) {
+  if (!in_iteration) return set_error(TPS_ESTATE, "call tps_stage_begin_iteration first");
+  if (mb < 0 || mb >= p.M) return set_error(TPS_EORDER, "micro-batch index out of range");
+  const char* name = kind == TPS_OP_F ? "F" : "B";
+  if (kind == TPS_OP_B && !f_done[mb]) return set_error(TPS_EORDER, "backward before forward of micro-batch " + std::to_string(mb));
+  if (kind == TPS_OP_B && b_done[mb]) return set_error(TPS_EORDER, "second backward of micro-batch " + std::to_string(mb));
+  if (kind == TPS_OP_F && f_done[mb]) return set_error(TPS_EORDER, "second forward of micro-batch " + std::to_string(mb) + " in one iteration");
+  if (cursor >= (int)p.op_kind.size() || p.op_kind[cursor] != kind || p.op_mb[cursor] != mb) {
+    std::string want = cursor < (int)p.op_kind.size()
+                           ? std::string(p.op_kind[cursor] == TPS_OP_F ? "F(" : "B(") + std::to_string(p.op_mb[cursor]) + ")"
+                           : "end of iteration";
+    return set_error(TPS_EORDER, std::string("call ") + name + "(" + std::to_string(mb) + ") out of the planned order; expected " + want);
+  }
+  return TPS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// F(mb) and B(mb)
+// ---------------------------------------------------------------------------
+int tps_stage::forward_one(int mb, const void* x, void* y) {
+  const bool off = p.host_slot[mb] >= 0;
+  if (p.oslot_bytes) TPS_TRY(acquire_oslot(p.oslot_f[mb], cs));
+  TPS_HIP(hipMemcpyAsync(tensor(0, TPS_T_X, mb, false), x, p.tbytes[TPS_T_X], hipMemcpyDeviceToDevice, cs));
+  for (int l = 0; l < p.L; ++l) {
+    int e = -1;
+    TPS_TRY(ensure_layer(l, false, &e));
+    TPS_TRY(prefetch_layer(l + 1));
+    void* yl = (l == p.L - 1) ? y : tensor(l + 1, TPS_T_X, mb, false);
+    TPS_TRY(fwd_layer(l, mb, params_of(l, &e), yl, 0xFFu & ~(1u << OP_GELU), false, false));
+    if (e >= 0) {
+      TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
+      win[e].last_use.valid = true;
+    }
+    if (off) TPS_TRY(d2h_layer(l, mb));
+  }
+  if (off) TPS_TRY(release_oslot(p.oslot_f[mb], xs));
+  return TPS_OK;
+}
+
+int tps_stage::backward_one(int mb, const void* dy, void* dx) {
+  const bool off = p.host_slot[mb] >= 0;
+  if (off) {
+    TPS_TRY(prefetch_mb(mb));
+    for (int l = 0; l < p.L; ++l) TPS_HIP(hipStreamWaitEvent(cs, ready_ev[mb][l], 0));
+  }
+  if (p.granularity == TPS_GRAN_SEGMENT) {
+    for (int l = 0; l < p.L; ++l) {
+      if (!p.replay_ops[l]) continue;
+      int e = -1;
+      TPS_TRY(ensure_layer(l, false, &e));
+      void* yl = (l == p.L - 1) ? nullptr : tensor(l + 1, TPS_T_X, mb, true);
+      TPS_TRY(fwd_layer(l, mb, params_of(l, &e), yl, p.replay_ops[l], true, true));
+      ++stats.replays;
+      if (e >= 0) {
+        TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
+        win[e].last_use.valid = true;
+      }
+    }
+  }
+  const void* cur = dy;
+  char* gA = work(p.work.gA);
+  char* gB = work(p.work.gB);
+  for (int l = p.L - 1; l >= 0; --l) {
+    int e = -1;
+    TPS_TRY(ensure_layer(l, true, &e));
+    TPS_TRY(prefetch_layer(l - 1));
+    const char* W = params_of(l, &e);
+    if (p.granularity == TPS_GRAN_LAYER && p.replay_ops[l]) {
+      TPS_TRY(fwd_layer(l, mb, W, nullptr, p.replay_ops[l], true, true));
+      ++stats.replays;
+    }
+    void* out = (l == 0) ? dx : (cur == gA ? gB : gA);
+    TPS_TRY(bwd_layer(l, mb, W, grads_of(l, e), cur, out));
+    if (e >= 0) {
+      TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
+      win[e].last_use.valid = true;
+    }
+    cur = out;
+  }
+  if (p.oslot_bytes) TPS_TRY(release_oslot(p.oslot_b[mb], cs));
+  return TPS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, const tps_memory* mem,
+                              tps_stage** out) {
+  clear_error();
+  if (!out || !params || !mem) return set_error(TPS_EINVAL, "tps_stage_init: null argument");
+  *out = nullptr;
+  tps_stage* st = new (std::nothrow) tps_stage();
+  if (!st) return set_error(TPS_ENOMEM, "tps_stage_init: host allocation");
+  int rc = make_plan(cfg, &st->p);
+  if (rc) { delete st; return rc; }
+  const Plan& p = st->p;
+  if (!params->layer_params || !params->layer_grads) { delete st; return set_error(TPS_EINVAL, "tps_stage_init: params"); }
+  for (int l = 0; l < p.L; ++l) {
+    if (!params->layer_params[l] || !params->layer_grads[l]) { delete st; return set_error(TPS_EINVAL, "tps_stage_init: null layer block"); }
+    st->lp.push_back(static_cast<char*>(params->layer_params[l]));
+    st->lg.push_back(params->layer_grads[l]);
+  }
+  if (!mem->device_arena || mem->device_bytes < p.arena_bytes) {
+    delete st;
+    return set_error(TPS_ENOMEM, "tps_stage_init: device arena of " + std::to_string(mem->device_bytes) +
+                                     " bytes, plan needs " + std::to_string(p.arena_bytes));
+  }
+  if ((reinterpret_cast<uintptr_t>(mem->device_arena) & 255u) != 0) { delete st; return set_error(TPS_EINVAL, "device arena must be 256-byte aligned"); }
+  if (p.host_bytes && (!mem->host_arena || mem->host_bytes < p.host_bytes)) {
+    delete st;
+    return set_error(TPS_ENOMEM, "tps_stage_init: pinned host arena of " + std::to_string(mem->host_bytes) +
+                                     " bytes, plan needs " + std::to_string(p.host_bytes));
+  }
+  st->arena = static_cast<char*>(mem->device_arena);
+  st->host = static_cast<char*>(mem->host_arena);
+  st->cs = static_cast<hipStream_t>(mem->compute_stream);
+  st->xs = static_cast<hipStream_t>(mem->copy_stream);
+  if ((p.host_bytes || p.weights == TPS_W_STREAM) && (!st->xs || st->xs == st->cs)) {
+    delete st;
+    return set_error(TPS_EINVAL, "offload and streamed weights need a copy stream distinct from the compute stream");
+  }
+  auto mkev = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
+  hipError_t he = hipGetDevice(&st->device);
+  if (he == hipSuccess) he = mkev(&st->ev_tmp);
+  st->oslot_ev.resize(p.n_oslots);
+  for (auto& s : st->oslot_ev)
+    if (he == hipSuccess) he = mkev(&s.ev);
+  st->ready_ev.assign(p.M, std::vector<hipEvent_t>(p.L, nullptr));
+  for (int mb = 0; mb < p.M && he == hipSuccess; ++mb)
+    if (p.host_slot[mb] >= 0)
+      for (int l = 0; l < p.L && he == hipSuccess; ++l) he = mkev(&st->ready_ev[mb][l]);
+  if (p.weights == TPS_W_STREAM) {
+    st->win.resize(p.window);
+    for (auto& w : st->win) {
+      if (he == hipSuccess) he = mkev(&w.param_ready.ev);
+      if (he == hipSuccess) he = mkev(&w.last_use.ev);
+      if (he == hipSuccess) he = mkev(&w.grads_out.ev);
+    }
+  }
+  if (he != hipSuccess) {
+    int r = check_hip(he, "tps_stage_init: event creation");
+    tps_stage_destroy(st);
+    return r;
+  }
+  st->f_done.assign(p.M, 0);
+  st->b_done.assign(p.M, 0);
+  st->prefetched.assign(p.M, 0);
+  st->grads_touched.assign(p.L, 0);
+  *out = st;
+  return TPS_OK;
+}
+
+extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
+  clear_error();
+  if (!st) return set_error(TPS_EINVAL, "null stage");
+  if (st->in_iteration && st->cursor != 0 && st->cursor < (int)st->p.op_kind.size())
+    return set_error(TPS_ESTATE, "previous iteration has unfinished ops");
+  st->cursor = 0;
+  std::fill(st->f_done.begin(), st->f_done.end(), 0);
+  std::fill(st->b_done.begin(), st->b_done.end(), 0);
+  std::fill(st->prefetched.begin(), st->prefetched.end(), 0);
+  st->stats = tps_stats{};
+  const Plan& p = st->p;
+  if (p.weights == TPS_W_STREAM) {
+    // host gradients of the previous iteration must be complete before reuse
+    int rc = st->flush_all_grads();
+    if (rc) return rc;
+    std::fill(st->grads_touched.begin(), st->grads_touched.end(), zero_grads ? 0 : 1);
+  } else if (zero_grads) {
+    for (int l = 0; l < p.L; ++l) {
+      hipError_t e = fill_zero_launch(st->lg[l], p.gbytes, st->cs);
+      if (e != hipSuccess) return check_hip(e, "zero grads");
+      ++st->stats.kernels;
+    }
+  }
+  st->in_iteration = true;
+  return TPS_OK;
+}
+
+static int finish_op(tps_stage* st) {
+  ++st->cursor;
+  st->stats.ops_done = st->cursor;
+  if (st->cursor == (int)st->p.op_kind.size()) return st->flush_all_grads();
+  return TPS_OK;
+}
+
+extern "C" int tps_stage_forward(tps_stage* st, int mb, const void* x, void* y) {
+  clear_error();
+  if (!st) return set_error(TPS_EINVAL, "null stage");
+  if (!x || !y) return set_error(TPS_EINVAL, "tps_stage_forward: null x or y");
+  TPS_TRY(st->check_op(TPS_OP_F, mb));
+  TPS_TRY(st->run_prefetches(st->cursor));
+  TPS_TRY(st->forward_one(mb, x, y));
+  st->f_done[mb] = 1;
+  return finish_op(st);
+}
+
+extern "C" int tps_stage_backward(tps_stage* st, int mb, const void* dy, void* dx) {
+  clear_error();
+  if (!st) return set_error(TPS_EINVAL, "null stage");
+  if (!dy || !dx) return set_error(TPS_EINVAL, "tps_stage_backward: null dy or dx");
+  TPS_TRY(st->check_op(TPS_OP_B, mb));
+  TPS_TRY(st->run_prefetches(st->cursor));
+  TPS_TRY(st->backward_one(mb, dy, dx));
+  st->b_done[mb] = 1;
+  return finish_op(st);
+}
+
+// Layer-major groups: all micro-batches of the group go through layer l
+// before layer l+1 (resp. l-1), so a streamed layer is brought in once.
+extern "C" int tps_stage_forward_group(tps_stage* st, int mb0, int n, const void* const* x, void* const* y) {
+  clear_error();
+  if (!st || !x || !y || n < 1) return set_error(TPS_EINVAL, "tps_stage_forward_group: arguments");
+  const Plan& p = st->p;
+  // validate the whole group against the order first
+  for (int i = 0; i < n; ++i) {
+    const int pos = st->cursor + i;
+    if (pos >= (int)p.op_kind.size() || p.op_kind[pos] != TPS_OP_F || p.op_mb[pos] != mb0 + i)
+      return set_error(TPS_EORDER, "forward group does not match the planned order");
+    if (!x[i] || !y[i]) return set_error(TPS_EINVAL, "forward group: null buffer");
+  }
+  TPS_TRY(st->check_op(TPS_OP_F, mb0));
+  if (n > 1)
+    for (int l = 1; l < p.L; ++l)
+      if (p.pol(l, TPS_T_X) == TPS_RECOMPUTE)
+        return set_error(TPS_EINVAL, "forward groups of more than one micro-batch need every layer input kept or offloaded");
+  for (int i = 0; i < n; ++i) TPS_TRY(st->run_prefetches(st->cursor + i));
+  for (int i = 0; i < n; ++i) {
+    const int mb = mb0 + i;
+    if (p.oslot_bytes) TPS_TRY(st->acquire_oslot(p.oslot_f[mb], st->cs));
+    TPS_HIP(hipMemcpyAsync(st->tensor(0, TPS_T_X, mb, false), x[i], p.tbytes[TPS_T_X], hipMemcpyDeviceToDevice, st->cs));
+  }
+  for (int l = 0; l < p.L; ++l) {
+    int e = -1;
+    TPS_TRY(st->ensure_layer(l, false, &e));
+    TPS_TRY(st->prefetch_layer(l + 1));
+    for (int i = 0; i < n; ++i) {
+      const int mb = mb0 + i;
+      void* yl = (l == p.L - 1) ? y[i] : st->tensor(l + 1, TPS_T_X, mb, false);
+      TPS_TRY(st->fwd_layer(l, mb, st->params_of(l, &e), yl, 0xFFu & ~(1u << OP_GELU), false, false));
+      if (p.host_slot[mb] >= 0) TPS_TRY(st->d2h_layer(l, mb));
+    }
+    if (e >= 0) {
+      TPS_HIP(hipEventRecord(st->win[e].last_use.ev, st->cs));
+      st->win[e].last_use.valid = true;
+    }
+  }
+  for (int i = 0; i < n; ++i) {
+    const int mb = mb0 + i;
+    if (p.host_slot[mb] >= 0) TPS_TRY(st->release_oslot(p.oslot_f[mb], st->xs));
+    st->f_done[mb] = 1;
+    ++st->cursor;
+  }
+  st->stats.ops_done = st->cursor;
+  if (st->cursor == (int)p.op_kind.size()) return st->flush_all_grads();
+  return TPS_OK;
+}
+
+extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const void* const* dy, void* const* dx) {
+  clear_error();
+  if (!st || !dy || !dx || n < 1) return set_error(TPS_EINVAL, "tps_stage_backward_group: arguments");
+  const Plan& p = st->p;
+  for (int i = 0; i < n; ++i) {
+    const int pos = st->cursor + i;
+    if (pos >= (int)p.op_kind.size() || p.op_kind[pos] != TPS_OP_B || p.op_mb[pos] != mb0 + i)
+      return set_error(TPS_EORDER, "backward group does not match the planned order");
+    if (!st->f_done[mb0 + i]) return set_error(TPS_EORDER, "backward before forward in group");
+    if (!dy[i] || !dx[i]) return set_error(TPS_EINVAL, "backward group: null buffer");
+  }
+  TPS_TRY(st->check_op(TPS_OP_B, mb0));
+  for (int i = 0; i < n; ++i) TPS_TRY(st->run_prefetches(st->cursor + i));
+  // gradients flow per micro-batch through ping-pong buffers; keep one pair
+  // per group member in the caller's dx buffers: dx[i] holds the running
+  // gradient of micro-batch i between layers.
+  for (int i = 0; i < n; ++i) {
+    const int mb = mb0 + i;
+    if (p.host_slot[mb] >= 0) {
+      TPS_TRY(st->prefetch_mb(mb));
+      for (int l = 0; l < p.L; ++l) TPS_HIP(hipStreamWaitEvent(st->cs, st->ready_ev[mb][l], 0));
+    }
+  }
+  if (p.granularity == TPS_GRAN_SEGMENT && n > 1) {
+    bool any = false;
+    for (int l = 0; l < p.L; ++l) any |= p.replay_ops[l] != 0;
+    if (any) return set_error(TPS_EINVAL, "segment replay shares one replay buffer: backward groups of more than one micro-batch need layer granularity");
+  }
+  char* gA = st->work(p.work.gA);
+  for (int l = p.L - 1; l >= 0; --l) {
+    int e = -1;
+    TPS_TRY(st->ensure_layer(l, true, &e));
+    TPS_TRY(st->prefetch_layer(l - 1));
+    const char* W = st->params_of(l, &e);
+    for (int i = 0; i < n; ++i) {
+      const int mb = mb0 + i;
+      if (p.granularity == TPS_GRAN_SEGMENT && l == p.L - 1) {
+        for (int r = 0; r < p.L; ++r) {
+          if (!p.replay_ops[r]) continue;
+          int er = -1;
+          TPS_TRY(st->ensure_layer(r, false, &er));
+          void* yl = (r == p.L - 1) ? nullptr : st->tensor(r + 1, TPS_T_X, mb, true);
+          TPS_TRY(st->fwd_layer(r, mb, st->params_of(r, &er), yl, p.replay_ops[r], true, true));
+          ++st->stats.replays;
+        }
+      }
+      if (p.granularity == TPS_GRAN_LAYER && p.replay_ops[l]) {
+        TPS_TRY(st->fwd_layer(l, mb, W, nullptr, p.replay_ops[l], true, true));
+        ++st->stats.replays;
+      }
+      // the running gradient of micro-batch i lives in dx[i] between layers
+      const void* in = (l == p.L - 1) ? dy[i] : dx[i];
+      TPS_TRY(st->bwd_layer(l, mb, W, st->grads_of(l, e), in, gA));
+      TPS_HIP(hipMemcpyAsync(dx[i], gA, p.tbytes[TPS_T_X], hipMemcpyDeviceToDevice, st->cs));
+    }
+    if (e >= 0) {
+      TPS_HIP(hipEventRecord(st->win[e].last_use.ev, st->cs));
+      st->win[e].last_use.valid = true;
+    }
+  }
+  for (int i = 0; i < n; ++i) {
+    const int mb = mb0 + i;
+    if (p.oslot_bytes) TPS_TRY(st->release_oslot(p.oslot_b[mb], st->cs));
+    st->b_done[mb] = 1;
+    ++st->cursor;
+  }
+  st->stats.ops_done = st->cursor;
+  if (st->cursor == (int)p.op_kind.size()) return st->flush_all_grads();
+  return TPS_OK;
+}
+
+extern "C" int tps_stage_sync(tps_stage* st) {
+  clear_error();
+  if (!st) return set_error(TPS_EINVAL, "null stage");
+  TPS_HIP(hipStreamSynchronize(st->cs));
+  if (st->xs) TPS_HIP(hipStreamSynchronize(st->xs));
+  return TPS_OK;
+}
+
+extern "C" int tps_stage_stats(const tps_stage* st, tps_stats* out) {
+  clear_error();
+  if (!st || !out) return set_error(TPS_EINVAL, "null argument");
+  *out = st->stats;
+  return TPS_OK;
+}
+
+extern "C" int tps_stage_destroy(tps_stage* st) {
+  clear_error();
+  if (!st) return TPS_OK;
+  if (st->cs) (void)hipStreamSynchronize(st->cs);
+  if (st->xs) (void)hipStreamSynchronize(st->xs);
+  if (st->ev_tmp) (void)hipEventDestroy(st->ev_tmp);
+  for (auto& s : st->oslot_ev)
+    if (s.ev) (void)hipEventDestroy(s.ev);
+  for (auto& v : st->ready_ev)
+    for (auto e : v)
+      if (e) (void)hipEventDestroy(e);
+  for (auto& w : st->win) {
+    if (w.param_ready.ev) (void)hipEventDestroy(w.param_ready.ev);
+    if (w.last_use.ev) (void)hipEventDestroy(w.last_use.ev);
+    if (w.grads_out.ev) (void)hipEventDestroy(w.grads_out.ev);
+  }
+  delete st;
+  return TPS_OK;
+}

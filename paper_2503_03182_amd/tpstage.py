@@ -1,0 +1,357 @@
+"""ctypes binding of libtpstage.so (include/tpstage.h, include/tpstage_ops.h).
+
+Argument marshalling only: every step of the stage runs in the library's HIP
+kernels.  PyTorch supplies device memory, pinned host memory and streams.  If
+the library has not been built, importing the binding raises at first use;
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass, field
+from typing import Optional, Sequence
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpstage.so")
+
+# --- constants (mirror tpstage.h) ------------------------------------------
+TPS_ABI_VERSION = 1
+TPS_OK, TPS_EINVAL, TPS_ENOMEM, TPS_EORDER, TPS_EHIP, TPS_ETIMEOUT, TPS_ESTATE = 0, -1, -2, -3, -4, -5, -6
+TPS_F32, TPS_BF16 = 0, 1
+KEEP, RECOMPUTE, OFFLOAD = 0, 1, 2
+TENSORS = ("x", "a", "qkv", "o", "lse", "x1", "c", "u", "g", "ln1", "ln2")
+T_INDEX = {n: i for i, n in enumerate(TENSORS)}
+W_RESIDENT, W_STREAM = 0, 1
+GRAN_LAYER, GRAN_SEGMENT = 0, 1
+OP_F, OP_B = 0, 1
+PARAMS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "g1", "be1", "g2", "be2")
+GEMM_NT, GEMM_NN, GEMM_TN = 0, 1, 2
+EPI_STORE, EPI_BIAS, EPI_BIAS_RESID, EPI_BIAS_GELU, EPI_GELU_GRAD, EPI_ACC_F32 = range(6)
+WS_COLSUM, WS_ATTN_BWD = 0, 1
+
+_ERRNAMES = {TPS_EINVAL: "TPS_EINVAL", TPS_ENOMEM: "TPS_ENOMEM", TPS_EORDER: "TPS_EORDER",
+             TPS_EHIP: "TPS_EHIP", TPS_ETIMEOUT: "TPS_ETIMEOUT", TPS_ESTATE: "TPS_ESTATE"}
+
+
+class TpsError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{_ERRNAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+# --- structures --------------------------------------------------------------
+class Config(C.Structure):
+    _fields_ = [
+        ("abi_version", C.c_int32), ("n_layers", C.c_int32), ("hidden", C.c_int32),
+        ("n_heads", C.c_int32), ("mlp", C.c_int32), ("seq", C.c_int32),
+        ("micro_batch", C.c_int32), ("n_micro", C.c_int32), ("dtype", C.c_int32),
+        ("ln_eps", C.c_float), ("policy", C.POINTER(C.c_uint8)), ("offload_mb_mask", C.c_uint64),
+        ("offload_auto", C.c_int32), ("weights", C.c_int32), ("window", C.c_int32),
+        ("recompute_granularity", C.c_int32), ("n_ops", C.c_int32), ("ops", C.POINTER(C.c_int32)),
+        ("inflight", C.c_int32), ("link_gbps_hint", C.c_float), ("tflops_hint", C.c_float),
+        ("lookahead", C.c_int32),
+    ]
+
+
+class PlanInfo(C.Structure):
+    _fields_ = [
+        ("device_arena_bytes", C.c_uint64), ("host_arena_bytes", C.c_uint64),
+        ("slot_bytes", C.c_uint64), ("n_slots", C.c_int32),
+        ("offload_slot_bytes", C.c_uint64), ("n_offload_slots", C.c_int32),
+        ("n_host_slots", C.c_int32), ("max_inflight", C.c_int32),
+        ("replay_bytes", C.c_uint64), ("work_bytes", C.c_uint64),
+        ("weight_window_bytes", C.c_uint64), ("param_bytes", C.c_uint64),
+        ("grad_bytes", C.c_uint64), ("keep_all_bytes", C.c_uint64),
+        ("predicted_peak_bytes", C.c_uint64), ("offload_mb_mask", C.c_uint64),
+        ("n_offload_mbs", C.c_int32), ("n_replay_layers", C.c_int32),
+        ("fwd_flops", C.c_double), ("bwd_flops", C.c_double), ("recompute_flops", C.c_double),
+        ("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64),
+    ]
+
+    def as_dict(self) -> dict:
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class Params(C.Structure):
+    _fields_ = [("layer_params", C.POINTER(C.c_void_p)), ("layer_grads", C.POINTER(C.c_void_p))]
+
+
+class Memory(C.Structure):
+    _fields_ = [("device_arena", C.c_void_p), ("device_bytes", C.c_uint64),
+                ("host_arena", C.c_void_p), ("host_bytes", C.c_uint64),
+                ("compute_stream", C.c_void_p), ("copy_stream", C.c_void_p)]
+
+
+class Stats(C.Structure):
+    _fields_ = [("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("kernels", C.c_uint64),
+                ("replays", C.c_uint64), ("ops_done", C.c_int32)]
+
+
+# --- library -----------------------------------------------------------------
+_lib = None
+
+EXPORTED = (
+    "tps_param_layout", "tps_plan", "tps_stage_init", "tps_stage_begin_iteration",
+    "tps_stage_forward", "tps_stage_backward", "tps_stage_forward_group",
+    "tps_stage_backward_group", "tps_stage_sync", "tps_stage_stats", "tps_stage_destroy",
+    "tps_last_error", "tps_op_gemm", "tps_op_layernorm_fwd", "tps_op_layernorm_bwd",
+    "tps_op_attention_fwd", "tps_op_attention_bwd", "tps_op_colsum", "tps_op_gelu",
+    "tps_op_workspace_bytes",
+)
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> C.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2503_03182_amd.build` (no fallback exists)")
+        L = C.CDLL(_LIB_PATH)
+        vp, i32, i64, u64 = C.c_void_p, C.c_int, C.c_int64, C.c_uint64
+        L.tps_last_error.restype = C.c_char_p
+        L.tps_param_layout.argtypes = [C.POINTER(Config), C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
+                                       C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]
+        L.tps_plan.argtypes = [C.POINTER(Config), C.POINTER(PlanInfo)]
+        L.tps_stage_init.argtypes = [C.POINTER(Config), C.POINTER(Params), C.POINTER(Memory), C.POINTER(vp)]
+        L.tps_stage_begin_iteration.argtypes = [vp, i32]
+        L.tps_stage_forward.argtypes = [vp, i32, vp, vp]
+        L.tps_stage_backward.argtypes = [vp, i32, vp, vp]
+        L.tps_stage_forward_group.argtypes = [vp, i32, i32, C.POINTER(vp), C.POINTER(vp)]
+        L.tps_stage_backward_group.argtypes = [vp, i32, i32, C.POINTER(vp), C.POINTER(vp)]
+        L.tps_stage_sync.argtypes = [vp]
+        L.tps_stage_stats.argtypes = [vp, C.POINTER(Stats)]
+        L.tps_stage_destroy.argtypes = [vp]
+        L.tps_op_gemm.argtypes = [i32, i32, i32, i32, i32, i32, vp, i64, vp, i64, vp, i64, vp, vp, i64, vp, i64, vp]
+        L.tps_op_layernorm_fwd.argtypes = [i32, i32, i32, vp, vp, vp, C.c_float, vp, vp, vp, vp]
+        L.tps_op_layernorm_bwd.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.tps_op_attention_fwd.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp]
+        L.tps_op_attention_bwd.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+        L.tps_op_colsum.argtypes = [i32, i32, i32, vp, i64, vp, vp, vp]
+        L.tps_op_gelu.argtypes = [i32, i64, vp, vp, vp]
+        L.tps_op_workspace_bytes.argtypes = [i32, i64, i64]
+        L.tps_op_workspace_bytes.restype = u64
+        _lib = L
+    return _lib
+
+
+def check(rc: int) -> None:
+    if rc != TPS_OK:
+        raise TpsError(rc, lib().tps_last_error().decode())
+
+
+# --- configuration -----------------------------------------------------------
+@dataclass
+class StageConfig:
+    n_layers: int
+    hidden: int
+    n_heads: int
+    mlp: int
+    seq: int
+    micro_batch: int
+    n_micro: int
+    dtype: str = "bf16"                      # "bf16" or "f32"
+    ln_eps: float = 1e-5
+    policy: Optional[list] = None            # [L] dicts name -> KEEP/RECOMPUTE/OFFLOAD
+    offload_mb_mask: int = 0
+    offload_auto: bool = False
+    weights: int = W_RESIDENT
+    window: int = 2
+    granularity: int = GRAN_SEGMENT
+    ops: Optional[Sequence] = None           # [("F"|"B", mb)]
+    inflight: int = 0
+    link_gbps_hint: float = 50.0
+    tflops_hint: float = 1000.0
+    lookahead: int = 1
+    _keep: list = field(default_factory=list, repr=False)
+
+    @property
+    def tokens(self) -> int:
+        return self.micro_batch * self.seq
+
+    @property
+    def dtype_code(self) -> int:
+        return TPS_BF16 if self.dtype == "bf16" else TPS_F32
+
+    def to_c(self) -> Config:
+        c = Config()
+        c.abi_version = TPS_ABI_VERSION
+        c.n_layers, c.hidden, c.n_heads, c.mlp = self.n_layers, self.hidden, self.n_heads, self.mlp
+        c.seq, c.micro_batch, c.n_micro = self.seq, self.micro_batch, self.n_micro
+        c.dtype = self.dtype_code
+        c.ln_eps = self.ln_eps
+        self._keep = []
+        if self.policy is not None:
+            flat = (C.c_uint8 * (self.n_layers * len(TENSORS)))()
+            for l in range(self.n_layers):
+                for name, mode in self.policy[l].items():
+                    flat[l * len(TENSORS) + T_INDEX[name]] = mode
+            self._keep.append(flat)
+            c.policy = C.cast(flat, C.POINTER(C.c_uint8))
+        c.offload_mb_mask = self.offload_mb_mask
+        c.offload_auto = int(self.offload_auto)
+        c.weights, c.window, c.recompute_granularity = self.weights, self.window, self.granularity
+        if self.ops is not None:
+            arr = (C.c_int32 * (2 * len(self.ops)))()
+            for i, (k, mb) in enumerate(self.ops):
+                arr[2 * i] = OP_F if k == "F" else OP_B
+                arr[2 * i + 1] = mb
+            self._keep.append(arr)
+            c.n_ops = len(self.ops)
+            c.ops = C.cast(arr, C.POINTER(C.c_int32))
+        c.inflight = self.inflight
+        c.link_gbps_hint, c.tflops_hint = self.link_gbps_hint, self.tflops_hint
+        c.lookahead = self.lookahead
+        return c
+
+    def order(self) -> list:
+        """The planned op order (the library's default when ops is None)."""
+        if self.ops is not None:
+            return list(self.ops)
+        M = self.n_micro
+        W = M if self.inflight <= 0 or self.inflight > M else self.inflight
+        out = [("F", i) for i in range(W)]
+        nxt = W
+        for i in range(M):
+            out.append(("B", i))
+            if nxt < M:
+                out.append(("F", nxt))
+                nxt += 1
+        return out
+
+
+def plan(cfg: StageConfig) -> dict:
+    info = PlanInfo()
+    c = cfg.to_c()
+    check(lib().tps_plan(C.byref(c), C.byref(info)))
+    return info.as_dict()
+
+
+def param_layout(cfg: StageConfig):
+    po = (C.c_uint64 * len(PARAMS))()
+    go = (C.c_uint64 * len(PARAMS))()
+    pb, gb = C.c_uint64(), C.c_uint64()
+    c = cfg.to_c()
+    check(lib().tps_param_layout(C.byref(c), po, C.byref(pb), go, C.byref(gb)))
+    return list(po), pb.value, list(go), gb.value
+
+
+# --- stage ---------------------------------------------------------------------
+class Stage:
+    """One pipeline stage on one GPU.  Device and pinned host arenas are torch
+    allocations sized by the plan; parameter and f32 gradient blocks are torch
+    byte tensors laid out by param_layout()."""
+
+    def __init__(self, cfg: StageConfig, layer_params, layer_grads, device="cuda",
+                 compute_stream=None, copy_stream=None):
+        import torch
+        self.cfg = cfg
+        self.info = plan(cfg)
+        self.device = torch.device(device)
+        self.arena = torch.empty(max(self.info["device_arena_bytes"], 256), dtype=torch.uint8, device=self.device)
+        hb = self.info["host_arena_bytes"]
+        self.host = torch.empty(hb, dtype=torch.uint8, pin_memory=True) if hb else None
+        self.cs = compute_stream or torch.cuda.Stream(device=self.device)
+        self.xs = copy_stream or torch.cuda.Stream(device=self.device)
+        self.layer_params, self.layer_grads = list(layer_params), list(layer_grads)
+        L = cfg.n_layers
+        self._pp = (C.c_void_p * L)(*[t.data_ptr() for t in self.layer_params])
+        self._gp = (C.c_void_p * L)(*[t.data_ptr() for t in self.layer_grads])
+        prm = Params(C.cast(self._pp, C.POINTER(C.c_void_p)), C.cast(self._gp, C.POINTER(C.c_void_p)))
+        mem = Memory(self.arena.data_ptr(), self.arena.numel(),
+                     self.host.data_ptr() if self.host is not None else None, hb,
+                     self.cs.cuda_stream, self.xs.cuda_stream)
+        self._c = cfg.to_c()
+        h = C.c_void_p()
+        check(lib().tps_stage_init(C.byref(self._c), C.byref(prm), C.byref(mem), C.byref(h)))
+        self.handle = h
+
+    def begin_iteration(self, zero_grads: bool = True) -> None:
+        check(lib().tps_stage_begin_iteration(self.handle, int(zero_grads)))
+
+    def forward(self, mb: int, x, y) -> None:
+        check(lib().tps_stage_forward(self.handle, mb, x.data_ptr(), y.data_ptr()))
+
+    def backward(self, mb: int, dy, dx) -> None:
+        check(lib().tps_stage_backward(self.handle, mb, dy.data_ptr(), dx.data_ptr()))
+
+    def forward_group(self, mb0: int, xs, ys) -> None:
+        n = len(xs)
+        a = (C.c_void_p * n)(*[t.data_ptr() for t in xs])
+        b = (C.c_void_p * n)(*[t.data_ptr() for t in ys])
+        check(lib().tps_stage_forward_group(self.handle, mb0, n, a, b))
+
+    def backward_group(self, mb0: int, dys, dxs) -> None:
+        n = len(dys)
+        a = (C.c_void_p * n)(*[t.data_ptr() for t in dys])
+        b = (C.c_void_p * n)(*[t.data_ptr() for t in dxs])
+        check(lib().tps_stage_backward_group(self.handle, mb0, n, a, b))
+
+    def sync(self) -> None:
+        check(lib().tps_stage_sync(self.handle))
+
+    def stats(self) -> dict:
+        s = Stats()
+        check(lib().tps_stage_stats(self.handle, C.byref(s)))
+        return {k: getattr(s, k) for k, _ in Stats._fields_}
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            lib().tps_stage_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# --- op-level calls (torch tensors in, kernels run on `stream`) ----------------
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream):
+    return None if stream is None else stream.cuda_stream
+
+
+def op_gemm(dtype, layout, epi, M, N, K, A, lda, B, ldb, Cm, ldc, bias=None, resid=None, ldr=0,
+            aux=None, ldaux=0, stream=None):
+    check(lib().tps_op_gemm(dtype, layout, epi, M, N, K, _ptr(A), lda, _ptr(B), ldb, _ptr(Cm), ldc,
+                            _ptr(bias), _ptr(resid), ldr, _ptr(aux), ldaux, _stream(stream)))
+
+
+def op_layernorm_fwd(dtype, rows, cols, x, gamma, beta, eps, out, mean=None, rstd=None, stream=None):
+    check(lib().tps_op_layernorm_fwd(dtype, rows, cols, _ptr(x), _ptr(gamma), _ptr(beta), eps, _ptr(out),
+                                     _ptr(mean), _ptr(rstd), _stream(stream)))
+
+
+def op_layernorm_bwd(dtype, rows, cols, dout, x, mean, rstd, gamma, resid, dx, dgamma, dbeta, ws, stream=None):
+    check(lib().tps_op_layernorm_bwd(dtype, rows, cols, _ptr(dout), _ptr(x), _ptr(mean), _ptr(rstd),
+                                     _ptr(gamma), _ptr(resid), _ptr(dx), _ptr(dgamma), _ptr(dbeta), _ptr(ws),
+                                     _stream(stream)))
+
+
+def op_attention_fwd(dtype, b, s, nh, d, qkv, o, lse, stream=None):
+    check(lib().tps_op_attention_fwd(dtype, b, s, nh, d, _ptr(qkv), _ptr(o), _ptr(lse), _stream(stream)))
+
+
+def op_attention_bwd(dtype, b, s, nh, d, qkv, o, lse, do, dqkv, ws, stream=None):
+    check(lib().tps_op_attention_bwd(dtype, b, s, nh, d, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(do), _ptr(dqkv),
+                                     _ptr(ws), _stream(stream)))
+
+
+def op_colsum(dtype, rows, cols, x, ldx, out, ws, stream=None):
+    check(lib().tps_op_colsum(dtype, rows, cols, _ptr(x), ldx, _ptr(out), _ptr(ws), _stream(stream)))
+
+
+def op_gelu(dtype, n, u, g, stream=None):
+    check(lib().tps_op_gelu(dtype, n, _ptr(u), _ptr(g), _stream(stream)))
+
+
+def op_workspace_bytes(kind, rows, cols) -> int:
+    return int(lib().tps_op_workspace_bytes(kind, rows, cols))

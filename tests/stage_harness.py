@@ -1,0 +1,160 @@
+"""Helpers shared by the GPU tests: marshal synthetic inputs to the device,
+run the stage through the C ABI in its planned order, read results back, and
+run the CPU oracle on the same (storage-rounded) inputs."""
+
+from __future__ import annotations
+
+import numpy as np
+
+from paper_2503_03182_amd import synth
+from paper_2503_03182_amd import tpstage as T
+
+
+def torch_dtype(dtype: str):
+    import torch
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+def to_dev(a: np.ndarray, dtype: str):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda").to(torch_dtype(dtype))
+
+
+def to_np(t) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def rel_l2(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
+
+
+def make_params(cfg):
+    """Per-layer packed parameter blocks (device) and zeroed f32 gradient
+    blocks, plus the float64 parameter dicts for the oracle."""
+    import torch
+    po, pb, go, gb = T.param_layout(cfg)
+    es = 2 if cfg.dtype == "bf16" else 4
+    blocks, grads, ora = [], [], []
+    stream_host = cfg.weights == T.W_STREAM
+    for l in range(cfg.n_layers):
+        vals = synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype)
+        blk = torch.zeros(pb, dtype=torch.uint8, device="cuda")
+        for i, name in enumerate(T.PARAMS):
+            v = to_dev(vals[name].reshape(-1), cfg.dtype)
+            n = v.numel()
+            blk[po[i]:po[i] + n * es].view(torch_dtype(cfg.dtype)).copy_(v)
+        if stream_host:
+            hb = torch.empty(pb, dtype=torch.uint8, pin_memory=True)
+            hb.copy_(blk)
+            blk = hb
+            g = torch.zeros(gb, dtype=torch.uint8, pin_memory=True)
+        else:
+            g = torch.zeros(gb, dtype=torch.uint8, device="cuda")
+        blocks.append(blk)
+        grads.append(g)
+        ora.append({k: v.astype(np.float64) for k, v in vals.items()})
+    return blocks, grads, ora
+
+
+def read_grads(cfg, grads):
+    import torch
+    po, pb, go, gb = T.param_layout(cfg)
+    h, f = cfg.hidden, cfg.mlp
+    shapes = synth.param_shapes(h, f)
+    out = []
+    for g in grads:
+        d = {}
+        for i, name in enumerate(T.PARAMS):
+            n = int(np.prod(shapes[name]))
+            d[name] = g[go[i]:go[i] + 4 * n].view(torch.float32).cpu().numpy().astype(np.float64).reshape(shapes[name])
+        out.append(d)
+    return out
+
+
+def inputs(cfg):
+    xs = [synth.stage_input(mb, cfg.tokens, cfg.hidden, cfg.dtype) for mb in range(cfg.n_micro)]
+    dys = [synth.output_grad(mb, cfg.tokens, cfg.hidden, cfg.dtype) for mb in range(cfg.n_micro)]
+    return xs, dys
+
+
+def run_gpu(cfg, xs=None, dys=None, iterations=1, group=False, params=None):
+    """Runs `iterations` iterations of the planned order; returns numpy results
+    of the last one: dict(ys, dxs, grads, stats, plan)."""
+    import torch
+    if xs is None:
+        xs, dys = inputs(cfg)
+    blocks, grads, _ = params if params is not None else make_params(cfg)
+    st = T.Stage(cfg, blocks, grads)
+    X = [to_dev(x, cfg.dtype) for x in xs]
+    DY = [to_dev(d, cfg.dtype) for d in dys]
+    Y = [torch.empty_like(x) for x in X]
+    DX = [torch.empty_like(x) for x in X]
+    torch.cuda.synchronize()
+    for _ in range(iterations):
+        st.begin_iteration(zero_grads=True)
+        order = cfg.order()
+        if group:
+            i = 0
+            while i < len(order):
+                k = order[i][0]
+                j = i
+                while j < len(order) and order[j][0] == k and order[j][1] == order[i][1] + (j - i):
+                    j += 1
+                mbs = [order[t][1] for t in range(i, j)]
+                if k == "F":
+                    st.forward_group(mbs[0], [X[m] for m in mbs], [Y[m] for m in mbs])
+                else:
+                    st.backward_group(mbs[0], [DY[m] for m in mbs], [DX[m] for m in mbs])
+                i = j
+        else:
+            for k, mb in order:
+                if k == "F":
+                    st.forward(mb, X[mb], Y[mb])
+                else:
+                    st.backward(mb, DY[mb], DX[mb])
+        st.sync()
+    out = dict(ys=[to_np(y) for y in Y], dxs=[to_np(d) for d in DX], grads=read_grads(cfg, grads),
+               stats=st.stats(), plan=st.info)
+    st.close()
+    return out
+
+
+def run_oracle(cfg, xs=None, dys=None, ora_params=None):
+    from oracle import decoder_stage as ora
+    if xs is None:
+        xs, dys = inputs(cfg)
+    if ora_params is None:
+        ora_params = [{k: v.astype(np.float64) for k, v in synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype).items()}
+                      for l in range(cfg.n_layers)]
+    return ora.run_stage(ora_params, [x.astype(np.float64) for x in xs], [d.astype(np.float64) for d in dys],
+                         cfg.n_heads, cfg.micro_batch, cfg.seq, cfg.ln_eps)
+
+
+def compare(gpu, ref, tol):
+    """Worst rel-L2 over y, dx of every micro-batch and every parameter grad."""
+    worst = {}
+    for mb in range(len(ref["ys"])):
+        worst[f"y{mb}"] = rel_l2(gpu["ys"][mb], ref["ys"][mb])
+        worst[f"dx{mb}"] = rel_l2(gpu["dxs"][mb], ref["dxs"][mb])
+    for l, g in enumerate(ref["grads"]):
+        for k, v in g.items():
+            worst[f"L{l}.{k}"] = rel_l2(gpu["grads"][l][k], v)
+    bad = {k: v for k, v in worst.items() if not v <= tol}
+    return worst, bad
+
+
+def bit_equal(a, b) -> list:
+    """Names of outputs that differ bitwise between two GPU runs."""
+    diff = []
+    for mb in range(len(a["ys"])):
+        if not np.array_equal(a["ys"][mb], b["ys"][mb]):
+            diff.append(f"y{mb}")
+        if not np.array_equal(a["dxs"][mb], b["dxs"][mb]):
+            diff.append(f"dx{mb}")
+    for l in range(len(a["grads"])):
+        for k in a["grads"][l]:
+            if not np.array_equal(a["grads"][l][k], b["grads"][l][k]):
+                diff.append(f"L{l}.{k}")
+    return diff

@@ -1,0 +1,190 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+symbol the headers declare, and the planner's layout, accounting and error
+conventions match closed forms computed here from the shapes."""
+
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2503_03182_amd import configs as W
+from paper_2503_03182_amd import tpstage as T
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+pytestmark = pytest.mark.skipif(not os.path.exists(T.lib_path()), reason="libtpstage.so not built")
+
+
+def _declared():
+    names = set()
+    for h in ("tpstage.h", "tpstage_ops.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names |= set(re.findall(r"\b(tps_[a-z_0-9]+)\s*\(", src))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = C.CDLL(T.lib_path())
+    declared = _declared()
+    assert len(declared) >= 19
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+    assert declared == set(T.EXPORTED)
+
+
+def _align(x):
+    return (x + 255) // 256 * 256
+
+
+def _tensor_bytes(cfg):
+    es = 2 if cfg.dtype == "bf16" else 4
+    Tk, h, f = cfg.tokens, cfg.hidden, cfg.mlp
+    b = {n: Tk * h * es for n in ("x", "a", "o", "x1", "c")}
+    b.update(qkv=Tk * 3 * h * es, u=Tk * f * es, g=Tk * f * es,
+             lse=cfg.micro_batch * cfg.n_heads * cfg.seq * 4, ln1=2 * Tk * 4, ln2=2 * Tk * 4)
+    return b
+
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_plan_accounting_closed_forms(name):
+    cfg = W.WORKLOADS[name]()
+    p = T.plan(cfg)
+    tb = _tensor_bytes(cfg)
+    L, M = cfg.n_layers, cfg.n_micro
+    pol = cfg.policy or [{t: T.KEEP for t in T.TENSORS} for _ in range(L)]
+    keep = sum(_align(tb[t]) for l in range(L) for t in T.TENSORS if pol[l][t] == T.KEEP)
+    off = sum(_align(tb[t]) for l in range(L) for t in T.TENSORS if pol[l][t] == T.OFFLOAD)
+    assert p["slot_bytes"] == keep
+    assert p["offload_slot_bytes"] == off
+    # all forwards first (W = M): every micro-batch is in flight at the peak
+    assert p["max_inflight"] == M
+    if keep:
+        assert p["n_slots"] == M
+    assert p["keep_all_bytes"] == M * L * sum(_align(v) for v in tb.values())
+    Tk, h, f, s, b = cfg.tokens, cfg.hidden, cfg.mlp, cfg.seq, cfg.micro_batch
+    unit = 2 * Tk * (4 * h * h + 2 * h * f) + 2 * b * h * s * (s + 1)
+    assert p["fwd_flops"] == pytest.approx(unit * L * M, rel=1e-12)
+    assert p["bwd_flops"] == pytest.approx(2 * unit * L * M, rel=1e-12)
+    n_off = bin(p["offload_mb_mask"]).count("1")
+    assert p["n_offload_mbs"] == n_off
+    if cfg.weights == T.W_RESIDENT:
+        assert p["h2d_bytes"] == n_off * off
+        assert p["predicted_peak_bytes"] == p["device_arena_bytes"] + L * (p["param_bytes"] + p["grad_bytes"])
+
+
+def test_replay_programs_and_recompute_flops():
+    # selective: attention and GeLU outputs -> replay attention and GeLU only
+    cfg = W.stage4_h2048()
+    p = T.plan(cfg)
+    Tk, h, s, b = cfg.tokens, cfg.hidden, cfg.seq, cfg.micro_batch
+    attn = 2 * b * h * s * (s + 1)
+    assert p["recompute_flops"] == pytest.approx(attn * cfg.n_layers * cfg.n_micro)
+    assert p["n_replay_layers"] == cfg.n_layers
+    # layer inputs kept: every operator but FC2 is replayed (its output, the
+    # next layer's input, is kept)
+    cfg = W.stage4_seq8192_recompute()
+    p = T.plan(cfg)
+    Tk, h, f, s, b = cfg.tokens, cfg.hidden, cfg.mlp, cfg.seq, cfg.micro_batch
+    per = 2 * Tk * (4 * h * h + h * f) + 2 * b * h * s * (s + 1)
+    assert p["recompute_flops"] == pytest.approx(per * cfg.n_layers * cfg.n_micro)
+    # only the stage input kept: the top layers also replay FC2 of the layer
+    # below to regenerate their inputs
+    cfg = W.tiny("recompute")
+    p = T.plan(cfg)
+    Tk, h, f, s, b = cfg.tokens, cfg.hidden, cfg.mlp, cfg.seq, cfg.micro_batch
+    full = 2 * Tk * (4 * h * h + 2 * h * f) + 2 * b * h * s * (s + 1)
+    # layer 1 needs its input: layer 0 replays fully (with FC2); layer 1 replays all but FC2
+    assert p["recompute_flops"] == pytest.approx((full + full - 2 * Tk * f * h) * cfg.n_micro)
+
+
+def test_slots_follow_the_order():
+    cfg = W.tiny("keep")
+    cfg.inflight = 2
+    p = T.plan(cfg)
+    assert p["max_inflight"] == 2 and p["n_slots"] == 2
+    assert p["device_arena_bytes"] < T.plan(W.tiny("keep"))["device_arena_bytes"]
+
+
+def test_offload_slots_and_auto_victims():
+    cfg = W.tiny("offload")
+    p = T.plan(cfg)
+    assert p["n_offload_mbs"] == cfg.n_micro
+    # every micro-batch offloaded: device staging for F plus the prefetched one
+    assert p["n_offload_slots"] <= 2
+    assert p["host_arena_bytes"] == p["n_host_slots"] * p["offload_slot_bytes"]
+    # victims chosen by slack are a pure function of the config
+    big = W.stage5_h5120_offload()
+    a, b2 = T.plan(big), T.plan(big)
+    assert a["offload_mb_mask"] == b2["offload_mb_mask"] != 0
+    # a link 1000x faster hides every micro-batch
+    big.link_gbps_hint = 50000.0
+    assert T.plan(big)["n_offload_mbs"] == big.n_micro
+    # a tiny link hides none
+    big.link_gbps_hint = 0.01
+    assert T.plan(big)["n_offload_mbs"] == 0
+
+
+def _expect(cfg, code, pattern):
+    with pytest.raises(T.TpsError) as e:
+        T.plan(cfg)
+    assert e.value.code == code
+    assert re.search(pattern, str(e.value)), str(e.value)
+
+
+def test_config_errors():
+    cfg = W.tiny()
+    cfg.n_heads = 8      # head dim 32
+    _expect(cfg, T.TPS_EINVAL, "head dim")
+    cfg = W.tiny()
+    cfg.hidden, cfg.n_heads = 260, 2
+    _expect(cfg, T.TPS_EINVAL, "head dim|multiple")
+    cfg = W.tiny("recompute")
+    cfg.policy[0]["x"] = T.RECOMPUTE
+    _expect(cfg, T.TPS_EINVAL, "stage input")
+    cfg = W.tiny("recompute")
+    cfg.granularity = T.GRAN_LAYER
+    _expect(cfg, T.TPS_EINVAL, "layer granularity")
+    cfg = W.tiny()
+    cfg.ops = [("F", 0), ("F", 0), ("B", 1), ("B", 2), ("F", 3), ("B", 3), ("F", 1), ("B", 0)]
+    _expect(cfg, T.TPS_EINVAL, "twice")
+    cfg = W.tiny()
+    cfg.ops = [("B", 0), ("F", 0), ("F", 1), ("B", 1), ("F", 2), ("B", 2), ("F", 3), ("B", 3)]
+    _expect(cfg, T.TPS_EINVAL, "follow")
+    cfg = W.tiny("offload")
+    cfg.offload_mb_mask = 1 << 5
+    _expect(cfg, T.TPS_EINVAL, "beyond n_micro")
+    cfg = W.tiny()
+    cfg.n_micro = 65
+    _expect(cfg, T.TPS_EINVAL, "n_micro")
+    c = W.tiny().to_c()
+    c.abi_version = 99
+    info = T.PlanInfo()
+    assert T.lib().tps_plan(C.byref(c), C.byref(info)) == T.TPS_EINVAL
+    assert b"abi_version" in T.lib().tps_last_error()
+
+
+def test_op_argument_errors_without_gpu():
+    # argument checks run before any launch, so they work without a device
+    with pytest.raises(T.TpsError) as e:
+        T.op_gemm(T.TPS_BF16, T.GEMM_NT, T.EPI_STORE, 64, 64, 60, None, 60, None, 60, None, 64)
+    assert e.value.code == T.TPS_EINVAL
+    with pytest.raises(T.TpsError):
+        T.op_attention_fwd(T.TPS_BF16, 1, 16, 2, 96, None, None, None)
+    with pytest.raises(T.TpsError):
+        T.op_layernorm_fwd(T.TPS_F32, 4, 20000, None, None, None, 1e-5, None)
+    assert T.op_workspace_bytes(T.WS_COLSUM, 100, 64) == 4 * 64 * 4
+    assert T.op_workspace_bytes(T.WS_ATTN_BWD, 256, 4) == 256 * 4 * 4
+
+
+def test_param_layout_offsets():
+    cfg = W.tiny()
+    po, pb, go, gb = T.param_layout(cfg)
+    h, f = cfg.hidden, cfg.mlp
+    sizes = [3 * h * h, 3 * h, h * h, h, f * h, f, h * f, h, h, h, h, h]
+    off = 0
+    for i, n in enumerate(sizes):
+        assert po[i] == off and po[i] % 256 == 0
+        off = _align(off + 4 * n)
+    assert pb == off
+    assert gb == pb   # f32 storage: same layout as the gradients
