@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Stage throughput on one MI355X.
+
+One step = one training iteration of the pipeline stage: F(mb) and B(mb) of
+every micro-batch in the planned order (forward, the policy's recompute and
+backward, with f32 gradient accumulation), all through the C ABI.  Inputs,
+parameters and output gradients are resident in HBM before the timed region.
+
+Prints one JSON line: stage TFLOP/s over the algorithmic flops the policy
+requires, % of the dense bf16 MFMA peak, peak HBM, the dominant kernel's
+roofline from HIP events around its launches inside the timed region, and the
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "stage TFLOP/s (fwd+recompute+bwd, % bf16 MFMA peak); peak HBM GB"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def build_stage(cfg):
+    import torch
+    from paper_2503_03182_amd import synth
+    from paper_2503_03182_amd import tpstage as T
+    po, pb, go, gb = T.param_layout(cfg)
+    td = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    es = 2 if cfg.dtype == "bf16" else 4
+    blocks, grads = [], []
+    for l in range(cfg.n_layers):
+        vals = synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype)
+        blk = torch.zeros(pb, dtype=torch.uint8, device="cuda")
+        for i, name in enumerate(T.PARAMS):
+            v = torch.from_numpy(vals[name].reshape(-1)).to("cuda").to(td)
+            blk[po[i]:po[i] + v.numel() * es].view(td).copy_(v)
+        if cfg.weights == T.W_STREAM:
+            hb = torch.empty(pb, dtype=torch.uint8, pin_memory=True)
+            hb.copy_(blk)
+            blk = hb
+            g = torch.zeros(gb, dtype=torch.uint8, pin_memory=True)
+        else:
+            g = torch.zeros(gb, dtype=torch.uint8, device="cuda")
+        blocks.append(blk)
+        grads.append(g)
+    xs, dys = [], []
+    for mb in range(cfg.n_micro):
+        xs.append(torch.from_numpy(synth.stage_input(mb, cfg.tokens, cfg.hidden, cfg.dtype)).to("cuda").to(td))
+        dys.append(torch.from_numpy(synth.output_grad(mb, cfg.tokens, cfg.hidden, cfg.dtype)).to("cuda").to(td))
+    ys = [torch.empty_like(x) for x in xs]
+    dxs = [torch.empty_like(x) for x in xs]
+    return blocks, grads, xs, dys, ys, dxs
+
+
+def cpu_baseline(cfg, unit_flops, budget_s):
+    """The oracle as it stands, on one (layer, micro-batch) unit of the
+    workload (forward, the policy's recompute, backward), repeated while the
+    budget lasts."""
+    import numpy as np
+    from oracle import decoder_stage as ora
+    from paper_2503_03182_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    params = [{k: v.astype(np.float64) for k, v in synth.layer_params(0, cfg.hidden, cfg.mlp, cfg.dtype).items()}]
+    x = [synth.stage_input(0, cfg.tokens, cfg.hidden, cfg.dtype).astype(np.float64)]
+    dy = [synth.output_grad(0, cfg.tokens, cfg.hidden, cfg.dtype).astype(np.float64)]
+    policy = None if cfg.policy is None else [cfg.policy[0]]
+    if policy is not None:
+        policy = [{k: (v if v != 2 else 0) for k, v in policy[0].items()}]   # offload is a copy on the CPU
+    times = []
+    t_end = time.perf_counter() + budget_s
+    while len(times) < 3 and (not times or time.perf_counter() < t_end):
+        t0 = time.perf_counter()
+        ora.run_stage(params, x, dy, cfg.n_heads, cfg.micro_batch, cfg.seq, cfg.ln_eps, policy=policy)
+        times.append(time.perf_counter() - t0)
+    med = statistics.median(times)
+    return {"value": round(unit_flops / med / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"one layer x one micro-batch unit of the workload (forward, the policy's recompute, "
+                      f"backward) in float64 numpy, median of {len(times)} run(s), {med:.2f} s each; "
+                      f"TFLOP/s over the same algorithmic flop count as the GPU number"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="stage4_h2048")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's share of the stage; --gpus {args.gpus} is not supported "
+              f"(multi-GPU runs are outside this build)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2503_03182_amd import configs
+    from paper_2503_03182_amd import tpstage as T
+
+    cfg = configs.WORKLOADS[args.workload]()
+    info = T.plan(cfg)
+    free0, total = torch.cuda.mem_get_info()
+    torch.cuda.reset_peak_memory_stats()
+    log(f"[bench] workload {args.workload}: building parameters and inputs")
+    blocks, grads, xs, dys, ys, dxs = build_stage(cfg)
+    stage = T.Stage(cfg, blocks, grads)
+    order = cfg.order()
+    step_flops = info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]
+
+    def step():
+        stage.begin_iteration(zero_grads=True)
+        for k, mb in order:
+            if k == "F":
+                stage.forward(mb, xs[mb], ys[mb])
+            else:
+                stage.backward(mb, dys[mb], dxs[mb])
+
+    for _ in range(args.warmup):
+        step()
+    stage.sync()
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+
+    # one instrumented step: per-kernel breakdown, picks the dominant kernel
+    stage.time_kernels("")
+    step()
+    stage.sync()
+    breakdown = sorted(stage.kernel_times(), key=lambda r: -r["ms"])
+    singles = [r for r in breakdown if r["name"].startswith("tps::")]
+    dominant = singles[0]["name"]
+    log(f"[bench] dominant kernel {dominant}")
+
+    # timed region: only the dominant kernel is bracketed with events
+    stage.time_kernels(dominant)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    stage.sync()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    dom = [r for r in stage.kernel_times() if r["name"] == dominant][0]
+    stage.time_kernels(None)
+    free1, _ = torch.cuda.mem_get_info()
+    log(f"[bench] timed {args.steps} steps in {t1 - t0:.3f} s")
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    value = step_flops * args.steps / (t1 - t0) / 1e12
+    achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+    step_ms_breakdown = sum(r["ms"] for r in breakdown)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic: seeded N(0,0.02) weights, N(0,1) stage inputs and output gradients",
+        "config": {
+            "workload": args.workload,
+            "layers": cfg.n_layers, "hidden": cfg.hidden, "heads": cfg.n_heads, "mlp": cfg.mlp,
+            "seq": cfg.seq, "micro_batch": cfg.micro_batch, "micro_batches": cfg.n_micro,
+            "policy": configs.WORKLOADS[args.workload].__doc__.split(";")[-1].strip().rstrip("."),
+            "order": "all forwards, then all backwards (in-flight = micro-batches)",
+            "parallelism": "one GPU",
+        },
+        "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "flops_per_step": step_flops,
+        "mfu_pct": round(100.0 * 3 * info["fwd_flops"] * args.steps / (t1 - t0) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "peak_hbm_gb": {
+            "planned": round(info["predicted_peak_bytes"] / 1e9, 3),
+            "torch_max_allocated": round(torch.cuda.max_memory_allocated() / 1e9, 3),
+            "device_used_delta": round((free0 - min(free0, free1)) / 1e9, 3),
+            "keep_all_activations": round(info["keep_all_bytes"] / 1e9, 3),
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": dominant,
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+            "launches": dom["launches"],
+            "avg_launch_us": round(dom["ms"] * 1e3 / max(dom["launches"], 1), 2),
+        },
+        "kernels_per_step": [
+            {"name": r["name"], "launches": r["launches"], "ms": round(r["ms"], 3),
+             "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 1) if r["flops"] else None,
+             "gbs": round(r["bytes"] / (r["ms"] * 1e-3) / 1e9, 1) if not r["flops"] else None}
+            for r in breakdown[:12]
+        ],
+        "instrumented_step_ms": round(step_ms_breakdown, 3),
+    }
+    stage.close()
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle sample")
+        unit = (info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]) / (cfg.n_layers * cfg.n_micro)
+        out["cpu_baseline"] = cpu_baseline(cfg, unit, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

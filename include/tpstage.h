@@ -187,6 +187,15 @@ typedef struct tps_stats {
   int32_t ops_done;             /* position in the planned order                */
 } tps_stats;
 
+typedef struct tps_kernel_time {
+  char name[120];               /* kernel (or fixed kernel sequence) name       */
+  uint64_t launches;
+  double ms;                    /* summed durations between HIP events recorded
+                                   on the compute stream around each launch     */
+  double flops;                 /* summed algorithmic flops                     */
+  double bytes;                 /* summed algorithmic HBM bytes                 */
+} tps_kernel_time;
+
 typedef struct tps_stage tps_stage;
 
 /* Layout of one layer's packed parameter block (storage dtype) and gradient
@@ -233,6 +242,19 @@ int tps_stage_backward_group(tps_stage* st, int mb0, int n, const void* const* d
 int tps_stage_sync(tps_stage* st);
 
 int tps_stage_stats(const tps_stage* st, tps_stats* out);
+
+/* Measurement: from now on bracket every launch whose kernel name starts
+ * with `prefix` with HIP timing events on the compute stream ("" times every
+ * kernel, NULL turns timing off), and clear the accumulated times.  Single-
+ * kernel launches carry the demangled kernel name a profiler prints; fixed
+ * multi-kernel sequences (attention backward, LayerNorm backward, column
+ * sums) carry one name for the sequence. */
+int tps_stage_time_kernels(tps_stage* st, const char* prefix);
+
+/* Waits for the compute stream, then reports per-name totals accumulated
+ * since the last tps_stage_time_kernels(); writes at most `max` entries and
+ * the number of names to *n_out. */
+int tps_stage_kernel_times(tps_stage* st, tps_kernel_time* out, int max, int* n_out);
 
 /* Releases events and host metadata (caller buffers are untouched). */
 int tps_stage_destroy(tps_stage* st);

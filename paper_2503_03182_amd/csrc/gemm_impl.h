@@ -245,13 +245,11 @@ static hipError_t launch_tile(GemmArgs g, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// Tile choice depends on the shape only (never on timing) and changes no
-// result bit: every tile shape sums K in the same order.
 template <int LAYOUT>
 static hipError_t launch_layout(int dtype, GemmArgs g, hipStream_t stream) {
+  const GemmTile t = gemm_select_tile(dtype, g.M, g.N);
   if (dtype == TPS_BF16) {
-    const int64_t t256 = (int64_t)((g.M + 255) / 256) * ((g.N + 127) / 128);
-    if (t256 >= 256) return launch_tile<bf16, 256, 128, 64, LAYOUT>(g, stream);
+    if (t.bm == 256) return launch_tile<bf16, 256, 128, 64, LAYOUT>(g, stream);
     return launch_tile<bf16, 128, 128, 64, LAYOUT>(g, stream);
   }
   return launch_tile<float, 128, 128, 32, LAYOUT>(g, stream);

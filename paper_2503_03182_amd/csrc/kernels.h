@@ -19,6 +19,16 @@ struct GemmArgs {
   int tiles_m, tiles_n;
 };
 
+// Tile shape of a GEMM launch.  Depends on the shape only (never on timing)
+// and changes no result bit: every tile shape sums K in the same order.
+struct GemmTile {
+  int bm, bn, bk;
+};
+GemmTile gemm_select_tile(int dtype, int M, int N);
+// Demangled name of the kernel instantiation a launch uses (as profilers
+// print it), e.g. "tps::gemm_kernel<__bf16, 256, 128, 64, 0>".
+const char* gemm_kernel_name(int dtype, int layout, int M, int N);
+
 hipError_t gemm_launch_nt(int dtype, GemmArgs g, hipStream_t stream);
 hipError_t gemm_launch_nn(int dtype, GemmArgs g, hipStream_t stream);
 hipError_t gemm_launch_tn(int dtype, GemmArgs g, hipStream_t stream);

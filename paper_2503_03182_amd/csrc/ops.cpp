@@ -126,6 +126,29 @@ extern "C" uint64_t tps_op_workspace_bytes(int kind, int64_t rows, int64_t cols)
 
 namespace tps {
 
+GemmTile gemm_select_tile(int dtype, int M, int N) {
+  if (dtype == TPS_BF16) {
+    const int64_t t256 = (int64_t)((M + 255) / 256) * ((N + 127) / 128);
+    if (t256 >= 256) return {256, 128, 64};
+    return {128, 128, 64};
+  }
+  return {128, 128, 32};
+}
+
+const char* gemm_kernel_name(int dtype, int layout, int M, int N) {
+  static const char* names[2][2][3] = {
+      {{"tps::gemm_kernel<float, 128, 128, 32, 0>", "tps::gemm_kernel<float, 128, 128, 32, 1>",
+        "tps::gemm_kernel<float, 128, 128, 32, 2>"},
+       {"tps::gemm_kernel<float, 128, 128, 32, 0>", "tps::gemm_kernel<float, 128, 128, 32, 1>",
+        "tps::gemm_kernel<float, 128, 128, 32, 2>"}},
+      {{"tps::gemm_kernel<__bf16, 128, 128, 64, 0>", "tps::gemm_kernel<__bf16, 128, 128, 64, 1>",
+        "tps::gemm_kernel<__bf16, 128, 128, 64, 2>"},
+       {"tps::gemm_kernel<__bf16, 256, 128, 64, 0>", "tps::gemm_kernel<__bf16, 256, 128, 64, 1>",
+        "tps::gemm_kernel<__bf16, 256, 128, 64, 2>"}}};
+  const GemmTile t = gemm_select_tile(dtype, M, N);
+  return names[dtype == TPS_BF16][t.bm == 256][layout];
+}
+
 hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, const void* A, int64_t lda,
                        const void* B, int64_t ldb, void* C, int64_t ldc, const void* bias, const void* resid,
                        int64_t ldr, void* aux, int64_t ldaux, hipStream_t stream) {

@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstring>
+#include <map>
 #include <string>
 #include <vector>
 
@@ -75,6 +76,21 @@ struct tps_stage {
   std::vector<char> grads_touched;  // [L] this iteration
   uint64_t tick = 0;
 
+  // kernel timing (measurement only)
+  struct TimedLaunch {
+    std::string name;
+    double flops, bytes;
+    hipEvent_t a, b;
+  };
+  bool timing = false;
+  std::string tprefix;
+  std::vector<TimedLaunch> tpending;
+  std::vector<hipEvent_t> tpool;
+  std::map<std::string, tps_kernel_time> tagg;
+  int kbegin(const char* name, double flops, double bytes);
+  int kend(int idx);
+  int kresolve();
+
   int cursor = 0;
   std::vector<char> f_done, b_done;
   bool in_iteration = false;
@@ -120,9 +136,17 @@ struct tps_stage {
            void* C, int64_t ldc, const void* bias = nullptr, const void* resid = nullptr, int64_t ldr = 0,
            void* aux = nullptr, int64_t ldaux = 0) {
     ++stats.kernels;
-    return check_hip(gemm_launch(p.dtype, layout, epi, M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux,
-                                 ldaux, cs),
-                     "gemm");
+    const double es = p.esize;
+    const double bytes = ((double)M * K + (double)N * K) * es +
+                         (epi == TPS_EPI_ACC_F32 ? 8.0 * M * N : (double)M * N * es);
+    const int t = kbegin(gemm_kernel_name(p.dtype, layout, M, N), 2.0 * M * N * K, bytes);
+    const int rc = check_hip(gemm_launch(p.dtype, layout, epi, M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr,
+                                         aux, ldaux, cs),
+                             "gemm");
+    return rc ? rc : kend(t);
+  }
+  const char* tname(const char* bf16_name, const char* f32_name) const {
+    return p.dtype == TPS_BF16 ? bf16_name : f32_name;
   }
   int fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots);
   int bwd_layer(int l, int mb, const char* W, float* G, const void* dy, void* dx);
@@ -224,6 +248,53 @@ int tps_stage::ensure_layer(int l, bool for_backward, int* entry) {
 }
 
 // ---------------------------------------------------------------------------
+// Kernel timing: events recorded on the compute stream around selected
+// launches, resolved when the totals are read.
+// ---------------------------------------------------------------------------
+int tps_stage::kbegin(const char* name, double flops, double bytes) {
+  if (!timing || strncmp(name, tprefix.c_str(), tprefix.size()) != 0) return -1;
+  hipEvent_t ev[2];
+  for (int i = 0; i < 2; ++i) {
+    if (!tpool.empty()) {
+      ev[i] = tpool.back();
+      tpool.pop_back();
+    } else {
+      TPS_HIP(hipEventCreate(&ev[i]));
+    }
+  }
+  TPS_HIP(hipEventRecord(ev[0], cs));
+  tpending.push_back({name, flops, bytes, ev[0], ev[1]});
+  return (int)tpending.size() - 1;
+}
+
+int tps_stage::kend(int idx) {
+  if (idx < 0) return TPS_OK;
+  TPS_HIP(hipEventRecord(tpending[idx].b, cs));
+  return TPS_OK;
+}
+
+int tps_stage::kresolve() {
+  for (auto& r : tpending) {
+    TPS_HIP(hipEventSynchronize(r.b));
+    float ms = 0.f;
+    TPS_HIP(hipEventElapsedTime(&ms, r.a, r.b));
+    tps_kernel_time& a = tagg[r.name];
+    if (a.launches == 0) {
+      memset(&a, 0, sizeof(a));
+      strncpy(a.name, r.name.c_str(), sizeof(a.name) - 1);
+    }
+    a.launches += 1;
+    a.ms += ms;
+    a.flops += r.flops;
+    a.bytes += r.bytes;
+    tpool.push_back(r.a);
+    tpool.push_back(r.b);
+  }
+  tpending.clear();
+  return TPS_OK;
+}
+
+// ---------------------------------------------------------------------------
 // One layer forward (or a replay of part of it).
 // ---------------------------------------------------------------------------
 int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots) {
@@ -243,30 +314,41 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
   float* ln1 = static_cast<float*>(ptr(TPS_T_LN1));
   float* ln2 = static_cast<float*>(ptr(TPS_T_LN2));
 
+  const double es = p.esize;
+  const char* ln_name = tname("tps::ln_fwd_kernel<__bf16>", "tps::ln_fwd_kernel<float>");
   if (ops & (1u << OP_LN1)) {
     ++stats.kernels;
+    const int k = kbegin(ln_name, 0.0, 2.0 * T * h * es);
     TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, x, par(TPS_P_G1), par(TPS_P_BE1), p.eps, a,
                                  opt(TPS_T_LN1) ? ln1 : nullptr, opt(TPS_T_LN1) ? ln1 + T : nullptr, cs));
+    TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_QKV))
     TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS, T, 3 * h, h, a, h, par(TPS_P_W_QKV), h, qkv, 3 * h, par(TPS_P_B_QKV)));
   if (ops & (1u << OP_ATTN)) {
     ++stats.kernels;
+    const int k = kbegin(tname("tps::attn_fwd_kernel<__bf16>", "tps::attn_fwd_kernel<float>"),
+                         2.0 * p.b * h * (double)p.s * (p.s + 1), 4.0 * T * h * es);
     TPS_HIP(attention_fwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, opt(TPS_T_LSE) ? lse : nullptr, cs));
+    TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_OPROJ))
     TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_RESID, T, h, h, o, h, par(TPS_P_W_O), h, x1, h, par(TPS_P_B_O), x, h));
   if (ops & (1u << OP_LN2)) {
     ++stats.kernels;
+    const int k = kbegin(ln_name, 0.0, 2.0 * T * h * es);
     TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, x1, par(TPS_P_G2), par(TPS_P_BE2), p.eps, c,
                                  opt(TPS_T_LN2) ? ln2 : nullptr, opt(TPS_T_LN2) ? ln2 + T : nullptr, cs));
+    TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_FC1))
     TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_GELU, T, f, h, c, h, par(TPS_P_W_1), h, g, f, par(TPS_P_B_1), nullptr, 0,
                  opt(TPS_T_U) ? u : nullptr, f));
   if (ops & (1u << OP_GELU)) {
     ++stats.kernels;
+    const int k = kbegin(tname("tps::gelu_kernel<__bf16>", "tps::gelu_kernel<float>"), 0.0, 2.0 * T * f * es);
     TPS_HIP(gelu_launch(p.dtype, (int64_t)T * f, u, g, cs));
+    TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_FC2))
     TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_RESID, T, h, f, g, f, par(TPS_P_W_2), f, y, h, par(TPS_P_B_2), x1, h));
@@ -293,32 +375,43 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, float* G, const void* dy,
   float* dvec = reinterpret_cast<float*>(work(p.work.dvec));
   float* ws = reinterpret_cast<float*>(work(p.work.ws));
 
+  const double es = p.esize;
+  const char* cs_name = "column sums (2 kernels)";
+  const char* lnb_name = "layernorm backward (3 kernels)";
+  auto colsum = [&](const void* src, int cols, float* out) -> int {
+    ++stats.kernels;
+    const int k = kbegin(cs_name, 0.0, (double)T * cols * es);
+    TPS_HIP(colsum_launch(p.dtype, T, cols, src, cols, out, ws, cs));
+    return kend(k);
+  };
+  auto lnbwd = [&](const void* dout, const void* xin, const float* st, int gi, int bi, const void* res, void* dst) -> int {
+    ++stats.kernels;
+    const int k = kbegin(lnb_name, 0.0, 5.0 * T * h * es);
+    TPS_HIP(layernorm_bwd_launch(p.dtype, T, h, dout, xin, st, st + T, par(gi), res, dst, grd(gi), grd(bi), ws, cs));
+    return kend(k);
+  };
   // MLP: y = x1 + GeLU(c W1^T + b1) W2^T + b2
   TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_GELU_GRAD, T, f, h, dy, h, par(TPS_P_W_2), f, du, f, nullptr, nullptr, 0, u, f));
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f));
-  ++stats.kernels;
-  TPS_HIP(colsum_launch(p.dtype, T, h, dy, h, grd(TPS_P_B_2), ws, cs));
+  TPS_TRY(colsum(dy, h, grd(TPS_P_B_2)));
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h));
-  ++stats.kernels;
-  TPS_HIP(colsum_launch(p.dtype, T, f, du, f, grd(TPS_P_B_1), ws, cs));
+  TPS_TRY(colsum(du, f, grd(TPS_P_B_1)));
   TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, f, du, f, par(TPS_P_W_1), h, t1, h));
-  ++stats.kernels;
-  TPS_HIP(layernorm_bwd_launch(p.dtype, T, h, t1, x1, ln2, ln2 + T, par(TPS_P_G2), dy, dx1, grd(TPS_P_G2),
-                               grd(TPS_P_BE2), ws, cs));
+  TPS_TRY(lnbwd(t1, x1, ln2, TPS_P_G2, TPS_P_BE2, dy, dx1));
   // attention block: x1 = x + o Wo^T + bo
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h));
-  ++stats.kernels;
-  TPS_HIP(colsum_launch(p.dtype, T, h, dx1, h, grd(TPS_P_B_O), ws, cs));
+  TPS_TRY(colsum(dx1, h, grd(TPS_P_B_O)));
   TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, h, dx1, h, par(TPS_P_W_O), h, t1, h));
-  ++stats.kernels;
-  TPS_HIP(attention_bwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, lse, t1, dqkv, dvec, cs));
+  {
+    ++stats.kernels;
+    const int k = kbegin("attention backward (3 kernels)", 4.0 * p.b * h * (double)p.s * (p.s + 1), 9.0 * T * h * es);
+    TPS_HIP(attention_bwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, lse, t1, dqkv, dvec, cs));
+    TPS_TRY(kend(k));
+  }
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h));
-  ++stats.kernels;
-  TPS_HIP(colsum_launch(p.dtype, T, 3 * h, dqkv, 3 * h, grd(TPS_P_B_QKV), ws, cs));
+  TPS_TRY(colsum(dqkv, 3 * h, grd(TPS_P_B_QKV)));
   TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, 3 * h, dqkv, 3 * h, par(TPS_P_W_QKV), h, t1, h));
-  ++stats.kernels;
-  TPS_HIP(layernorm_bwd_launch(p.dtype, T, h, t1, x, ln1, ln1 + T, par(TPS_P_G1), dx1, dx, grd(TPS_P_G1),
-                               grd(TPS_P_BE1), ws, cs));
+  TPS_TRY(lnbwd(t1, x, ln1, TPS_P_G1, TPS_P_BE1, dx1, dx));
   return TPS_OK;
 }
 
@@ -710,6 +803,31 @@ extern "C" int tps_stage_stats(const tps_stage* st, tps_stats* out) {
   return TPS_OK;
 }
 
+extern "C" int tps_stage_time_kernels(tps_stage* st, const char* prefix) {
+  clear_error();
+  if (!st) return set_error(TPS_EINVAL, "null stage");
+  TPS_HIP(hipStreamSynchronize(st->cs));
+  TPS_TRY(st->kresolve());
+  st->tagg.clear();
+  st->timing = prefix != nullptr;
+  st->tprefix = prefix ? prefix : "";
+  return TPS_OK;
+}
+
+extern "C" int tps_stage_kernel_times(tps_stage* st, tps_kernel_time* out, int max, int* n_out) {
+  clear_error();
+  if (!st || (!out && max > 0)) return set_error(TPS_EINVAL, "null argument");
+  TPS_HIP(hipStreamSynchronize(st->cs));
+  TPS_TRY(st->kresolve());
+  int n = 0;
+  for (auto& kv : st->tagg) {
+    if (n < max) out[n] = kv.second;
+    ++n;
+  }
+  if (n_out) *n_out = n;
+  return TPS_OK;
+}
+
 extern "C" int tps_stage_destroy(tps_stage* st) {
   clear_error();
   if (!st) return TPS_OK;
@@ -721,6 +839,11 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
   for (auto& v : st->ready_ev)
     for (auto e : v)
       if (e) (void)hipEventDestroy(e);
+  for (auto& r : st->tpending) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (auto e : st->tpool) (void)hipEventDestroy(e);
   for (auto& w : st->win) {
     if (w.param_ready.ev) (void)hipEventDestroy(w.param_ready.ev);
     if (w.last_use.ev) (void)hipEventDestroy(w.last_use.ev);

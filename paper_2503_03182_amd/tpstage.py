@@ -82,6 +82,11 @@ class Memory(C.Structure):
                 ("compute_stream", C.c_void_p), ("copy_stream", C.c_void_p)]
 
 
+class KernelTime(C.Structure):
+    _fields_ = [("name", C.c_char * 120), ("launches", C.c_uint64), ("ms", C.c_double),
+                ("flops", C.c_double), ("bytes", C.c_double)]
+
+
 class Stats(C.Structure):
     _fields_ = [("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("kernels", C.c_uint64),
                 ("replays", C.c_uint64), ("ops_done", C.c_int32)]
@@ -96,7 +101,7 @@ EXPORTED = (
     "tps_stage_backward_group", "tps_stage_sync", "tps_stage_stats", "tps_stage_destroy",
     "tps_last_error", "tps_op_gemm", "tps_op_layernorm_fwd", "tps_op_layernorm_bwd",
     "tps_op_attention_fwd", "tps_op_attention_bwd", "tps_op_colsum", "tps_op_gelu",
-    "tps_op_workspace_bytes",
+    "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
 )
 
 
@@ -125,6 +130,8 @@ def lib() -> C.CDLL:
         L.tps_stage_sync.argtypes = [vp]
         L.tps_stage_stats.argtypes = [vp, C.POINTER(Stats)]
         L.tps_stage_destroy.argtypes = [vp]
+        L.tps_stage_time_kernels.argtypes = [vp, C.c_char_p]
+        L.tps_stage_kernel_times.argtypes = [vp, C.POINTER(KernelTime), i32, C.POINTER(C.c_int)]
         L.tps_op_gemm.argtypes = [i32, i32, i32, i32, i32, i32, vp, i64, vp, i64, vp, i64, vp, vp, i64, vp, i64, vp]
         L.tps_op_layernorm_fwd.argtypes = [i32, i32, i32, vp, vp, vp, C.c_float, vp, vp, vp, vp]
         L.tps_op_layernorm_bwd.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -297,6 +304,19 @@ class Stage:
         s = Stats()
         check(lib().tps_stage_stats(self.handle, C.byref(s)))
         return {k: getattr(s, k) for k, _ in Stats._fields_}
+
+    def time_kernels(self, prefix: Optional[str]) -> None:
+        """Bracket launches whose kernel name starts with prefix with HIP
+        events ("" = all, None = off); clears accumulated times."""
+        check(lib().tps_stage_time_kernels(self.handle, None if prefix is None else prefix.encode()))
+
+    def kernel_times(self) -> list:
+        n = C.c_int()
+        check(lib().tps_stage_kernel_times(self.handle, None, 0, C.byref(n)))
+        arr = (KernelTime * max(n.value, 1))()
+        check(lib().tps_stage_kernel_times(self.handle, arr, n.value, C.byref(n)))
+        return [dict(name=a.name.decode(), launches=a.launches, ms=a.ms, flops=a.flops, bytes=a.bytes)
+                for a in arr[:n.value]]
 
     def close(self) -> None:
         if getattr(self, "handle", None):
