@@ -16,6 +16,7 @@
 // results depend only on (M, N, K) and the data.
 #pragma once
 #include <type_traits>
+#include "gemm_v2.h"
 #include "kernels.h"
 #include "tps_device.h"
 
@@ -247,7 +248,11 @@ static hipError_t launch_tile(GemmArgs g, hipStream_t stream) {
 
 template <int LAYOUT>
 static hipError_t launch_layout(int dtype, GemmArgs g, hipStream_t stream) {
-  const GemmTile t = gemm_select_tile(dtype, g.M, g.N);
+  const GemmTile t = gemm_select_tile(dtype, LAYOUT, g);
+  if (t.v2) {
+    if (t.bm == 256) return launch_v2<LAYOUT, 256, 256, 2, 4>(g, stream);
+    return launch_v2<LAYOUT, 128, 128, 2, 2>(g, stream);
+  }
   if (dtype == TPS_BF16) {
     if (t.bm == 256) return launch_tile<bf16, 256, 128, 64, LAYOUT>(g, stream);
     return launch_tile<bf16, 128, 128, 64, LAYOUT>(g, stream);

@@ -1,0 +1,272 @@
+// bf16 GEMM main path for tile-aligned shapes (M % BM, N % BN, K % 64 == 0).
+//
+// Operand tiles are copied global -> LDS with direct-to-LDS loads (each lane's
+// 16 bytes land at LDS base + 16 * lane), in their natural memory layout:
+//   K-contiguous operand (A of NT/NN, B of NT): [rows][64] bf16, 128-byte rows;
+//   M/N-contiguous operand (A of TN, B of NN/TN): [64][rows] bf16.
+// 16-byte chunks are XOR-swizzled within a row (the global address of each
+// lane is permuted so the chunk lands at its swizzled slot), which keeps the
+// fragment reads free of LDS bank conflicts:
+//   K-contiguous: ds_read_b128 gives a lane 8 consecutive k of one row;
+//   M/N-contiguous: two ds_read_tr16_b64 give a lane 8 consecutive k of one
+//   column (the read transposes 4 x 4 blocks of 16-bit values across lanes).
+// Two LDS stages: the loads of tile k+1 are in flight while tile k is
+// multiplied.  8 waves (2 per SIMD), each owning a (BM/WGM) x (BN/WGN) block of
+// 32x32x16 MFMA tiles.  The K loop is sequential in steps of 16, like the
+// generic path, so the result depends only on (M, N, K) and the data.
+#pragma once
+#include "kernels.h"
+#include "tps_device.h"
+
+namespace tps {
+
+namespace v2 {
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+
+constexpr int BK = 64;
+
+// byte offset of chunk c (16 bytes) of row r in a K-contiguous tile
+__device__ __forceinline__ int kc_off(int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); }
+// byte offset of chunk c of row r in an M/N-contiguous tile with ROWB-byte rows
+template <int ROWB>
+__device__ __forceinline__ int mc_off(int r, int c) { return r * ROWB + ((c ^ ((r & 3) << 1)) << 4); }
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Issue the direct-to-LDS loads of one operand tile.  ROWS = tile extent along
+// M or N.  KC: operand is K-contiguous (global [rows][ld], tile rows x 64);
+// otherwise M/N-contiguous (global [k][ld], tile 64 x rows).
+template <int ROWS, bool KC, int NTHREADS>
+__device__ __forceinline__ void issue_tile(const bf16* g, int64_t ld, int row0, int k0, char* lds) {
+  constexpr int TILE_BYTES = ROWS * BK * 2;
+  constexpr int PER_WAVE = TILE_BYTES / 1024 / (NTHREADS / 64);   // 1 KB per wave instruction
+  static_assert(TILE_BYTES % (1024 * (NTHREADS / 64)) == 0, "tile must split evenly over waves");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < PER_WAVE; ++i) {
+    const int inst = wave * PER_WAVE + i;
+    const int slot = inst * 64 + lane;       // 16-byte slot in the tile
+    const bf16* src;
+    if constexpr (KC) {
+      const int r = slot >> 3, p = slot & 7;
+      const int c = p ^ ((r >> 1) & 7);
+      src = g + (int64_t)(row0 + r) * ld + k0 + c * 8;
+    } else {
+      constexpr int CPR = ROWS / 8;           // chunks per row
+      const int r = slot / CPR, p = slot % CPR;
+      const int c = p ^ ((r & 3) << 1);
+      src = g + (int64_t)(k0 + r) * ld + row0 + c * 8;
+    }
+    __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(lds + inst * 1024), 16, 0, 0);
+  }
+}
+
+// MFMA fragment (8 consecutive k of one row / column) for k-step ks.
+template <int ROWS, bool KC>
+__device__ __forceinline__ bf16x8 frag(const char* lds, int row_base, int ks, int lane) {
+  if constexpr (KC) {
+    const int r = row_base + (lane & 31);
+    const int c = ks * 2 + (lane >> 5);
+    return *reinterpret_cast<const bf16x8*>(lds + kc_off(r, c));
+  } else {
+    constexpr int ROWB = ROWS * 2;
+    const int g = lane >> 4, s = lane & 15;
+    const int col = row_base + ((g & 1) << 4) + ((s & 3) << 2);   // m (or n) this lane addresses
+    const int k = ks * 16 + ((g >> 1) << 3) + (s >> 2);
+    const int c = col >> 3, within = (col & 7) * 2;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(lds + mc_off<ROWB>(k, c) + within));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(lds + mc_off<ROWB>(k + 4, c) + within));
+    typedef __attribute__((ext_vector_type(8))) short s16x8;
+    s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return *reinterpret_cast<bf16x8*>(&v);
+  }
+}
+
+}  // namespace v2
+
+template <int LAYOUT, int BM, int BN, int WGM, int WGN, int EPI>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * WGM * WGN, 64 * WGM * WGN),
+                          amdgpu_waves_per_eu(2, 2)))
+void gemm_v2_kernel(GemmArgs g) {
+  using namespace v2;
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+  constexpr bool A_KC = (LAYOUT != TPS_GEMM_TN);
+  constexpr bool B_KC = (LAYOUT == TPS_GEMM_NT);
+  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2, STAGE = A_BYTES + B_BYTES;
+  constexpr int LOADS = (A_BYTES + B_BYTES) / 1024 / (NT / 64);   // per thread per tile
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+
+  const int nblk = g.tiles_m * g.tiles_n;
+  int pid = blockIdx.x;
+  if ((nblk & 7) == 0) pid = (pid & 7) * (nblk >> 3) + (pid >> 3);
+  constexpr int GROUP = 8;
+  const int group = pid / (GROUP * g.tiles_n);
+  const int first_m = group * GROUP;
+  const int gm = min(GROUP, g.tiles_m - first_m);
+  const int tile_m = first_m + (pid % (GROUP * g.tiles_n)) % gm;
+  const int tile_n = (pid % (GROUP * g.tiles_n)) / gm;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
+
+  const bf16* A = static_cast<const bf16*>(g.A);
+  const bf16* B = static_cast<const bf16*>(g.B);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = g.K / BK;
+  issue_tile<BM, A_KC, NT>(A, g.lda, m0, 0, smem);
+  issue_tile<BN, B_KC, NT>(B, g.ldb, n0, 0, smem + A_BYTES);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      char* nxt = smem + (cur ^ 1) * STAGE;
+      issue_tile<BM, A_KC, NT>(A, g.lda, m0, (kt + 1) * BK, nxt);
+      issue_tile<BN, B_KC, NT>(B, g.ldb, n0, (kt + 1) * BK, nxt + A_BYTES);
+      wait_vmcnt<LOADS>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    __syncthreads();
+    const char* as = smem + cur * STAGE;
+    const char* bs = as + A_BYTES;
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8 fa[TM], fb[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) fa[i] = frag<BM, A_KC>(as, wm * WM + i * 32, ks, lane);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) fb[j] = frag<BN, B_KC>(bs, wn * WN + j * 32, ks, lane);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = Mma<bf16>::run(fa[i], fb[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue through LDS: per 32-row strip, each wave parks its accumulators
+  // ([32][WN] f32) in its own LDS region, reads them back row-contiguous and
+  // applies the epilogue on 8 consecutive columns with 16-byte accesses.
+  constexpr int LDE = WN + 8;   // f32 row pitch (keeps the parking writes conflict-free)
+  static_assert(WGM * WGN * 32 * LDE * 4 <= 2 * STAGE, "epilogue staging must fit in LDS");
+  float* strip = reinterpret_cast<float*>(smem) + wave * 32 * LDE;
+  constexpr int CPR = WN / 8;             // 8-column chunks per row
+  constexpr int RPP = 64 / CPR;           // rows per pass
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) strip[acc_row(r, lane) * LDE + j * 32 + (lane & 31)] = acc[i][j][r];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int q = 0; q < 32 / RPP; ++q) {
+      const int rl = q * RPP + lane / CPR, cl = (lane % CPR) * 8;
+      const f32x4 v0 = *reinterpret_cast<const f32x4*>(strip + rl * LDE + cl);
+      const f32x4 v1 = *reinterpret_cast<const f32x4*>(strip + rl * LDE + cl + 4);
+      const float v[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+      const int row = m0 + wm * WM + i * 32 + rl, col = n0 + wn * WN + cl;
+      if constexpr (EPI == TPS_EPI_ACC_F32) {
+        f32x4* c = reinterpret_cast<f32x4*>(static_cast<float*>(g.C) + (int64_t)row * g.ldc + col);
+        f32x4 c0 = c[0], c1 = c[1];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          c0[t] += v[t];
+          c1[t] += v[4 + t];
+        }
+        c[0] = c0;
+        c[1] = c1;
+      } else {
+        float out[8];
+        Vec16<bf16> bias, res, aux;
+        if constexpr (EPI == TPS_EPI_BIAS || EPI == TPS_EPI_BIAS_RESID || EPI == TPS_EPI_BIAS_GELU)
+          bias = load16(static_cast<const bf16*>(g.bias) + col);
+        if constexpr (EPI == TPS_EPI_BIAS_RESID)
+          res = load16(static_cast<const bf16*>(g.resid) + (int64_t)row * g.ldr + col);
+        if constexpr (EPI == TPS_EPI_GELU_GRAD)
+          aux = load16(static_cast<const bf16*>(g.aux) + (int64_t)row * g.ldaux + col);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          if constexpr (EPI == TPS_EPI_STORE) {
+            out[t] = v[t];
+          } else if constexpr (EPI == TPS_EPI_BIAS) {
+            out[t] = v[t] + to_f32(bias.get(t));
+          } else if constexpr (EPI == TPS_EPI_BIAS_RESID) {
+            out[t] = v[t] + to_f32(bias.get(t)) + to_f32(res.get(t));
+          } else if constexpr (EPI == TPS_EPI_BIAS_GELU) {
+            const bf16 u = from_f32<bf16>(v[t] + to_f32(bias.get(t)));
+            aux.set(t, u);
+            out[t] = gelu_f(to_f32(u));
+          } else {
+            out[t] = v[t] * gelu_grad_f(to_f32(aux.get(t)));
+          }
+        }
+        if constexpr (EPI == TPS_EPI_BIAS_GELU)
+          if (g.aux) store16(static_cast<bf16*>(g.aux) + (int64_t)row * g.ldaux + col, aux);
+        Vec16<bf16> o;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) o.set(t, from_f32<bf16>(out[t]));
+        store16(static_cast<bf16*>(g.C) + (int64_t)row * g.ldc + col, o);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
+template <int LAYOUT, int BM, int BN, int WGM, int WGN, int EPI>
+static hipError_t launch_v2_epi(GemmArgs g, hipStream_t stream) {
+  g.tiles_m = g.M / BM;
+  g.tiles_n = g.N / BN;
+  hipLaunchKernelGGL((gemm_v2_kernel<LAYOUT, BM, BN, WGM, WGN, EPI>), dim3(g.tiles_m * g.tiles_n),
+                     dim3(64 * WGM * WGN), 0, stream, g);
+  return hipGetLastError();
+}
+
+// Epilogues each layout uses in the stage (others fall back to the generic path).
+template <int LAYOUT>
+constexpr bool v2_has_epi(int epi) {
+  return LAYOUT == TPS_GEMM_NT ? (epi == TPS_EPI_STORE || epi == TPS_EPI_BIAS || epi == TPS_EPI_BIAS_RESID ||
+                                  epi == TPS_EPI_BIAS_GELU)
+       : LAYOUT == TPS_GEMM_NN ? (epi == TPS_EPI_STORE || epi == TPS_EPI_GELU_GRAD)
+                               : (epi == TPS_EPI_STORE || epi == TPS_EPI_ACC_F32);
+}
+
+template <int LAYOUT, int BM, int BN, int WGM, int WGN>
+static hipError_t launch_v2(GemmArgs g, hipStream_t stream) {
+  if constexpr (LAYOUT == TPS_GEMM_NT) {
+    switch (g.epi) {
+      case TPS_EPI_BIAS: return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_BIAS>(g, stream);
+      case TPS_EPI_BIAS_RESID: return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_BIAS_RESID>(g, stream);
+      case TPS_EPI_BIAS_GELU: return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_BIAS_GELU>(g, stream);
+      default: return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_STORE>(g, stream);
+    }
+  } else if constexpr (LAYOUT == TPS_GEMM_NN) {
+    if (g.epi == TPS_EPI_GELU_GRAD) return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_GELU_GRAD>(g, stream);
+    return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_STORE>(g, stream);
+  } else {
+    if (g.epi == TPS_EPI_ACC_F32) return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_ACC_F32>(g, stream);
+    return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_STORE>(g, stream);
+  }
+}
+
+}  // namespace tps

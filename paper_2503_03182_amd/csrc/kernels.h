@@ -23,11 +23,12 @@ struct GemmArgs {
 // and changes no result bit: every tile shape sums K in the same order.
 struct GemmTile {
   int bm, bn, bk;
+  int v2;   // 1: tile-aligned bf16 path with direct-to-LDS loads
 };
-GemmTile gemm_select_tile(int dtype, int M, int N);
+GemmTile gemm_select_tile(int dtype, int layout, const GemmArgs& g);
 // Demangled name of the kernel instantiation a launch uses (as profilers
-// print it), e.g. "tps::gemm_kernel<__bf16, 256, 128, 64, 0>".
-const char* gemm_kernel_name(int dtype, int layout, int M, int N);
+// print it), e.g. "tps::gemm_v2_kernel<0, 256, 256, 2, 4>".
+const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g);
 
 hipError_t gemm_launch_nt(int dtype, GemmArgs g, hipStream_t stream);
 hipError_t gemm_launch_nn(int dtype, GemmArgs g, hipStream_t stream);

@@ -1,5 +1,6 @@
 // Op-level C ABI (tpstage_ops.h): argument checks, then one kernel launch
 // sequence on the caller's stream.
+#include <cstdio>
 #include <string>
 
 #include "errors.h"
@@ -126,17 +127,36 @@ extern "C" uint64_t tps_op_workspace_bytes(int kind, int64_t rows, int64_t cols)
 
 namespace tps {
 
-GemmTile gemm_select_tile(int dtype, int M, int N) {
-  if (dtype == TPS_BF16) {
-    const int64_t t256 = (int64_t)((M + 255) / 256) * ((N + 127) / 128);
-    if (t256 >= 256) return {256, 128, 64};
-    return {128, 128, 64};
-  }
-  return {128, 128, 32};
+static bool v2_epilogue(int layout, int epi) {
+  if (layout == TPS_GEMM_NT)
+    return epi == TPS_EPI_STORE || epi == TPS_EPI_BIAS || epi == TPS_EPI_BIAS_RESID || epi == TPS_EPI_BIAS_GELU;
+  if (layout == TPS_GEMM_NN) return epi == TPS_EPI_STORE || epi == TPS_EPI_GELU_GRAD;
+  return epi == TPS_EPI_STORE || epi == TPS_EPI_ACC_F32;
 }
 
-const char* gemm_kernel_name(int dtype, int layout, int M, int N) {
-  static const char* names[2][2][3] = {
+static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+GemmTile gemm_select_tile(int dtype, int layout, const GemmArgs& g) {
+  const int M = g.M, N = g.N, K = g.K;
+  if (dtype == TPS_BF16) {
+    // tile-aligned path: every operand 16-byte aligned with leading dimensions
+    // in whole 16-byte chunks, and an epilogue it instantiates
+    bool ok = K % 64 == 0 && K > 0 && g.lda % 8 == 0 && g.ldb % 8 == 0 && v2_epilogue(layout, g.epi) &&
+              al16(g.A) && al16(g.B) && al16(g.C) && g.ldc % 8 == 0;
+    if (g.epi == TPS_EPI_BIAS || g.epi == TPS_EPI_BIAS_RESID || g.epi == TPS_EPI_BIAS_GELU) ok = ok && al16(g.bias);
+    if (g.epi == TPS_EPI_BIAS_RESID) ok = ok && al16(g.resid) && g.ldr % 8 == 0;
+    if (g.epi == TPS_EPI_BIAS_GELU || g.epi == TPS_EPI_GELU_GRAD) ok = ok && al16(g.aux) && g.ldaux % 8 == 0;
+    if (ok && M % 256 == 0 && N % 256 == 0 && (int64_t)(M / 256) * (N / 256) >= 160) return {256, 256, 64, 1};
+    if (ok && M % 128 == 0 && N % 128 == 0) return {128, 128, 64, 1};
+    const int64_t t256 = (int64_t)((M + 255) / 256) * ((N + 127) / 128);
+    if (t256 >= 256) return {256, 128, 64, 0};
+    return {128, 128, 64, 0};
+  }
+  return {128, 128, 32, 0};
+}
+
+const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g) {
+  static const char* v1[2][2][3] = {
       {{"tps::gemm_kernel<float, 128, 128, 32, 0>", "tps::gemm_kernel<float, 128, 128, 32, 1>",
         "tps::gemm_kernel<float, 128, 128, 32, 2>"},
        {"tps::gemm_kernel<float, 128, 128, 32, 0>", "tps::gemm_kernel<float, 128, 128, 32, 1>",
@@ -145,8 +165,20 @@ const char* gemm_kernel_name(int dtype, int layout, int M, int N) {
         "tps::gemm_kernel<__bf16, 128, 128, 64, 2>"},
        {"tps::gemm_kernel<__bf16, 256, 128, 64, 0>", "tps::gemm_kernel<__bf16, 256, 128, 64, 1>",
         "tps::gemm_kernel<__bf16, 256, 128, 64, 2>"}}};
-  const GemmTile t = gemm_select_tile(dtype, M, N);
-  return names[dtype == TPS_BF16][t.bm == 256][layout];
+  // [tile][layout][epilogue]
+  static char v2[2][3][6][64];
+  static bool init = false;
+  if (!init) {
+    for (int t = 0; t < 2; ++t)
+      for (int l = 0; l < 3; ++l)
+        for (int e = 0; e < 6; ++e)
+          snprintf(v2[t][l][e], sizeof(v2[t][l][e]), "tps::gemm_v2_kernel<%d, %s, %d>", l,
+                   t ? "256, 256, 2, 4" : "128, 128, 2, 2", e);
+    init = true;
+  }
+  const GemmTile t = gemm_select_tile(dtype, layout, g);
+  if (t.v2) return v2[t.bm == 256][layout][g.epi];
+  return v1[dtype == TPS_BF16][t.bm == 256][layout];
 }
 
 hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, const void* A, int64_t lda,

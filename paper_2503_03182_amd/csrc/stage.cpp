@@ -139,7 +139,8 @@ struct tps_stage {
     const double es = p.esize;
     const double bytes = ((double)M * K + (double)N * K) * es +
                          (epi == TPS_EPI_ACC_F32 ? 8.0 * M * N : (double)M * N * es);
-    const int t = kbegin(gemm_kernel_name(p.dtype, layout, M, N), 2.0 * M * N * K, bytes);
+    const GemmArgs ga{M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux, ldaux, epi, 0, 0};
+    const int t = kbegin(gemm_kernel_name(p.dtype, layout, ga), 2.0 * M * N * K, bytes);
     const int rc = check_hip(gemm_launch(p.dtype, layout, epi, M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr,
                                          aux, ldaux, cs),
                              "gemm");

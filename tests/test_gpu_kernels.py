@@ -26,7 +26,10 @@ def _round(a, dtype):
     return synth.round_to_storage(np.asarray(a, dtype=np.float32), dtype).astype(np.float64)
 
 
-GEMM_SHAPES = [(200, 264, 136), (1000, 520, 72), (64, 64, 8), (2072, 4104, 264)]
+# ragged shapes take the generic path; tile-aligned ones (M, N multiples of
+# 128 or 256, K of 64) take the direct-to-LDS path at both tile sizes
+GEMM_SHAPES = [(200, 264, 136), (1000, 520, 72), (64, 64, 8), (2072, 4104, 264),
+               (256, 384, 192), (4096, 2560, 128)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -51,10 +54,11 @@ def test_gemm_store(dtype, layout, shape):
     assert rel_l2(to_np(dC), ref) < TOL[dtype]
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_gemm_epilogues(dtype):
+@pytest.mark.parametrize("dtype,shape", [("f32", (296, 392, 200)), ("bf16", (296, 392, 200)),
+                                         ("bf16", (512, 768, 256)), ("bf16", (4096, 2560, 128))])
+def test_gemm_epilogues(dtype, shape):
     import torch
-    M, N, K = 296, 392, 200
+    M, N, K = shape
     A = _t(21, (M, K), dtype)
     B = _t(22, (N, K), dtype, 0.1)
     bias = _t(23, (N,), dtype)
