@@ -543,17 +543,25 @@ static hipError_t bwd_launch(int b, int s, int nh, const void* qkv, const void* 
 
 hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, void* o,
                                 float* lse, hipStream_t st) {
-  if (dtype == TPS_BF16)
-    return d == 64 ? fwd_launch<bf16, 64>(b, s, nh, qkv, o, lse, st) : fwd_launch<bf16, 128>(b, s, nh, qkv, o, lse, st);
+  if (dtype == TPS_BF16) return attention_fwd_v2_launch(b, s, nh, d, qkv, o, lse, st);
   return d == 64 ? fwd_launch<float, 64>(b, s, nh, qkv, o, lse, st) : fwd_launch<float, 128>(b, s, nh, qkv, o, lse, st);
 }
 
 hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, const void* o,
                                 const float* lse, const void* dout, void* dqkv, float* dvec,
                                 hipStream_t st) {
-  if (dtype == TPS_BF16)
-    return d == 64 ? bwd_launch<bf16, 64>(b, s, nh, qkv, o, lse, dout, dqkv, dvec, st)
-                   : bwd_launch<bf16, 128>(b, s, nh, qkv, o, lse, dout, dqkv, dvec, st);
+  if (dtype == TPS_BF16) {
+    const int64_t rows_heads = (int64_t)b * s * nh;
+    if (d == 128)
+      hipLaunchKernelGGL((attn_bwd_dot_kernel<bf16, 128>), dim3((unsigned)((rows_heads + 255) / 256)), dim3(256), 0, st,
+                         static_cast<const bf16*>(o), static_cast<const bf16*>(dout), dvec, b, s, nh);
+    else
+      hipLaunchKernelGGL((attn_bwd_dot_kernel<bf16, 64>), dim3((unsigned)((rows_heads + 255) / 256)), dim3(256), 0, st,
+                         static_cast<const bf16*>(o), static_cast<const bf16*>(dout), dvec, b, s, nh);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return attention_bwd_v2_launch(b, s, nh, d, qkv, lse, dout, dqkv, dvec, st);
+  }
   return d == 64 ? bwd_launch<float, 64>(b, s, nh, qkv, o, lse, dout, dqkv, dvec, st)
                  : bwd_launch<float, 128>(b, s, nh, qkv, o, lse, dout, dqkv, dvec, st);
 }

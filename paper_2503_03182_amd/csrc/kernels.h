@@ -47,6 +47,12 @@ hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const vo
                                 const float* lse, const void* dout, void* dqkv, float* dvec,
                                 hipStream_t st);
 
+// bf16 kernels on 16x16x32 MFMAs with paired causal blocks (attention_v2.hip)
+hipError_t attention_fwd_v2_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
+                                   hipStream_t st);
+hipError_t attention_bwd_v2_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
+                                   void* dqkv, const float* dvec, hipStream_t st);
+
 hipError_t layernorm_fwd_launch(int dtype, int rows, int cols, const void* x, const void* gamma,
                                 const void* beta, float eps, void* out, float* mean, float* rstd,
                                 hipStream_t st);

@@ -10,7 +10,6 @@ namespace tps {
 
 namespace {
 
-constexpr int kRowsPerPart = kColsumRowsPerPart;
 
 __device__ __forceinline__ float block_sum(float v, float* red) {
   v = wave_sum(v);
@@ -131,48 +130,59 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dout,
   }
 }
 
-// Pass 1 of a column reduction: ws[part][k][c] = sum over the part's rows.
-// k = 0: sum x (or dout); k = 1 (LN mode): sum dout * zhat.
+// Pass 1 of a column reduction: block (column group of 64, row segment).
+// Thread (row lane rl, chunk cc) sums rows rl, rl+32, ... of the segment for
+// 8 columns; the 32 row lanes are then added in ascending order.
+// k = 0: sum x (or dout); k = 1 (LN mode): sum dout * (xin - mean) * rstd.
 template <typename T, bool LN>
 __global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ x, int64_t ldx,
                                                           const T* __restrict__ xin, const float* __restrict__ mean,
                                                           const float* __restrict__ rstd, float* __restrict__ ws,
-                                                          int rows, int cols) {
+                                                          int rows, int cols, int seg_rows) {
   constexpr int VEC = 16 / sizeof(T);
-  const int col = (blockIdx.x * 256 + threadIdx.x) * VEC;
-  if (col >= cols) return;
-  const int part = blockIdx.y;
-  const int r0 = part * kRowsPerPart, r1 = min(rows, r0 + kRowsPerPart);
+  constexpr int COLS = 8 * VEC;                 // columns per block
+  __shared__ float red[LN ? 2 : 1][32][COLS + 1];
+  const int cc = threadIdx.x & 7, rl = threadIdx.x >> 3;
+  const int col = blockIdx.x * COLS + cc * VEC;
+  const int r0 = blockIdx.y * seg_rows, r1 = min(rows, r0 + seg_rows);
   float a[VEC], z[VEC];
 #pragma unroll
   for (int i = 0; i < VEC; ++i) a[i] = z[i] = 0.f;
-  for (int r = r0; r < r1; ++r) {
-    const Vec16<T> v = load16(x + (int64_t)r * ldx + col);
-    if constexpr (LN) {
-      const Vec16<T> xv = load16(xin + (int64_t)r * cols + col);
-      const float mu = mean[r], rs = rstd[r];
+  if (col < cols) {
+    for (int r = r0 + rl; r < r1; r += 32) {
+      const Vec16<T> v = load16(x + (int64_t)r * ldx + col);
+      if constexpr (LN) {
+        const Vec16<T> xv = load16(xin + (int64_t)r * cols + col);
+        const float mu = mean[r], rs = rstd[r];
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) {
-        const float d = to_f32(v.get(i));
-        a[i] += d;
-        z[i] += d * ((to_f32(xv.get(i)) - mu) * rs);
+        for (int i = 0; i < VEC; ++i) {
+          const float d = to_f32(v.get(i));
+          a[i] += d;
+          z[i] += d * ((to_f32(xv.get(i)) - mu) * rs);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) a[i] += to_f32(v.get(i));
       }
-    } else {
-#pragma unroll
-      for (int i = 0; i < VEC; ++i) a[i] += to_f32(v.get(i));
     }
   }
+#pragma unroll
+  for (int i = 0; i < VEC; ++i) {
+    red[0][rl][cc * VEC + i] = a[i];
+    if constexpr (LN) red[1][rl][cc * VEC + i] = z[i];
+  }
+  __syncthreads();
   const int nk = LN ? 2 : 1;
-  float* w = ws + (int64_t)part * nk * cols;
-#pragma unroll
-  for (int i = 0; i < VEC; ++i) w[col + i] = a[i];
-  if constexpr (LN) {
-#pragma unroll
-    for (int i = 0; i < VEC; ++i) w[cols + col + i] = z[i];
+  if (threadIdx.x < COLS * nk) {
+    const int k = threadIdx.x / COLS, c = threadIdx.x % COLS;
+    const int gc = blockIdx.x * COLS + c;
+    float acc = 0.f;
+    for (int i = 0; i < 32; ++i) acc += red[k][i][c];
+    if (gc < cols) ws[((int64_t)blockIdx.y * nk + k) * cols + gc] = acc;
   }
 }
 
-// Pass 2: out_k[c] += sum over parts in ascending order.
+// Pass 2: out_k[c] += sum over segments in ascending order.
 __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ ws, int parts, int nk,
                                                            int cols, float* __restrict__ out0,
                                                            float* __restrict__ out1) {
@@ -226,14 +236,15 @@ template <typename T>
 hipError_t colsum_typed(int rows, int cols, const void* x, int64_t ldx, const void* xin, const float* mean,
                         const float* rstd, float* out0, float* out1, float* ws, bool ln, hipStream_t st) {
   constexpr int VEC = 16 / sizeof(T);
-  const int parts = (rows + kRowsPerPart - 1) / kRowsPerPart;
-  dim3 grid((cols / VEC + 255) / 256, parts);
+  const int seg = (int)colsum_seg_rows(rows);
+  const int parts = (int)colsum_segments(rows);
+  dim3 grid((cols + 8 * VEC - 1) / (8 * VEC), parts);
   if (ln)
     hipLaunchKernelGGL((colsum_part_kernel<T, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
-                       static_cast<const T*>(xin), mean, rstd, ws, rows, cols);
+                       static_cast<const T*>(xin), mean, rstd, ws, rows, cols, seg);
   else
     hipLaunchKernelGGL((colsum_part_kernel<T, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
-                       static_cast<const T*>(nullptr), mean, rstd, ws, rows, cols);
+                       static_cast<const T*>(nullptr), mean, rstd, ws, rows, cols, seg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, ws, parts, ln ? 2 : 1,

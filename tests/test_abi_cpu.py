@@ -173,7 +173,9 @@ def test_op_argument_errors_without_gpu():
         T.op_attention_fwd(T.TPS_BF16, 1, 16, 2, 96, None, None, None)
     with pytest.raises(T.TpsError):
         T.op_layernorm_fwd(T.TPS_F32, 4, 20000, None, None, None, 1e-5, None)
-    assert T.op_workspace_bytes(T.WS_COLSUM, 100, 64) == 4 * 64 * 4
+    # 100 rows: segments of 64 rows (multiple of 32, at least 64) -> 2 partials per column
+    assert T.op_workspace_bytes(T.WS_COLSUM, 100, 64) == 2 * 64 * 4
+    assert T.op_workspace_bytes(T.WS_COLSUM, 8192, 64) == 16 * 64 * 4
     assert T.op_workspace_bytes(T.WS_ATTN_BWD, 256, 4) == 256 * 4 * 4
 
 
