@@ -33,6 +33,30 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def kernel_source_hash() -> str:
+    """sha256 over the HIP/C++ sources of the library (sorted by name)."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2503_03182_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the counter runs recorded in
+    profiles/, or None when they were taken on other kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_dominant_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    rec = dict(line.rstrip("\n").split("\t", 1) for line in open(path) if "\t" in line)
+    if rec.get("kernel") != kernel or rec.get("source_sha256") != kernel_source_hash():
+        return None
+    return float(rec["bytes_per_launch"])
+
+
 def build_stage(cfg):
     import torch
     from paper_2503_03182_amd import synth
@@ -105,7 +129,20 @@ def main():
     ap.add_argument("--workload", default="stage4_h2048")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain 512 MiB device-to-device copy (reference for HBM byte counters)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = 512 << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU's share of the stage; --gpus {args.gpus} is not supported "
               f"(multi-GPU runs are outside this build)", file=sys.stderr)
@@ -203,7 +240,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(args.workload, dominant),
             "launches": dom["launches"],
             "avg_launch_us": round(dom["ms"] * 1e3 / max(dom["launches"], 1), 2),
         },
