@@ -10,10 +10,12 @@
 //   K-contiguous: ds_read_b128 gives a lane 8 consecutive k of one row;
 //   M/N-contiguous: two ds_read_tr16_b64 give a lane 8 consecutive k of one
 //   column (the read transposes 4 x 4 blocks of 16-bit values across lanes).
-// Two LDS stages: the loads of tile k+1 are in flight while tile k is
-// multiplied.  8 waves (2 per SIMD), each owning a (BM/WGM) x (BN/WGN) block of
-// 32x32x16 MFMA tiles.  The K loop is sequential in steps of 16, like the
-// generic path, so the result depends only on (M, N, K) and the data.
+// STAGES LDS stages hold consecutive K tiles: STAGES-1 tiles are in flight
+// while one is multiplied, with one barrier per tile.  Waves own a
+// (BM/WGM) x (BN/WGN) block of 32x32x16 MFMA tiles; with KSPLIT = 2 a second
+// group of waves takes the upper half of every K tile and the two partial
+// sums are added in a fixed order at the end (two waves per SIMD on small
+// grids).  Within each wave the K loop is sequential in steps of 16.
 #pragma once
 #include "kernels.h"
 #include "tps_device.h"
@@ -25,13 +27,22 @@ namespace v2 {
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((ext_vector_type(4))) short s16x4;
 
-constexpr int BK = 64;
-
-// byte offset of chunk c (16 bytes) of row r in a K-contiguous tile
-__device__ __forceinline__ int kc_off(int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); }
-// byte offset of chunk c of row r in an M/N-contiguous tile with ROWB-byte rows
+// Byte offset of chunk c (16 bytes) of row r in a K-contiguous tile with BK
+// columns.  ds_read_b128 serves 16 lanes = 16 consecutive rows at one chunk
+// per pass; the swizzle spreads them over all 64 banks:
+//   BK = 64 (128-byte rows, odd rows in the other bank half): c ^ ((r >> 1) & 7);
+//   BK = 32 (64-byte rows, four rows per 256 bytes): c ^ ((r >> 2) & 3).
+template <int BK>
+__device__ __forceinline__ int kc_off(int r, int c) {
+  if constexpr (BK == 64) return r * 128 + ((c ^ ((r >> 1) & 7)) << 4);
+  else return r * 64 + ((c ^ ((r >> 2) & 3)) << 4);
+}
+// Byte offset of chunk c of row r in an M/N-contiguous tile with ROWB-byte rows
+// (ROWB >= 256).  A pass of ds_read_tr16_b64 serves 32 lanes reading 4 rows x
+// 4 chunks; XOR-ing chunk bits 2-3 with the row puts the 16 chunks on 16
+// different bank groups.
 template <int ROWB>
-__device__ __forceinline__ int mc_off(int r, int c) { return r * ROWB + ((c ^ ((r & 3) << 1)) << 4); }
+__device__ __forceinline__ int mc_off(int r, int c) { return r * ROWB + ((c ^ ((r & 3) << 2)) << 4); }
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -42,7 +53,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 // Issue the direct-to-LDS loads of one operand tile.  ROWS = tile extent along
 // M or N.  KC: operand is K-contiguous (global [rows][ld], tile rows x 64);
 // otherwise M/N-contiguous (global [k][ld], tile 64 x rows).
-template <int ROWS, bool KC, int NTHREADS>
+template <int ROWS, bool KC, int NTHREADS, int BK>
 __device__ __forceinline__ void issue_tile(const bf16* g, int64_t ld, int row0, int k0, char* lds) {
   constexpr int TILE_BYTES = ROWS * BK * 2;
   constexpr int PER_WAVE = TILE_BYTES / 1024 / (NTHREADS / 64);   // 1 KB per wave instruction
@@ -54,13 +65,14 @@ __device__ __forceinline__ void issue_tile(const bf16* g, int64_t ld, int row0, 
     const int slot = inst * 64 + lane;       // 16-byte slot in the tile
     const bf16* src;
     if constexpr (KC) {
-      const int r = slot >> 3, p = slot & 7;
-      const int c = p ^ ((r >> 1) & 7);
+      constexpr int CPR = BK / 8;
+      const int r = slot / CPR, p = slot % CPR;
+      const int c = (BK == 64) ? (p ^ ((r >> 1) & 7)) : (p ^ ((r >> 2) & 3));
       src = g + (int64_t)(row0 + r) * ld + k0 + c * 8;
     } else {
       constexpr int CPR = ROWS / 8;           // chunks per row
       const int r = slot / CPR, p = slot % CPR;
-      const int c = p ^ ((r & 3) << 1);
+      const int c = p ^ ((r & 3) << 2);
       src = g + (int64_t)(k0 + r) * ld + row0 + c * 8;
     }
     __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(lds + inst * 1024), 16, 0, 0);
@@ -68,12 +80,12 @@ __device__ __forceinline__ void issue_tile(const bf16* g, int64_t ld, int row0, 
 }
 
 // MFMA fragment (8 consecutive k of one row / column) for k-step ks.
-template <int ROWS, bool KC>
+template <int ROWS, bool KC, int BK>
 __device__ __forceinline__ bf16x8 frag(const char* lds, int row_base, int ks, int lane) {
   if constexpr (KC) {
     const int r = row_base + (lane & 31);
     const int c = ks * 2 + (lane >> 5);
-    return *reinterpret_cast<const bf16x8*>(lds + kc_off(r, c));
+    return *reinterpret_cast<const bf16x8*>(lds + kc_off<BK>(r, c));
   } else {
     constexpr int ROWB = ROWS * 2;
     const int g = lane >> 4, s = lane & 15;
@@ -92,18 +104,20 @@ __device__ __forceinline__ bf16x8 frag(const char* lds, int row_base, int ks, in
 
 }  // namespace v2
 
-template <int LAYOUT, int BM, int BN, int WGM, int WGN, int EPI>
-__global__ __attribute__((amdgpu_flat_work_group_size(64 * WGM * WGN, 64 * WGM * WGN),
+template <int LAYOUT, int BM, int BN, int WGM, int WGN, int KSPLIT, int BK, int STAGES, int EPI>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * WGM * WGN * KSPLIT, 64 * WGM * WGN * KSPLIT),
                           amdgpu_waves_per_eu(2, 2)))
 void gemm_v2_kernel(GemmArgs g) {
   using namespace v2;
-  constexpr int NT = 64 * WGM * WGN;
+  constexpr int NT = 64 * WGM * WGN * KSPLIT;
   constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
+  constexpr int KS = BK / 16 / KSPLIT;   // k-steps of 16 per wave per tile
   constexpr bool A_KC = (LAYOUT != TPS_GEMM_TN);
   constexpr bool B_KC = (LAYOUT == TPS_GEMM_NT);
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2, STAGE = A_BYTES + B_BYTES;
   constexpr int LOADS = (A_BYTES + B_BYTES) / 1024 / (NT / 64);   // per thread per tile
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  static_assert(KS >= 1 && STAGES >= 2, "pipeline shape");
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
   const int nblk = g.tiles_m * g.tiles_n;
   int pid = blockIdx.x;
@@ -118,7 +132,8 @@ void gemm_v2_kernel(GemmArgs g) {
 
   const bf16* A = static_cast<const bf16*>(g.A);
   const bf16* B = static_cast<const bf16*>(g.B);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave_all = threadIdx.x >> 6;
+  const int wk = wave_all / (WGM * WGN), wave = wave_all % (WGM * WGN);
   const int wm = wave / WGN, wn = wave % WGN;
 
   f32x16 acc[TM][TN];
@@ -130,41 +145,103 @@ void gemm_v2_kernel(GemmArgs g) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = g.K / BK;
-  issue_tile<BM, A_KC, NT>(A, g.lda, m0, 0, smem);
-  issue_tile<BN, B_KC, NT>(B, g.ldb, n0, 0, smem + A_BYTES);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      char* nxt = smem + (cur ^ 1) * STAGE;
-      issue_tile<BM, A_KC, NT>(A, g.lda, m0, (kt + 1) * BK, nxt);
-      issue_tile<BN, B_KC, NT>(B, g.ldb, n0, (kt + 1) * BK, nxt + A_BYTES);
-      wait_vmcnt<LOADS>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    __syncthreads();
-    const char* as = smem + cur * STAGE;
+  auto mma_tile = [&](const char* as) {
     const char* bs = as + A_BYTES;
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
+    for (int kk = 0; kk < KS; ++kk) {
+      const int ks = wk * KS + kk;
       bf16x8 fa[TM], fb[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i) fa[i] = frag<BM, A_KC>(as, wm * WM + i * 32, ks, lane);
+      for (int i = 0; i < TM; ++i) fa[i] = frag<BM, A_KC, BK>(as, wm * WM + i * 32, ks, lane);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) fb[j] = frag<BN, B_KC>(bs, wn * WN + j * 32, ks, lane);
+      for (int j = 0; j < TN; ++j) fb[j] = frag<BN, B_KC, BK>(bs, wn * WN + j * 32, ks, lane);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = Mma<bf16>::run(fa[i], fb[j], acc[i][j]);
     }
+  };
+  if constexpr (STAGES == 2) {
+    // tile k+1 in flight while tile k is multiplied; a second barrier keeps
+    // the stage being refilled out of use
+    issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, 0, smem);
+    issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, 0, smem + A_BYTES);
+    for (int kt = 0; kt < nk; ++kt) {
+      if (kt + 1 < nk) {
+        char* nxt = smem + ((kt + 1) & 1) * STAGE;
+        issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, (kt + 1) * BK, nxt);
+        issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, (kt + 1) * BK, nxt + A_BYTES);
+        wait_vmcnt<LOADS>();
+      } else {
+        wait_vmcnt<0>();
+      }
+      __syncthreads();
+      mma_tile(smem + (kt & 1) * STAGE);
+      __syncthreads();
+    }
+  } else {
+    // prologue: tiles 0 .. STAGES-2 in flight
+#pragma unroll
+    for (int t = 0; t < STAGES - 1; ++t) {
+      if (t < nk) {
+        issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, t * BK, smem + t * STAGE);
+        issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, t * BK, smem + t * STAGE + A_BYTES);
+      }
+    }
+    for (int kt = 0; kt < nk; ++kt) {
+      // tile kt has landed once at most (tiles in flight after it) loads remain
+      const int ahead = min(STAGES - 2, nk - 1 - kt);
+      if constexpr (STAGES == 4) {
+        if (ahead >= 2) wait_vmcnt<2 * LOADS>();
+        else if (ahead == 1) wait_vmcnt<LOADS>();
+        else wait_vmcnt<0>();
+      } else {
+        if (ahead >= 1) wait_vmcnt<LOADS>();
+        else wait_vmcnt<0>();
+      }
+      __syncthreads();
+      // the stage refilled here was last read in iteration kt - 1, which every
+      // wave finished before the barrier above
+      if (kt + STAGES - 1 < nk) {
+        char* nxt = smem + ((kt + STAGES - 1) % STAGES) * STAGE;
+        issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, (kt + STAGES - 1) * BK, nxt);
+        issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, (kt + STAGES - 1) * BK, nxt + A_BYTES);
+      }
+      mma_tile(smem + (kt % STAGES) * STAGE);
+    }
+  }
+  __syncthreads();   // LDS is reused below
+
+  if constexpr (KSPLIT == 2) {
+    // fixed-order combine: the lower-K group adds the upper-K group's sums
+    float* park = reinterpret_cast<float*>(smem) + wave * (TM * TN * 16 * 64);
+    static_assert(WGM * WGN * TM * TN * 16 * 64 * 4 <= STAGES * STAGE, "combine must fit in LDS");
+    if (wk == 1) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) park[((i * TN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
+    }
     __syncthreads();
+    if (wk == 0) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] += park[((i * TN + j) * 16 + r) * 64 + lane];
+    }
+    __syncthreads();
+    if (wk != 0) return;
   }
 
   // Epilogue through LDS: per 32-row strip, each wave parks its accumulators
   // ([32][WN] f32) in its own LDS region, reads them back row-contiguous and
   // applies the epilogue on 8 consecutive columns with 16-byte accesses.
   constexpr int LDE = WN + 8;   // f32 row pitch (keeps the parking writes conflict-free)
-  static_assert(WGM * WGN * 32 * LDE * 4 <= 2 * STAGE, "epilogue staging must fit in LDS");
+  static_assert(WGM * WGN * 32 * LDE * 4 <= STAGES * STAGE, "epilogue staging must fit in LDS");
   float* strip = reinterpret_cast<float*>(smem) + wave * 32 * LDE;
   constexpr int CPR = WN / 8;             // 8-column chunks per row
   constexpr int RPP = 64 / CPR;           // rows per pass
@@ -233,12 +310,23 @@ void gemm_v2_kernel(GemmArgs g) {
   }
 }
 
+// Pipeline shape per layout (measured on MI355X): both operands K-contiguous
+// (NT) take BK 32 with 4 stages, and 128x128 tiles add a second K-group of
+// waves; layouts with transposing reads (NN, TN) take BK 64 with 2 stages.
+template <int LAYOUT, int BM>
+struct V2Shape {
+  static constexpr int KSPLIT = (LAYOUT == TPS_GEMM_NT && BM == 128) ? 2 : 1;
+  static constexpr int BK = (LAYOUT == TPS_GEMM_NT) ? 32 : 64;
+  static constexpr int STAGES = (LAYOUT == TPS_GEMM_NT) ? 4 : 2;
+};
+
 template <int LAYOUT, int BM, int BN, int WGM, int WGN, int EPI>
 static hipError_t launch_v2_epi(GemmArgs g, hipStream_t stream) {
+  typedef V2Shape<LAYOUT, BM> S;
   g.tiles_m = g.M / BM;
   g.tiles_n = g.N / BN;
-  hipLaunchKernelGGL((gemm_v2_kernel<LAYOUT, BM, BN, WGM, WGN, EPI>), dim3(g.tiles_m * g.tiles_n),
-                     dim3(64 * WGM * WGN), 0, stream, g);
+  hipLaunchKernelGGL((gemm_v2_kernel<LAYOUT, BM, BN, WGM, WGN, S::KSPLIT, S::BK, S::STAGES, EPI>),
+                     dim3(g.tiles_m * g.tiles_n), dim3(64 * WGM * WGN * S::KSPLIT), 0, stream, g);
   return hipGetLastError();
 }
 
