@@ -250,8 +250,8 @@ template <int LAYOUT>
 static hipError_t launch_layout(int dtype, GemmArgs g, hipStream_t stream) {
   const GemmTile t = gemm_select_tile(dtype, LAYOUT, g);
   if (t.v2) {
-    if (t.bm == 256) return launch_v2<LAYOUT, 256, 256, 2, 4>(g, stream);
-    return launch_v2<LAYOUT, 128, 128, 2, 2>(g, stream);
+    if (t.bm == 256) return launch_v2<LAYOUT, 256, 256>(g, stream);
+    return launch_v2<LAYOUT, 128, 128>(g, stream);
   }
   if (dtype == TPS_BF16) {
     if (t.bm == 256) return launch_tile<bf16, 256, 128, 64, LAYOUT>(g, stream);

@@ -106,7 +106,7 @@ __device__ __forceinline__ bf16x8 frag(const char* lds, int row_base, int ks, in
 
 template <int LAYOUT, int BM, int BN, int WGM, int WGN, int KSPLIT, int BK, int STAGES, int EPI>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * WGM * WGN * KSPLIT, 64 * WGM * WGN * KSPLIT),
-                          amdgpu_waves_per_eu(2, 2)))
+                          amdgpu_waves_per_eu(WGM * WGN * KSPLIT >= 8 ? 2 : 1, WGM * WGN * KSPLIT >= 8 ? 2 : 1)))
 void gemm_v2_kernel(GemmArgs g) {
   using namespace v2;
   constexpr int NT = 64 * WGM * WGN * KSPLIT;
@@ -145,20 +145,27 @@ void gemm_v2_kernel(GemmArgs g) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = g.K / BK;
+  // fragments of k-step kk+1 are read while the MFMAs of k-step kk run
   auto mma_tile = [&](const char* as) {
     const char* bs = as + A_BYTES;
+    bf16x8 fa[2][TM], fb[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[0][i] = frag<BM, A_KC, BK>(as, wm * WM + i * 32, wk * KS, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[0][j] = frag<BN, B_KC, BK>(bs, wn * WN + j * 32, wk * KS, lane);
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      const int ks = wk * KS + kk;
-      bf16x8 fa[TM], fb[TN];
+      const int cur = kk & 1;
+      if (kk + 1 < KS) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) fa[i] = frag<BM, A_KC, BK>(as, wm * WM + i * 32, ks, lane);
+        for (int i = 0; i < TM; ++i) fa[cur ^ 1][i] = frag<BM, A_KC, BK>(as, wm * WM + i * 32, wk * KS + kk + 1, lane);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) fb[j] = frag<BN, B_KC, BK>(bs, wn * WN + j * 32, ks, lane);
+        for (int j = 0; j < TN; ++j) fb[cur ^ 1][j] = frag<BN, B_KC, BK>(bs, wn * WN + j * 32, wk * KS + kk + 1, lane);
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = Mma<bf16>::run(fa[i], fb[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = Mma<bf16>::run(fa[cur][i], fb[cur][j], acc[i][j]);
     }
   };
   if constexpr (STAGES == 2) {
@@ -310,23 +317,13 @@ void gemm_v2_kernel(GemmArgs g) {
   }
 }
 
-// Pipeline shape per layout (measured on MI355X): both operands K-contiguous
-// (NT) take BK 32 with 4 stages, and 128x128 tiles add a second K-group of
-// waves; layouts with transposing reads (NN, TN) take BK 64 with 2 stages.
-template <int LAYOUT, int BM>
-struct V2Shape {
-  static constexpr int KSPLIT = (LAYOUT == TPS_GEMM_NT && BM == 128) ? 2 : 1;
-  static constexpr int BK = (LAYOUT == TPS_GEMM_NT) ? 32 : 64;
-  static constexpr int STAGES = (LAYOUT == TPS_GEMM_NT) ? 4 : 2;
-};
-
-template <int LAYOUT, int BM, int BN, int WGM, int WGN, int EPI>
+template <int LAYOUT, int BM, int BN, int EPI>
 static hipError_t launch_v2_epi(GemmArgs g, hipStream_t stream) {
-  typedef V2Shape<LAYOUT, BM> S;
+  constexpr V2Config c = v2_config(LAYOUT, BM == 256);
   g.tiles_m = g.M / BM;
   g.tiles_n = g.N / BN;
-  hipLaunchKernelGGL((gemm_v2_kernel<LAYOUT, BM, BN, WGM, WGN, S::KSPLIT, S::BK, S::STAGES, EPI>),
-                     dim3(g.tiles_m * g.tiles_n), dim3(64 * WGM * WGN * S::KSPLIT), 0, stream, g);
+  hipLaunchKernelGGL((gemm_v2_kernel<LAYOUT, BM, BN, c.wgm, c.wgn, c.ksplit, c.bk, c.stages, EPI>),
+                     dim3(g.tiles_m * g.tiles_n), dim3(64 * c.wgm * c.wgn * c.ksplit), 0, stream, g);
   return hipGetLastError();
 }
 
@@ -339,21 +336,21 @@ constexpr bool v2_has_epi(int epi) {
                                : (epi == TPS_EPI_STORE || epi == TPS_EPI_ACC_F32);
 }
 
-template <int LAYOUT, int BM, int BN, int WGM, int WGN>
+template <int LAYOUT, int BM, int BN>
 static hipError_t launch_v2(GemmArgs g, hipStream_t stream) {
   if constexpr (LAYOUT == TPS_GEMM_NT) {
     switch (g.epi) {
-      case TPS_EPI_BIAS: return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_BIAS>(g, stream);
-      case TPS_EPI_BIAS_RESID: return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_BIAS_RESID>(g, stream);
-      case TPS_EPI_BIAS_GELU: return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_BIAS_GELU>(g, stream);
-      default: return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_STORE>(g, stream);
+      case TPS_EPI_BIAS: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS>(g, stream);
+      case TPS_EPI_BIAS_RESID: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS_RESID>(g, stream);
+      case TPS_EPI_BIAS_GELU: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS_GELU>(g, stream);
+      default: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_STORE>(g, stream);
     }
   } else if constexpr (LAYOUT == TPS_GEMM_NN) {
-    if (g.epi == TPS_EPI_GELU_GRAD) return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_GELU_GRAD>(g, stream);
-    return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_STORE>(g, stream);
+    if (g.epi == TPS_EPI_GELU_GRAD) return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_GELU_GRAD>(g, stream);
+    return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_STORE>(g, stream);
   } else {
-    if (g.epi == TPS_EPI_ACC_F32) return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_ACC_F32>(g, stream);
-    return launch_v2_epi<LAYOUT, BM, BN, WGM, WGN, TPS_EPI_STORE>(g, stream);
+    if (g.epi == TPS_EPI_ACC_F32) return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_ACC_F32>(g, stream);
+    return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_STORE>(g, stream);
   }
 }
 

@@ -26,6 +26,18 @@ struct GemmTile {
   int v2;   // 1: tile-aligned bf16 path with direct-to-LDS loads
 };
 GemmTile gemm_select_tile(int dtype, int layout, const GemmArgs& g);
+
+// Shape of the tile-aligned bf16 kernel per (layout, tile), chosen by
+// measurement on MI355X: waves along M and N, K-groups of waves, K tile and
+// LDS stages.
+struct V2Config {
+  int wgm, wgn, ksplit, bk, stages;
+};
+constexpr V2Config v2_config(int layout, bool big) {
+  return layout == TPS_GEMM_NT ? (big ? V2Config{2, 4, 1, 32, 4} : V2Config{2, 2, 2, 64, 3})
+       : layout == TPS_GEMM_NN ? (big ? V2Config{2, 4, 1, 64, 2} : V2Config{2, 2, 2, 64, 3})
+                               : (big ? V2Config{2, 2, 1, 64, 2} : V2Config{2, 2, 2, 64, 3});
+}
 // Demangled name of the kernel instantiation a launch uses (as profilers
 // print it), e.g. "tps::gemm_v2_kernel<0, 256, 256, 2, 4>".
 const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g);

@@ -141,7 +141,7 @@ GemmTile gemm_select_tile(int dtype, int layout, const GemmArgs& g) {
   if (dtype == TPS_BF16) {
     // tile-aligned path: every operand 16-byte aligned with leading dimensions
     // in whole 16-byte chunks, and an epilogue it instantiates
-    bool ok = K % (layout == TPS_GEMM_NT ? 32 : 64) == 0 && K > 0 && g.lda % 8 == 0 && g.ldb % 8 == 0 && v2_epilogue(layout, g.epi) &&
+    bool ok = K % 64 == 0 && K > 0 && g.lda % 8 == 0 && g.ldb % 8 == 0 && v2_epilogue(layout, g.epi) &&
               al16(g.A) && al16(g.B) && al16(g.C) && g.ldc % 8 == 0;
     if (g.epi == TPS_EPI_BIAS || g.epi == TPS_EPI_BIAS_RESID || g.epi == TPS_EPI_BIAS_GELU) ok = ok && al16(g.bias);
     if (g.epi == TPS_EPI_BIAS_RESID) ok = ok && al16(g.resid) && g.ldr % 8 == 0;
@@ -172,9 +172,12 @@ const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g) {
     for (int t = 0; t < 2; ++t)
       for (int l = 0; l < 3; ++l)
         for (int e = 0; e < 6; ++e)
-          snprintf(v2[t][l][e], sizeof(v2[t][l][e]), "tps::gemm_v2_kernel<%d, %s, %d, %s, %d>", l,
-                   t ? "256, 256, 2, 4" : "128, 128, 2, 2", (l == TPS_GEMM_NT && !t) ? 2 : 1,
-                   l == TPS_GEMM_NT ? "32, 4" : "64, 2", e);
+        {
+          const V2Config c = v2_config(l, t == 1);
+          const int tile = t ? 256 : 128;
+          snprintf(v2[t][l][e], sizeof(v2[t][l][e]), "tps::gemm_v2_kernel<%d, %d, %d, %d, %d, %d, %d, %d, %d>", l,
+                   tile, tile, c.wgm, c.wgn, c.ksplit, c.bk, c.stages, e);
+        }
     init = true;
   }
   const GemmTile t = gemm_select_tile(dtype, layout, g);
