@@ -331,7 +331,7 @@ static hipError_t launch_v2_epi(GemmArgs g, hipStream_t stream) {
 template <int LAYOUT>
 constexpr bool v2_has_epi(int epi) {
   return LAYOUT == TPS_GEMM_NT ? (epi == TPS_EPI_STORE || epi == TPS_EPI_BIAS || epi == TPS_EPI_BIAS_RESID ||
-                                  epi == TPS_EPI_BIAS_GELU)
+                                  epi == TPS_EPI_BIAS_GELU || epi == TPS_EPI_GELU_GRAD)
        : LAYOUT == TPS_GEMM_NN ? (epi == TPS_EPI_STORE || epi == TPS_EPI_GELU_GRAD)
                                : (epi == TPS_EPI_STORE || epi == TPS_EPI_ACC_F32);
 }
@@ -343,6 +343,7 @@ static hipError_t launch_v2(GemmArgs g, hipStream_t stream) {
       case TPS_EPI_BIAS: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS>(g, stream);
       case TPS_EPI_BIAS_RESID: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS_RESID>(g, stream);
       case TPS_EPI_BIAS_GELU: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS_GELU>(g, stream);
+      case TPS_EPI_GELU_GRAD: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_GELU_GRAD>(g, stream);
       default: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_STORE>(g, stream);
     }
   } else if constexpr (LAYOUT == TPS_GEMM_NN) {

@@ -80,5 +80,8 @@ hipError_t colsum_launch(int dtype, int rows, int cols, const void* x, int64_t l
 uint64_t colsum_ws_bytes(int64_t rows, int64_t cols);
 hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st);
 hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st);
+// out[c][r] = in[r][c] for in [rows, cols]; rows and cols multiples of 8
+hipError_t transpose_launch(int dtype, int rows, int cols, const void* in, int64_t ldi, void* out, int64_t ldo,
+                            hipStream_t st);
 
 }  // namespace tps

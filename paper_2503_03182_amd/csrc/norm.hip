@@ -212,6 +212,33 @@ __global__ __launch_bounds__(256) void gelu_kernel(const T* __restrict__ u, T* _
   }
 }
 
+// out[c][r] = in[r][c] over 64 x 64 tiles through LDS; rows, cols multiples of 8.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, int64_t ldi, T* __restrict__ out,
+                                                        int64_t ldo, int rows, int cols) {
+  constexpr int VEC = 16 / sizeof(T);
+  __shared__ T tile[64][64 + 1];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  for (int v = threadIdx.x; v < 64 * 64 / VEC; v += 256) {
+    const int r = v / (64 / VEC), c = (v % (64 / VEC)) * VEC;
+    if (r0 + r < rows && c0 + c < cols) {
+      const Vec16<T> x = load16(in + (int64_t)(r0 + r) * ldi + c0 + c);
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) tile[r][c + i] = x.get(i);
+    }
+  }
+  __syncthreads();
+  for (int v = threadIdx.x; v < 64 * 64 / VEC; v += 256) {
+    const int c = v / (64 / VEC), r = (v % (64 / VEC)) * VEC;
+    if (c0 + c < cols && r0 + r < rows) {
+      Vec16<T> y;
+#pragma unroll
+      for (int i = 0; i < VEC; ++i) y.set(i, tile[r + i][c]);
+      store16(out + (int64_t)(c0 + c) * ldo + r0 + r, y);
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void fill_zero_kernel(u32x4* p, uint64_t n16, uint8_t* tail, uint32_t ntail) {
   const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
   const uint64_t stride = (uint64_t)gridDim.x * 256;
@@ -305,6 +332,19 @@ hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t
     const int64_t blocks = (n / 4 + 255) / 256 + 1;
     hipLaunchKernelGGL((gelu_kernel<float>), dim3((unsigned)blocks), dim3(256), 0, st, (const float*)u, (float*)g, n);
   }
+  return hipGetLastError();
+}
+
+hipError_t transpose_launch(int dtype, int rows, int cols, const void* in, int64_t ldi, void* out, int64_t ldo,
+                            hipStream_t st) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  const dim3 grid((cols + 63) / 64, (rows + 63) / 64);
+  if (dtype == TPS_BF16)
+    hipLaunchKernelGGL((transpose_kernel<bf16>), grid, dim3(256), 0, st, (const bf16*)in, ldi, (bf16*)out, ldo, rows,
+                       cols);
+  else
+    hipLaunchKernelGGL((transpose_kernel<float>), grid, dim3(256), 0, st, (const float*)in, ldi, (float*)out, ldo, rows,
+                       cols);
   return hipGetLastError();
 }
 

@@ -351,13 +351,24 @@ int make_plan(const tps_config* c, Plan* out) {
   p.work_bytes = p.work.ws + p.ws_bytes;
 
   p.wwin_bytes = p.weights == TPS_W_STREAM ? (uint64_t)p.window * (p.pbytes + p.gbytes) : 0;
+  {
+    const uint64_t mats[4] = {3 * h * h, h * h, f * h, h * f};
+    uint64_t o = 0;
+    for (int i = 0; i < 4; ++i) {
+      p.wtoff[i] = o;
+      o = align256(o + mats[i] * es);
+    }
+    p.wt_bytes = o;
+    p.wt_region = (p.weights == TPS_W_STREAM ? (uint64_t)p.window : (uint64_t)p.L) * p.wt_bytes;
+  }
 
   p.off_kslots = 0;
   p.off_oslots = align256((uint64_t)p.n_kslots * p.kslot_bytes);
   p.off_replay = p.off_oslots + align256((uint64_t)p.n_oslots * p.oslot_bytes);
   p.off_work = p.off_replay + align256(p.replay_bytes);
   p.off_wwin = p.off_work + align256(p.work_bytes);
-  p.arena_bytes = p.off_wwin + p.wwin_bytes;
+  p.off_wt = p.off_wwin + align256(p.wwin_bytes);
+  p.arena_bytes = p.off_wt + p.wt_region;
   p.host_bytes = (uint64_t)p.n_host_slots * p.oslot_bytes;
 
   int n_off = 0;

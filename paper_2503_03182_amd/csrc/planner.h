@@ -65,10 +65,16 @@ struct Plan {
   uint64_t work_bytes = 0;
   uint64_t ws_bytes = 0;
 
+  // transposed weight matrices (B operands of the input-gradient GEMMs):
+  // Wqkv^T [h, 3h], Wo^T [h, h], W1^T [h, f], W2^T [f, h] per layer
+  uint64_t wtoff[4] = {}, wt_bytes = 0;
+  uint64_t wt_region = 0;   // L blocks (resident) or window blocks (streamed)
+
   // streamed weights window
   uint64_t wwin_bytes = 0;
 
   // arena
+  uint64_t off_wt = 0;
   uint64_t off_kslots = 0, off_oslots = 0, off_replay = 0, off_work = 0, off_wwin = 0;
   uint64_t arena_bytes = 0, host_bytes = 0;
 

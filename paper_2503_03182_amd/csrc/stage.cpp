@@ -52,6 +52,7 @@ struct WinEntry {
   SlotEvent param_ready;       // H2D of the parameters finished (copy stream)
   SlotEvent last_use;          // last kernel reading the entry (compute stream)
   SlotEvent grads_out;         // D2H of the grads finished (copy stream)
+  bool wt_valid = false;       // transposed copies match the parameters
   uint64_t tick = 0;
 };
 
@@ -126,6 +127,10 @@ struct tps_stage {
   // --- parameters (resident or streamed window) ------------------------------
   const char* params_of(int l, int* entry);
   float* grads_of(int l, int entry);
+  char* wt_of(int l, int entry) const {
+    return arena + p.off_wt + (uint64_t)(p.weights == TPS_W_STREAM ? entry : l) * p.wt_bytes;
+  }
+  int refresh_wt(int l, int entry);
   int ensure_layer(int l, bool for_backward, int* entry);
   int prefetch_layer(int l);
   int flush_grads(int entry);
@@ -150,7 +155,7 @@ struct tps_stage {
     return p.dtype == TPS_BF16 ? bf16_name : f32_name;
   }
   int fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots);
-  int bwd_layer(int l, int mb, const char* W, float* G, const void* dy, void* dx);
+  int bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx);
   int forward_one(int mb, const void* x, void* y);
   int backward_one(int mb, const void* dy, void* dx);
   int prefetch_mb(int mb);
@@ -173,6 +178,21 @@ const char* tps_stage::params_of(int l, int* entry) {
 float* tps_stage::grads_of(int l, int entry) {
   if (p.weights == TPS_W_RESIDENT) return lg[l];
   return reinterpret_cast<float*>(arena + p.off_wwin + (uint64_t)entry * (p.pbytes + p.gbytes) + p.pbytes);
+}
+
+// Transposed copies of the four weight matrices (operands of the input-
+// gradient GEMMs, which then read both operands K-contiguous).
+int tps_stage::refresh_wt(int l, int e) {
+  int ent = e;
+  const char* P = params_of(l, &ent);
+  char* W = wt_of(l, e);
+  const int h = p.h, f = p.f;
+  TPS_HIP(transpose_launch(p.dtype, 3 * h, h, P + p.poff[TPS_P_W_QKV], h, W + p.wtoff[0], 3 * h, cs));
+  TPS_HIP(transpose_launch(p.dtype, h, h, P + p.poff[TPS_P_W_O], h, W + p.wtoff[1], h, cs));
+  TPS_HIP(transpose_launch(p.dtype, f, h, P + p.poff[TPS_P_W_1], h, W + p.wtoff[2], f, cs));
+  TPS_HIP(transpose_launch(p.dtype, h, f, P + p.poff[TPS_P_W_2], f, W + p.wtoff[3], h, cs));
+  stats.kernels += 4;
+  return TPS_OK;
 }
 
 int tps_stage::flush_grads(int e) {
@@ -209,6 +229,7 @@ int tps_stage::prefetch_layer(int l) {
   if (w.last_use.valid) TPS_HIP(hipStreamWaitEvent(xs, w.last_use.ev, 0));
   w.layer = l;
   w.tick = ++tick;
+  w.wt_valid = false;
   int e = victim;
   TPS_HIP(hipMemcpyAsync(const_cast<char*>(params_of(l, &e)), lp[l], p.pbytes, hipMemcpyHostToDevice, xs));
   stats.h2d_bytes += p.pbytes;
@@ -227,6 +248,10 @@ int tps_stage::ensure_layer(int l, bool for_backward, int* entry) {
   WinEntry& w = win[e];
   w.tick = ++tick;
   TPS_HIP(hipStreamWaitEvent(cs, w.param_ready.ev, 0));
+  if (for_backward && !w.wt_valid) {
+    TPS_TRY(refresh_wt(l, e));
+    w.wt_valid = true;
+  }
   if (for_backward && !w.grads_live) {
     // the grad block of this entry may still be leaving for another layer
     if (w.grads_out.valid) TPS_HIP(hipStreamWaitEvent(cs, w.grads_out.ev, 0));
@@ -360,7 +385,7 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
 // ---------------------------------------------------------------------------
 // One layer backward; parameter gradients accumulate into G (f32).
 // ---------------------------------------------------------------------------
-int tps_stage::bwd_layer(int l, int mb, const char* W, float* G, const void* dy, void* dx) {
+int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx) {
   const int T = p.T, h = p.h, f = p.f;
   auto ptr = [&](int t) { return tensor(l, t, mb, true); };
   auto par = [&](int i) { return W + p.poff[i]; };
@@ -393,17 +418,22 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, float* G, const void* dy,
     return kend(k);
   };
   // MLP: y = x1 + GeLU(c W1^T + b1) W2^T + b2
-  TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_GELU_GRAD, T, f, h, dy, h, par(TPS_P_W_2), f, du, f, nullptr, nullptr, 0, u, f));
+  // input gradients as NT products against the transposed weights
+  const char* w2t = WT + p.wtoff[3];   // [f, h]
+  const char* w1t = WT + p.wtoff[2];   // [h, f]
+  const char* wot = WT + p.wtoff[1];   // [h, h]
+  const char* wqt = WT + p.wtoff[0];   // [h, 3h]
+  TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_GELU_GRAD, T, f, h, dy, h, w2t, h, du, f, nullptr, nullptr, 0, u, f));
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f));
   TPS_TRY(colsum(dy, h, grd(TPS_P_B_2)));
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h));
   TPS_TRY(colsum(du, f, grd(TPS_P_B_1)));
-  TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, f, du, f, par(TPS_P_W_1), h, t1, h));
+  TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, f, du, f, w1t, f, t1, h));
   TPS_TRY(lnbwd(t1, x1, ln2, TPS_P_G2, TPS_P_BE2, dy, dx1));
   // attention block: x1 = x + o Wo^T + bo
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h));
   TPS_TRY(colsum(dx1, h, grd(TPS_P_B_O)));
-  TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, h, dx1, h, par(TPS_P_W_O), h, t1, h));
+  TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, h, dx1, h, wot, h, t1, h));
   {
     ++stats.kernels;
     const int k = kbegin("attention backward (3 kernels)", 4.0 * p.b * h * (double)p.s * (p.s + 1), 9.0 * T * h * es);
@@ -412,7 +442,7 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, float* G, const void* dy,
   }
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h));
   TPS_TRY(colsum(dqkv, 3 * h, grd(TPS_P_B_QKV)));
-  TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, h, 3 * h, dqkv, 3 * h, par(TPS_P_W_QKV), h, t1, h));
+  TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, 3 * h, dqkv, 3 * h, wqt, 3 * h, t1, h));
   TPS_TRY(lnbwd(t1, x, ln1, TPS_P_G1, TPS_P_BE1, dx1, dx));
   return TPS_OK;
 }
@@ -533,7 +563,7 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
       ++stats.replays;
     }
     void* out = (l == 0) ? dx : (cur == gA ? gB : gA);
-    TPS_TRY(bwd_layer(l, mb, W, grads_of(l, e), cur, out));
+    TPS_TRY(bwd_layer(l, mb, W, wt_of(l, e), grads_of(l, e), cur, out));
     if (e >= 0) {
       TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
       win[e].last_use.valid = true;
@@ -629,11 +659,18 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
     int rc = st->flush_all_grads();
     if (rc) return rc;
     std::fill(st->grads_touched.begin(), st->grads_touched.end(), zero_grads ? 0 : 1);
-  } else if (zero_grads) {
+  } else {
+    if (zero_grads) {
+      for (int l = 0; l < p.L; ++l) {
+        hipError_t e = fill_zero_launch(st->lg[l], p.gbytes, st->cs);
+        if (e != hipSuccess) return check_hip(e, "zero grads");
+        ++st->stats.kernels;
+      }
+    }
+    // parameters may have changed since the last iteration
     for (int l = 0; l < p.L; ++l) {
-      hipError_t e = fill_zero_launch(st->lg[l], p.gbytes, st->cs);
-      if (e != hipSuccess) return check_hip(e, "zero grads");
-      ++st->stats.kernels;
+      int rc = st->refresh_wt(l, -1);
+      if (rc) return rc;
     }
   }
   st->in_iteration = true;
@@ -771,7 +808,7 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
       }
       // the running gradient of micro-batch i lives in dx[i] between layers
       const void* in = (l == p.L - 1) ? dy[i] : dx[i];
-      TPS_TRY(st->bwd_layer(l, mb, W, st->grads_of(l, e), in, gA));
+      TPS_TRY(st->bwd_layer(l, mb, W, st->wt_of(l, e), st->grads_of(l, e), in, gA));
       TPS_HIP(hipMemcpyAsync(dx[i], gA, p.tbytes[TPS_T_X], hipMemcpyDeviceToDevice, st->cs));
     }
     if (e >= 0) {
