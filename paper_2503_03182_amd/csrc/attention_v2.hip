@@ -8,8 +8,9 @@
 // n+1 tiles of work and every workgroup the same amount.
 //
 // Data movement.  Key/value (or query/output-gradient) tiles of 64 rows are
-// copied global -> LDS with direct-to-LDS loads in their natural [row][d]
-// layout, double buffered: tile t+1 is in flight while tile t is used.  16-byte
+// staged in LDS in their natural [row][d] layout, double buffered: tile t+1 is
+// loaded into registers while tile t is used and written to the other stage
+// afterwards, with one barrier per tile.  16-byte
 // chunks are XOR-swizzled per row so that both access patterns are free of
 // bank conflicts:
 //   ds_read_b128 (16 rows, one chunk): an MFMA operand with d contiguous;
@@ -30,7 +31,6 @@ namespace tps {
 
 namespace av2 {
 
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((ext_vector_type(4))) short s16x4;
 typedef __attribute__((ext_vector_type(8))) short s16x8;
 
@@ -57,29 +57,32 @@ __device__ __forceinline__ int swz(int r) {
 template <int D>
 __device__ __forceinline__ int off(int r, int c) { return r * (D * 2) + ((c ^ swz<D>(r)) << 4); }
 
-// Direct-to-LDS loads of rows row0..row0+63 (clamped to nrows-1; callers mask
-// the clamped rows) of a [rows][ld] bf16 matrix starting at g, D columns.
+// Tile of rows row0..row0+63 (clamped to nrows-1; callers mask the clamped
+// rows) of a [rows][ld] bf16 matrix starting at g, D columns, staged through
+// registers: load() issues the global loads, store() writes the swizzled LDS
+// tile.  Wave w moves 1 KB slots w, w+8, ...; lane l the 16 bytes at l * 16.
 template <int D>
-__device__ __forceinline__ void issue(const bf16* g, int64_t ld, int row0, int nrows, char* lds) {
-  constexpr int CPR = D / 8, INST = BT * CPR / 64;   // wave instructions per tile
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+struct TileRegs {
+  static constexpr int CPR = D / 8, INST = BT * CPR / 64, N = (INST + 7) / 8;
+  u32x4 v[N];
+  __device__ __forceinline__ void load(const bf16* g, int64_t ld, int row0, int nrows) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int i = wave; i < INST; i += 8) {
-    const int slot = i * 64 + lane;
-    const int r = slot / CPR, p = slot % CPR;
-    const int c = p ^ swz<D>(r);
-    const int row = min(row0 + r, nrows - 1);
-    __builtin_amdgcn_global_load_lds((const void*)(g + (int64_t)row * ld + c * 8), (lds_void*)(lds + i * 1024), 16, 0,
-                                     0);
+    for (int n = 0; n < N; ++n) {
+      const int slot = (wave + 8 * n) * 64 + lane;
+      const int r = slot / CPR, p = slot % CPR;
+      const int c = p ^ swz<D>(r);
+      const int row = min(row0 + r, nrows - 1);
+      v[n] = *reinterpret_cast<const u32x4*>(g + (int64_t)row * ld + c * 8);
+    }
   }
-}
-template <int D>
-constexpr int issue_count() { return (BT * D / 8 / 64 + 7) / 8; }   // per thread, per tile
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
+  __device__ __forceinline__ void store(char* lds) const {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int n = 0; n < N; ++n) *reinterpret_cast<u32x4*>(lds + (wave + 8 * n) * 1024 + lane * 16) = v[n];
+  }
+};
+static_assert(TileRegs<64>::INST == 8 && TileRegs<128>::INST == 16, "every wave moves whole slots");
 
 // Operand with d contiguous: rows rbase + (l % 16), d = 32 ks + 8 (l / 16) .. +8.
 template <int D>
@@ -115,6 +118,11 @@ __device__ __forceinline__ bf16x8 frag_acc(const float* lo, const float* hi) {
   return f;
 }
 
+// Consume a value before the tile loop: the wait for its global load is
+// placed here, so no wait inside the loop has to drain the tile loads
+// issued after it.
+__device__ __forceinline__ void settle(const bf16x8& v) { asm volatile("" ::"v"(v)); }
+
 __device__ __forceinline__ bf16x8 load_row_frag(const bf16* p) {
   u32x4 w = *reinterpret_cast<const u32x4*>(p);
   return *reinterpret_cast<bf16x8*>(&w);
@@ -148,7 +156,6 @@ void attn_fwd_v2_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
                         int nh, float scale) {
   using namespace av2;
   constexpr int TILE = BT * D * 2, STAGE = 2 * TILE, NKS = D / 32, NDT = D / 16;
-  constexpr int LOADS = 2 * issue_count<D>();
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int H = nh * D;
@@ -170,6 +177,8 @@ void attn_fwd_v2_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
     const int qq = min(q, s - 1);
     qf[ks] = load_row_frag(base + (int64_t)qq * ld + pr.head * D + ks * 32 + G * 8);
   }
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) settle(qf[ks]);
   f32x4 oacc[NDT];
 #pragma unroll
   for (int t = 0; t < NDT; ++t) oacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -177,18 +186,19 @@ void attn_fwd_v2_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
   const float sl2 = scale * kLog2e;
 
   const int ntile = pr.jB + 1;   // the longer block of the pair sets the loop length
-  issue<D>(Kg, ld, 0, s, smem);
-  issue<D>(Vg, ld, 0, s, smem + TILE);
+  // tile t+1 is loaded into registers while tile t is used, then written to
+  // the other LDS stage (last read in iteration t-1, before its barrier)
+  TileRegs<D> kr, vr;
+  kr.load(Kg, ld, 0, s);
+  vr.load(Vg, ld, 0, s);
+  kr.store(smem);
+  vr.store(smem + TILE);
+  __syncthreads();
   for (int t = 0; t < ntile; ++t) {
     if (t + 1 < ntile) {
-      char* nxt = smem + ((t + 1) & 1) * STAGE;
-      issue<D>(Kg, ld, (t + 1) * BT, s, nxt);
-      issue<D>(Vg, ld, (t + 1) * BT, s, nxt + TILE);
-      wait_vmcnt<LOADS>();
-    } else {
-      wait_vmcnt<0>();
+      kr.load(Kg, ld, (t + 1) * BT, s);
+      vr.load(Vg, ld, (t + 1) * BT, s);
     }
-    __syncthreads();
     if (active && t <= jblk) {
       const char* ks_lds = smem + (t & 1) * STAGE;
       const char* vs_lds = ks_lds + TILE;
@@ -241,6 +251,10 @@ void attn_fwd_v2_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
         for (int dt = 0; dt < NDT; ++dt) oacc[dt] = mma(frag_cols<D>(vs_lds, 32 * kc, dt * 16, lane), pb, oacc[dt]);
       }
     }
+    if (t + 1 < ntile) {
+      kr.store(smem + ((t + 1) & 1) * STAGE);
+      vr.store(smem + ((t + 1) & 1) * STAGE + TILE);
+    }
     __syncthreads();
   }
   float l_tot = l_run + __shfl_xor(l_run, 16, kWave);
@@ -271,7 +285,6 @@ void attn_bwd_dkdv_v2_kernel(const bf16* __restrict__ qkv, const bf16* __restric
                              int b, int s, int nh, float scale) {
   using namespace av2;
   constexpr int TILE = BT * D * 2, STAGE = 2 * TILE + 2 * BT * 4, NKS = D / 32, NDT = D / 16;
-  constexpr int LOADS = 2 * issue_count<D>();
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int H = nh * D;
@@ -296,6 +309,11 @@ void attn_bwd_dkdv_v2_kernel(const bf16* __restrict__ qkv, const bf16* __restric
       kf[ks] = load_row_frag(base + (int64_t)kk * ld + H + pr.head * D + ks * 32 + G * 8);
       vf[ks] = load_row_frag(base + (int64_t)kk * ld + 2 * H + pr.head * D + ks * 32 + G * 8);
     }
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      settle(kf[ks]);
+      settle(vf[ks]);
+    }
   }
   f32x4 dk[NDT], dv[NDT];
 #pragma unroll
@@ -304,27 +322,38 @@ void attn_bwd_dkdv_v2_kernel(const bf16* __restrict__ qkv, const bf16* __restric
 
   // query tiles from the earlier block of the pair to the end
   const int t0 = pr.jA;
-  auto stage_tile = [&](int t, char* st) {
-    issue<D>(Qg, ld, t * BT, s, st);
-    issue<D>(dOg, H, t * BT, s, st + TILE);
+  // query tile t+1 (Q, dO and its lse / D entries) is loaded into registers
+  // while tile t is used, then written to the other LDS stage
+  TileRegs<D> qr, dr;
+  // (lse and D are read raw and transformed at the store, so the load of
+  // tile t+1 is not waited for before tile t's work)
+  float lse_r = 0.f, dv_r = 0.f;
+  auto load_tile = [&](int t) {
+    qr.load(Qg, ld, t * BT, s);
+    dr.load(dOg, H, t * BT, s);
+    if (threadIdx.x < BT) {
+      const int qq = min(t * BT + (int)threadIdx.x, s - 1);
+      lse_r = lse_g[qq];
+      dv_r = dv_g[qq];
+    }
   };
-  stage_tile(t0, smem);
+  auto store_tile = [&](int t, char* st) {
+    qr.store(st);
+    dr.store(st + TILE);
+    if (threadIdx.x < BT) {
+      const bool in = t * BT + (int)threadIdx.x < s;
+      reinterpret_cast<float*>(st + 2 * TILE)[threadIdx.x] = in ? lse_r * kLog2e : INFINITY;
+      reinterpret_cast<float*>(st + 2 * TILE)[BT + threadIdx.x] = in ? dv_r : 0.f;
+    }
+  };
+  load_tile(t0);
+  store_tile(t0, smem);
+  __syncthreads();
   for (int t = t0; t < nblk; ++t) {
     char* cur = smem + ((t - t0) & 1) * STAGE;
-    float* lse_s = reinterpret_cast<float*>(cur + 2 * TILE);
-    float* dv_s = lse_s + BT;
-    if (threadIdx.x < BT) {
-      const int qq = t * BT + threadIdx.x;
-      lse_s[threadIdx.x] = (qq < s) ? lse_g[qq] * kLog2e : INFINITY;
-      dv_s[threadIdx.x] = (qq < s) ? dv_g[qq] : 0.f;
-    }
-    if (t + 1 < nblk) {
-      stage_tile(t + 1, smem + ((t + 1 - t0) & 1) * STAGE);
-      wait_vmcnt<LOADS>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    __syncthreads();
+    const float* lse_s = reinterpret_cast<const float*>(cur + 2 * TILE);
+    const float* dv_s = lse_s + BT;
+    if (t + 1 < nblk) load_tile(t + 1);
     if (active && t >= jblk) {
       const char* qs_lds = cur;
       const char* ds_lds = cur + TILE;
@@ -357,6 +386,7 @@ void attn_bwd_dkdv_v2_kernel(const bf16* __restrict__ qkv, const bf16* __restric
         }
       }
     }
+    if (t + 1 < nblk) store_tile(t + 1, smem + ((t + 1 - t0) & 1) * STAGE);
     __syncthreads();
   }
   if (active && key < s) {
@@ -387,7 +417,6 @@ void attn_bwd_dq_v2_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
                            int b, int s, int nh, float scale) {
   using namespace av2;
   constexpr int TILE = BT * D * 2, STAGE = 2 * TILE, NKS = D / 32, NDT = D / 16;
-  constexpr int LOADS = 2 * issue_count<D>();
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int H = nh * D;
@@ -411,6 +440,11 @@ void attn_bwd_dq_v2_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
       qf[ks] = load_row_frag(base + (int64_t)qq * ld + pr.head * D + ks * 32 + G * 8);
       df[ks] = load_row_frag(dOg + (int64_t)qq * H + ks * 32 + G * 8);
     }
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      settle(qf[ks]);
+      settle(df[ks]);
+    }
   }
   const float sl2 = scale * kLog2e;
   const float lse2 = (q < s) ? lse[((int64_t)pr.batch * nh + pr.head) * s + q] * kLog2e : INFINITY;
@@ -420,18 +454,19 @@ void attn_bwd_dq_v2_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
   for (int t = 0; t < NDT; ++t) dq[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int ntile = pr.jB + 1;
-  issue<D>(Kg, ld, 0, s, smem);
-  issue<D>(Vg, ld, 0, s, smem + TILE);
+  // tile t+1 is loaded into registers while tile t is used, then written to
+  // the other LDS stage (last read in iteration t-1, before its barrier)
+  TileRegs<D> kr, vr;
+  kr.load(Kg, ld, 0, s);
+  vr.load(Vg, ld, 0, s);
+  kr.store(smem);
+  vr.store(smem + TILE);
+  __syncthreads();
   for (int t = 0; t < ntile; ++t) {
     if (t + 1 < ntile) {
-      char* nxt = smem + ((t + 1) & 1) * STAGE;
-      issue<D>(Kg, ld, (t + 1) * BT, s, nxt);
-      issue<D>(Vg, ld, (t + 1) * BT, s, nxt + TILE);
-      wait_vmcnt<LOADS>();
-    } else {
-      wait_vmcnt<0>();
+      kr.load(Kg, ld, (t + 1) * BT, s);
+      vr.load(Vg, ld, (t + 1) * BT, s);
     }
-    __syncthreads();
     if (active && t <= jblk) {
       const char* ks_lds = smem + (t & 1) * STAGE;
       const char* vs_lds = ks_lds + TILE;
@@ -458,6 +493,10 @@ void attn_bwd_dq_v2_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) dq[dt] = mma(frag_cols<D>(ks_lds, 32 * kc, dt * 16, lane), sb, dq[dt]);
       }
+    }
+    if (t + 1 < ntile) {
+      kr.store(smem + ((t + 1) & 1) * STAGE);
+      vr.store(smem + ((t + 1) & 1) * STAGE + TILE);
     }
     __syncthreads();
   }

@@ -17,6 +17,8 @@
 // sums are added in a fixed order at the end (two waves per SIMD on small
 // grids).  Within each wave the K loop is sequential in steps of 16.
 #pragma once
+#include <utility>
+
 #include "kernels.h"
 #include "tps_device.h"
 
@@ -79,26 +81,105 @@ __device__ __forceinline__ void issue_tile(const bf16* g, int64_t ld, int row0, 
   }
 }
 
-// MFMA fragment (8 consecutive k of one row / column) for k-step ks.
-template <int ROWS, bool KC, int BK>
-__device__ __forceinline__ bf16x8 frag(const char* lds, int row_base, int ks, int lane) {
+// LDS fragment reads are issued as inline assembly.  The compiler orders
+// every LDS read it can see after all outstanding direct-to-LDS loads
+// (s_waitcnt vmcnt(0)), which would drain the load pipeline once per K tile;
+// reads it cannot see are ordered by the explicit lgkmcnt / vmcnt waits and
+// barriers below instead.
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
+template <int OFF>
+__device__ __forceinline__ bf16x8 ds_b128(uint32_t a) {
+  bf16x8 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(OFF));
+  return v;
+}
+template <int OFF>
+__device__ __forceinline__ s16x4 ds_tr16(uint32_t a) {
+  s16x4 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(OFF));
+  return v;
+}
+// Wait until at most N LDS reads are outstanding (LDS reads complete in
+// issue order; no scalar loads are in flight inside the K loop).
+template <int N>
+__device__ __forceinline__ void wait_lgkm() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+// The value is not consumed before this point (pins uses after a wait).
+__device__ __forceinline__ void pin(bf16x8& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Per-lane LDS byte offsets of the fragments a wave reads from one stage,
+// for the KSW k-steps of 16 starting at k-step ks0 of the tile.
+//   K-contiguous: fragment i (row block i) of k-step ks sits at
+//     row (row_base + 32 i + lane % 32), chunk 2 ks + lane / 32; the row swizzle
+//     repeats every 32 rows, so only the chunk term depends on ks:
+//     off(i, ks) = base[ks] + 4096 i (BK = 64) or 2048 i (BK = 32).
+//   M/N-contiguous: fragment j of k-step ks is two transposing reads at
+//     k rows (16 ks + 8 (g / 2) + s / 4) and 4 further; the column swizzle
+//     depends on k mod 4 only, so off(j, ks) = base[j] + 16 (ks - ks0) ROWB.
+template <int ROWS, bool KC, int BK, int NF, int KSW>
+struct FragAddr {
+  uint32_t base[KC ? KSW : NF];
+  __device__ __forceinline__ void init(int row_base, int ks0, int lane) {
+    if constexpr (KC) {
+      const int r = row_base + (lane & 31);
+#pragma unroll
+      for (int kk = 0; kk < KSW; ++kk) base[kk] = kc_off<BK>(r, (ks0 + kk) * 2 + (lane >> 5));
+    } else {
+      constexpr int ROWB = ROWS * 2;
+      const int g = lane >> 4, s = lane & 15;
+      const int k = 16 * ks0 + ((g >> 1) << 3) + (s >> 2);
+#pragma unroll
+      for (int j = 0; j < NF; ++j) {
+        const int col = row_base + 32 * j + ((g & 1) << 4) + ((s & 3) << 2);
+        base[j] = mc_off<ROWB>(k, col >> 3) + (col & 7) * 2;
+      }
+    }
+  }
+};
+
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time.
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// LDS reads per fragment set (each transposed fragment takes two reads).
+template <bool KC, int NF>
+constexpr int frag_reads() { return KC ? NF : 2 * NF; }
+
+// Issue the LDS reads of the NF fragments of the wave's k-step KK from the
+// stage at LDS byte address `stage`.
+template <int ROWS, bool KC, int BK, int NF, int KSW, int KK>
+__device__ __forceinline__ void read_frags(bf16x8 (&f)[NF], const FragAddr<ROWS, KC, BK, NF, KSW>& a,
+                                           uint32_t stage) {
   if constexpr (KC) {
-    const int r = row_base + (lane & 31);
-    const int c = ks * 2 + (lane >> 5);
-    return *reinterpret_cast<const bf16x8*>(lds + kc_off<BK>(r, c));
+    constexpr int RS = BK * 64;   // bytes between row blocks of 32
+    const uint32_t p = stage + a.base[KK];
+    if constexpr (NF > 0) f[0] = ds_b128<0>(p);
+    if constexpr (NF > 1) f[1] = ds_b128<RS>(p);
+    if constexpr (NF > 2) f[2] = ds_b128<2 * RS>(p);
+    if constexpr (NF > 3) f[3] = ds_b128<3 * RS>(p);
+    static_assert(NF <= 4, "fragments per k-step");
   } else {
     constexpr int ROWB = ROWS * 2;
-    const int g = lane >> 4, s = lane & 15;
-    const int col = row_base + ((g & 1) << 4) + ((s & 3) << 2);   // m (or n) this lane addresses
-    const int k = ks * 16 + ((g >> 1) << 3) + (s >> 2);
-    const int c = col >> 3, within = (col & 7) * 2;
-    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (__attribute__((address_space(3))) s16x4*)(lds + mc_off<ROWB>(k, c) + within));
-    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (__attribute__((address_space(3))) s16x4*)(lds + mc_off<ROWB>(k + 4, c) + within));
     typedef __attribute__((ext_vector_type(8))) short s16x8;
-    s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    return *reinterpret_cast<bf16x8*>(&v);
+#pragma unroll
+    for (int j = 0; j < NF; ++j) {
+      const uint32_t p = stage + a.base[j];
+      const s16x4 lo = ds_tr16<16 * KK * ROWB>(p);
+      const s16x4 hi = ds_tr16<16 * KK * ROWB + 4 * ROWB>(p);
+      s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      f[j] = *reinterpret_cast<bf16x8*>(&v);
+    }
   }
 }
 
@@ -145,28 +226,44 @@ void gemm_v2_kernel(GemmArgs g) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = g.K / BK;
+  FragAddr<BM, A_KC, BK, TM, KS> fra;
+  FragAddr<BN, B_KC, BK, TN, KS> frb;
+  fra.init(wm * WM, wk * KS, lane);
+  frb.init(wn * WN, wk * KS, lane);
+  const uint32_t lds0 = lds_u32(smem);
   // fragments of k-step kk+1 are read while the MFMAs of k-step kk run
-  auto mma_tile = [&](const char* as) {
-    const char* bs = as + A_BYTES;
+  auto mma_tile = [&](uint32_t as) {
+    constexpr int RA = frag_reads<A_KC, TM>(), RB = frag_reads<B_KC, TN>();
+    static_assert(RA <= 15 && RB <= 15, "lgkmcnt range");
+    const uint32_t bs = as + A_BYTES;
     bf16x8 fa[2][TM], fb[2][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) fa[0][i] = frag<BM, A_KC, BK>(as, wm * WM + i * 32, wk * KS, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) fb[0][j] = frag<BN, B_KC, BK>(bs, wn * WN + j * 32, wk * KS, lane);
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < KS) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i) fa[cur ^ 1][i] = frag<BM, A_KC, BK>(as, wm * WM + i * 32, wk * KS + kk + 1, lane);
-#pragma unroll
-        for (int j = 0; j < TN; ++j) fb[cur ^ 1][j] = frag<BN, B_KC, BK>(bs, wn * WN + j * 32, wk * KS + kk + 1, lane);
+    read_frags<BM, A_KC, BK, TM, KS, 0>(fa[0], fra, as);
+    read_frags<BN, B_KC, BK, TN, KS, 0>(fb[0], frb, bs);
+    static_for<KS>([&](auto kc) {
+      constexpr int kk = decltype(kc)::value, cur = kk & 1;
+      if constexpr (kk + 1 < KS) {
+        read_frags<BM, A_KC, BK, TM, KS, kk + 1>(fa[cur ^ 1], fra, as);
+        if constexpr (RA + RB <= 15) {
+          read_frags<BN, B_KC, BK, TN, KS, kk + 1>(fb[cur ^ 1], frb, bs);
+          wait_lgkm<RA + RB>();
+        } else {
+          wait_lgkm<RA>();
+          read_frags<BN, B_KC, BK, TN, KS, kk + 1>(fb[cur ^ 1], frb, bs);
+        }
+      } else {
+        wait_lgkm<0>();
       }
+#pragma unroll
+      for (int i = 0; i < TM; ++i) pin(fa[cur][i]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) pin(fb[cur][j]);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = Mma<bf16>::run(fa[cur][i], fb[cur][j], acc[i][j]);
-    }
+      // keep the k-steps in program order (reads of kk+1 ahead of MFMAs of kk)
+      __builtin_amdgcn_sched_barrier(0);
+    });
   };
   if constexpr (STAGES == 2) {
     // tile k+1 in flight while tile k is multiplied; a second barrier keeps
@@ -182,9 +279,9 @@ void gemm_v2_kernel(GemmArgs g) {
       } else {
         wait_vmcnt<0>();
       }
-      __syncthreads();
-      mma_tile(smem + (kt & 1) * STAGE);
-      __syncthreads();
+      lds_barrier();
+      mma_tile(lds0 + (kt & 1) * STAGE);
+      lds_barrier();
     }
   } else {
     // prologue: tiles 0 .. STAGES-2 in flight
@@ -206,15 +303,15 @@ void gemm_v2_kernel(GemmArgs g) {
         if (ahead >= 1) wait_vmcnt<LOADS>();
         else wait_vmcnt<0>();
       }
-      __syncthreads();
-      // the stage refilled here was last read in iteration kt - 1, which every
-      // wave finished before the barrier above
+      // every wave's share of tile kt is in LDS, and every wave has finished
+      // reading the stage refilled below (tile kt - 1, read in iteration kt - 1)
+      lds_barrier();
       if (kt + STAGES - 1 < nk) {
         char* nxt = smem + ((kt + STAGES - 1) % STAGES) * STAGE;
         issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, (kt + STAGES - 1) * BK, nxt);
         issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, (kt + STAGES - 1) * BK, nxt + A_BYTES);
       }
-      mma_tile(smem + (kt % STAGES) * STAGE);
+      mma_tile(lds0 + (kt % STAGES) * STAGE);
     }
   }
   __syncthreads();   // LDS is reused below
