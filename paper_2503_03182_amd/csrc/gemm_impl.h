@@ -16,7 +16,7 @@
 // results depend only on (M, N, K) and the data.
 #pragma once
 #include <type_traits>
-#include "gemm_v2.h"
+#include "gemm_pipe.h"
 #include "kernels.h"
 #include "tps_device.h"
 
@@ -249,9 +249,9 @@ static hipError_t launch_tile(GemmArgs g, hipStream_t stream) {
 template <int LAYOUT>
 static hipError_t launch_layout(int dtype, GemmArgs g, hipStream_t stream) {
   const GemmTile t = gemm_select_tile(dtype, LAYOUT, g);
-  if (t.v2) {
-    if (t.bm == 256) return launch_v2<LAYOUT, 256, 256>(g, stream);
-    return launch_v2<LAYOUT, 128, 128>(g, stream);
+  if (t.aligned) {
+    if (t.bm == 256) return launch_pipe<LAYOUT, 256, 256>(g, stream);
+    return launch_pipe<LAYOUT, 128, 128>(g, stream);
   }
   if (dtype == TPS_BF16) {
     if (t.bm == 256) return launch_tile<bf16, 256, 128, 64, LAYOUT>(g, stream);

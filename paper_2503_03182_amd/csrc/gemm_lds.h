@@ -1,21 +1,18 @@
-// bf16 GEMM main path for tile-aligned shapes (M % BM, N % BN, K % 64 == 0).
+// Building blocks of the bf16 GEMMs on gfx950 (gemm_pipe.h):
 //
-// Operand tiles are copied global -> LDS with direct-to-LDS loads (each lane's
-// 16 bytes land at LDS base + 16 * lane), in their natural memory layout:
-//   K-contiguous operand (A of NT/NN, B of NT): [rows][64] bf16, 128-byte rows;
-//   M/N-contiguous operand (A of TN, B of NN/TN): [64][rows] bf16.
+// LDS tile layouts.  Operand tiles are stored in their natural memory layout:
+//   K-contiguous operand (A of NT/NN, B of NT): [rows][BK] bf16;
+//   M/N-contiguous operand (A of TN, B of NN/TN): [BK][rows] bf16.
 // 16-byte chunks are XOR-swizzled within a row (the global address of each
 // lane is permuted so the chunk lands at its swizzled slot), which keeps the
 // fragment reads free of LDS bank conflicts:
 //   K-contiguous: ds_read_b128 gives a lane 8 consecutive k of one row;
-//   M/N-contiguous: two ds_read_tr16_b64 give a lane 8 consecutive k of one
+//   M/N-contiguous: two ds_read_b64_tr_b16 give a lane 8 consecutive k of one
 //   column (the read transposes 4 x 4 blocks of 16-bit values across lanes).
-// STAGES LDS stages hold consecutive K tiles: STAGES-1 tiles are in flight
-// while one is multiplied, with one barrier per tile.  Waves own a
-// (BM/WGM) x (BN/WGN) block of 32x32x16 MFMA tiles; with KSPLIT = 2 a second
-// group of waves takes the upper half of every K tile and the two partial
-// sums are added in a fixed order at the end (two waves per SIMD on small
-// grids).  Within each wave the K loop is sequential in steps of 16.
+//
+// Fragment reads are issued as inline assembly with explicit waits (see
+// below), and the epilogue parks accumulators in LDS to apply bias /
+// residual / GeLU / GeLU' / f32 accumulation with 16-byte accesses.
 #pragma once
 #include <utility>
 
@@ -24,7 +21,7 @@
 
 namespace tps {
 
-namespace v2 {
+namespace gl {
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((ext_vector_type(4))) short s16x4;
@@ -183,169 +180,18 @@ __device__ __forceinline__ void read_frags(bf16x8 (&f)[NF], const FragAddr<ROWS,
   }
 }
 
-}  // namespace v2
+}  // namespace gl
 
-template <int LAYOUT, int BM, int BN, int WGM, int WGN, int KSPLIT, int BK, int STAGES, int EPI>
-__global__ __attribute__((amdgpu_flat_work_group_size(64 * WGM * WGN * KSPLIT, 64 * WGM * WGN * KSPLIT),
-                          amdgpu_waves_per_eu(WGM * WGN * KSPLIT >= 8 ? 2 : 1, WGM * WGN * KSPLIT >= 8 ? 2 : 1)))
-void gemm_v2_kernel(GemmArgs g) {
-  using namespace v2;
-  constexpr int NT = 64 * WGM * WGN * KSPLIT;
-  constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
-  constexpr int KS = BK / 16 / KSPLIT;   // k-steps of 16 per wave per tile
-  constexpr bool A_KC = (LAYOUT != TPS_GEMM_TN);
-  constexpr bool B_KC = (LAYOUT == TPS_GEMM_NT);
-  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2, STAGE = A_BYTES + B_BYTES;
-  constexpr int LOADS = (A_BYTES + B_BYTES) / 1024 / (NT / 64);   // per thread per tile
-  static_assert(KS >= 1 && STAGES >= 2, "pipeline shape");
-  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
-
-  const int nblk = g.tiles_m * g.tiles_n;
-  int pid = blockIdx.x;
-  if ((nblk & 7) == 0) pid = (pid & 7) * (nblk >> 3) + (pid >> 3);
-  constexpr int GROUP = 8;
-  const int group = pid / (GROUP * g.tiles_n);
-  const int first_m = group * GROUP;
-  const int gm = min(GROUP, g.tiles_m - first_m);
-  const int tile_m = first_m + (pid % (GROUP * g.tiles_n)) % gm;
-  const int tile_n = (pid % (GROUP * g.tiles_n)) / gm;
-  const int m0 = tile_m * BM, n0 = tile_n * BN;
-
-  const bf16* A = static_cast<const bf16*>(g.A);
-  const bf16* B = static_cast<const bf16*>(g.B);
-  const int lane = threadIdx.x & 63, wave_all = threadIdx.x >> 6;
-  const int wk = wave_all / (WGM * WGN), wave = wave_all % (WGM * WGN);
-  const int wm = wave / WGN, wn = wave % WGN;
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  const int nk = g.K / BK;
-  FragAddr<BM, A_KC, BK, TM, KS> fra;
-  FragAddr<BN, B_KC, BK, TN, KS> frb;
-  fra.init(wm * WM, wk * KS, lane);
-  frb.init(wn * WN, wk * KS, lane);
-  const uint32_t lds0 = lds_u32(smem);
-  // fragments of k-step kk+1 are read while the MFMAs of k-step kk run
-  auto mma_tile = [&](uint32_t as) {
-    constexpr int RA = frag_reads<A_KC, TM>(), RB = frag_reads<B_KC, TN>();
-    static_assert(RA <= 15 && RB <= 15, "lgkmcnt range");
-    const uint32_t bs = as + A_BYTES;
-    bf16x8 fa[2][TM], fb[2][TN];
-    read_frags<BM, A_KC, BK, TM, KS, 0>(fa[0], fra, as);
-    read_frags<BN, B_KC, BK, TN, KS, 0>(fb[0], frb, bs);
-    static_for<KS>([&](auto kc) {
-      constexpr int kk = decltype(kc)::value, cur = kk & 1;
-      if constexpr (kk + 1 < KS) {
-        read_frags<BM, A_KC, BK, TM, KS, kk + 1>(fa[cur ^ 1], fra, as);
-        if constexpr (RA + RB <= 15) {
-          read_frags<BN, B_KC, BK, TN, KS, kk + 1>(fb[cur ^ 1], frb, bs);
-          wait_lgkm<RA + RB>();
-        } else {
-          wait_lgkm<RA>();
-          read_frags<BN, B_KC, BK, TN, KS, kk + 1>(fb[cur ^ 1], frb, bs);
-        }
-      } else {
-        wait_lgkm<0>();
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i) pin(fa[cur][i]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) pin(fb[cur][j]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = Mma<bf16>::run(fa[cur][i], fb[cur][j], acc[i][j]);
-      // keep the k-steps in program order (reads of kk+1 ahead of MFMAs of kk)
-      __builtin_amdgcn_sched_barrier(0);
-    });
-  };
-  if constexpr (STAGES == 2) {
-    // tile k+1 in flight while tile k is multiplied; a second barrier keeps
-    // the stage being refilled out of use
-    issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, 0, smem);
-    issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, 0, smem + A_BYTES);
-    for (int kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk) {
-        char* nxt = smem + ((kt + 1) & 1) * STAGE;
-        issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, (kt + 1) * BK, nxt);
-        issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, (kt + 1) * BK, nxt + A_BYTES);
-        wait_vmcnt<LOADS>();
-      } else {
-        wait_vmcnt<0>();
-      }
-      lds_barrier();
-      mma_tile(lds0 + (kt & 1) * STAGE);
-      lds_barrier();
-    }
-  } else {
-    // prologue: tiles 0 .. STAGES-2 in flight
-#pragma unroll
-    for (int t = 0; t < STAGES - 1; ++t) {
-      if (t < nk) {
-        issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, t * BK, smem + t * STAGE);
-        issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, t * BK, smem + t * STAGE + A_BYTES);
-      }
-    }
-    for (int kt = 0; kt < nk; ++kt) {
-      // tile kt has landed once at most (tiles in flight after it) loads remain
-      const int ahead = min(STAGES - 2, nk - 1 - kt);
-      if constexpr (STAGES == 4) {
-        if (ahead >= 2) wait_vmcnt<2 * LOADS>();
-        else if (ahead == 1) wait_vmcnt<LOADS>();
-        else wait_vmcnt<0>();
-      } else {
-        if (ahead >= 1) wait_vmcnt<LOADS>();
-        else wait_vmcnt<0>();
-      }
-      // every wave's share of tile kt is in LDS, and every wave has finished
-      // reading the stage refilled below (tile kt - 1, read in iteration kt - 1)
-      lds_barrier();
-      if (kt + STAGES - 1 < nk) {
-        char* nxt = smem + ((kt + STAGES - 1) % STAGES) * STAGE;
-        issue_tile<BM, A_KC, NT, BK>(A, g.lda, m0, (kt + STAGES - 1) * BK, nxt);
-        issue_tile<BN, B_KC, NT, BK>(B, g.ldb, n0, (kt + STAGES - 1) * BK, nxt + A_BYTES);
-      }
-      mma_tile(lds0 + (kt % STAGES) * STAGE);
-    }
-  }
-  __syncthreads();   // LDS is reused below
-
-  if constexpr (KSPLIT == 2) {
-    // fixed-order combine: the lower-K group adds the upper-K group's sums
-    float* park = reinterpret_cast<float*>(smem) + wave * (TM * TN * 16 * 64);
-    static_assert(WGM * WGN * TM * TN * 16 * 64 * 4 <= STAGES * STAGE, "combine must fit in LDS");
-    if (wk == 1) {
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) park[((i * TN + j) * 16 + r) * 64 + lane] = acc[i][j][r];
-    }
-    __syncthreads();
-    if (wk == 0) {
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[i][j][r] += park[((i * TN + j) * 16 + r) * 64 + lane];
-    }
-    __syncthreads();
-    if (wk != 0) return;
-  }
-
-  // Epilogue through LDS: per 32-row strip, each wave parks its accumulators
-  // ([32][WN] f32) in its own LDS region, reads them back row-contiguous and
-  // applies the epilogue on 8 consecutive columns with 16-byte accesses.
+// Epilogue through LDS: per 32-row strip, each wave parks its accumulators
+// ([32][WN] f32) in its own LDS region, reads them back row-contiguous and
+// applies the epilogue on 8 consecutive columns with 16-byte accesses.
+// LDS_BYTES: LDS the kernel owns (all of it is free when this runs).
+template <int EPI, int BM, int BN, int WGM, int WGN, int TM, int TN, int LDS_BYTES>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[TM][TN], char* smem, int m0, int n0,
+                                              int wm, int wn, int lane, int wave) {
+  constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int LDE = WN + 8;   // f32 row pitch (keeps the parking writes conflict-free)
-  static_assert(WGM * WGN * 32 * LDE * 4 <= STAGES * STAGE, "epilogue staging must fit in LDS");
+  static_assert(WGM * WGN * 32 * LDE * 4 <= LDS_BYTES, "epilogue staging must fit in LDS");
   float* strip = reinterpret_cast<float*>(smem) + wave * 32 * LDE;
   constexpr int CPR = WN / 8;             // 8-column chunks per row
   constexpr int RPP = 64 / CPR;           // rows per pass
@@ -411,44 +257,6 @@ void gemm_v2_kernel(GemmArgs g) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  }
-}
-
-template <int LAYOUT, int BM, int BN, int EPI>
-static hipError_t launch_v2_epi(GemmArgs g, hipStream_t stream) {
-  constexpr V2Config c = v2_config(LAYOUT, BM == 256);
-  g.tiles_m = g.M / BM;
-  g.tiles_n = g.N / BN;
-  hipLaunchKernelGGL((gemm_v2_kernel<LAYOUT, BM, BN, c.wgm, c.wgn, c.ksplit, c.bk, c.stages, EPI>),
-                     dim3(g.tiles_m * g.tiles_n), dim3(64 * c.wgm * c.wgn * c.ksplit), 0, stream, g);
-  return hipGetLastError();
-}
-
-// Epilogues each layout uses in the stage (others fall back to the generic path).
-template <int LAYOUT>
-constexpr bool v2_has_epi(int epi) {
-  return LAYOUT == TPS_GEMM_NT ? (epi == TPS_EPI_STORE || epi == TPS_EPI_BIAS || epi == TPS_EPI_BIAS_RESID ||
-                                  epi == TPS_EPI_BIAS_GELU || epi == TPS_EPI_GELU_GRAD)
-       : LAYOUT == TPS_GEMM_NN ? (epi == TPS_EPI_STORE || epi == TPS_EPI_GELU_GRAD)
-                               : (epi == TPS_EPI_STORE || epi == TPS_EPI_ACC_F32);
-}
-
-template <int LAYOUT, int BM, int BN>
-static hipError_t launch_v2(GemmArgs g, hipStream_t stream) {
-  if constexpr (LAYOUT == TPS_GEMM_NT) {
-    switch (g.epi) {
-      case TPS_EPI_BIAS: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS>(g, stream);
-      case TPS_EPI_BIAS_RESID: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS_RESID>(g, stream);
-      case TPS_EPI_BIAS_GELU: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_BIAS_GELU>(g, stream);
-      case TPS_EPI_GELU_GRAD: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_GELU_GRAD>(g, stream);
-      default: return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_STORE>(g, stream);
-    }
-  } else if constexpr (LAYOUT == TPS_GEMM_NN) {
-    if (g.epi == TPS_EPI_GELU_GRAD) return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_GELU_GRAD>(g, stream);
-    return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_STORE>(g, stream);
-  } else {
-    if (g.epi == TPS_EPI_ACC_F32) return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_ACC_F32>(g, stream);
-    return launch_v2_epi<LAYOUT, BM, BN, TPS_EPI_STORE>(g, stream);
   }
 }
 

@@ -23,23 +23,20 @@ struct GemmArgs {
 // and changes no result bit: every tile shape sums K in the same order.
 struct GemmTile {
   int bm, bn, bk;
-  int v2;   // 1: tile-aligned bf16 path with direct-to-LDS loads
+  int aligned;   // 1: tile-aligned bf16 path (gemm_pipe.h)
 };
 GemmTile gemm_select_tile(int dtype, int layout, const GemmArgs& g);
 
-// Shape of the tile-aligned bf16 kernel per (layout, tile), chosen by
-// measurement on MI355X: waves along M and N, K-groups of waves, K tile and
-// LDS stages.
-struct V2Config {
-  int wgm, wgn, ksplit, bk, stages;
+// Shape of the tile-aligned bf16 kernel per tile size, chosen by measurement
+// on MI355X: waves along M and N, K tile and LDS ring depth.  256 x 256
+// tiles run two waves per SIMD (128 x 64 per wave); 128 x 128 tiles, used
+// when 256 x 256 would leave most CUs idle, one wave per SIMD (64 x 64).
+struct V3Config {
+  int wgm, wgn, bk, stages;
 };
-constexpr V2Config v2_config(int layout, bool big) {
-  return layout == TPS_GEMM_NT ? (big ? V2Config{2, 4, 1, 32, 4} : V2Config{2, 2, 2, 64, 3})
-       : layout == TPS_GEMM_NN ? (big ? V2Config{2, 4, 1, 64, 2} : V2Config{2, 2, 2, 64, 3})
-                               : (big ? V2Config{2, 2, 1, 64, 2} : V2Config{2, 2, 2, 64, 3});
-}
+constexpr V3Config v3_config(bool big) { return big ? V3Config{2, 4, 64, 2} : V3Config{2, 2, 64, 3}; }
 // Demangled name of the kernel instantiation a launch uses (as profilers
-// print it), e.g. "tps::gemm_v2_kernel<0, 256, 256, 2, 4>".
+// print it), e.g. "tps::gemm_bf16_kernel<0, 256, 256, 2, 4, 64, 2, 1>".
 const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g);
 
 hipError_t gemm_launch_nt(int dtype, GemmArgs g, hipStream_t stream);
