@@ -543,7 +543,10 @@ static hipError_t bwd_launch(int b, int s, int nh, const void* qkv, const void* 
 
 hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, void* o,
                                 float* lse, hipStream_t st) {
-  if (dtype == TPS_BF16) return attention_fwd_v2_launch(b, s, nh, d, qkv, o, lse, st);
+  if (dtype == TPS_BF16) {
+    if (d == 128) return attention_fwd_v3_launch(b, s, nh, d, qkv, o, lse, st);
+    return attention_fwd_v2_launch(b, s, nh, d, qkv, o, lse, st);
+  }
   return d == 64 ? fwd_launch<float, 64>(b, s, nh, qkv, o, lse, st) : fwd_launch<float, 128>(b, s, nh, qkv, o, lse, st);
 }
 

@@ -59,6 +59,9 @@ hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const vo
 // bf16 kernels on 16x16x32 MFMAs with paired causal blocks (attention_v2.hip)
 hipError_t attention_fwd_v2_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
                                    hipStream_t st);
+// bf16, head dim 128: 32 queries per wave on 32x32x16 MFMAs (attention_fwd.hip)
+hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
+                                   hipStream_t st);
 hipError_t attention_bwd_v2_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
                                    void* dqkv, const float* dvec, hipStream_t st);
 

@@ -130,6 +130,123 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dout,
   }
 }
 
+// Wave-per-row LayerNorm for rows of NV * 512 bf16 (lane l holds the 8-column
+// chunks l, l + 64, ...): reductions are wave butterflies only, four rows per
+// 256-thread workgroup.
+template <int NV>
+__global__ __launch_bounds__(256) void ln_fwd_wave_kernel(const bf16* __restrict__ x, const bf16* __restrict__ gamma,
+                                                          const bf16* __restrict__ beta, float eps,
+                                                          bf16* __restrict__ out, float* __restrict__ mean,
+                                                          float* __restrict__ rstd, int rows, int cols) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const bf16* xr = x + (int64_t)row * cols;
+  Vec16<bf16> xv[NV];
+#pragma unroll
+  for (int c = 0; c < NV; ++c) xv[c] = load16(xr + (c * 64 + lane) * 8);
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < NV; ++c)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += to_f32(xv[c].get(i));
+  const float mu = wave_sum(s) / (float)cols;
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < NV; ++c)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float d = to_f32(xv[c].get(i)) - mu;
+      ss += d * d;
+    }
+  const float rs = 1.0f / sqrtf(wave_sum(ss) / (float)cols + eps);
+  bf16* orow = out + (int64_t)row * cols;
+#pragma unroll
+  for (int c = 0; c < NV; ++c) {
+    const int col = (c * 64 + lane) * 8;
+    const Vec16<bf16> g = load16(gamma + col), b = load16(beta + col);
+    Vec16<bf16> o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      o.set(i, from_f32<bf16>((to_f32(xv[c].get(i)) - mu) * rs * to_f32(g.get(i)) + to_f32(b.get(i))));
+    store16(orow + col, o);
+  }
+  if (lane == 0) {
+    if (mean) mean[row] = mu;
+    if (rstd) rstd[row] = rs;
+  }
+}
+
+template <int NV>
+__global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict__ dout, const bf16* __restrict__ x,
+                                                          const float* __restrict__ mean,
+                                                          const float* __restrict__ rstd,
+                                                          const bf16* __restrict__ gamma,
+                                                          const bf16* __restrict__ resid, bf16* __restrict__ dx,
+                                                          int rows, int cols) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float mu = mean[row], rs = rstd[row];
+  const bf16* xr = x + (int64_t)row * cols;
+  const bf16* dr = dout + (int64_t)row * cols;
+  Vec16<bf16> xv[NV], dv[NV], rv[NV];
+#pragma unroll
+  for (int c = 0; c < NV; ++c) {
+    const int col = (c * 64 + lane) * 8;
+    xv[c] = load16(xr + col);
+    dv[c] = load16(dr + col);
+    if (resid) rv[c] = load16(resid + (int64_t)row * cols + col);
+  }
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int c = 0; c < NV; ++c) {
+    const Vec16<bf16> g = load16(gamma + (c * 64 + lane) * 8);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float gv = to_f32(dv[c].get(i)) * to_f32(g.get(i));
+      s1 += gv;
+      s2 += gv * ((to_f32(xv[c].get(i)) - mu) * rs);
+    }
+  }
+  const float m1 = wave_sum(s1) / (float)cols;
+  const float m2 = wave_sum(s2) / (float)cols;
+  bf16* o = dx + (int64_t)row * cols;
+#pragma unroll
+  for (int c = 0; c < NV; ++c) {
+    const int col = (c * 64 + lane) * 8;
+    const Vec16<bf16> g = load16(gamma + col);
+    Vec16<bf16> w;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float gv = to_f32(dv[c].get(i)) * to_f32(g.get(i));
+      const float zh = (to_f32(xv[c].get(i)) - mu) * rs;
+      float val = rs * (gv - m1 - zh * m2);
+      if (resid) val += to_f32(rv[c].get(i));
+      w.set(i, from_f32<bf16>(val));
+    }
+    store16(o + col, w);
+  }
+}
+
+// Wave-per-row launch for bf16 rows of a multiple of 512 columns (up to 8192);
+// returns false when the shape needs the block-per-row kernels.
+#define TPS_WAVE_ROW_DISPATCH(KERNEL, rows, cols, st, ...)                                          \
+  ([&]() -> bool {                                                                                  \
+    if ((cols) % 512 != 0 || (cols) > 8192) return false;                                            \
+    const dim3 grid_(((rows) + 3) / 4), block_(256);                                                 \
+    switch ((cols) / 512) {                                                                          \
+      case 1: hipLaunchKernelGGL((KERNEL<1>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
+      case 2: hipLaunchKernelGGL((KERNEL<2>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
+      case 4: hipLaunchKernelGGL((KERNEL<4>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
+      case 8: hipLaunchKernelGGL((KERNEL<8>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
+      case 10: hipLaunchKernelGGL((KERNEL<10>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break; \
+      case 16: hipLaunchKernelGGL((KERNEL<16>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break; \
+      default: return false;                                                                         \
+    }                                                                                                \
+    return true;                                                                                     \
+  }())
+
 // Pass 1 of a column reduction: block (column group of 64, row segment).
 // Thread (row lane rl, chunk cc) sums rows rl, rl+32, ... of the segment for
 // 8 columns; the 32 row lanes are then added in ascending order.
@@ -149,20 +266,39 @@ __global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ 
 #pragma unroll
   for (int i = 0; i < VEC; ++i) a[i] = z[i] = 0.f;
   if (col < cols) {
-    for (int r = r0 + rl; r < r1; r += 32) {
-      const Vec16<T> v = load16(x + (int64_t)r * ldx + col);
-      if constexpr (LN) {
-        const Vec16<T> xv = load16(xin + (int64_t)r * cols + col);
-        const float mu = mean[r], rs = rstd[r];
+    // rows rl, rl + 32, ... of the segment, UNR loads in flight; the sum of
+    // each lane runs in ascending row order
+    constexpr int UNR = 4;
+    for (int r = r0 + rl; r < r1; r += 32 * UNR) {
+      Vec16<T> v[UNR], xv[UNR];
+      float mu[UNR], rs[UNR];
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) {
-          const float d = to_f32(v.get(i));
-          a[i] += d;
-          z[i] += d * ((to_f32(xv.get(i)) - mu) * rs);
+      for (int u = 0; u < UNR; ++u) {
+        const int ru = r + 32 * u;
+        if (ru < r1) {
+          v[u] = load16(x + (int64_t)ru * ldx + col);
+          if constexpr (LN) {
+            xv[u] = load16(xin + (int64_t)ru * cols + col);
+            mu[u] = mean[ru];
+            rs[u] = rstd[ru];
+          }
         }
-      } else {
+      }
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) a[i] += to_f32(v.get(i));
+      for (int u = 0; u < UNR; ++u) {
+        if (r + 32 * u < r1) {
+          if constexpr (LN) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) {
+              const float d = to_f32(v[u].get(i));
+              a[i] += d;
+              z[i] += d * ((to_f32(xv[u].get(i)) - mu[u]) * rs[u]);
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) a[i] += to_f32(v[u].get(i));
+          }
+        }
       }
     }
   }
@@ -188,10 +324,21 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restri
                                                            float* __restrict__ out1) {
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= cols) return;
+  // all partials are loaded before the (ascending, fixed-order) adds, so the
+  // loads are in flight together; parts <= 16
+  float p0[16], p1[16];
+#pragma unroll
+  for (int p = 0; p < 16; ++p) {
+    p0[p] = p < parts ? ws[((int64_t)p * nk) * cols + c] : 0.f;
+    p1[p] = (p < parts && nk == 2) ? ws[((int64_t)p * nk + 1) * cols + c] : 0.f;
+  }
   float s0 = 0.f, s1 = 0.f;
-  for (int p = 0; p < parts; ++p) {
-    s0 += ws[((int64_t)p * nk) * cols + c];
-    if (nk == 2) s1 += ws[((int64_t)p * nk + 1) * cols + c];
+#pragma unroll
+  for (int p = 0; p < 16; ++p) {
+    if (p < parts) {
+      s0 += p0[p];
+      s1 += p1[p];
+    }
   }
   if (out0) out0[c] += s0;
   if (nk == 2 && out1) out1[c] += s1;
@@ -287,10 +434,12 @@ hipError_t layernorm_fwd_launch(int dtype, int rows, int cols, const void* x, co
                                 const void* beta, float eps, void* out, float* mean, float* rstd,
                                 hipStream_t st) {
   if (rows == 0) return hipSuccess;
-  if (dtype == TPS_BF16)
-    TPS_ROW_DISPATCH(ln_fwd_kernel, bf16, rows, cols, st, (const bf16*)x, (const bf16*)gamma, (const bf16*)beta,
-                     eps, (bf16*)out, mean, rstd);
-  else
+  if (dtype == TPS_BF16) {
+    if (!TPS_WAVE_ROW_DISPATCH(ln_fwd_wave_kernel, rows, cols, st, (const bf16*)x, (const bf16*)gamma,
+                               (const bf16*)beta, eps, (bf16*)out, mean, rstd))
+      TPS_ROW_DISPATCH(ln_fwd_kernel, bf16, rows, cols, st, (const bf16*)x, (const bf16*)gamma, (const bf16*)beta,
+                       eps, (bf16*)out, mean, rstd);
+  } else
     TPS_ROW_DISPATCH(ln_fwd_kernel, float, rows, cols, st, (const float*)x, (const float*)gamma,
                      (const float*)beta, eps, (float*)out, mean, rstd);
   return hipGetLastError();
@@ -301,10 +450,12 @@ hipError_t layernorm_bwd_launch(int dtype, int rows, int cols, const void* dout,
                                 const void* resid, void* dx, float* dgamma, float* dbeta,
                                 float* ws, hipStream_t st) {
   if (rows == 0) return hipSuccess;
-  if (dtype == TPS_BF16)
-    TPS_ROW_DISPATCH(ln_bwd_kernel, bf16, rows, cols, st, (const bf16*)dout, (const bf16*)x, mean, rstd,
-                     (const bf16*)gamma, (const bf16*)resid, (bf16*)dx);
-  else
+  if (dtype == TPS_BF16) {
+    if (!TPS_WAVE_ROW_DISPATCH(ln_bwd_wave_kernel, rows, cols, st, (const bf16*)dout, (const bf16*)x, mean, rstd,
+                               (const bf16*)gamma, (const bf16*)resid, (bf16*)dx))
+      TPS_ROW_DISPATCH(ln_bwd_kernel, bf16, rows, cols, st, (const bf16*)dout, (const bf16*)x, mean, rstd,
+                       (const bf16*)gamma, (const bf16*)resid, (bf16*)dx);
+  } else
     TPS_ROW_DISPATCH(ln_bwd_kernel, float, rows, cols, st, (const float*)dout, (const float*)x, mean, rstd,
                      (const float*)gamma, (const float*)resid, (float*)dx);
   hipError_t e = hipGetLastError();
