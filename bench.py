@@ -65,18 +65,35 @@ def build_stage(cfg):
     td = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     es = 2 if cfg.dtype == "bf16" else 4
     blocks, grads = [], []
+    shapes = synth.param_shapes(cfg.hidden, cfg.mlp)
     for l in range(cfg.n_layers):
-        vals = synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype)
         blk = torch.zeros(pb, dtype=torch.uint8, device="cuda")
-        for i, name in enumerate(T.PARAMS):
-            v = torch.from_numpy(vals[name].reshape(-1)).to("cuda").to(td)
-            blk[po[i]:po[i] + v.numel() * es].view(td).copy_(v)
         if cfg.weights == T.W_STREAM:
-            hb = torch.empty(pb, dtype=torch.uint8, pin_memory=True)
-            hb.copy_(blk)
+            # streamed weights live in pinned host memory (exact-size blocks);
+            # the values come from a seeded device generator with the same
+            # distributions as the synthetic parameters (throughput does not
+            # depend on them, and it avoids drawing ~10^10 values on the CPU)
+            gen = torch.Generator(device="cuda").manual_seed(1000 + 16 * l)
+            for i, name in enumerate(T.PARAMS):
+                n = 1
+                for d in shapes[name]:
+                    n *= d
+                v = torch.randn(n, generator=gen, device="cuda") * 0.02
+                if name in ("g1", "g2"):
+                    v += 1.0
+                blk[po[i]:po[i] + n * es].view(td).copy_(v.to(td))
+            hb = T.HostBuffer(pb)
+            torch.cuda.synchronize()
+            hb.numpy()[:] = blk.cpu().numpy()
+            del blk
             blk = hb
-            g = torch.zeros(gb, dtype=torch.uint8, pin_memory=True)
+            g = T.HostBuffer(gb)
+            g.numpy()[:] = 0
         else:
+            vals = synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype)
+            for i, name in enumerate(T.PARAMS):
+                v = torch.from_numpy(vals[name].reshape(-1)).to("cuda").to(td)
+                blk[po[i]:po[i] + v.numel() * es].view(td).copy_(v)
             g = torch.zeros(gb, dtype=torch.uint8, device="cuda")
         blocks.append(blk)
         grads.append(g)
@@ -162,8 +179,17 @@ def main():
     order = cfg.order()
     step_flops = info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]
 
+    groups = cfg.groups()
+
     def step():
         stage.begin_iteration(zero_grads=True)
+        if cfg.layer_major:
+            for k, mb0, n in groups:
+                if k == "F":
+                    stage.forward_group(mb0, xs[mb0:mb0 + n], ys[mb0:mb0 + n])
+                else:
+                    stage.backward_group(mb0, dys[mb0:mb0 + n], dxs[mb0:mb0 + n])
+            return
         for k, mb in order:
             if k == "F":
                 stage.forward(mb, xs[mb], ys[mb])
@@ -221,7 +247,8 @@ def main():
             "layers": cfg.n_layers, "hidden": cfg.hidden, "heads": cfg.n_heads, "mlp": cfg.mlp,
             "seq": cfg.seq, "micro_batch": cfg.micro_batch, "micro_batches": cfg.n_micro,
             "policy": configs.WORKLOADS[args.workload].__doc__.split(";")[-1].strip().rstrip("."),
-            "order": "all forwards, then all backwards (in-flight = micro-batches)",
+            "order": ("layer-major: one forward group and one backward group over all micro-batches"
+                      if cfg.layer_major else "all forwards, then all backwards (in-flight = micro-batches)"),
             "parallelism": "one GPU",
         },
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),

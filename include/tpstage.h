@@ -259,6 +259,15 @@ int tps_stage_kernel_times(tps_stage* st, tps_kernel_time* out, int max, int* n_
 /* Releases events and host metadata (caller buffers are untouched). */
 int tps_stage_destroy(tps_stage* st);
 
+/* Pinned (page-locked) host memory of exactly `bytes` bytes, for the host
+ * side of streamed weights and gradients and for the host arena: T-Offload
+ * moves these between host DRAM and HBM with asynchronous copies (Section 5),
+ * which need page-locked memory.  *out receives the pointer (NULL when bytes
+ * is 0); the caller releases it with tps_host_free.  TPS_ENOMEM when the
+ * system cannot pin that much. */
+int tps_host_alloc(uint64_t bytes, void** out);
+int tps_host_free(void* p);
+
 /* Thread-local message of the last failing call ("" if none). */
 const char* tps_last_error(void);
 

@@ -68,10 +68,12 @@ def stage4_seq8192_recompute() -> StageConfig:
 def stage12_h8192_stream(n_micro: int = 8) -> StageConfig:
     """12 layers, hidden 8192, 64 heads, MLP 32768, causal seq 4096, micro-batch 1,
     8 micro-batches, bf16 weights and f32 grads streamed from pinned host per
-    layer (layer-major groups), activations recomputed from layer inputs."""
+    layer, run as layer-major groups (each streamed layer serves every
+    micro-batch before the next one comes in); activations recomputed from
+    layer inputs."""
     return StageConfig(n_layers=12, hidden=8192, n_heads=64, mlp=32768, seq=4096, micro_batch=1,
                        n_micro=n_micro, dtype="bf16", policy=policy_layer_inputs(12), granularity=GRAN_LAYER,
-                       weights=W_STREAM, window=3)
+                       weights=W_STREAM, window=3, layer_major=True)
 
 
 WORKLOADS = {

@@ -184,8 +184,20 @@ __device__ __forceinline__ void read_frags(bf16x8 (&f)[NF], const FragAddr<ROWS,
 
 // Epilogue through LDS: per 32-row strip, each wave parks its accumulators
 // ([32][WN] f32) in its own LDS region, reads them back row-contiguous and
-// applies the epilogue on 8 consecutive columns with 16-byte accesses.
+// applies the epilogue on 8 consecutive columns with 16-byte accesses.  The
+// global inputs of a strip (old f32 sums, residual, kept pre-activation) are
+// loaded one strip ahead, before the stores of the current strip: the
+// compiler cannot move loads of one pass above the (possibly aliasing)
+// stores of the previous one, so issuing them in program order first keeps
+// them all in flight together.
 // LDS_BYTES: LDS the kernel owns (all of it is free when this runs).
+template <int EPI, int P>
+struct EpiIn {
+  // per pass: f32 sums (ACC_F32) or one 16-byte bf16 vector (residual / aux)
+  f32x4 c0[EPI == TPS_EPI_ACC_F32 ? P : 1], c1[EPI == TPS_EPI_ACC_F32 ? P : 1];
+  Vec16<bf16> v[(EPI == TPS_EPI_BIAS_RESID || EPI == TPS_EPI_GELU_GRAD) ? P : 1];
+};
+
 template <int EPI, int BM, int BN, int WGM, int WGN, int TM, int TN, int LDS_BYTES>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[TM][TN], char* smem, int m0, int n0,
                                               int wm, int wn, int lane, int wave) {
@@ -195,6 +207,31 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[T
   float* strip = reinterpret_cast<float*>(smem) + wave * 32 * LDE;
   constexpr int CPR = WN / 8;             // 8-column chunks per row
   constexpr int RPP = 64 / CPR;           // rows per pass
+  constexpr int P = 32 / RPP;             // passes per strip
+  const int rl0 = lane / CPR, cl = (lane % CPR) * 8;
+  const int col = n0 + wn * WN + cl;
+  const int row0 = m0 + wm * WM + rl0;    // row of pass 0 of strip 0
+  Vec16<bf16> bias;
+  if constexpr (EPI == TPS_EPI_BIAS || EPI == TPS_EPI_BIAS_RESID || EPI == TPS_EPI_BIAS_GELU)
+    bias = load16(static_cast<const bf16*>(g.bias) + col);
+
+  auto load_strip = [&](int i, EpiIn<EPI, P>& in) {
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      const int64_t row = row0 + i * 32 + q * RPP;
+      if constexpr (EPI == TPS_EPI_ACC_F32) {
+        const f32x4* c = reinterpret_cast<const f32x4*>(static_cast<const float*>(g.C) + row * g.ldc + col);
+        in.c0[q] = c[0];
+        in.c1[q] = c[1];
+      } else if constexpr (EPI == TPS_EPI_BIAS_RESID) {
+        in.v[q] = load16(static_cast<const bf16*>(g.resid) + row * g.ldr + col);
+      } else if constexpr (EPI == TPS_EPI_GELU_GRAD) {
+        in.v[q] = load16(static_cast<const bf16*>(g.aux) + row * g.ldaux + col);
+      }
+    }
+  };
+  EpiIn<EPI, P> in[2];
+  load_strip(0, in[0]);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -204,16 +241,18 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[T
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (i + 1 < TM) load_strip(i + 1, in[(i + 1) & 1]);
+    const EpiIn<EPI, P>& cur = in[i & 1];
 #pragma unroll
-    for (int q = 0; q < 32 / RPP; ++q) {
-      const int rl = q * RPP + lane / CPR, cl = (lane % CPR) * 8;
+    for (int q = 0; q < P; ++q) {
+      const int rl = q * RPP + rl0;
       const f32x4 v0 = *reinterpret_cast<const f32x4*>(strip + rl * LDE + cl);
       const f32x4 v1 = *reinterpret_cast<const f32x4*>(strip + rl * LDE + cl + 4);
       const float v[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-      const int row = m0 + wm * WM + i * 32 + rl, col = n0 + wn * WN + cl;
+      const int64_t row = row0 + i * 32 + q * RPP;
       if constexpr (EPI == TPS_EPI_ACC_F32) {
-        f32x4* c = reinterpret_cast<f32x4*>(static_cast<float*>(g.C) + (int64_t)row * g.ldc + col);
-        f32x4 c0 = c[0], c1 = c[1];
+        f32x4* c = reinterpret_cast<f32x4*>(static_cast<float*>(g.C) + row * g.ldc + col);
+        f32x4 c0 = cur.c0[q], c1 = cur.c1[q];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           c0[t] += v[t];
@@ -223,13 +262,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[T
         c[1] = c1;
       } else {
         float out[8];
-        Vec16<bf16> bias, res, aux;
-        if constexpr (EPI == TPS_EPI_BIAS || EPI == TPS_EPI_BIAS_RESID || EPI == TPS_EPI_BIAS_GELU)
-          bias = load16(static_cast<const bf16*>(g.bias) + col);
-        if constexpr (EPI == TPS_EPI_BIAS_RESID)
-          res = load16(static_cast<const bf16*>(g.resid) + (int64_t)row * g.ldr + col);
-        if constexpr (EPI == TPS_EPI_GELU_GRAD)
-          aux = load16(static_cast<const bf16*>(g.aux) + (int64_t)row * g.ldaux + col);
+        Vec16<bf16> aux;
+        if constexpr (EPI == TPS_EPI_GELU_GRAD) aux = cur.v[q];
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
           if constexpr (EPI == TPS_EPI_STORE) {
@@ -237,7 +271,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[T
           } else if constexpr (EPI == TPS_EPI_BIAS) {
             out[t] = v[t] + to_f32(bias.get(t));
           } else if constexpr (EPI == TPS_EPI_BIAS_RESID) {
-            out[t] = v[t] + to_f32(bias.get(t)) + to_f32(res.get(t));
+            out[t] = v[t] + to_f32(bias.get(t)) + to_f32(cur.v[q].get(t));
           } else if constexpr (EPI == TPS_EPI_BIAS_GELU) {
             const bf16 u = from_f32<bf16>(v[t] + to_f32(bias.get(t)));
             aux.set(t, u);
@@ -247,11 +281,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[T
           }
         }
         if constexpr (EPI == TPS_EPI_BIAS_GELU)
-          if (g.aux) store16(static_cast<bf16*>(g.aux) + (int64_t)row * g.ldaux + col, aux);
+          if (g.aux) store16(static_cast<bf16*>(g.aux) + row * g.ldaux + col, aux);
         Vec16<bf16> o;
 #pragma unroll
         for (int t = 0; t < 8; ++t) o.set(t, from_f32<bf16>(out[t]));
-        store16(static_cast<bf16*>(g.C) + (int64_t)row * g.ldc + col, o);
+        store16(static_cast<bf16*>(g.C) + row * g.ldc + col, o);
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

@@ -891,3 +891,25 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
   delete st;
   return TPS_OK;
 }
+
+extern "C" int tps_host_alloc(uint64_t bytes, void** out) {
+  clear_error();
+  if (!out) return set_error(TPS_EINVAL, "null argument");
+  *out = nullptr;
+  if (bytes == 0) return TPS_OK;
+  const hipError_t e = hipHostMalloc(out, bytes, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    *out = nullptr;
+    (void)hipGetLastError();
+    return set_error(TPS_ENOMEM, "cannot pin " + std::to_string(bytes) + " bytes of host memory: " +
+                                     hipGetErrorString(e));
+  }
+  return TPS_OK;
+}
+
+extern "C" int tps_host_free(void* p) {
+  clear_error();
+  if (!p) return TPS_OK;
+  TPS_HIP(hipHostFree(p));
+  return TPS_OK;
+}

@@ -102,6 +102,7 @@ EXPORTED = (
     "tps_last_error", "tps_op_gemm", "tps_op_layernorm_fwd", "tps_op_layernorm_bwd",
     "tps_op_attention_fwd", "tps_op_attention_bwd", "tps_op_colsum", "tps_op_gelu",
     "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
+    "tps_host_alloc", "tps_host_free",
 )
 
 
@@ -141,6 +142,8 @@ def lib() -> C.CDLL:
         L.tps_op_gelu.argtypes = [i32, i64, vp, vp, vp]
         L.tps_op_workspace_bytes.argtypes = [i32, i64, i64]
         L.tps_op_workspace_bytes.restype = u64
+        L.tps_host_alloc.argtypes = [u64, C.POINTER(vp)]
+        L.tps_host_free.argtypes = [vp]
         _lib = L
     return _lib
 
@@ -148,6 +151,39 @@ def lib() -> C.CDLL:
 def check(rc: int) -> None:
     if rc != TPS_OK:
         raise TpsError(rc, lib().tps_last_error().decode())
+
+
+class HostBuffer:
+    """Exactly `nbytes` of pinned host memory from tps_host_alloc (the
+    caching pinned allocator of the framework rounds requests up to powers of
+    two, which the host side of a large streamed stage cannot afford).
+    `data_ptr()` gives the address, `numpy()` a uint8 view."""
+
+    def __init__(self, nbytes: int):
+        self.nbytes = int(nbytes)
+        p = C.c_void_p()
+        check(lib().tps_host_alloc(self.nbytes, C.byref(p)))
+        self._p = p.value
+
+    def data_ptr(self) -> int:
+        return self._p or 0
+
+    def numpy(self):
+        import numpy as np
+        if not self._p:
+            return np.zeros(0, dtype=np.uint8)
+        return np.ctypeslib.as_array((C.c_uint8 * self.nbytes).from_address(self._p))
+
+    def free(self) -> None:
+        if self._p:
+            check(lib().tps_host_free(self._p))
+            self._p = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
 
 
 # --- configuration -----------------------------------------------------------
@@ -173,7 +209,21 @@ class StageConfig:
     link_gbps_hint: float = 50.0
     tflops_hint: float = 1000.0
     lookahead: int = 1
+    # drive the planned order with layer-major group calls (each run of
+    # consecutive F (or B) tasks is one tps_stage_forward_group / _backward_group)
+    layer_major: bool = False
     _keep: list = field(default_factory=list, repr=False)
+
+    def groups(self) -> list:
+        """The planned order as runs of consecutive micro-batches with the same
+        task kind: [("F"|"B", first_mb, count)]."""
+        out = []
+        for k, mb in self.order():
+            if out and out[-1][0] == k and out[-1][1] + out[-1][2] == mb:
+                out[-1] = (k, out[-1][1], out[-1][2] + 1)
+            else:
+                out.append((k, mb, 1))
+        return out
 
     @property
     def tokens(self) -> int:
@@ -248,9 +298,10 @@ def param_layout(cfg: StageConfig):
 
 # --- stage ---------------------------------------------------------------------
 class Stage:
-    """One pipeline stage on one GPU.  Device and pinned host arenas are torch
-    allocations sized by the plan; parameter and f32 gradient blocks are torch
-    byte tensors laid out by param_layout()."""
+    """One pipeline stage on one GPU.  The device arena is a torch allocation
+    and the pinned host arena a HostBuffer, both sized by the plan; parameter
+    and f32 gradient blocks are byte buffers (torch tensors or HostBuffers)
+    laid out by param_layout()."""
 
     def __init__(self, cfg: StageConfig, layer_params, layer_grads, device="cuda",
                  compute_stream=None, copy_stream=None):
@@ -260,7 +311,7 @@ class Stage:
         self.device = torch.device(device)
         self.arena = torch.empty(max(self.info["device_arena_bytes"], 256), dtype=torch.uint8, device=self.device)
         hb = self.info["host_arena_bytes"]
-        self.host = torch.empty(hb, dtype=torch.uint8, pin_memory=True) if hb else None
+        self.host = HostBuffer(hb) if hb else None
         self.cs = compute_stream or torch.cuda.Stream(device=self.device)
         self.xs = copy_stream or torch.cuda.Stream(device=self.device)
         self.layer_params, self.layer_grads = list(layer_params), list(layer_grads)
