@@ -58,6 +58,14 @@ def stage5_h5120_offload() -> StageConfig:
                        link_gbps_hint=50.0, tflops_hint=1000.0)
 
 
+def stage5_h5120_resident() -> StageConfig:
+    """The activation-offload workload's shapes with every activation kept in
+    HBM (no offload): the reference point for how much of the offload the
+    copy engines hide."""
+    return StageConfig(n_layers=5, hidden=5120, n_heads=40, mlp=20480, seq=2048, micro_batch=1, n_micro=16,
+                       dtype="bf16", policy=policy_all(5, KEEP))
+
+
 def stage4_seq8192_recompute() -> StageConfig:
     """4 layers, hidden 4096, 32 heads, MLP 16384, causal seq 8192, micro-batch 1,
     8 micro-batches, bf16; full-layer recompute keeping only layer inputs."""
@@ -80,6 +88,7 @@ WORKLOADS = {
     "tiny": tiny,
     "stage4_h2048": stage4_h2048,
     "stage5_h5120_offload": stage5_h5120_offload,
+    "stage5_h5120_resident": stage5_h5120_resident,
     "stage4_seq8192_recompute": stage4_seq8192_recompute,
     "stage12_h8192_stream": stage12_h8192_stream,
 }
