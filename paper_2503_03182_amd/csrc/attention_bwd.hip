@@ -1,0 +1,399 @@
+// Fused causal attention backward, bf16, head dim 128, on 32x32x16 MFMAs.
+//
+// With P = softmax_causal(q k^T / sqrt d), D_i = sum_d dO_id O_id (computed by
+// attn_bwd_dot_kernel) and lse the forward's log-sum-exp:
+//   P_ij  = exp(s q_i.k_j - lse_i),   dP_ij = dO_i . v_j,
+//   dS_ij = P_ij (dP_ij - D_i),
+//   dV_j  = sum_i P_ij dO_i,  dK_j = s sum_i dS_ij q_i,  dQ_i = s sum_j dS_ij k_j,
+// summed over the causal triangle j <= i.  Two kernels, both deterministic
+// (every output element is produced by one wave in a fixed order, no atomics):
+//
+// dK/dV (attn_bwd_dkdv_v3_kernel): a 4-wave workgroup owns 128 keys, 32 per
+//   wave, K and V fragments in registers; 64-query tiles of Q, dO, lse and D
+//   stream through a two-stage LDS ring.  With keys along the MFMA N
+//   dimension (one key per lane):
+//     S  = Q K^T, dP = dO V^T        (Q, dO rows from LDS)
+//     dV^T += dO^T P, dK^T += Q^T dS (dO^T, Q^T through transposing reads, in
+//                                     the accumulators' query order)
+//   64 MFMAs per tile; one wave per SIMD (the dK/dV accumulators take AGPRs).
+// dQ (attn_bwd_dq_v3_kernel): a 4-wave workgroup owns 128 queries, 32 per
+//   wave, Q and dO fragments plus lse and D in registers; 64-key tiles of K
+//   and V stream through the ring.  With queries along N:
+//     S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T
+//   48 MFMAs per tile; one wave per SIMD (Q, dO fragments and dQ
+//   accumulators do not fit the register budget of two).
+// Workgroups are launched heaviest first.  Rows past the sequence end load as
+// zeros: their Q and dO rows contribute nothing to dK/dV, and keys past the end
+// lie beyond every query, so the causal mask removes them from dQ.
+#include "attn_tiles.h"
+
+namespace tps {
+
+using namespace at;
+
+// ---------------------------------------------------------------------------
+// dK, dV
+// ---------------------------------------------------------------------------
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
+                             const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
+                             int b, int s, int nh, float scale) {
+  constexpr int VEC = 1024;                    // LDS bytes per per-row vector (64 f32 + landing pad)
+  constexpr int STAGE = 2 * TILE + 2 * VEC;    // Q, dO, lse, D
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+
+  const int H = nh * D;
+  const int64_t ld = 3 * (int64_t)H;
+  const int idx = blockIdx.x;
+  const int head = idx % nh;
+  const int batch = (idx / nh) % b;
+  const int kb = idx / (nh * b);                // first key blocks carry the most queries
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 5;
+  const int k0 = kb * 128 + wave * 32;         // first key of this wave
+  const int key = k0 + (lane & 31);
+
+  const bf16* base = qkv + (int64_t)batch * s * ld;
+  // K^T and V^T fragments (B operands): lane holds key's d = 16 ks + 8 g .. +8
+  bf16x8 kf[D / 16], vf[D / 16];
+  {
+    const bf16* krow = base + (int64_t)min(key, s - 1) * ld + H + head * D + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      kf[ks] = load_frag_settled(krow + 16 * ks);
+      vf[ks] = load_frag_settled(krow + H + 16 * ks);
+    }
+  }
+  // query tiles from the one holding this workgroup's first key to the end
+  const int t0 = (kb * 128) / BT;
+  const int ntile = (s + BT - 1) / BT;
+  const int wave_first = k0 / BT;               // earlier tiles have no query >= any key of the wave
+
+  TileSrc qsrc, dsrc;
+  qsrc.init(base + head * D, ld, s, wave, lane);
+  dsrc.init(dout + (int64_t)batch * s * H + head * D, H, s, wave, lane);
+  VecSrc lsrc, vsrc;
+  lsrc.init(lse + ((int64_t)batch * nh + head) * s, s);
+  vsrc.init(dvec + ((int64_t)batch * nh + head) * s, s);
+  auto load_tile = [&](int t, int st) {
+    char* p = smem + st * STAGE;
+    qsrc.load(t * BT, p, wave);
+    dsrc.load(t * BT, p + TILE, wave);
+    if (wave == 0) {
+      lsrc.load(t * BT, p + 2 * TILE, lane);
+      vsrc.load(t * BT, p + 2 * TILE + VEC, lane);
+    }
+  };
+  FragOff fo;
+  fo.init(lane);
+  const uint32_t lds0 = lds_u32(smem);
+
+  f32x16 dk[D / 32], dv[D / 32];
+#pragma unroll
+  for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dk[mt][r] = dv[mt][r] = 0.f;
+  const float sl2 = scale * kLog2e;
+  // causal test on a diagonal tile: query 64 t + c < key  <=>  c < key - 4 g - 64 t,
+  // c = 32 qb + 8 (j / 4) + j % 4 the query offset of accumulator j of block qb
+  const int kthr = key - 4 * g;
+
+  auto tile = [&](int t, auto diag_c) {
+    constexpr bool DIAG = decltype(diag_c)::value;
+    const uint32_t qs = lds0 + (t & 1) * STAGE, ds = qs + TILE, ls = ds + TILE, vs = ls + VEC;
+    // ---- S = Q K^T and dP = dO V^T: 2 query blocks x 8 d-steps each
+    f32x16 sacc[2], pacc[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[qb][r] = pacc[qb][r] = 0.f;
+    bf16x8 fr[32];
+    // issue order i: operand (Q, dO) = i % 2, query block = (i / 2) % 2, d-step = i / 4
+    auto read_f = [&](auto ic) {
+      constexpr int i = decltype(ic)::value, w = i % 2, qb = (i / 2) % 2, ks = i / 4;
+      fr[i] = ds_b128<qb * 32 * ROWB>((w ? ds : qs) + fo.row[ks]);
+    };
+    static_for<10>([&](auto ic) { read_f(ic); });
+    static_for<32>([&](auto ic) {
+      constexpr int i = decltype(ic)::value, w = i % 2, qb = (i / 2) % 2, ks = i / 4;
+      constexpr int issued = (i + 10 < 32) ? i + 10 : 32;
+      wait_lgkm<issued - i - 1>();
+      pin(fr[i]);
+      if constexpr (w == 0) sacc[qb] = Mma<bf16>::run(fr[i], kf[ks], sacc[qb]);
+      else pacc[qb] = Mma<bf16>::run(fr[i], vf[ks], pacc[qb]);
+      if constexpr (i + 10 < 32) read_f(std::integral_constant<int, i + 10>{});
+    });
+    // ---- lse and D of the rows this lane holds: rows 32 qb + 8 (j / 4) + 4 g + (j % 4)
+    f32x4 lv[2][4], dvv[2][4];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int j4 = 0; j4 < 4; ++j4) {
+        const uint32_t o = (uint32_t)((32 * qb + 8 * j4 + 4 * g) * 4);
+        asm volatile("ds_read_b128 %0, %1" : "=v"(lv[qb][j4]) : "v"(ls + o));
+        asm volatile("ds_read_b128 %0, %1" : "=v"(dvv[qb][j4]) : "v"(vs + o));
+      }
+    wait_lgkm<0>();
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int j4 = 0; j4 < 4; ++j4) {
+        pin(lv[qb][j4]);
+        pin(dvv[qb][j4]);
+      }
+    // ---- P, dS
+    float p[2][16], d[2][16];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[qb][j], sl2, -lv[qb][j / 4][j % 4] * kLog2e));
+        if constexpr (DIAG) {
+          if (32 * qb + 8 * (j / 4) + (j % 4) < kthr - t * BT) pv = 0.f;
+        }
+        p[qb][j] = pv;
+        d[qb][j] = pv * (pacc[qb][j] - dvv[qb][j / 4][j % 4]);
+      }
+    bf16x8 pb[4], sb[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      pb[u] = to_frag(&p[u / 2][8 * (u % 2)]);
+      sb[u] = to_frag(&d[u / 2][8 * (u % 2)]);
+    }
+    // ---- dV^T += dO^T P, dK^T += Q^T dS: 4 query steps x 4 d tiles each
+    s16x4 lo[32], hi[32];
+    // issue order i: operand (dO^T, Q^T) = i % 2, d tile = (i / 2) % 4, query step u = i / 8
+    auto read_t = [&](auto ic) {
+      constexpr int i = decltype(ic)::value, w = i % 2, mt = (i / 2) % 4, u = i / 8;
+      constexpr int roff = 16 * u * ROWB;
+      const uint32_t src = w ? qs : ds;
+      lo[i] = ds_tr16<roff>(src + fo.lo[mt]);
+      hi[i] = ds_tr16<roff>(src + fo.hi[mt]);
+    };
+    static_for<7>([&](auto ic) { read_t(ic); });
+    static_for<32>([&](auto ic) {
+      constexpr int i = decltype(ic)::value, w = i % 2, mt = (i / 2) % 4, u = i / 8;
+      constexpr int issued = (i + 7 < 32) ? i + 7 : 32;
+      wait_lgkm<2 * (issued - i - 1)>();
+      s16x8 v8 = {lo[i][0], lo[i][1], lo[i][2], lo[i][3], hi[i][0], hi[i][1], hi[i][2], hi[i][3]};
+      bf16x8 f = *reinterpret_cast<bf16x8*>(&v8);
+      pin(f);
+      if constexpr (w == 0) dv[mt] = Mma<bf16>::run(f, pb[u], dv[mt]);
+      else dk[mt] = Mma<bf16>::run(f, sb[u], dk[mt]);
+      if constexpr (i + 7 < 32) read_t(std::integral_constant<int, i + 7>{});
+    });
+  };
+
+  // tile t lives in stage t & 1
+  load_tile(t0, t0 & 1);
+  if (t0 + 1 < ntile) {
+    load_tile(t0 + 1, (t0 + 1) & 1);
+    if (wave == 0) wait_vm<10>();   // tile t0 landed (10 loads per tile for wave 0, 8 for the others)
+    else wait_vm<8>();
+  } else {
+    wait_vm<0>();
+  }
+  lds_barrier();
+  for (int t = t0; t < ntile; ++t) {
+    if (t >= wave_first) {
+      if (t * BT < k0 + 31) tile(t, std::true_type{});   // some query of the tile precedes some key
+      else tile(t, std::false_type{});
+    }
+    // hand the stage back: tile t+1 has landed, every wave is done with tile t
+    wait_vm<0>();
+    lds_barrier();
+    if (t + 2 < ntile) load_tile(t + 2, t & 1);
+  }
+
+  // ---- store: lane holds dK^T / dV^T [32 mt + acc_row(j, l)][key]
+  if (key < s) {
+    bf16* row = dqkv + ((int64_t)batch * s + key) * ld + head * D;
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+      for (int j4 = 0; j4 < 4; ++j4) {
+        typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+        bf16x4 wk, wv;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          wk[j] = (bf16)(dk[mt][4 * j4 + j] * scale);
+          wv[j] = (bf16)dv[mt][4 * j4 + j];
+        }
+        const int c = 32 * mt + acc_row(4 * j4, lane);
+        *reinterpret_cast<bf16x4*>(row + H + c) = wk;
+        *reinterpret_cast<bf16x4*>(row + 2 * H + c) = wv;
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dQ
+// ---------------------------------------------------------------------------
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
+                           const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
+                           int b, int s, int nh, float scale) {
+  constexpr int STAGE = 2 * TILE;   // K, V
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+
+  const int H = nh * D;
+  const int64_t ld = 3 * (int64_t)H;
+  const int nqb = (s + 127) / 128;
+  const int idx = blockIdx.x;
+  const int head = idx % nh;
+  const int batch = (idx / nh) % b;
+  const int qb = nqb - 1 - idx / (nh * b);     // heaviest blocks first
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 5;
+  const int q0 = qb * 128 + wave * 32;
+  const int q = q0 + (lane & 31);
+
+  const bf16* base = qkv + (int64_t)batch * s * ld;
+  const int qc = min(q, s - 1);
+  bf16x8 qf[D / 16], df[D / 16];
+  {
+    const bf16* qrow = base + (int64_t)qc * ld + head * D + 8 * g;
+    const bf16* drow = dout + ((int64_t)batch * s + qc) * H + head * D + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      qf[ks] = load_frag_settled(qrow + 16 * ks);
+      df[ks] = load_frag_settled(drow + 16 * ks);
+    }
+  }
+  const float lse2 = lse[((int64_t)batch * nh + head) * s + qc] * kLog2e;
+  const float dq_dot = dvec[((int64_t)batch * nh + head) * s + qc];
+  const int last_q = min(qb * 128 + 127, s - 1);
+  const int ntile = last_q / BT + 1;
+  const int wave_last = min(q0 + 31, s - 1) / BT;
+
+  TileSrc ksrc, vsrc;
+  ksrc.init(base + H + head * D, ld, s, wave, lane);
+  vsrc.init(base + 2 * H + head * D, ld, s, wave, lane);
+  auto load_tile = [&](int t, int st) {
+    ksrc.load(t * BT, smem + st * STAGE, wave);
+    vsrc.load(t * BT, smem + st * STAGE + TILE, wave);
+  };
+  FragOff fo;
+  fo.init(lane);
+  const uint32_t lds0 = lds_u32(smem);
+
+  f32x16 dq[D / 32];
+#pragma unroll
+  for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dq[mt][r] = 0.f;
+  const float sl2 = scale * kLog2e;
+  const int qthr = q - 4 * g;
+
+  auto tile = [&](int t, auto diag_c) {
+    constexpr bool DIAG = decltype(diag_c)::value;
+    const uint32_t ks_ = lds0 + (t & 1) * STAGE, vs = ks_ + TILE;
+    // ---- S^T = K Q^T and dP^T = V dO^T: 2 key blocks x 8 d-steps each
+    f32x16 sacc[2], pacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[kb][r] = pacc[kb][r] = 0.f;
+    bf16x8 fr[32];
+    auto read_f = [&](auto ic) {
+      constexpr int i = decltype(ic)::value, w = i % 2, kb = (i / 2) % 2, ks = i / 4;
+      fr[i] = ds_b128<kb * 32 * ROWB>((w ? vs : ks_) + fo.row[ks]);
+    };
+    constexpr int WF = 10;   // fragments in flight
+    static_for<WF>([&](auto ic) { read_f(ic); });
+    static_for<32>([&](auto ic) {
+      constexpr int i = decltype(ic)::value, w = i % 2, kb = (i / 2) % 2, ks = i / 4;
+      constexpr int issued = (i + WF < 32) ? i + WF : 32;
+      wait_lgkm<issued - i - 1>();
+      pin(fr[i]);
+      if constexpr (w == 0) sacc[kb] = Mma<bf16>::run(fr[i], qf[ks], sacc[kb]);
+      else pacc[kb] = Mma<bf16>::run(fr[i], df[ks], pacc[kb]);
+      if constexpr (i + WF < 32) read_f(std::integral_constant<int, i + WF>{});
+    });
+    // ---- dS^T = P^T (dP^T - D), P^T = exp2(S^T s log2e - lse log2e)
+    float d[2][16];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], sl2, -lse2));
+        if constexpr (DIAG) {
+          if (32 * kb + 8 * (j / 4) + (j % 4) > qthr - t * BT) pv = 0.f;
+        }
+        d[kb][j] = pv * (pacc[kb][j] - dq_dot);
+      }
+    bf16x8 sb[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) sb[u] = to_frag(&d[u / 2][8 * (u % 2)]);
+    // ---- dQ^T += K^T dS^T: 4 key steps x 4 d tiles
+    s16x4 lo[16], hi[16];
+    auto read_t = [&](auto ic) {
+      constexpr int i = decltype(ic)::value, mt = i % 4, u = i / 4;
+      constexpr int roff = 16 * u * ROWB;
+      lo[i] = ds_tr16<roff>(ks_ + fo.lo[mt]);
+      hi[i] = ds_tr16<roff>(ks_ + fo.hi[mt]);
+    };
+    constexpr int WT = 7;   // transposed fragments in flight
+    static_for<WT>([&](auto ic) { read_t(ic); });
+    static_for<16>([&](auto ic) {
+      constexpr int i = decltype(ic)::value, mt = i % 4, u = i / 4;
+      constexpr int issued = (i + WT < 16) ? i + WT : 16;
+      wait_lgkm<2 * (issued - i - 1)>();
+      s16x8 v8 = {lo[i][0], lo[i][1], lo[i][2], lo[i][3], hi[i][0], hi[i][1], hi[i][2], hi[i][3]};
+      bf16x8 f = *reinterpret_cast<bf16x8*>(&v8);
+      pin(f);
+      dq[mt] = Mma<bf16>::run(f, sb[u], dq[mt]);
+      if constexpr (i + WT < 16) read_t(std::integral_constant<int, i + WT>{});
+    });
+  };
+
+  load_tile(0, 0);
+  if (ntile > 1) {
+    load_tile(1, 1);
+    wait_vm<8>();
+  } else {
+    wait_vm<0>();
+  }
+  lds_barrier();
+  for (int t = 0; t < ntile; ++t) {
+    if (t <= wave_last) {
+      if ((t + 1) * BT - 1 > q0) tile(t, std::true_type{});
+      else tile(t, std::false_type{});
+    }
+    wait_vm<0>();
+    lds_barrier();
+    if (t + 2 < ntile) load_tile(t + 2, t & 1);
+  }
+
+  if (q < s) {
+    bf16* row = dqkv + ((int64_t)batch * s + q) * ld + head * D;
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+      for (int j4 = 0; j4 < 4; ++j4) {
+        typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+        bf16x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = (bf16)(dq[mt][4 * j4 + j] * scale);
+        *reinterpret_cast<bf16x4*>(row + 32 * mt + acc_row(4 * j4, lane)) = w;
+      }
+  }
+}
+
+hipError_t attention_bwd_v3_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
+                                   void* dqkv, const float* dvec, hipStream_t st) {
+  if (d != D) return hipErrorInvalidValue;
+  const float scale = 1.0f / sqrtf((float)d);
+  const int nblk = (s + 127) / 128;
+  hipLaunchKernelGGL(attn_bwd_dkdv_v3_kernel, dim3(nblk * nh * b), dim3(256), 0, st, (const bf16*)qkv,
+                     (const bf16*)dout, lse, dvec, (bf16*)dqkv, b, s, nh, scale);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_bwd_dq_v3_kernel, dim3(nblk * nh * b), dim3(256), 0, st, (const bf16*)qkv,
+                     (const bf16*)dout, lse, dvec, (bf16*)dqkv, b, s, nh, scale);
+  return hipGetLastError();
+}
+
+}  // namespace tps

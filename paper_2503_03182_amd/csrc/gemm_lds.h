@@ -107,6 +107,7 @@ __device__ __forceinline__ void wait_lgkm() {
 }
 // The value is not consumed before this point (pins uses after a wait).
 __device__ __forceinline__ void pin(bf16x8& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ void pin(f32x4& v) { asm volatile("" : "+v"(v)); }
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 // Per-lane LDS byte offsets of the fragments a wave reads from one stage,

@@ -62,6 +62,9 @@ hipError_t attention_fwd_v2_launch(int b, int s, int nh, int d, const void* qkv,
 // bf16, head dim 128: 32 queries per wave on 32x32x16 MFMAs (attention_fwd.hip)
 hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
                                    hipStream_t st);
+// bf16, head dim 128: dK/dV by 32-key waves, dQ by 32-query waves (attention_bwd.hip)
+hipError_t attention_bwd_v3_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
+                                   void* dqkv, const float* dvec, hipStream_t st);
 hipError_t attention_bwd_v2_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
                                    void* dqkv, const float* dvec, hipStream_t st);
 

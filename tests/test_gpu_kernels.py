@@ -182,7 +182,12 @@ def test_attention_fwd(dtype, b, s, nh, d):
     assert np.abs(lse.cpu().numpy() - lse_ref).max() < (1e-4 if dtype == "f32" else 2e-2)
 
 
-@pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_CASES)
+# grids of at least 512 blocks of 128 rows take the 32-row-per-wave backward;
+# ragged lengths in both
+ATTN_BWD_CASES = ATTN_CASES + [("bf16", 2, 130, 128, 128), ("bf16", 2, 520, 52, 128)]
+
+
+@pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_BWD_CASES)
 def test_attention_bwd(dtype, b, s, nh, d):
     import torch
     h = nh * d
