@@ -1,10 +1,15 @@
 // Fused causal attention forward, bf16, head dim 128, on 32x32x16 MFMAs.
 //
-// Work split.  A workgroup of 4 waves owns 128 consecutive queries of one
-// (batch, head); each wave owns 32 of them, so every K/V fragment it reads
-// from LDS feeds 32 queries (LDS traffic per MFMA flop is half that of a
-// 16-query wave).  Workgroups are launched heaviest first (last query block
-// first), so the causal triangle's short blocks fill in behind the long ones.
+// Work split.  A workgroup of 2 QW waves owns 32 QW consecutive queries of one
+// (batch, head) and splits both ways: wave w takes the 32 queries of slice
+// w % QW against the key tiles of part w / QW (part 0: the first ceil(n/2) of
+// the block's n key tiles, part 1: the rest, which hold the diagonal).  The
+// causal triangle's longest chain of key tiles per wave is thus halved, which
+// balances the grid when there are few (batch, head) pairs, and each K/V
+// fragment a wave reads from LDS still feeds 32 queries.  At the end the two
+// parts of each query slice are merged in a fixed order (part 0, then part 1)
+// through LDS: m = max(m0, m1), O = O0 2^(m0-m) + O1 2^(m1-m), same for the
+// row sums.  Workgroups are launched heaviest first.
 //
 // Per 64-key tile and wave (transposed formulation, queries along MFMA N):
 //   S^T[key, q]  = K Q^T          16 MFMAs; K from LDS (ds_read_b128),
@@ -14,69 +19,36 @@
 //                                 (l ^ 32) the other 16;
 //   O^T[d, q]   += V^T P^T        16 MFMAs; P^T straight from the S^T
 //                                 accumulators, V^T from LDS through
-//                                 transposing reads.  The contraction index k
-//                                 of a 16-key step maps to key
-//                                 8 (i / 4) + 4 (k / 8) + i % 4 (i = k % 8), the
-//                                 order in which the S^T accumulators hold
-//                                 keys; V rows are read in that order.
+//                                 transposing reads in the accumulators' key
+//                                 order (attn_tiles.h).
 //
-// Data movement.  K and V tiles (64 x 128 bf16 each) are copied global -> LDS
-// by buffer loads that write LDS directly, into a two-stage ring; chunks of
-// 16 bytes are XOR-swizzled per row (f(r) = 4 (r & 3) + ((r >> 2) & 3)) so
-// that both the 16-row ds_read_b128 and the 4-row transposing reads are free
-// of bank conflicts.  LDS reads are inline assembly with explicit lgkmcnt
-// waits (the compiler would otherwise drain all tile loads before each LDS
-// read); one barrier per tile hands the stage of tile t back for tile t+2.
+// Data movement.  Each key part streams its K and V tiles (64 x 128 bf16 each)
+// global -> LDS by buffer loads that write LDS directly, into its own
+// two-stage ring; LDS reads are inline assembly with explicit lgkmcnt waits
+// (the compiler would otherwise drain all tile loads before each LDS read);
+// one barrier per tile hands the stage of tile t back for tile t+2.
 //
 // Numerics: scores are scaled into the log2 domain (scale * log2 e), the
-// softmax uses exp2; lse is returned in natural log.  Every reduction runs in
-// a fixed order, so results are bitwise reproducible.
-#include "gemm_lds.h"
-#include "kernels.h"
-#include "tps_device.h"
+// softmax uses exp2; lse is returned in natural log.  Causal masking runs only
+// on tiles that cross the diagonal; O is rescaled only when some lane's
+// running max grew (the multiplier is exactly 1 otherwise).  Every reduction
+// runs in a fixed order, so results are bitwise reproducible.
+#include "attn_tiles.h"
 
 namespace tps {
 
-namespace af {
+using namespace at;
 
-using gl::ds_b128;
-using gl::ds_tr16;
-using gl::lds_barrier;
-using gl::lds_u32;
-using gl::pin;
-using gl::static_for;
-using gl::wait_lgkm;
-
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((ext_vector_type(4))) short s16x4;
-typedef __attribute__((ext_vector_type(8))) short s16x8;
-
-constexpr int D = 128;          // head dim
-constexpr int BQ = 128;         // queries per workgroup
-constexpr int BK = 64;          // keys per tile
-constexpr int ROWB = D * 2;     // bytes per LDS row
-constexpr int TILE = BK * ROWB; // one K or V tile (16 KB)
-constexpr int STAGE = 2 * TILE; // K and V
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
-
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
-// byte offset of 16-byte chunk c of row r in a tile
-__device__ __forceinline__ int off(int r, int c) { return r * ROWB + ((c ^ swz(r)) << 4); }
-
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-}  // namespace af
-
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(2, 2)))
-void attn_fwd_v3_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, float* __restrict__ lse, int b, int s,
+template <int QW, int PARTS>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * QW * PARTS, 64 * QW * PARTS),
+                          amdgpu_waves_per_eu(QW / 2, QW / 2)))
+void attn_fwd_sk_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, float* __restrict__ lse, int b, int s,
                         int nh, float scale) {
-  using namespace af;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  constexpr int BQ = 32 * QW;        // queries per workgroup
+  constexpr int STAGE = 2 * TILE;    // K and V
+  constexpr int RING = 2 * STAGE;    // one key part's two stages
+  static_assert(PARTS == 1 || PARTS == 2, "key parts");
+  __shared__ __attribute__((aligned(1024))) char smem[PARTS * RING];
 
   const int H = nh * D;
   const int64_t ld = 3 * (int64_t)H;
@@ -87,82 +59,40 @@ void attn_fwd_v3_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
   const int qb = nqb - 1 - idx / (nh * b);   // heaviest blocks first
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int q0 = qb * BQ + wave * 32;        // first query of this wave
+  const int slice = wave % QW, part = wave / QW;
+  const int q0 = qb * BQ + slice * 32;   // first query of this wave
   const int q = q0 + (lane & 31);            // this lane's query
-  const int g = lane >> 5;                   // half of the 64 lanes
+  const int g = lane >> 5;
 
   const bf16* base = qkv + (int64_t)batch * s * ld;
-  // tiles the workgroup streams, and the last one this wave needs
-  const int last_q = min(qb * BQ + BQ, s) - 1;
-  const int ntile = last_q / BK + 1;
-  const int wave_last = min(q0 + 31, s - 1) / BK;
+  // key tiles of the block, and this part's share of them
+  const int nt = (min(qb * BQ + BQ, s) - 1) / BT + 1;
+  const int nt0 = PARTS == 1 ? nt : (nt + 1) / 2;
+  const int tb = part ? nt0 : 0;             // first tile of this part
+  const int np = part ? nt - nt0 : nt0;      // tiles of this part
+  const int nit = nt0;                       // loop trips (both parts, for the barriers)
+  const int wave_last = min(q0 + 31, s - 1) / BT;
 
   // Q^T fragments (B operand): lane holds q's d = 16 ks + 8 g .. +8
   bf16x8 qf[D / 16];
   {
     const bf16* qrow = base + (int64_t)min(q, s - 1) * ld + head * D + 8 * g;
 #pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      const u32x4 w = *reinterpret_cast<const u32x4*>(qrow + 16 * ks);
-      qf[ks] = *reinterpret_cast<const bf16x8*>(&w);
-    }
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) asm volatile("" ::"v"(qf[ks]));   // wait for them here
+    for (int ks = 0; ks < D / 16; ++ks) qf[ks] = load_frag_settled(qrow + 16 * ks);
   }
 
-  // Tile loads: 16 one-KB instructions for K and 16 for V; wave w issues
-  // instructions 4w .. 4w+3 of each.  Instruction i covers rows 4i .. 4i+3;
-  // lane l writes LDS slot (row 4i + l / 16, chunk l % 16), which holds
-  // logical chunk (l % 16) ^ swz(row); swz depends on i only through i % 4.
-  // buffer ranges end at this sequence's last row: rows past s read as zeros
-  const int64_t kbytes = ((int64_t)(s - 1) * ld + D) * 2;
-  const int nrec = kbytes < 0x7FFFFFFF ? (int)kbytes : 0x7FFFFFFF;
-  const __amdgpu_buffer_rsrc_t rk =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(base + H + head * D), (short)0, nrec, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rv =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(base + 2 * H + head * D), (short)0, nrec, 0x00020000);
-  uint32_t voff[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int i = wave * 4 + j;
-    const int r = 4 * i + (lane >> 4);
-    const int c = (lane & 15) ^ swz(r);
-    voff[j] = (uint32_t)(((int64_t)(lane >> 4) * ld + c * 8) * 2);
-  }
-  // The row offset goes into the per-lane offset, which the buffer range
-  // check covers (rows at or past s then load zeros).
+  TileSrcN<QW> ksrc, vsrc;
+  ksrc.init(base + H + head * D, ld, s, slice, lane);
+  vsrc.init(base + 2 * H + head * D, ld, s, slice, lane);
+  char* const ring = smem + part * RING;
   auto load_tile = [&](int t, int st) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = wave * 4 + j;
-      const uint32_t vo = voff[j] + (uint32_t)(((int64_t)t * BK + 4 * i) * ld * 2);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(smem + st * STAGE + i * 1024), 16, vo, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(smem + st * STAGE + TILE + i * 1024), 16, vo, 0, 0, 0);
-    }
+    ksrc.load(t * BT, ring + st * STAGE);
+    vsrc.load(t * BT, ring + st * STAGE + TILE);
   };
-
-  // per-lane LDS offsets
-  //  K fragment (key block kb, d-step ks): row 32 kb + l % 32, chunk 2 ks + g
-  uint32_t koff[D / 16];
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) koff[ks] = off(lane & 31, 2 * ks + g);
-  //  V^T fragment (d tile mt, 16-key step u of the tile): two 4-row
-  //  transposing reads at rows 16 u + 4 g + (s >> 2) (lo) and 8 further (hi),
-  //  columns 32 mt + 16 (G & 1) + 4 (s & 3) (G = l / 16, s = l % 16).  The row
-  //  swizzle repeats every 16 rows, so u enters as an immediate; lo and hi
-  //  differ in it.
-  uint32_t voffl[D / 32], voffh[D / 32];
-  {
-    const int G = lane >> 4, sl = lane & 15;
-    const int r = 4 * (G >> 1) + (sl >> 2);
-#pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt) {
-      const int col = 32 * mt + 16 * (G & 1) + 4 * (sl & 3);
-      voffl[mt] = off(r, col >> 3) + (col & 7) * 2;
-      voffh[mt] = off(r + 8, col >> 3) + (col & 7) * 2;
-    }
-  }
-  const uint32_t lds0 = lds_u32(smem);
+  constexpr int LPT = 2 * TileSrcN<QW>::IPW;   // load instructions per wave per tile
+  FragOff fo;
+  fo.init(lane);
+  const uint32_t ring0 = lds_u32(ring);
 
   f32x16 oacc[D / 32];
 #pragma unroll
@@ -171,23 +101,13 @@ void attn_fwd_v3_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
     for (int r = 0; r < 16; ++r) oacc[mt][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
   const float sl2 = scale * kLog2e;
-
-  load_tile(0, 0);
-  if (ntile > 1) {
-    load_tile(1, 1);
-    wait_vm<8>();   // tile 0 landed (8 load instructions per wave per tile)
-  } else {
-    wait_vm<0>();
-  }
-  lds_barrier();
-
-  // per-lane constant of the causal test: key 64 t + c > q  <=>  c > q - 4 g - 64 t,
+  // causal test on a diagonal tile: key 64 t + c > q  <=>  c > q - 4 g - 64 t,
   // c = 32 kb + 8 (j / 4) + j % 4 the key offset of accumulator j of block kb
   const int qthr = q - 4 * g;
   // one 64-key tile; DIAG: some key of the tile lies past some query of the wave
-  auto tile = [&](int t, auto diag_c) {
+  auto tile = [&](int t, int st, auto diag_c) {
     constexpr bool DIAG = decltype(diag_c)::value;
-    const uint32_t ks_lds = lds0 + (t & 1) * STAGE, vs_lds = ks_lds + TILE;
+    const uint32_t ks_lds = ring0 + st * STAGE, vs_lds = ks_lds + TILE;
     // ---- S^T = K Q^T: 2 key blocks x 8 d-steps, K fragments 8 ahead
     f32x16 sacc[2];
 #pragma unroll
@@ -197,7 +117,7 @@ void attn_fwd_v3_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
     bf16x8 kf[16];
     auto read_k = [&](auto ic) {
       constexpr int i = decltype(ic)::value, kb = i % 2, ks = i / 2;
-      kf[i] = ds_b128<kb * 32 * ROWB>(ks_lds + koff[ks]);
+      kf[i] = ds_b128<kb * 32 * ROWB>(ks_lds + fo.row[ks]);
     };
     static_for<8>([&](auto ic) { read_k(ic); });
     static_for<16>([&](auto ic) {
@@ -212,7 +132,7 @@ void attn_fwd_v3_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
     // ---- online softmax on raw scores (the scale is positive, so the max
     // commutes with it; it enters the exponent's FMA)
     if constexpr (DIAG) {
-      const int thr = qthr - t * BK;
+      const int thr = qthr - t * BT;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -258,8 +178,8 @@ void attn_fwd_v3_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
     auto read_v = [&](auto ic) {
       constexpr int i = decltype(ic)::value, u = i / 4, m2 = i % 4;   // u: 16-key step of the tile
       constexpr int roff = 16 * u * ROWB;
-      vlo[i] = ds_tr16<roff>(vs_lds + voffl[m2]);
-      vhi[i] = ds_tr16<roff>(vs_lds + voffh[m2]);
+      vlo[i] = ds_tr16<roff>(vs_lds + fo.lo[m2]);
+      vhi[i] = ds_tr16<roff>(vs_lds + fo.hi[m2]);
     };
     static_for<7>([&](auto ic) { read_v(ic); });
     static_for<16>([&](auto ic) {
@@ -274,16 +194,53 @@ void attn_fwd_v3_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
     });
   };
 
-  for (int t = 0; t < ntile; ++t) {
-    if (t <= wave_last) {
-      if ((t + 1) * BK - 1 > q0) tile(t, std::true_type{});
-      else tile(t, std::false_type{});
+  // prologue: the first two tiles of each part
+  if (np > 0) load_tile(tb, 0);
+  if (np > 1) {
+    load_tile(tb + 1, 1);
+    wait_vm<LPT>();   // the first tile landed
+  } else {
+    wait_vm<0>();
+  }
+  lds_barrier();
+  for (int it = 0; it < nit; ++it) {
+    const int t = tb + it;
+    if (it < np && t <= wave_last) {
+      if ((t + 1) * BT - 1 > q0) tile(t, it & 1, std::true_type{});
+      else tile(t, it & 1, std::false_type{});
     }
-    // hand stage t back: tile t+1 (the only loads in flight) has landed and
-    // every wave is done with tile t
+    // hand the stage back: the next tile (the only loads in flight) has
+    // landed and every wave is done with this one
     wait_vm<0>();
     lds_barrier();
-    if (t + 2 < ntile) load_tile(t + 2, t & 1);
+    if (it + 2 < np) load_tile(t + 2, it & 1);
+  }
+
+  // ---- merge the key parts of each query slice through LDS (ring memory is
+  // free after the loop's last barrier): part 1 parks m, l and O^T
+  if constexpr (PARTS == 2) {
+    float* park = reinterpret_cast<float*>(smem) + slice * (D / 32 * 16 + 2) * 64;
+    if (part == 1) {
+#pragma unroll
+      for (int m2 = 0; m2 < D / 32; ++m2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) park[(m2 * 16 + r) * 64 + lane] = oacc[m2][r];
+      park[(D / 32 * 16) * 64 + lane] = m_run;
+      park[(D / 32 * 16 + 1) * 64 + lane] = l_run;
+    }
+    __syncthreads();
+    if (part == 1) return;
+    {
+      const float m1 = park[(D / 32 * 16) * 64 + lane], l1 = park[(D / 32 * 16 + 1) * 64 + lane];
+      const float m = fmaxf(m_run, m1);   // part 0 always holds key 0 <= q: m is finite
+      const float a0 = __builtin_amdgcn_exp2f(m_run - m), a1 = __builtin_amdgcn_exp2f(m1 - m);
+#pragma unroll
+      for (int m2 = 0; m2 < D / 32; ++m2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[m2][r] = oacc[m2][r] * a0 + park[(m2 * 16 + r) * 64 + lane] * a1;
+      l_run = l_run * a0 + l1 * a1;
+      m_run = m;
+    }
   }
 
   // ---- normalise and store: lane holds O^T[32 mt + acc_row(j, l)][q]
@@ -306,11 +263,22 @@ void attn_fwd_v3_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
 }
 
 hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse, hipStream_t st) {
-  if (d != af::D) return hipErrorInvalidValue;
+  if (d != D) return hipErrorInvalidValue;
   const float scale = 1.0f / sqrtf((float)d);
-  const int nqb = (s + af::BQ - 1) / af::BQ;
-  hipLaunchKernelGGL(attn_fwd_v3_kernel, dim3(nqb * nh * b), dim3(256), 0, st, (const bf16*)qkv, (bf16*)o, lse, b, s,
-                     nh, scale);
+  // 128 queries per workgroup: with two resident workgroups per CU when the
+  // grid fills the chip twice over, else with the key tiles split in two
+  // parts inside the workgroup; 64 queries in two parts below one workgroup
+  // per CU
+  const int n128 = (s + 127) / 128 * nh * b;
+  const bf16* x = (const bf16*)qkv;
+  if (n128 >= 512) {
+    hipLaunchKernelGGL((attn_fwd_sk_kernel<4, 1>), dim3(n128), dim3(256), 0, st, x, (bf16*)o, lse, b, s, nh, scale);
+  } else if (n128 >= 256) {
+    hipLaunchKernelGGL((attn_fwd_sk_kernel<4, 2>), dim3(n128), dim3(512), 0, st, x, (bf16*)o, lse, b, s, nh, scale);
+  } else {
+    hipLaunchKernelGGL((attn_fwd_sk_kernel<2, 2>), dim3((s + 63) / 64 * nh * b), dim3(256), 0, st, x, (bf16*)o, lse,
+                       b, s, nh, scale);
+  }
   return hipGetLastError();
 }
 

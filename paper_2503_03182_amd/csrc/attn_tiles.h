@@ -53,35 +53,42 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, int64_t
 }
 
 // Rows of one head's 128 columns in a [rows][ld] bf16 matrix, copied into
-// LDS tiles by 16 one-KB buffer-to-LDS instructions, 4 per wave of a 4-wave
-// workgroup.  Instruction i covers rows 4i .. 4i+3; lane l writes LDS slot
-// (row 4i + l / 16, chunk l % 16), which holds logical chunk
-// (l % 16) ^ swz(row); swz depends on i only through i % 4.  The row offset
-// is part of the per-lane (range-checked) offset: rows at or past `rows` read
-// as zeros.
-struct TileSrc {
+// LDS tiles by 16 one-KB buffer-to-LDS instructions shared by NW waves (16 /
+// NW each).  Instruction i covers rows 4i .. 4i+3; lane l writes LDS slot
+// (row 4i + l / 16, chunk l % 16), which holds logical chunk (l % 16) ^
+// swz(row); swz depends on i only through i % 4.  The row offset is part of
+// the per-lane (range-checked) offset: rows at or past `rows` read as zeros.
+template <int NW>
+struct TileSrcN {
+  static constexpr int IPW = 16 / NW;   // instructions per wave per tile
+  static_assert(IPW % 4 == 0, "instruction parity pattern");
   __amdgpu_buffer_rsrc_t r;
   uint32_t voff[4];
   int64_t ld;
+  int w;   // this wave's index among the NW
   __device__ __forceinline__ void init(const bf16* base, int64_t ld_, int rows, int wave, int lane) {
     ld = ld_;
+    w = wave;
     r = rsrc(base, ((int64_t)(rows - 1) * ld + D) * 2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int i = wave * 4 + j;
-      const int row = 4 * i + (lane >> 4);
+      const int row = 4 * j + (lane >> 4);   // i % 4 == j
       const int c = (lane & 15) ^ swz(row);
       voff[j] = (uint32_t)(((int64_t)(lane >> 4) * ld + c * 8) * 2);
     }
   }
-  __device__ __forceinline__ void load(int row0, char* tile, int wave) const {
+  __device__ __forceinline__ void load(int row0, char* tile) const {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = wave * 4 + j;
-      const uint32_t vo = voff[j] + (uint32_t)(((int64_t)row0 + 4 * i) * ld * 2);
+    for (int j = 0; j < IPW; ++j) {
+      const int i = w * IPW + j;
+      const uint32_t vo = voff[j % 4] + (uint32_t)(((int64_t)row0 + 4 * i) * ld * 2);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)(tile + i * 1024), 16, vo, 0, 0, 0);
     }
   }
+};
+// four waves per tile (the backward kernels)
+struct TileSrc : TileSrcN<4> {
+  __device__ __forceinline__ void load(int row0, char* tile, int) const { TileSrcN<4>::load(row0, tile); }
 };
 
 // 64 consecutive f32 of a per-row vector (lse, D), one buffer-to-LDS

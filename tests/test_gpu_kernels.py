@@ -167,7 +167,14 @@ ATTN_CASES = [  # (dtype, b, s, heads, d)
 ]
 
 
-@pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_CASES)
+# head dim 128: grids of 256 to 511 blocks of 128 rows take the forward with
+# the key tiles split in two parts per workgroup, of at least 512 such blocks
+# the forward without the split and the 32-row-per-wave backward; ragged
+# lengths throughout
+ATTN_BIG_CASES = [("bf16", 2, 130, 128, 128), ("bf16", 2, 520, 52, 128), ("bf16", 1, 1000, 40, 128)]
+
+
+@pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_CASES + ATTN_BIG_CASES)
 def test_attention_fwd(dtype, b, s, nh, d):
     import torch
     h = nh * d
@@ -182,12 +189,7 @@ def test_attention_fwd(dtype, b, s, nh, d):
     assert np.abs(lse.cpu().numpy() - lse_ref).max() < (1e-4 if dtype == "f32" else 2e-2)
 
 
-# grids of at least 512 blocks of 128 rows take the 32-row-per-wave backward;
-# ragged lengths in both
-ATTN_BWD_CASES = ATTN_CASES + [("bf16", 2, 130, 128, 128), ("bf16", 2, 520, 52, 128)]
-
-
-@pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_BWD_CASES)
+@pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_CASES + ATTN_BIG_CASES)
 def test_attention_bwd(dtype, b, s, nh, d):
     import torch
     h = nh * d
