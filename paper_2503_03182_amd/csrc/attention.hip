@@ -563,10 +563,7 @@ hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const vo
                          static_cast<const bf16*>(o), static_cast<const bf16*>(dout), dvec, b, s, nh);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // 32-row waves with one wave per SIMD need at least two 128-row blocks per
-    // CU to balance the causal triangle; smaller grids keep the 16-row pairs
-    if (d == 128 && (int64_t)((s + 127) / 128) * nh * b >= 512)
-      return attention_bwd_v3_launch(b, s, nh, d, qkv, lse, dout, dqkv, dvec, st);
+    if (d == 128) return attention_bwd_v3_launch(b, s, nh, d, qkv, lse, dout, dqkv, dvec, st);
     return attention_bwd_v2_launch(b, s, nh, d, qkv, lse, dout, dqkv, dvec, st);
   }
   return d == 64 ? bwd_launch<float, 64>(b, s, nh, qkv, o, lse, dout, dqkv, dvec, st)

@@ -6,19 +6,24 @@
 //   dS_ij = P_ij (dP_ij - D_i),
 //   dV_j  = sum_i P_ij dO_i,  dK_j = s sum_i dS_ij q_i,  dQ_i = s sum_j dS_ij k_j,
 // summed over the causal triangle j <= i.  Two kernels, both deterministic
-// (every output element is produced by one wave in a fixed order, no atomics):
+// (every output element is produced by one wave, or summed from two waves'
+// partials, in a fixed order; no atomics).  Each runs one wave per SIMD and
+// comes in two shapes: 4 slices of 32 rows (128 rows per workgroup) with one
+// tile stream, or 2 slices (64 rows) whose tile range is split in two parts,
+// each part with its own stream and ring, summed part 0 first through LDS at
+// the end; the second halves the longest chain of tiles of small grids.
 //
-// dK/dV (attn_bwd_dkdv_v3_kernel): a 4-wave workgroup owns 128 keys, 32 per
-//   wave, K and V fragments in registers; 64-query tiles of Q, dO, lse and D
-//   stream through a two-stage LDS ring.  With keys along the MFMA N
+// dK/dV (attn_bwd_dkdv_v3_kernel): a workgroup owns 32 keys per slice, K and
+//   V fragments in registers; 64-query tiles of Q, dO, lse and D stream
+//   through a two-stage LDS ring.  With keys along the MFMA N
 //   dimension (one key per lane):
 //     S  = Q K^T, dP = dO V^T        (Q, dO rows from LDS)
 //     dV^T += dO^T P, dK^T += Q^T dS (dO^T, Q^T through transposing reads, in
 //                                     the accumulators' query order)
 //   64 MFMAs per tile; one wave per SIMD (the dK/dV accumulators take AGPRs).
-// dQ (attn_bwd_dq_v3_kernel): a 4-wave workgroup owns 128 queries, 32 per
-//   wave, Q and dO fragments plus lse and D in registers; 64-key tiles of K
-//   and V stream through the ring.  With queries along N:
+// dQ (attn_bwd_dq_v3_kernel): a workgroup owns 32 queries per slice, Q and
+//   dO fragments plus lse and D in registers; 64-key tiles of K and V stream
+//   through the ring.  With queries along N:
 //     S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T
 //   48 MFMAs per tile; one wave per SIMD (Q, dO fragments and dQ
 //   accumulators do not fit the register budget of two).
@@ -34,13 +39,17 @@ using namespace at;
 // ---------------------------------------------------------------------------
 // dK, dV
 // ---------------------------------------------------------------------------
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+template <int KW, int PARTS>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * KW * PARTS, 64 * KW * PARTS), amdgpu_waves_per_eu(1, 1)))
 void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
                              const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
                              int b, int s, int nh, float scale) {
   constexpr int VEC = 1024;                    // LDS bytes per per-row vector (64 f32 + landing pad)
   constexpr int STAGE = 2 * TILE + 2 * VEC;    // Q, dO, lse, D
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  constexpr int RING = 2 * STAGE;              // one query part's two stages
+  constexpr int BKEY = 32 * KW;                // keys per workgroup
+  static_assert(PARTS == 1 || PARTS == 2, "query parts");
+  __shared__ __attribute__((aligned(1024))) char smem[PARTS * RING];
 
   const int H = nh * D;
   const int64_t ld = 3 * (int64_t)H;
@@ -51,7 +60,8 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
-  const int k0 = kb * 128 + wave * 32;         // first key of this wave
+  const int slice = wave % KW, part = wave / KW;
+  const int k0 = kb * BKEY + slice * 32;       // first key of this wave
   const int key = k0 + (lane & 31);
 
   const bf16* base = qkv + (int64_t)batch * s * ld;
@@ -65,29 +75,38 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
       vf[ks] = load_frag_settled(krow + H + 16 * ks);
     }
   }
-  // query tiles from the one holding this workgroup's first key to the end
-  const int t0 = (kb * 128) / BT;
+  // query tiles from the one holding this workgroup's first key to the end,
+  // and this part's share of them
+  const int t0 = (kb * BKEY) / BT;
   const int ntile = (s + BT - 1) / BT;
-  const int wave_first = k0 / BT;               // earlier tiles have no query >= any key of the wave
+  const int n = ntile - t0;
+  const int n0 = PARTS == 1 ? n : (n + 1) / 2;
+  const int tb = part ? t0 + n0 : t0;          // first tile of this part
+  const int np = part ? n - n0 : n0;           // tiles of this part
+  const int nit = n0;                          // loop trips (both parts, for the barriers)
+  const int wave_first = k0 / BT;              // earlier tiles have no query >= any key of the wave
 
-  TileSrc qsrc, dsrc;
-  qsrc.init(base + head * D, ld, s, wave, lane);
-  dsrc.init(dout + (int64_t)batch * s * H + head * D, H, s, wave, lane);
+  TileSrcN<KW> qsrc, dsrc;
+  qsrc.init(base + head * D, ld, s, slice, lane);
+  dsrc.init(dout + (int64_t)batch * s * H + head * D, H, s, slice, lane);
   VecSrc lsrc, vsrc;
   lsrc.init(lse + ((int64_t)batch * nh + head) * s, s);
   vsrc.init(dvec + ((int64_t)batch * nh + head) * s, s);
+  char* const ring = smem + part * RING;
   auto load_tile = [&](int t, int st) {
-    char* p = smem + st * STAGE;
-    qsrc.load(t * BT, p, wave);
-    dsrc.load(t * BT, p + TILE, wave);
-    if (wave == 0) {
+    char* p = ring + st * STAGE;
+    qsrc.load(t * BT, p);
+    dsrc.load(t * BT, p + TILE);
+    if (slice == 0) {
       lsrc.load(t * BT, p + 2 * TILE, lane);
       vsrc.load(t * BT, p + 2 * TILE + VEC, lane);
     }
   };
+  // load instructions per tile: the tiles' share, plus the vectors for slice 0
+  constexpr int LPT = 2 * TileSrcN<KW>::IPW;
   FragOff fo;
   fo.init(lane);
-  const uint32_t lds0 = lds_u32(smem);
+  const uint32_t lds0 = lds_u32(ring);
 
   f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -99,9 +118,9 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
   // c = 32 qb + 8 (j / 4) + j % 4 the query offset of accumulator j of block qb
   const int kthr = key - 4 * g;
 
-  auto tile = [&](int t, auto diag_c) {
+  auto tile = [&](int t, int st, auto diag_c) {
     constexpr bool DIAG = decltype(diag_c)::value;
-    const uint32_t qs = lds0 + (t & 1) * STAGE, ds = qs + TILE, ls = ds + TILE, vs = ls + VEC;
+    const uint32_t qs = lds0 + st * STAGE, ds = qs + TILE, ls = ds + TILE, vs = ls + VEC;
     // ---- S = Q K^T and dP = dO V^T: 2 query blocks x 8 d-steps each
     f32x16 sacc[2], pacc[2];
 #pragma unroll
@@ -185,25 +204,51 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
     });
   };
 
-  // tile t lives in stage t & 1
-  load_tile(t0, t0 & 1);
-  if (t0 + 1 < ntile) {
-    load_tile(t0 + 1, (t0 + 1) & 1);
-    if (wave == 0) wait_vm<10>();   // tile t0 landed (10 loads per tile for wave 0, 8 for the others)
-    else wait_vm<8>();
+  // the part's i-th tile lives in stage i & 1
+  if (np > 0) load_tile(tb, 0);
+  if (np > 1) {
+    load_tile(tb + 1, 1);
+    if (slice == 0) wait_vm<LPT + 2>();   // the first tile landed
+    else wait_vm<LPT>();
   } else {
     wait_vm<0>();
   }
   lds_barrier();
-  for (int t = t0; t < ntile; ++t) {
-    if (t >= wave_first) {
-      if (t * BT < k0 + 31) tile(t, std::true_type{});   // some query of the tile precedes some key
-      else tile(t, std::false_type{});
+  for (int it = 0; it < nit; ++it) {
+    const int t = tb + it;
+    if (it < np && t >= wave_first) {
+      if (t * BT < k0 + 31) tile(t, it & 1, std::true_type{});   // some query of the tile precedes some key
+      else tile(t, it & 1, std::false_type{});
     }
-    // hand the stage back: tile t+1 has landed, every wave is done with tile t
+    // hand the stage back: the next tile has landed, every wave is done with this one
     wait_vm<0>();
     lds_barrier();
-    if (t + 2 < ntile) load_tile(t + 2, t & 1);
+    if (it + 2 < np) load_tile(t + 2, it & 1);
+  }
+
+  // ---- sum the query parts of each key slice through LDS (ring memory is
+  // free after the loop's last barrier; no tile load is in flight): part 1
+  // parks its dK^T, dV^T, part 0 adds them to its own
+  if constexpr (PARTS == 2) {
+    float* park = reinterpret_cast<float*>(smem) + slice * (2 * D / 32 * 16) * 64;
+    if (part == 1) {
+#pragma unroll
+      for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          park[(mt * 16 + r) * 64 + lane] = dk[mt][r];
+          park[((D / 32 + mt) * 16 + r) * 64 + lane] = dv[mt][r];
+        }
+    }
+    __syncthreads();
+    if (part == 1) return;
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        dk[mt][r] += park[(mt * 16 + r) * 64 + lane];
+        dv[mt][r] += park[((D / 32 + mt) * 16 + r) * 64 + lane];
+      }
   }
 
   // ---- store: lane holds dK^T / dV^T [32 mt + acc_row(j, l)][key]
@@ -230,16 +275,20 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
 // ---------------------------------------------------------------------------
 // dQ
 // ---------------------------------------------------------------------------
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+template <int QW, int PARTS>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * QW * PARTS, 64 * QW * PARTS), amdgpu_waves_per_eu(1, 1)))
 void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
                            const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
                            int b, int s, int nh, float scale) {
   constexpr int STAGE = 2 * TILE;   // K, V
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  constexpr int RING = 2 * STAGE;   // one key part's two stages
+  constexpr int BQ = 32 * QW;       // queries per workgroup
+  static_assert(PARTS == 1 || PARTS == 2, "key parts");
+  __shared__ __attribute__((aligned(1024))) char smem[PARTS * RING];
 
   const int H = nh * D;
   const int64_t ld = 3 * (int64_t)H;
-  const int nqb = (s + 127) / 128;
+  const int nqb = (s + BQ - 1) / BQ;
   const int idx = blockIdx.x;
   const int head = idx % nh;
   const int batch = (idx / nh) % b;
@@ -247,7 +296,8 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
-  const int q0 = qb * 128 + wave * 32;
+  const int slice = wave % QW, part = wave / QW;
+  const int q0 = qb * BQ + slice * 32;
   const int q = q0 + (lane & 31);
 
   const bf16* base = qkv + (int64_t)batch * s * ld;
@@ -264,20 +314,27 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
   }
   const float lse2 = lse[((int64_t)batch * nh + head) * s + qc] * kLog2e;
   const float dq_dot = dvec[((int64_t)batch * nh + head) * s + qc];
-  const int last_q = min(qb * 128 + 127, s - 1);
-  const int ntile = last_q / BT + 1;
+  // key tiles of the workgroup, and this part's share of them
+  const int last_q = min(qb * BQ + BQ - 1, s - 1);
+  const int nt = last_q / BT + 1;
+  const int nt0 = PARTS == 1 ? nt : (nt + 1) / 2;
+  const int tb = part ? nt0 : 0;               // first tile of this part
+  const int np = part ? nt - nt0 : nt0;        // tiles of this part
+  const int nit = nt0;                         // loop trips (both parts, for the barriers)
   const int wave_last = min(q0 + 31, s - 1) / BT;
 
-  TileSrc ksrc, vsrc;
-  ksrc.init(base + H + head * D, ld, s, wave, lane);
-  vsrc.init(base + 2 * H + head * D, ld, s, wave, lane);
+  TileSrcN<QW> ksrc, vsrc;
+  ksrc.init(base + H + head * D, ld, s, slice, lane);
+  vsrc.init(base + 2 * H + head * D, ld, s, slice, lane);
+  char* const ring = smem + part * RING;
   auto load_tile = [&](int t, int st) {
-    ksrc.load(t * BT, smem + st * STAGE, wave);
-    vsrc.load(t * BT, smem + st * STAGE + TILE, wave);
+    ksrc.load(t * BT, ring + st * STAGE);
+    vsrc.load(t * BT, ring + st * STAGE + TILE);
   };
+  constexpr int LPT = 2 * TileSrcN<QW>::IPW;   // load instructions per wave per tile
   FragOff fo;
   fo.init(lane);
-  const uint32_t lds0 = lds_u32(smem);
+  const uint32_t lds0 = lds_u32(ring);
 
   f32x16 dq[D / 32];
 #pragma unroll
@@ -287,9 +344,9 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
   const float sl2 = scale * kLog2e;
   const int qthr = q - 4 * g;
 
-  auto tile = [&](int t, auto diag_c) {
+  auto tile = [&](int t, int st, auto diag_c) {
     constexpr bool DIAG = decltype(diag_c)::value;
-    const uint32_t ks_ = lds0 + (t & 1) * STAGE, vs = ks_ + TILE;
+    const uint32_t ks_ = lds0 + st * STAGE, vs = ks_ + TILE;
     // ---- S^T = K Q^T and dP^T = V dO^T: 2 key blocks x 8 d-steps each
     f32x16 sacc[2], pacc[2];
 #pragma unroll
@@ -349,22 +406,40 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
     });
   };
 
-  load_tile(0, 0);
-  if (ntile > 1) {
-    load_tile(1, 1);
-    wait_vm<8>();
+  if (np > 0) load_tile(tb, 0);
+  if (np > 1) {
+    load_tile(tb + 1, 1);
+    wait_vm<LPT>();   // the first tile landed
   } else {
     wait_vm<0>();
   }
   lds_barrier();
-  for (int t = 0; t < ntile; ++t) {
-    if (t <= wave_last) {
-      if ((t + 1) * BT - 1 > q0) tile(t, std::true_type{});
-      else tile(t, std::false_type{});
+  for (int it = 0; it < nit; ++it) {
+    const int t = tb + it;
+    if (it < np && t <= wave_last) {
+      if ((t + 1) * BT - 1 > q0) tile(t, it & 1, std::true_type{});
+      else tile(t, it & 1, std::false_type{});
     }
     wait_vm<0>();
     lds_barrier();
-    if (t + 2 < ntile) load_tile(t + 2, t & 1);
+    if (it + 2 < np) load_tile(t + 2, it & 1);
+  }
+
+  // ---- sum the key parts of each query slice through LDS, part 0 first
+  if constexpr (PARTS == 2) {
+    float* park = reinterpret_cast<float*>(smem) + slice * (D / 32 * 16) * 64;
+    if (part == 1) {
+#pragma unroll
+      for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) park[(mt * 16 + r) * 64 + lane] = dq[mt][r];
+    }
+    __syncthreads();
+    if (part == 1) return;
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dq[mt][r] += park[(mt * 16 + r) * 64 + lane];
   }
 
   if (q < s) {
@@ -386,13 +461,30 @@ hipError_t attention_bwd_v3_launch(int b, int s, int nh, int d, const void* qkv,
                                    void* dqkv, const float* dvec, hipStream_t st) {
   if (d != D) return hipErrorInvalidValue;
   const float scale = 1.0f / sqrtf((float)d);
-  const int nblk = (s + 127) / 128;
-  hipLaunchKernelGGL(attn_bwd_dkdv_v3_kernel, dim3(nblk * nh * b), dim3(256), 0, st, (const bf16*)qkv,
-                     (const bf16*)dout, lse, dvec, (bf16*)dqkv, b, s, nh, scale);
+  const bf16* x = (const bf16*)qkv;
+  const bf16* dy = (const bf16*)dout;
+  bf16* dx = (bf16*)dqkv;
+  // 128 rows per workgroup once the grid has more blocks than there are CUs,
+  // else 64 rows with the other operand's tiles split in two parts inside the
+  // workgroup (half the longest chain of tiles, at a higher cost per tile)
+  const int n128 = (s + 127) / 128 * nh * b;
+  const bool split = n128 <= 256;
+  if (!split) {
+    hipLaunchKernelGGL((attn_bwd_dkdv_v3_kernel<4, 1>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh,
+                       scale);
+  } else {
+    hipLaunchKernelGGL((attn_bwd_dkdv_v3_kernel<2, 2>), dim3((s + 63) / 64 * nh * b), dim3(256), 0, st, x, dy, lse,
+                       dvec, dx, b, s, nh, scale);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_bwd_dq_v3_kernel, dim3(nblk * nh * b), dim3(256), 0, st, (const bf16*)qkv,
-                     (const bf16*)dout, lse, dvec, (bf16*)dqkv, b, s, nh, scale);
+  if (!split) {
+    hipLaunchKernelGGL((attn_bwd_dq_v3_kernel<4, 1>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh,
+                       scale);
+  } else {
+    hipLaunchKernelGGL((attn_bwd_dq_v3_kernel<2, 2>), dim3((s + 63) / 64 * nh * b), dim3(256), 0, st, x, dy, lse,
+                       dvec, dx, b, s, nh, scale);
+  }
   return hipGetLastError();
 }
 

@@ -262,6 +262,16 @@ void attn_fwd_sk_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
   }
 }
 
+// grid thresholds (blocks of 128 queries) of the three forward shapes
+constexpr int kFwdNoSplit = 512, kFwdWide = 256;
+
+const char* attention_fwd_v3_name(int b, int s, int nh) {
+  const int n128 = (s + 127) / 128 * nh * b;
+  return n128 >= kFwdNoSplit ? "tps::attn_fwd_sk_kernel<4, 1>"
+         : n128 >= kFwdWide  ? "tps::attn_fwd_sk_kernel<4, 2>"
+                             : "tps::attn_fwd_sk_kernel<2, 2>";
+}
+
 hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse, hipStream_t st) {
   if (d != D) return hipErrorInvalidValue;
   const float scale = 1.0f / sqrtf((float)d);
@@ -271,9 +281,9 @@ hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv,
   // per CU
   const int n128 = (s + 127) / 128 * nh * b;
   const bf16* x = (const bf16*)qkv;
-  if (n128 >= 512) {
+  if (n128 >= kFwdNoSplit) {
     hipLaunchKernelGGL((attn_fwd_sk_kernel<4, 1>), dim3(n128), dim3(256), 0, st, x, (bf16*)o, lse, b, s, nh, scale);
-  } else if (n128 >= 256) {
+  } else if (n128 >= kFwdWide) {
     hipLaunchKernelGGL((attn_fwd_sk_kernel<4, 2>), dim3(n128), dim3(512), 0, st, x, (bf16*)o, lse, b, s, nh, scale);
   } else {
     hipLaunchKernelGGL((attn_fwd_sk_kernel<2, 2>), dim3((s + 63) / 64 * nh * b), dim3(256), 0, st, x, (bf16*)o, lse,

@@ -86,10 +86,6 @@ struct TileSrcN {
     }
   }
 };
-// four waves per tile (the backward kernels)
-struct TileSrc : TileSrcN<4> {
-  __device__ __forceinline__ void load(int row0, char* tile, int) const { TileSrcN<4>::load(row0, tile); }
-};
 
 // 64 consecutive f32 of a per-row vector (lse, D), one buffer-to-LDS
 // instruction (lanes 0-15 carry the 64 values; the other lanes' 16 bytes land

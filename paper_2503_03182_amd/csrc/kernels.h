@@ -59,9 +59,12 @@ hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const vo
 // bf16 kernels on 16x16x32 MFMAs with paired causal blocks (attention_v2.hip)
 hipError_t attention_fwd_v2_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
                                    hipStream_t st);
-// bf16, head dim 128: 32 queries per wave on 32x32x16 MFMAs (attention_fwd.hip)
+// bf16, head dim 128: 32 queries per wave on 32x32x16 MFMAs, key tiles split
+// in two parts per workgroup on small grids (attention_fwd.hip); the name of
+// the kernel instance a shape launches
 hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
                                    hipStream_t st);
+const char* attention_fwd_v3_name(int b, int s, int nh);
 // bf16, head dim 128: dK/dV by 32-key waves, dQ by 32-query waves (attention_bwd.hip)
 hipError_t attention_bwd_v3_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
                                    void* dqkv, const float* dvec, hipStream_t st);

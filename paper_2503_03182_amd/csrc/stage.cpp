@@ -353,7 +353,7 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
     TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS, T, 3 * h, h, a, h, par(TPS_P_W_QKV), h, qkv, 3 * h, par(TPS_P_B_QKV)));
   if (ops & (1u << OP_ATTN)) {
     ++stats.kernels;
-    const int k = kbegin(p.dtype == TPS_BF16 ? (p.d == 128 ? "tps::attn_fwd_v3_kernel" : "tps::attn_fwd_v2_kernel<64>")
+    const int k = kbegin(p.dtype == TPS_BF16 ? (p.d == 128 ? attention_fwd_v3_name(p.b, p.s, p.nh) : "tps::attn_fwd_v2_kernel<64>")
                                              : "tps::attn_fwd_kernel<float>",
                          2.0 * p.b * h * (double)p.s * (p.s + 1), 4.0 * T * h * es);
     TPS_HIP(attention_fwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, opt(TPS_T_LSE) ? lse : nullptr, cs));

@@ -171,7 +171,8 @@ ATTN_CASES = [  # (dtype, b, s, heads, d)
 # the key tiles split in two parts per workgroup, of at least 512 such blocks
 # the forward without the split and the 32-row-per-wave backward; ragged
 # lengths throughout
-ATTN_BIG_CASES = [("bf16", 2, 130, 128, 128), ("bf16", 2, 520, 52, 128), ("bf16", 1, 1000, 40, 128)]
+ATTN_BIG_CASES = [("bf16", 2, 130, 128, 128), ("bf16", 2, 520, 52, 128), ("bf16", 1, 1000, 40, 128),
+                  ("bf16", 1, 1500, 4, 128)]
 
 
 @pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_CASES + ATTN_BIG_CASES)
