@@ -118,89 +118,90 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
   // c = 32 qb + 8 (j / 4) + j % 4 the query offset of accumulator j of block qb
   const int kthr = key - 4 * g;
 
+  // One 64-query tile, as two 32-query halves each taken through the whole
+  // chain (S, dP -> P, dS -> dV, dK): only one half's scores, probabilities
+  // and per-row vectors are live at a time, which keeps the K/V fragments and
+  // the dK/dV accumulators resident in registers.
   auto tile = [&](int t, int st, auto diag_c) {
     constexpr bool DIAG = decltype(diag_c)::value;
     const uint32_t qs = lds0 + st * STAGE, ds = qs + TILE, ls = ds + TILE, vs = ls + VEC;
-    // ---- S = Q K^T and dP = dO V^T: 2 query blocks x 8 d-steps each
-    f32x16 sacc[2], pacc[2];
+    static_for<2>([&](auto qc) {
+      constexpr int qb = decltype(qc)::value;
+      // ---- S = Q K^T and dP = dO V^T for queries 32 qb .. +32: 8 d-steps each
+      f32x16 sacc, pacc;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[qb][r] = pacc[qb][r] = 0.f;
-    bf16x8 fr[32];
-    // issue order i: operand (Q, dO) = i % 2, query block = (i / 2) % 2, d-step = i / 4
-    auto read_f = [&](auto ic) {
-      constexpr int i = decltype(ic)::value, w = i % 2, qb = (i / 2) % 2, ks = i / 4;
-      fr[i] = ds_b128<qb * 32 * ROWB>((w ? ds : qs) + fo.row[ks]);
-    };
-    static_for<10>([&](auto ic) { read_f(ic); });
-    static_for<32>([&](auto ic) {
-      constexpr int i = decltype(ic)::value, w = i % 2, qb = (i / 2) % 2, ks = i / 4;
-      constexpr int issued = (i + 10 < 32) ? i + 10 : 32;
-      wait_lgkm<issued - i - 1>();
-      pin(fr[i]);
-      if constexpr (w == 0) sacc[qb] = Mma<bf16>::run(fr[i], kf[ks], sacc[qb]);
-      else pacc[qb] = Mma<bf16>::run(fr[i], vf[ks], pacc[qb]);
-      if constexpr (i + 10 < 32) read_f(std::integral_constant<int, i + 10>{});
-    });
-    // ---- lse and D of the rows this lane holds: rows 32 qb + 8 (j / 4) + 4 g + (j % 4)
-    f32x4 lv[2][4], dvv[2][4];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+      for (int r = 0; r < 16; ++r) sacc[r] = pacc[r] = 0.f;
+      bf16x8 fr[16];
+      // issue order i: operand (Q, dO) = i % 2, d-step = i / 2
+      auto read_f = [&](auto ic) {
+        constexpr int i = decltype(ic)::value, w = i % 2, ks = i / 2;
+        fr[i] = ds_b128<qb * 32 * ROWB>((w ? ds : qs) + fo.row[ks]);
+      };
+      constexpr int WF = 8;   // fragments in flight
+      static_for<WF>([&](auto ic) { read_f(ic); });
+      static_for<16>([&](auto ic) {
+        constexpr int i = decltype(ic)::value, w = i % 2, ks = i / 2;
+        constexpr int issued = (i + WF < 16) ? i + WF : 16;
+        wait_lgkm<issued - i - 1>();
+        pin(fr[i]);
+        if constexpr (w == 0) sacc = Mma<bf16>::run(fr[i], kf[ks], sacc);
+        else pacc = Mma<bf16>::run(fr[i], vf[ks], pacc);
+        if constexpr (i + WF < 16) read_f(std::integral_constant<int, i + WF>{});
+      });
+      // ---- lse and D of the rows this lane holds: 32 qb + 8 (j / 4) + 4 g + (j % 4)
+      f32x4 lv[4], dvv[4];
 #pragma unroll
       for (int j4 = 0; j4 < 4; ++j4) {
         const uint32_t o = (uint32_t)((32 * qb + 8 * j4 + 4 * g) * 4);
-        asm volatile("ds_read_b128 %0, %1" : "=v"(lv[qb][j4]) : "v"(ls + o));
-        asm volatile("ds_read_b128 %0, %1" : "=v"(dvv[qb][j4]) : "v"(vs + o));
+        asm volatile("ds_read_b128 %0, %1" : "=v"(lv[j4]) : "v"(ls + o));
+        asm volatile("ds_read_b128 %0, %1" : "=v"(dvv[j4]) : "v"(vs + o));
       }
-    wait_lgkm<0>();
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+      wait_lgkm<0>();
 #pragma unroll
       for (int j4 = 0; j4 < 4; ++j4) {
-        pin(lv[qb][j4]);
-        pin(dvv[qb][j4]);
+        pin(lv[j4]);
+        pin(dvv[j4]);
       }
-    // ---- P, dS
-    float p[2][16], d[2][16];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+      // ---- P, dS
+      float p[16], d[16];
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[qb][j], sl2, -lv[qb][j / 4][j % 4] * kLog2e));
+        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[j], sl2, -lv[j / 4][j % 4] * kLog2e));
         if constexpr (DIAG) {
           if (32 * qb + 8 * (j / 4) + (j % 4) < kthr - t * BT) pv = 0.f;
         }
-        p[qb][j] = pv;
-        d[qb][j] = pv * (pacc[qb][j] - dvv[qb][j / 4][j % 4]);
+        p[j] = pv;
+        d[j] = pv * (pacc[j] - dvv[j / 4][j % 4]);
       }
-    bf16x8 pb[4], sb[4];
+      bf16x8 pb[2], sb[2];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      pb[u] = to_frag(&p[u / 2][8 * (u % 2)]);
-      sb[u] = to_frag(&d[u / 2][8 * (u % 2)]);
-    }
-    // ---- dV^T += dO^T P, dK^T += Q^T dS: 4 query steps x 4 d tiles each
-    s16x4 lo[32], hi[32];
-    // issue order i: operand (dO^T, Q^T) = i % 2, d tile = (i / 2) % 4, query step u = i / 8
-    auto read_t = [&](auto ic) {
-      constexpr int i = decltype(ic)::value, w = i % 2, mt = (i / 2) % 4, u = i / 8;
-      constexpr int roff = 16 * u * ROWB;
-      const uint32_t src = w ? qs : ds;
-      lo[i] = ds_tr16<roff>(src + fo.lo[mt]);
-      hi[i] = ds_tr16<roff>(src + fo.hi[mt]);
-    };
-    static_for<7>([&](auto ic) { read_t(ic); });
-    static_for<32>([&](auto ic) {
-      constexpr int i = decltype(ic)::value, w = i % 2, mt = (i / 2) % 4, u = i / 8;
-      constexpr int issued = (i + 7 < 32) ? i + 7 : 32;
-      wait_lgkm<2 * (issued - i - 1)>();
-      s16x8 v8 = {lo[i][0], lo[i][1], lo[i][2], lo[i][3], hi[i][0], hi[i][1], hi[i][2], hi[i][3]};
-      bf16x8 f = *reinterpret_cast<bf16x8*>(&v8);
-      pin(f);
-      if constexpr (w == 0) dv[mt] = Mma<bf16>::run(f, pb[u], dv[mt]);
-      else dk[mt] = Mma<bf16>::run(f, sb[u], dk[mt]);
-      if constexpr (i + 7 < 32) read_t(std::integral_constant<int, i + 7>{});
+      for (int u = 0; u < 2; ++u) {
+        pb[u] = to_frag(&p[8 * u]);
+        sb[u] = to_frag(&d[8 * u]);
+      }
+      // ---- dV^T += dO^T P, dK^T += Q^T dS: 2 query steps x 4 d tiles each
+      s16x4 lo[16], hi[16];
+      // issue order i: operand (dO^T, Q^T) = i % 2, d tile = (i / 2) % 4, query step u = i / 8
+      auto read_t = [&](auto ic) {
+        constexpr int i = decltype(ic)::value, w = i % 2, mt = (i / 2) % 4, u = i / 8;
+        constexpr int roff = 16 * (2 * qb + u) * ROWB;
+        const uint32_t src = w ? qs : ds;
+        lo[i] = ds_tr16<roff>(src + fo.lo[mt]);
+        hi[i] = ds_tr16<roff>(src + fo.hi[mt]);
+      };
+      constexpr int WT = 7;   // transposed fragments in flight
+      static_for<WT>([&](auto ic) { read_t(ic); });
+      static_for<16>([&](auto ic) {
+        constexpr int i = decltype(ic)::value, w = i % 2, mt = (i / 2) % 4, u = i / 8;
+        constexpr int issued = (i + WT < 16) ? i + WT : 16;
+        wait_lgkm<2 * (issued - i - 1)>();
+        s16x8 v8 = {lo[i][0], lo[i][1], lo[i][2], lo[i][3], hi[i][0], hi[i][1], hi[i][2], hi[i][3]};
+        bf16x8 f = *reinterpret_cast<bf16x8*>(&v8);
+        pin(f);
+        if constexpr (w == 0) dv[mt] = Mma<bf16>::run(f, pb[u], dv[mt]);
+        else dk[mt] = Mma<bf16>::run(f, sb[u], dk[mt]);
+        if constexpr (i + WT < 16) read_t(std::integral_constant<int, i + WT>{});
+      });
     });
   };
 
@@ -214,17 +215,29 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
     wait_vm<0>();
   }
   lds_barrier();
-  for (int it = 0; it < nit; ++it) {
-    const int t = tb + it;
-    if (it < np && t >= wave_first) {
-      if (t * BT < k0 + 31) tile(t, it & 1, std::true_type{});   // some query of the tile precedes some key
-      else tile(t, it & 1, std::false_type{});
-    }
-    // hand the stage back: the next tile has landed, every wave is done with this one
+  // hand the stage of trip `it` back: the next tile has landed, every wave
+  // is done with this one
+  auto trip_end = [&](int it) {
     wait_vm<0>();
     lds_barrier();
-    if (it + 2 < np) load_tile(t + 2, it & 1);
+    if (it + 2 < np) load_tile(tb + it + 2, it & 1);
+  };
+  // The wave skips the part's tiles before the one holding its first key,
+  // then takes the tiles where some query precedes some key (masked), then
+  // the rest; one loop per kind keeps the accumulators in place.
+  const int n_skip = min(max(wave_first - tb, 0), np);
+  const int n_diag = min(max((k0 + 30) / BT + 1 - tb, n_skip), np);
+  int it = 0;
+  for (; it < n_skip; ++it) trip_end(it);
+  for (; it < n_diag; ++it) {
+    tile(tb + it, it & 1, std::true_type{});
+    trip_end(it);
   }
+  for (; it < np; ++it) {
+    tile(tb + it, it & 1, std::false_type{});
+    trip_end(it);
+  }
+  for (; it < nit; ++it) trip_end(it);
 
   // ---- sum the query parts of each key slice through LDS (ring memory is
   // free after the loop's last barrier; no tile load is in flight): part 1
@@ -414,16 +427,25 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
     wait_vm<0>();
   }
   lds_barrier();
-  for (int it = 0; it < nit; ++it) {
-    const int t = tb + it;
-    if (it < np && t <= wave_last) {
-      if ((t + 1) * BT - 1 > q0) tile(t, it & 1, std::true_type{});
-      else tile(t, it & 1, std::false_type{});
-    }
+  auto trip_end = [&](int it) {
     wait_vm<0>();
     lds_barrier();
-    if (it + 2 < np) load_tile(t + 2, it & 1);
+    if (it + 2 < np) load_tile(tb + it + 2, it & 1);
+  };
+  // a prefix of the part's tiles (up to the one holding the wave's last
+  // query), those crossing the diagonal last; one loop per kind
+  const int n_comp = max(0, min(np, wave_last + 1 - tb));
+  const int n_plain = max(0, min(n_comp, (q0 + 1) / BT - tb));   // tiles whose last key <= q0
+  int it = 0;
+  for (; it < n_plain; ++it) {
+    tile(tb + it, it & 1, std::false_type{});
+    trip_end(it);
   }
+  for (; it < n_comp; ++it) {
+    tile(tb + it, it & 1, std::true_type{});
+    trip_end(it);
+  }
+  for (; it < nit; ++it) trip_end(it);
 
   // ---- sum the key parts of each query slice through LDS, part 0 first
   if constexpr (PARTS == 2) {

@@ -203,18 +203,29 @@ void attn_fwd_sk_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
     wait_vm<0>();
   }
   lds_barrier();
-  for (int it = 0; it < nit; ++it) {
-    const int t = tb + it;
-    if (it < np && t <= wave_last) {
-      if ((t + 1) * BT - 1 > q0) tile(t, it & 1, std::true_type{});
-      else tile(t, it & 1, std::false_type{});
-    }
-    // hand the stage back: the next tile (the only loads in flight) has
-    // landed and every wave is done with this one
+  // hand the stage of trip `it` back: the next tile (the only loads in
+  // flight) has landed and every wave is done with this one
+  auto trip_end = [&](int it) {
     wait_vm<0>();
     lds_barrier();
-    if (it + 2 < np) load_tile(t + 2, it & 1);
+    if (it + 2 < np) load_tile(tb + it + 2, it & 1);
+  };
+  // The wave computes a prefix of the part's tiles (up to the one holding its
+  // last query), the tiles that cross the diagonal last; one loop per kind
+  // and a barrier-only loop for the remaining trips keep the accumulators in
+  // place (a join of paths inside one loop makes the compiler copy them).
+  const int n_comp = max(0, min(np, wave_last + 1 - tb));
+  const int n_plain = max(0, min(n_comp, (q0 + 1) / BT - tb));   // tiles whose last key <= q0
+  int it = 0;
+  for (; it < n_plain; ++it) {
+    tile(tb + it, it & 1, std::false_type{});
+    trip_end(it);
   }
+  for (; it < n_comp; ++it) {
+    tile(tb + it, it & 1, std::true_type{});
+    trip_end(it);
+  }
+  for (; it < nit; ++it) trip_end(it);
 
   // ---- merge the key parts of each query slice through LDS (ring memory is
   // free after the loop's last barrier): part 1 parks m, l and O^T
