@@ -84,6 +84,26 @@ hipError_t layernorm_bwd_launch(int dtype, int rows, int cols, const void* dout,
 hipError_t colsum_launch(int dtype, int rows, int cols, const void* x, int64_t ldx, float* out,
                          float* ws, hipStream_t st);
 uint64_t colsum_ws_bytes(int64_t rows, int64_t cols);
+// Column sums accumulated over calls: pass 1 of colsum_launch adding each
+// row segment's sums into part[segment * seg_stride + c] (colsum_segments(rows)
+// segments), and the LayerNorm backward with its dbeta / dgamma sums added the
+// same way (dbeta at part_dbeta, dgamma k_stride floats after it).  The
+// finalize call sums the segments of every column of a partial block (ranges
+// of columns each owned by an f32 vector inside `grads`), adds the sums there
+// and clears the partials.
+struct ColMap {
+  int n;              // ranges (<= 8)
+  int c0[9];          // range r covers columns c0[r] .. c0[r+1]
+  int64_t goff[8];    // float offset of range r's vector in grads
+};
+hipError_t colsum_acc_launch(int dtype, int rows, int cols, const void* x, int64_t ldx, float* part,
+                             int64_t seg_stride, hipStream_t st);
+hipError_t layernorm_bwd_acc_launch(int dtype, int rows, int cols, const void* dout, const void* x,
+                                    const float* mean, const float* rstd, const void* gamma, const void* resid,
+                                    void* dx, float* part_dbeta, int64_t k_stride, int64_t seg_stride,
+                                    hipStream_t st);
+hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_t seg_stride, float* grads,
+                                  hipStream_t st);
 hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st);
 hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st);
 // out[c][r] = in[r][c] for in [rows, cols]; rows and cols multiples of 8

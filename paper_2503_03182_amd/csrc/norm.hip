@@ -251,11 +251,16 @@ __global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict
 // Thread (row lane rl, chunk cc) sums rows rl, rl+32, ... of the segment for
 // 8 columns; the 32 row lanes are then added in ascending order.
 // k = 0: sum x (or dout); k = 1 (LN mode): sum dout * (xin - mean) * rstd.
-template <typename T, bool LN>
+// The segment's sum of column c for output k goes to
+// dst[segment * seg_stride + k * k_stride + c], stored (ACC false) or added
+// to what is there (ACC true: one owner per element, so calls in stream order
+// accumulate in a fixed order).
+template <typename T, bool LN, bool ACC>
 __global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ x, int64_t ldx,
                                                           const T* __restrict__ xin, const float* __restrict__ mean,
-                                                          const float* __restrict__ rstd, float* __restrict__ ws,
-                                                          int rows, int cols, int seg_rows) {
+                                                          const float* __restrict__ rstd, float* __restrict__ dst,
+                                                          int64_t seg_stride, int64_t k_stride, int rows, int cols,
+                                                          int seg_rows) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int COLS = 8 * VEC;                 // columns per block
   __shared__ float red[LN ? 2 : 1][32][COLS + 1];
@@ -314,7 +319,11 @@ __global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ 
     const int gc = blockIdx.x * COLS + c;
     float acc = 0.f;
     for (int i = 0; i < 32; ++i) acc += red[k][i][c];
-    if (gc < cols) ws[((int64_t)blockIdx.y * nk + k) * cols + gc] = acc;
+    if (gc < cols) {
+      float* d = dst + (int64_t)blockIdx.y * seg_stride + k * k_stride + gc;
+      if constexpr (ACC) *d += acc;
+      else *d = acc;
+    }
   }
 }
 
@@ -342,6 +351,28 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restri
   }
   if (out0) out0[c] += s0;
   if (nk == 2 && out1) out1[c] += s1;
+}
+
+// Sums the segment partials of each column of a partial block (columns in
+// ranges m.c0[r] .. m.c0[r+1], range r owned by the f32 vector at grads +
+// m.goff[r]) in ascending segment order, adds them to that vector and clears
+// the partials.
+__global__ __launch_bounds__(256) void colsum_finalize_kernel(ColMap m, float* __restrict__ part, int segs,
+                                                              int64_t seg_stride, float* __restrict__ grads) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= m.c0[m.n]) return;
+  int r = 0;
+  while (r + 1 < m.n && c >= m.c0[r + 1]) ++r;
+  float v[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) v[i] = i < segs ? part[(int64_t)i * seg_stride + c] : 0.f;
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    if (i < segs) acc += v[i];
+  for (int i = 16; i < segs; ++i) acc += part[(int64_t)i * seg_stride + c];
+  for (int i = 0; i < segs; ++i) part[(int64_t)i * seg_stride + c] = 0.f;
+  grads[m.goff[r] + (c - m.c0[r])] += acc;
 }
 
 template <typename T>
@@ -413,12 +444,13 @@ hipError_t colsum_typed(int rows, int cols, const void* x, int64_t ldx, const vo
   const int seg = (int)colsum_seg_rows(rows);
   const int parts = (int)colsum_segments(rows);
   dim3 grid((cols + 8 * VEC - 1) / (8 * VEC), parts);
+  const int64_t nk = ln ? 2 : 1;
   if (ln)
-    hipLaunchKernelGGL((colsum_part_kernel<T, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
-                       static_cast<const T*>(xin), mean, rstd, ws, rows, cols, seg);
+    hipLaunchKernelGGL((colsum_part_kernel<T, true, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
+                       static_cast<const T*>(xin), mean, rstd, ws, nk * cols, (int64_t)cols, rows, cols, seg);
   else
-    hipLaunchKernelGGL((colsum_part_kernel<T, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
-                       static_cast<const T*>(nullptr), mean, rstd, ws, rows, cols, seg);
+    hipLaunchKernelGGL((colsum_part_kernel<T, false, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
+                       static_cast<const T*>(nullptr), mean, rstd, ws, nk * cols, (int64_t)cols, rows, cols, seg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, ws, parts, ln ? 2 : 1,
@@ -426,9 +458,44 @@ hipError_t colsum_typed(int rows, int cols, const void* x, int64_t ldx, const vo
   return hipGetLastError();
 }
 
+// Pass 1 only, accumulating into a caller's partial block.
+template <typename T>
+hipError_t colsum_acc_typed(int rows, int cols, const void* x, int64_t ldx, const void* xin, const float* mean,
+                            const float* rstd, float* part0, int64_t k_stride, int64_t seg_stride, bool ln,
+                            hipStream_t st) {
+  constexpr int VEC = 16 / sizeof(T);
+  const int seg = (int)colsum_seg_rows(rows);
+  const int parts = (int)colsum_segments(rows);
+  dim3 grid((cols + 8 * VEC - 1) / (8 * VEC), parts);
+  if (ln)
+    hipLaunchKernelGGL((colsum_part_kernel<T, true, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
+                       static_cast<const T*>(xin), mean, rstd, part0, seg_stride, k_stride, rows, cols, seg);
+  else
+    hipLaunchKernelGGL((colsum_part_kernel<T, false, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
+                       static_cast<const T*>(nullptr), mean, rstd, part0, seg_stride, k_stride, rows, cols, seg);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 uint64_t colsum_ws_bytes(int64_t rows, int64_t cols) { return colsum_ws_elems(rows, cols) * 4; }
+
+hipError_t colsum_acc_launch(int dtype, int rows, int cols, const void* x, int64_t ldx, float* part,
+                             int64_t seg_stride, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  if (dtype == TPS_BF16)
+    return colsum_acc_typed<bf16>(rows, cols, x, ldx, nullptr, nullptr, nullptr, part, 0, seg_stride, false, st);
+  return colsum_acc_typed<float>(rows, cols, x, ldx, nullptr, nullptr, nullptr, part, 0, seg_stride, false, st);
+}
+
+hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_t seg_stride, float* grads,
+                                  hipStream_t st) {
+  const int cols = m.c0[m.n];
+  if (cols == 0) return hipSuccess;
+  hipLaunchKernelGGL(colsum_finalize_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, m, part, segs, seg_stride,
+                     grads);
+  return hipGetLastError();
+}
 
 hipError_t layernorm_fwd_launch(int dtype, int rows, int cols, const void* x, const void* gamma,
                                 const void* beta, float eps, void* out, float* mean, float* rstd,
@@ -464,6 +531,19 @@ hipError_t layernorm_bwd_launch(int dtype, int rows, int cols, const void* dout,
   if (dtype == TPS_BF16)
     return colsum_typed<bf16>(rows, cols, dout, cols, x, mean, rstd, dbeta, dgamma, ws, true, st);
   return colsum_typed<float>(rows, cols, dout, cols, x, mean, rstd, dbeta, dgamma, ws, true, st);
+}
+
+hipError_t layernorm_bwd_acc_launch(int dtype, int rows, int cols, const void* dout, const void* x,
+                                    const float* mean, const float* rstd, const void* gamma, const void* resid,
+                                    void* dx, float* part_dbeta, int64_t k_stride, int64_t seg_stride,
+                                    hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  hipError_t e = layernorm_bwd_launch(dtype, rows, cols, dout, x, mean, rstd, gamma, resid, dx, nullptr, nullptr,
+                                      nullptr, st);
+  if (e != hipSuccess) return e;
+  if (dtype == TPS_BF16)
+    return colsum_acc_typed<bf16>(rows, cols, dout, cols, x, mean, rstd, part_dbeta, k_stride, seg_stride, true, st);
+  return colsum_acc_typed<float>(rows, cols, dout, cols, x, mean, rstd, part_dbeta, k_stride, seg_stride, true, st);
 }
 
 hipError_t colsum_launch(int dtype, int rows, int cols, const void* x, int64_t ldx, float* out,

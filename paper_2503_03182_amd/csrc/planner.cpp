@@ -350,6 +350,15 @@ int make_plan(const tps_config* c, Plan* out) {
   p.ws_bytes = align256(4 * std::max(colsum_ws_elems(p.T, std::max(3 * p.h, p.f)), colsum_ws_elems(p.T, 2 * p.h)));
   p.work_bytes = p.work.ws + p.ws_bytes;
 
+  {
+    const int64_t H = (int64_t)h, F = (int64_t)f;
+    const int64_t widths[Plan::BP_COUNT] = {3 * H, H, F, H, H, H, H, H};
+    p.bpc[0] = 0;
+    for (int i = 0; i < Plan::BP_COUNT; ++i) p.bpc[i + 1] = p.bpc[i] + widths[i];
+    p.bpart_segs = (int)colsum_segments(T);
+    p.bpart_bytes = align256((uint64_t)p.bpart_segs * p.bpc[Plan::BP_COUNT] * 4);
+  }
+
   p.wwin_bytes = p.weights == TPS_W_STREAM ? (uint64_t)p.window * (p.pbytes + p.gbytes) : 0;
   {
     const uint64_t mats[4] = {3 * h * h, h * h, f * h, h * f};
@@ -367,7 +376,8 @@ int make_plan(const tps_config* c, Plan* out) {
   p.off_replay = p.off_oslots + align256((uint64_t)p.n_oslots * p.oslot_bytes);
   p.off_work = p.off_replay + align256(p.replay_bytes);
   p.off_wwin = p.off_work + align256(p.work_bytes);
-  p.off_wt = p.off_wwin + align256(p.wwin_bytes);
+  p.off_bpart = p.off_wwin + align256(p.wwin_bytes);
+  p.off_wt = p.off_bpart + (uint64_t)p.L * p.bpart_bytes;
   p.arena_bytes = p.off_wt + p.wt_region;
   p.host_bytes = (uint64_t)p.n_host_slots * p.oslot_bytes;
 

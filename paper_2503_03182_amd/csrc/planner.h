@@ -65,6 +65,15 @@ struct Plan {
   uint64_t work_bytes = 0;
   uint64_t ws_bytes = 0;
 
+  // per-layer f32 partial sums of the bias and LayerNorm parameter gradients:
+  // [segments][bpart_cols] with column ranges (bpc[]) for b_qkv, b_o, b_1,
+  // b_2, beta1, gamma1, beta2, gamma2; summed over segments into the grads
+  // when those are handed over
+  enum { BP_QKV, BP_O, BP_1, BP_2, BP_BE1, BP_G1, BP_BE2, BP_G2, BP_COUNT };
+  int64_t bpc[BP_COUNT + 1] = {};
+  int bpart_segs = 0;
+  uint64_t bpart_bytes = 0;   // one layer's block
+
   // transposed weight matrices (B operands of the input-gradient GEMMs):
   // Wqkv^T [h, 3h], Wo^T [h, h], W1^T [h, f], W2^T [f, h] per layer
   uint64_t wtoff[4] = {}, wt_bytes = 0;
@@ -75,7 +84,7 @@ struct Plan {
 
   // arena
   uint64_t off_wt = 0;
-  uint64_t off_kslots = 0, off_oslots = 0, off_replay = 0, off_work = 0, off_wwin = 0;
+  uint64_t off_kslots = 0, off_oslots = 0, off_replay = 0, off_work = 0, off_wwin = 0, off_bpart = 0;
   uint64_t arena_bytes = 0, host_bytes = 0;
 
   // accounting

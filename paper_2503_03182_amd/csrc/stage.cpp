@@ -63,6 +63,7 @@ struct tps_stage {
   std::vector<char*> lp;     // per-layer parameter block (device, or pinned host when streamed)
   std::vector<float*> lg;    // per-layer f32 gradient block (device, or pinned host when streamed)
   char* arena = nullptr;
+  bool bpart_clean = false;   // the bias partial blocks are all zero (no layer backward cut short)
   char* host = nullptr;
   hipStream_t cs = nullptr, xs = nullptr;
   int device = 0;
@@ -112,6 +113,7 @@ struct tps_stage {
     }
   }
   char* work(uint64_t off) const { return arena + p.off_work + off; }
+  float* bpart(int l) const { return reinterpret_cast<float*>(arena + p.off_bpart + (uint64_t)l * p.bpart_bytes); }
 
   // --- events ---------------------------------------------------------------
   int release_oslot(int slot, hipStream_t on) {
@@ -135,6 +137,7 @@ struct tps_stage {
   int prefetch_layer(int l);
   int flush_grads(int entry);
   int flush_all_grads();
+  int finalize_bias_grads(int l, float* G);
 
   // --- compute ----------------------------------------------------------------
   int gemm(int layout, int epi, int M, int N, int K, const void* A, int64_t lda, const void* B, int64_t ldb,
@@ -193,6 +196,21 @@ int tps_stage::refresh_wt(int l, int e) {
   TPS_HIP(transpose_launch(p.dtype, h, f, P + p.poff[TPS_P_W_2], f, W + p.wtoff[3], h, cs));
   stats.kernels += 4;
   return TPS_OK;
+}
+
+// Adds the layer's bias / LayerNorm partial sums of one micro-batch to its
+// gradient block G (on the compute stream) and clears them.
+int tps_stage::finalize_bias_grads(int l, float* G) {
+  static const int which[Plan::BP_COUNT] = {TPS_P_B_QKV, TPS_P_B_O, TPS_P_B_1, TPS_P_B_2,
+                                            TPS_P_BE1,   TPS_P_G1,  TPS_P_BE2, TPS_P_G2};
+  ColMap m{};
+  m.n = Plan::BP_COUNT;
+  for (int r = 0; r <= Plan::BP_COUNT; ++r) m.c0[r] = (int)p.bpc[r];
+  for (int r = 0; r < Plan::BP_COUNT; ++r) m.goff[r] = (int64_t)(p.goff[which[r]] / 4);
+  const int k = kbegin("bias gradient finalize", 0.0, (double)p.bpart_segs * p.bpc[Plan::BP_COUNT] * 8.0);
+  TPS_HIP(colsum_finalize_launch(m, bpart(l), p.bpart_segs, p.bpc[Plan::BP_COUNT], G, cs));
+  ++stats.kernels;
+  return kend(k);
 }
 
 int tps_stage::flush_grads(int e) {
@@ -403,18 +421,26 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   float* ws = reinterpret_cast<float*>(work(p.work.ws));
 
   const double es = p.esize;
-  const char* cs_name = "column sums (2 kernels)";
-  const char* lnb_name = "layernorm backward (3 kernels)";
-  auto colsum = [&](const void* src, int cols, float* out) -> int {
+  const char* cs_name = "column sums";
+  const char* lnb_name = "layernorm backward (2 kernels)";
+  // bias and LayerNorm parameter gradients: per-segment column sums go to
+  // the layer's partial block, summed into G by one kernel at the end
+  float* bp = bpart(l);
+  bpart_clean = false;
+  const int64_t bstride = p.bpc[Plan::BP_COUNT];
+  auto colsum = [&](const void* src, int cols, int range) -> int {
     ++stats.kernels;
     const int k = kbegin(cs_name, 0.0, (double)T * cols * es);
-    TPS_HIP(colsum_launch(p.dtype, T, cols, src, cols, out, ws, cs));
+    TPS_HIP(colsum_acc_launch(p.dtype, T, cols, src, cols, bp + p.bpc[range], bstride, cs));
     return kend(k);
   };
-  auto lnbwd = [&](const void* dout, const void* xin, const float* st, int gi, int bi, const void* res, void* dst) -> int {
+  // beta's columns precede gamma's in the partial block
+  auto lnbwd = [&](const void* dout, const void* xin, const float* st, int gi, int be_range, const void* res,
+                   void* dst) -> int {
     ++stats.kernels;
     const int k = kbegin(lnb_name, 0.0, 5.0 * T * h * es);
-    TPS_HIP(layernorm_bwd_launch(p.dtype, T, h, dout, xin, st, st + T, par(gi), res, dst, grd(gi), grd(bi), ws, cs));
+    TPS_HIP(layernorm_bwd_acc_launch(p.dtype, T, h, dout, xin, st, st + T, par(gi), res, dst, bp + p.bpc[be_range],
+                                     h, bstride, cs));
     return kend(k);
   };
   // MLP: y = x1 + GeLU(c W1^T + b1) W2^T + b2
@@ -425,14 +451,14 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   const char* wqt = WT + p.wtoff[0];   // [h, 3h]
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_GELU_GRAD, T, f, h, dy, h, w2t, h, du, f, nullptr, nullptr, 0, u, f));
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f));
-  TPS_TRY(colsum(dy, h, grd(TPS_P_B_2)));
+  TPS_TRY(colsum(dy, h, Plan::BP_2));
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h));
-  TPS_TRY(colsum(du, f, grd(TPS_P_B_1)));
+  TPS_TRY(colsum(du, f, Plan::BP_1));
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, f, du, f, w1t, f, t1, h));
-  TPS_TRY(lnbwd(t1, x1, ln2, TPS_P_G2, TPS_P_BE2, dy, dx1));
+  TPS_TRY(lnbwd(t1, x1, ln2, TPS_P_G2, Plan::BP_BE2, dy, dx1));
   // attention block: x1 = x + o Wo^T + bo
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h));
-  TPS_TRY(colsum(dx1, h, grd(TPS_P_B_O)));
+  TPS_TRY(colsum(dx1, h, Plan::BP_O));
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, h, dx1, h, wot, h, t1, h));
   {
     ++stats.kernels;
@@ -441,9 +467,11 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
     TPS_TRY(kend(k));
   }
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h));
-  TPS_TRY(colsum(dqkv, 3 * h, grd(TPS_P_B_QKV)));
+  TPS_TRY(colsum(dqkv, 3 * h, Plan::BP_QKV));
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, 3 * h, dqkv, 3 * h, wqt, 3 * h, t1, h));
-  TPS_TRY(lnbwd(t1, x, ln1, TPS_P_G1, TPS_P_BE1, dx1, dx));
+  TPS_TRY(lnbwd(t1, x, ln1, TPS_P_G1, Plan::BP_BE1, dx1, dx));
+  TPS_TRY(finalize_bias_grads(l, G));
+  bpart_clean = true;
   return TPS_OK;
 }
 
@@ -654,6 +682,13 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
   std::fill(st->prefetched.begin(), st->prefetched.end(), 0);
   st->stats = tps_stats{};
   const Plan& p = st->p;
+  if (!st->bpart_clean) {
+    // first iteration, or a layer backward was cut short by an error
+    hipError_t e = fill_zero_launch(st->arena + p.off_bpart, (uint64_t)p.L * p.bpart_bytes, st->cs);
+    if (e != hipSuccess) return check_hip(e, "clear bias partials");
+    ++st->stats.kernels;
+    st->bpart_clean = true;
+  }
   if (p.weights == TPS_W_STREAM) {
     // host gradients of the previous iteration must be complete before reuse
     int rc = st->flush_all_grads();
