@@ -201,7 +201,10 @@ void gemm_bf16_kernel(GemmArgs g) {
   read_frags<BM, A_KC, BK, TM, KS, 0>(fa[0], fra, lds0);
   read_frags<BN, B_KC, BK, TN, KS, 0>(fb[0], frb, lds0 + A_BYTES);
 
-  for (int kt = 0; kt < nk; ++kt) {
+  // one K tile; REFILL: the stage is refilled with tile kt+STAGES (every tile
+  // but the last STAGES), which also fixes the number of tiles in flight
+  auto k_tile = [&](int kt, auto refill_c) {
+    constexpr bool REFILL = decltype(refill_c)::value;
     const int cur = kt % STAGES;
     const uint32_t as = lds0 + cur * STAGE, bs = as + A_BYTES;
     static_for<KS>([&](auto kc) {
@@ -234,7 +237,8 @@ void gemm_bf16_kernel(GemmArgs g) {
         for (int j = 0; j < TN; ++j) pin(fb[fc][j]);
         // tile kt+1 has landed once the tiles after it are the only loads
         // left (on the last tile: once nothing is left)
-        wait_tiles<STAGES - 2, LPT>(max(0, min(STAGES - 2, nk - 2 - kt)));
+        if constexpr (REFILL) wait_vm<(STAGES - 2) * LPT>();
+        else wait_tiles<STAGES - 2, LPT>(max(0, min(STAGES - 2, nk - 2 - kt)));
         // all waves: tile kt+1 visible, tile kt's stage no longer read
         lds_barrier();
         // first fragments of tile kt+1 (after the last tile: in-bounds reads
@@ -243,18 +247,16 @@ void gemm_bf16_kernel(GemmArgs g) {
         read_frags<BM, A_KC, BK, TM, KS, 0>(fa[fc ^ 1], fra, nst);
         read_frags<BN, B_KC, BK, TN, KS, 0>(fb[fc ^ 1], frb, nst + A_BYTES);
         // refill the stage of tile kt with tile kt+STAGES, one load per MFMA
-        const bool refill = kt + STAGES < nk;
         static_for<TM * TN>([&](auto mc) {
           constexpr int m = decltype(mc)::value, i = m / TN, j = m % TN;
           acc[i][j] = Mma<bf16>::run(fa[fc][i], fb[fc][j], acc[i][j]);
-          if constexpr (m < A_IPW) {
-            if (refill) load_a(m, kt + STAGES, cur);
-          } else if constexpr (m < LPT) {
-            if (refill) load_b(m - A_IPW, kt + STAGES, cur);
+          if constexpr (REFILL) {
+            if constexpr (m < A_IPW) load_a(m, kt + STAGES, cur);
+            else if constexpr (m < LPT) load_b(m - A_IPW, kt + STAGES, cur);
           }
           __builtin_amdgcn_sched_barrier(0);
         });
-        if (refill) {
+        if constexpr (REFILL) {
           static_for<(LPT > TM * TN ? LPT - TM * TN : 0)>([&](auto lc) {
             constexpr int m = TM * TN + decltype(lc)::value;
             if constexpr (m < A_IPW) load_a(m, kt + STAGES, cur);
@@ -266,7 +268,10 @@ void gemm_bf16_kernel(GemmArgs g) {
     });
     // with an odd number of k-steps the fragment buffers would swap roles
     static_assert(KS % 2 == 0, "k-steps per tile must be even");
-  }
+  };
+  int kt = 0;
+  for (; kt < nk - STAGES; ++kt) k_tile(kt, std::true_type{});
+  for (; kt < nk; ++kt) k_tile(kt, std::false_type{});
   wait_vm<0>();
   wait_lgkm<0>();
   __syncthreads();   // LDS is reused below
