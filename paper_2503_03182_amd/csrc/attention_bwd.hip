@@ -5,29 +5,27 @@
 //   P_ij  = exp(s q_i.k_j - lse_i),   dP_ij = dO_i . v_j,
 //   dS_ij = P_ij (dP_ij - D_i),
 //   dV_j  = sum_i P_ij dO_i,  dK_j = s sum_i dS_ij q_i,  dQ_i = s sum_j dS_ij k_j,
-// summed over the causal triangle j <= i.  Two kernels, both deterministic
-// (every output element is produced by one wave, or summed from two waves'
-// partials, in a fixed order; no atomics).  Each runs one wave per SIMD and
-// comes in two shapes: 4 slices of 32 rows (128 rows per workgroup) with one
-// tile stream, or 2 slices (64 rows) whose tile range is split in two parts,
-// each part with its own stream and ring, summed part 0 first through LDS at
-// the end; the second halves the longest chain of tiles of small grids.
+// summed over the causal triangle j <= i.  Deterministic: every output element
+// is produced by one wave in a fixed order (no atomics).  A block of 128 rows
+// is owned by a 4-wave workgroup (one wave per SIMD, 32 rows per wave) that
+// streams 64-row tiles of the other operands through a two-stage LDS ring.
+// The dK/dV and dQ blocks run as two kernels, or fused: dK/dV of key block j
+// followed by dQ of query block j in one workgroup, which gives every
+// workgroup the same number of tiles.
 //
-// dK/dV (attn_bwd_dkdv_v3_kernel): a workgroup owns 32 keys per slice, K and
-//   V fragments in registers; 64-query tiles of Q, dO, lse and D stream
-//   through a two-stage LDS ring.  With keys along the MFMA N
+// dK/dV (dkdv_block): K and V fragments of the wave's 32 keys in registers;
+//   64-query tiles of Q, dO, lse and D stream through the ring.  With keys along the MFMA N
 //   dimension (one key per lane):
 //     S  = Q K^T, dP = dO V^T        (Q, dO rows from LDS)
 //     dV^T += dO^T P, dK^T += Q^T dS (dO^T, Q^T through transposing reads, in
 //                                     the accumulators' query order)
 //   64 MFMAs per tile; one wave per SIMD (the dK/dV accumulators take AGPRs).
-// dQ (attn_bwd_dq_v3_kernel): a workgroup owns 32 queries per slice, Q and
-//   dO fragments plus lse and D in registers; 64-key tiles of K and V stream
-//   through the ring.  With queries along N:
+// dQ (dq_block): Q and dO fragments of the wave's 32 queries plus their lse
+//   and D in registers; 64-key tiles of K and V stream through the ring.  With queries along N:
 //     S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T
 //   48 MFMAs per tile; one wave per SIMD (Q, dO fragments and dQ
 //   accumulators do not fit the register budget of two).
-// Workgroups are launched heaviest first.  Rows past the sequence end load as
+// Unfused workgroups are launched heaviest first.  Rows past the sequence end load as
 // zeros: their Q and dO rows contribute nothing to dK/dV, and keys past the end
 // lie beyond every query, so the causal mask removes them from dQ.
 #include "attn_tiles.h"
@@ -39,28 +37,29 @@ using namespace at;
 // ---------------------------------------------------------------------------
 // dK, dV
 // ---------------------------------------------------------------------------
-template <int KW, int PARTS>
-__global__ __attribute__((amdgpu_flat_work_group_size(64 * KW * PARTS, 64 * KW * PARTS), amdgpu_waves_per_eu(1, 1)))
-void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
-                             const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
-                             int b, int s, int nh, float scale) {
-  constexpr int VEC = 1024;                    // LDS bytes per per-row vector (64 f32 + landing pad)
+constexpr int kVecBytes = 1024;   // LDS bytes per per-row vector (64 f32 + landing pad)
+// LDS of a dK/dV block: a ring of two stages of Q, dO, lse, D
+constexpr int kDkdvLds = 2 * (2 * TILE + 2 * kVecBytes);
+// LDS of a dQ block: a ring of two stages of K, V
+constexpr int kDqLds = 2 * (2 * TILE);
+
+// dK, dV of key block kb (32 KW keys) of one (batch, head); smem holds
+// kDkdvLds bytes.
+template <int KW>
+__device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
+                                           const float* __restrict__ lse, const float* __restrict__ dvec,
+                                           bf16* __restrict__ dqkv, int b, int s, int nh, float scale, int kb,
+                                           int head, int batch, char* smem) {
+  constexpr int VEC = kVecBytes;
   constexpr int STAGE = 2 * TILE + 2 * VEC;    // Q, dO, lse, D
-  constexpr int RING = 2 * STAGE;              // one query part's two stages
   constexpr int BKEY = 32 * KW;                // keys per workgroup
-  static_assert(PARTS == 1 || PARTS == 2, "query parts");
-  __shared__ __attribute__((aligned(1024))) char smem[PARTS * RING];
 
   const int H = nh * D;
   const int64_t ld = 3 * (int64_t)H;
-  const int idx = blockIdx.x;
-  const int head = idx % nh;
-  const int batch = (idx / nh) % b;
-  const int kb = idx / (nh * b);                // first key blocks carry the most queries
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
-  const int slice = wave % KW, part = wave / KW;
+  const int slice = wave;
   const int k0 = kb * BKEY + slice * 32;       // first key of this wave
   const int key = k0 + (lane & 31);
 
@@ -75,15 +74,9 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
       vf[ks] = load_frag_settled(krow + H + 16 * ks);
     }
   }
-  // query tiles from the one holding this workgroup's first key to the end,
-  // and this part's share of them
-  const int t0 = (kb * BKEY) / BT;
-  const int ntile = (s + BT - 1) / BT;
-  const int n = ntile - t0;
-  const int n0 = PARTS == 1 ? n : (n + 1) / 2;
-  const int tb = part ? t0 + n0 : t0;          // first tile of this part
-  const int np = part ? n - n0 : n0;           // tiles of this part
-  const int nit = n0;                          // loop trips (both parts, for the barriers)
+  // query tiles from the one holding this workgroup's first key to the end
+  const int tb = (kb * BKEY) / BT;
+  const int np = (s + BT - 1) / BT - tb;
   const int wave_first = k0 / BT;              // earlier tiles have no query >= any key of the wave
 
   TileSrcN<KW> qsrc, dsrc;
@@ -92,7 +85,7 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
   VecSrc lsrc, vsrc;
   lsrc.init(lse + ((int64_t)batch * nh + head) * s, s);
   vsrc.init(dvec + ((int64_t)batch * nh + head) * s, s);
-  char* const ring = smem + part * RING;
+  char* const ring = smem;
   auto load_tile = [&](int t, int st) {
     char* p = ring + st * STAGE;
     qsrc.load(t * BT, p);
@@ -205,7 +198,7 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
     });
   };
 
-  // the part's i-th tile lives in stage i & 1
+  // the i-th tile lives in stage i & 1
   if (np > 0) load_tile(tb, 0);
   if (np > 1) {
     load_tile(tb + 1, 1);
@@ -222,7 +215,7 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
     lds_barrier();
     if (it + 2 < np) load_tile(tb + it + 2, it & 1);
   };
-  // The wave skips the part's tiles before the one holding its first key,
+  // The wave skips the tiles before the one holding its first key,
   // then takes the tiles where some query precedes some key (masked), then
   // the rest; one loop per kind keeps the accumulators in place.
   const int n_skip = min(max(wave_first - tb, 0), np);
@@ -236,32 +229,6 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
   for (; it < np; ++it) {
     tile(tb + it, it & 1, std::false_type{});
     trip_end(it);
-  }
-  for (; it < nit; ++it) trip_end(it);
-
-  // ---- sum the query parts of each key slice through LDS (ring memory is
-  // free after the loop's last barrier; no tile load is in flight): part 1
-  // parks its dK^T, dV^T, part 0 adds them to its own
-  if constexpr (PARTS == 2) {
-    float* park = reinterpret_cast<float*>(smem) + slice * (2 * D / 32 * 16) * 64;
-    if (part == 1) {
-#pragma unroll
-      for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          park[(mt * 16 + r) * 64 + lane] = dk[mt][r];
-          park[((D / 32 + mt) * 16 + r) * 64 + lane] = dv[mt][r];
-        }
-    }
-    __syncthreads();
-    if (part == 1) return;
-#pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        dk[mt][r] += park[(mt * 16 + r) * 64 + lane];
-        dv[mt][r] += park[((D / 32 + mt) * 16 + r) * 64 + lane];
-      }
   }
 
   // ---- store: lane holds dK^T / dV^T [32 mt + acc_row(j, l)][key]
@@ -285,31 +252,37 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
   }
 }
 
+template <int KW>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * KW, 64 * KW), amdgpu_waves_per_eu(1, 1)))
+void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
+                             const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
+                             int b, int s, int nh, float scale) {
+  __shared__ __attribute__((aligned(1024))) char smem[kDkdvLds];
+  const int idx = blockIdx.x;
+  // first key blocks carry the most queries
+  dkdv_block<KW>(qkv, dout, lse, dvec, dqkv, b, s, nh, scale, idx / (nh * b), idx % nh, (idx / nh) % b,
+                        smem);
+}
+
 // ---------------------------------------------------------------------------
 // dQ
 // ---------------------------------------------------------------------------
-template <int QW, int PARTS>
-__global__ __attribute__((amdgpu_flat_work_group_size(64 * QW * PARTS, 64 * QW * PARTS), amdgpu_waves_per_eu(1, 1)))
-void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
-                           const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
-                           int b, int s, int nh, float scale) {
+// dQ of query block qb (32 QW queries) of one (batch, head); smem holds
+// kDqLds bytes.
+template <int QW>
+__device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
+                                         const float* __restrict__ lse, const float* __restrict__ dvec,
+                                         bf16* __restrict__ dqkv, int b, int s, int nh, float scale, int qb, int head,
+                                         int batch, char* smem) {
   constexpr int STAGE = 2 * TILE;   // K, V
-  constexpr int RING = 2 * STAGE;   // one key part's two stages
   constexpr int BQ = 32 * QW;       // queries per workgroup
-  static_assert(PARTS == 1 || PARTS == 2, "key parts");
-  __shared__ __attribute__((aligned(1024))) char smem[PARTS * RING];
 
   const int H = nh * D;
   const int64_t ld = 3 * (int64_t)H;
-  const int nqb = (s + BQ - 1) / BQ;
-  const int idx = blockIdx.x;
-  const int head = idx % nh;
-  const int batch = (idx / nh) % b;
-  const int qb = nqb - 1 - idx / (nh * b);     // heaviest blocks first
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
-  const int slice = wave % QW, part = wave / QW;
+  const int slice = wave;
   const int q0 = qb * BQ + slice * 32;
   const int q = q0 + (lane & 31);
 
@@ -327,19 +300,16 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
   }
   const float lse2 = lse[((int64_t)batch * nh + head) * s + qc] * kLog2e;
   const float dq_dot = dvec[((int64_t)batch * nh + head) * s + qc];
-  // key tiles of the workgroup, and this part's share of them
+  // key tiles up to the workgroup's last query
   const int last_q = min(qb * BQ + BQ - 1, s - 1);
-  const int nt = last_q / BT + 1;
-  const int nt0 = PARTS == 1 ? nt : (nt + 1) / 2;
-  const int tb = part ? nt0 : 0;               // first tile of this part
-  const int np = part ? nt - nt0 : nt0;        // tiles of this part
-  const int nit = nt0;                         // loop trips (both parts, for the barriers)
+  const int tb = 0;
+  const int np = last_q / BT + 1;
   const int wave_last = min(q0 + 31, s - 1) / BT;
 
   TileSrcN<QW> ksrc, vsrc;
   ksrc.init(base + H + head * D, ld, s, slice, lane);
   vsrc.init(base + 2 * H + head * D, ld, s, slice, lane);
-  char* const ring = smem + part * RING;
+  char* const ring = smem;
   auto load_tile = [&](int t, int st) {
     ksrc.load(t * BT, ring + st * STAGE);
     vsrc.load(t * BT, ring + st * STAGE + TILE);
@@ -432,8 +402,9 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
     lds_barrier();
     if (it + 2 < np) load_tile(tb + it + 2, it & 1);
   };
-  // a prefix of the part's tiles (up to the one holding the wave's last
-  // query), those crossing the diagonal last; one loop per kind
+  // a prefix of the tiles (up to the one holding the wave's last query),
+  // those crossing the diagonal last; one loop per kind, then barrier-only
+  // trips while the other waves finish
   const int n_comp = max(0, min(np, wave_last + 1 - tb));
   const int n_plain = max(0, min(n_comp, (q0 + 1) / BT - tb));   // tiles whose last key <= q0
   int it = 0;
@@ -445,24 +416,7 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
     tile(tb + it, it & 1, std::true_type{});
     trip_end(it);
   }
-  for (; it < nit; ++it) trip_end(it);
-
-  // ---- sum the key parts of each query slice through LDS, part 0 first
-  if constexpr (PARTS == 2) {
-    float* park = reinterpret_cast<float*>(smem) + slice * (D / 32 * 16) * 64;
-    if (part == 1) {
-#pragma unroll
-      for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) park[(mt * 16 + r) * 64 + lane] = dq[mt][r];
-    }
-    __syncthreads();
-    if (part == 1) return;
-#pragma unroll
-    for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) dq[mt][r] += park[(mt * 16 + r) * 64 + lane];
-  }
+  for (; it < np; ++it) trip_end(it);
 
   if (q < s) {
     bf16* row = dqkv + ((int64_t)batch * s + q) * ld + head * D;
@@ -479,6 +433,36 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
   }
 }
 
+template <int QW>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * QW, 64 * QW), amdgpu_waves_per_eu(1, 1)))
+void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
+                           const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
+                           int b, int s, int nh, float scale) {
+  __shared__ __attribute__((aligned(1024))) char smem[kDqLds];
+  const int idx = blockIdx.x;
+  const int nqb = (s + 32 * QW - 1) / (32 * QW);
+  // heaviest blocks first
+  dq_block<QW>(qkv, dout, lse, dvec, dqkv, b, s, nh, scale, nqb - 1 - idx / (nh * b), idx % nh,
+                      (idx / nh) % b, smem);
+}
+
+// dK, dV of key block j and then dQ of query block j (128 rows each): with n
+// tiles of 64 rows in the sequence, the first streams the n - 2 j query tiles
+// from the one holding key 128 j on, the second the 2 j + 2 key tiles up to
+// its last query, so every workgroup streams n + 2 tiles whatever j (the
+// causal triangle is balanced without splitting any block).
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+void attn_bwd_fused_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout, const float* __restrict__ lse,
+                           const float* __restrict__ dvec, bf16* __restrict__ dqkv, int b, int s, int nh,
+                           float scale) {
+  __shared__ __attribute__((aligned(1024))) char smem[kDkdvLds > kDqLds ? kDkdvLds : kDqLds];
+  const int idx = blockIdx.x;
+  const int j = idx / (nh * b), head = idx % nh, batch = (idx / nh) % b;
+  dkdv_block<4>(qkv, dout, lse, dvec, dqkv, b, s, nh, scale, j, head, batch, smem);
+  __syncthreads();   // the LDS ring is reused
+  dq_block<4>(qkv, dout, lse, dvec, dqkv, b, s, nh, scale, j, head, batch, smem);
+}
+
 hipError_t attention_bwd_v3_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
                                    void* dqkv, const float* dvec, hipStream_t st) {
   if (d != D) return hipErrorInvalidValue;
@@ -486,27 +470,19 @@ hipError_t attention_bwd_v3_launch(int b, int s, int nh, int d, const void* qkv,
   const bf16* x = (const bf16*)qkv;
   const bf16* dy = (const bf16*)dout;
   bf16* dx = (bf16*)dqkv;
-  // 128 rows per workgroup once the grid has more blocks than there are CUs,
-  // else 64 rows with the other operand's tiles split in two parts inside the
-  // workgroup (half the longest chain of tiles, at a higher cost per tile)
+  // Fused workgroups all take the same time, so they pack the CUs well when
+  // there is at most one per CU or many per CU; in between, the two kernels
+  // (heaviest blocks first) fill the last round better.
   const int n128 = (s + 127) / 128 * nh * b;
-  const bool split = n128 <= 256;
-  if (!split) {
-    hipLaunchKernelGGL((attn_bwd_dkdv_v3_kernel<4, 1>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh,
-                       scale);
-  } else {
-    hipLaunchKernelGGL((attn_bwd_dkdv_v3_kernel<2, 2>), dim3((s + 63) / 64 * nh * b), dim3(256), 0, st, x, dy, lse,
-                       dvec, dx, b, s, nh, scale);
+  if (n128 <= 256 || n128 >= 1024) {
+    hipLaunchKernelGGL(attn_bwd_fused_kernel, dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh, scale);
+    return hipGetLastError();
   }
+  hipLaunchKernelGGL((attn_bwd_dkdv_v3_kernel<4>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh,
+                     scale);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (!split) {
-    hipLaunchKernelGGL((attn_bwd_dq_v3_kernel<4, 1>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh,
-                       scale);
-  } else {
-    hipLaunchKernelGGL((attn_bwd_dq_v3_kernel<2, 2>), dim3((s + 63) / 64 * nh * b), dim3(256), 0, st, x, dy, lse,
-                       dvec, dx, b, s, nh, scale);
-  }
+  hipLaunchKernelGGL((attn_bwd_dq_v3_kernel<4>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh, scale);
   return hipGetLastError();
 }
 

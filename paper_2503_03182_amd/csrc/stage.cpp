@@ -462,7 +462,7 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, h, dx1, h, wot, h, t1, h));
   {
     ++stats.kernels;
-    const int k = kbegin("attention backward (3 kernels)", 4.0 * p.b * h * (double)p.s * (p.s + 1), 9.0 * T * h * es);
+    const int k = kbegin("attention backward", 4.0 * p.b * h * (double)p.s * (p.s + 1), 9.0 * T * h * es);
     TPS_HIP(attention_bwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, lse, t1, dqkv, dvec, cs));
     TPS_TRY(kend(k));
   }
