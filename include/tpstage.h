@@ -177,7 +177,14 @@ typedef struct tps_memory {
                                    when that is 0)                              */
   uint64_t host_bytes;
   void* compute_stream;         /* hipStream_t for kernels                      */
-  void* copy_stream;            /* hipStream_t for host-link copies             */
+  void* copy_stream;            /* hipStream_t for device -> host copies (and
+                                   for host -> device ones when prefetch_stream
+                                   is NULL)                                     */
+  void* prefetch_stream;        /* hipStream_t for host -> device copies, or
+                                   NULL; a stream of its own lets both link
+                                   directions run at once (the offloads of later
+                                   micro-batches under the prefetches of earlier
+                                   ones, Section 5)                             */
 } tps_memory;
 
 typedef struct tps_stats {

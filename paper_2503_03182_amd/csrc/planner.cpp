@@ -34,6 +34,35 @@ struct SlotPool {
   void release(int s) { free_.insert(s); }
 };
 
+// Slots that become free at a time (the end of a copy).  acquire(t) takes
+// the smallest index free by t; acquire(t, latest, &when) may also wait for
+// the slot that frees first if that happens by `latest` (when: the time the
+// slot is taken); otherwise a new slot.
+struct TimedSlotPool {
+  std::vector<double> free_at;   // < 0: in use
+  int count() const { return (int)free_at.size(); }
+  int acquire(double t, double latest = -1, double* when = nullptr) {
+    if (when) *when = t;
+    int best = -1;
+    for (size_t s = 0; s < free_at.size(); ++s) {
+      if (free_at[s] < 0) continue;
+      if (free_at[s] <= t) {
+        best = (int)s;
+        break;
+      }
+      if (free_at[s] <= latest && (best < 0 || free_at[s] < free_at[best])) best = (int)s;
+    }
+    if (best < 0) {
+      free_at.push_back(-1);
+      return (int)free_at.size() - 1;
+    }
+    if (when) *when = std::max(t, free_at[best]);
+    free_at[best] = -1;
+    return best;
+  }
+  void release(int s, double t) { free_at[s] = t; }
+};
+
 }  // namespace
 
 double op_flops(const Plan& p, int op) {
@@ -157,6 +186,68 @@ static double simulate_offload(const Plan& p, const std::vector<char>& victim, d
   return t;
 }
 
+// Slot and host-slot assignment along the order for p.offload_mask, timed
+// with the model of the order (tF, tB: one micro-batch's forward and
+// backward, tc: one micro-batch's offload copy): an offloaded micro-batch's
+// staging slot is free once its device -> host copy (queued behind earlier
+// ones) is done, a host slot once the prefetch out of it is done, so a
+// forward never waits on a copy for its slot; the slot count is what the
+// overlap costs in memory.  Returns the number of staging slots.
+static int assign_slots(Plan& p, double tF, double tB, double tc) {
+  p.host_slot.assign(p.M, -1);
+  p.kslot.assign(p.M, -1);
+  p.oslot_f.assign(p.M, -1);
+  p.oslot_b.assign(p.M, -1);
+  p.prefetch_at.assign(p.op_kind.size(), {});
+  for (int mb = 0; mb < p.M; ++mb)
+    if ((p.offload_mask >> mb) & 1ull) {
+      const int at = std::max(p.pos_f[mb] + 1, p.pos_b[mb] - p.lookahead);
+      p.prefetch_at[at].push_back(mb);
+    }
+  SlotPool kpool;
+  TimedSlotPool opool, hpool;
+  int inflight = 0;
+  double t = 0, d2h_free = 0, h2d_free = 0;
+  std::vector<double> d2h_end(p.M, 0), h2d_end(p.M, 0);
+  for (size_t i = 0; i < p.op_kind.size(); ++i) {
+    for (int mb : p.prefetch_at[i]) {
+      // a prefetch may wait for a slot up to one copy time (a forward may not)
+      double st = std::max({t, h2d_free, d2h_end[mb]});
+      p.oslot_b[mb] = opool.acquire(st, st + tc, &st);
+      h2d_end[mb] = h2d_free = st + tc;
+      hpool.release(p.host_slot[mb], h2d_end[mb]);
+    }
+    const int mb = p.op_mb[i];
+    const bool off = (p.offload_mask >> mb) & 1ull;
+    if (p.op_kind[i] == TPS_OP_F) {
+      ++inflight;
+      p.max_inflight = std::max(p.max_inflight, inflight);
+      p.kslot[mb] = kpool.acquire();
+      p.oslot_f[mb] = opool.acquire(t);
+      t += tF;
+      if (off) {
+        // the copy to host queues behind earlier ones and waits for a host slot
+        double st = std::max(t, d2h_free);
+        p.host_slot[mb] = hpool.acquire(st, st + tc, &st);
+        d2h_end[mb] = d2h_free = st + tc;
+        opool.release(p.oslot_f[mb], d2h_end[mb]);
+      } else {
+        p.oslot_b[mb] = p.oslot_f[mb];
+      }
+    } else {
+      if (off) t = std::max(t, h2d_end[mb]);
+      t += tB;
+      --inflight;
+      kpool.release(p.kslot[mb]);
+      opool.release(p.oslot_b[mb], t);
+    }
+  }
+  p.n_kslots = p.kslot_bytes ? kpool.count : 0;
+  p.n_oslots = p.oslot_bytes ? opool.count() : 0;
+  p.n_host_slots = p.oslot_bytes ? hpool.count() : 0;
+  return opool.count();
+}
+
 int make_plan(const tps_config* c, Plan* out) {
   if (!c || !out) return inval("null argument");
   if (c->abi_version != TPS_ABI_VERSION) return inval("abi_version mismatch");
@@ -258,15 +349,18 @@ int make_plan(const tps_config* c, Plan* out) {
       if (p.replay_ops[l] & (1u << op)) replay_mb += op_flops(p, op);
   p.recompute_flops = replay_mb * p.M;
 
+  // timing model of the order (compute and host-link rates from the hints):
+  // forward and backward of one micro-batch, one micro-batch's offload copy
+  const double rate = (c->tflops_hint > 0 ? c->tflops_hint : 1000.0) * 1e12;
+  const double link = (c->link_gbps_hint > 0 ? c->link_gbps_hint : 50.0) * 1e9;
+  const double tF = unit_fwd * p.L / rate;
+  const double tB = (2.0 * unit_fwd * p.L + replay_mb) / rate;
+  const double tc = (double)p.oslot_bytes / link;
+
   // offload victims
   if (c->offload_auto) {
     p.offload_mask = 0;
     if (p.oslot_bytes > 0) {
-      const double rate = (c->tflops_hint > 0 ? c->tflops_hint : 1000.0) * 1e12;
-      const double link = (c->link_gbps_hint > 0 ? c->link_gbps_hint : 50.0) * 1e9;
-      const double tF = unit_fwd * p.L / rate;
-      const double tB = (2.0 * unit_fwd * p.L + replay_mb) / rate;
-      const double tc = (double)p.oslot_bytes / link;
       std::vector<char> none(p.M, 0), chosen(p.M, 0);
       const double base = simulate_offload(p, none, tF, tB, tc);
       // slack between the end of F(mb) and the start of B(mb) without copies
@@ -283,12 +377,23 @@ int make_plan(const tps_config* c, Plan* out) {
       std::vector<int> cand(p.M);
       std::iota(cand.begin(), cand.end(), 0);
       std::stable_sort(cand.begin(), cand.end(), [&](int a, int b2) { return slack[a] > slack[b2]; });
+      // a victim is taken if the round keeps its time and the staging peak
+      // drops (a micro-batch whose copies do not keep it off the device over
+      // the peak would only add link traffic)
+      int peak = assign_slots(p, tF, tB, tc);
       for (int mb : cand) {
         chosen[mb] = 1;
-        if (simulate_offload(p, chosen, tF, tB, tc) > base * 1.01) chosen[mb] = 0;
+        if (simulate_offload(p, chosen, tF, tB, tc) <= base * 1.01) {
+          p.offload_mask |= 1ull << mb;
+          const int n = assign_slots(p, tF, tB, tc);
+          if (n < peak) {
+            peak = n;
+            continue;
+          }
+          p.offload_mask &= ~(1ull << mb);
+        }
+        chosen[mb] = 0;
       }
-      for (int mb = 0; mb < p.M; ++mb)
-        if (chosen[mb]) p.offload_mask |= 1ull << mb;
     }
   } else {
     p.offload_mask = c->offload_mb_mask;
@@ -297,45 +402,7 @@ int make_plan(const tps_config* c, Plan* out) {
   if (p.oslot_bytes == 0) p.offload_mask = 0;
 
   // slot and host-slot assignment over the order
-  p.host_slot.assign(p.M, -1);
-  p.kslot.assign(p.M, -1);
-  p.oslot_f.assign(p.M, -1);
-  p.oslot_b.assign(p.M, -1);
-  p.prefetch_at.assign(p.op_kind.size(), {});
-  for (int mb = 0; mb < p.M; ++mb)
-    if ((p.offload_mask >> mb) & 1ull) {
-      const int at = std::max(p.pos_f[mb] + 1, p.pos_b[mb] - p.lookahead);
-      p.prefetch_at[at].push_back(mb);
-    }
-  SlotPool kpool, opool, hpool;
-  int inflight = 0;
-  for (size_t i = 0; i < p.op_kind.size(); ++i) {
-    for (int mb : p.prefetch_at[i]) {
-      p.oslot_b[mb] = opool.acquire();
-      hpool.release(p.host_slot[mb]);   // later copies into it queue behind this one
-    }
-    const int mb = p.op_mb[i];
-    const bool off = (p.offload_mask >> mb) & 1ull;
-    if (p.op_kind[i] == TPS_OP_F) {
-      ++inflight;
-      p.max_inflight = std::max(p.max_inflight, inflight);
-      p.kslot[mb] = kpool.acquire();
-      p.oslot_f[mb] = opool.acquire();
-      if (off) {
-        p.host_slot[mb] = hpool.acquire();
-        opool.release(p.oslot_f[mb]);
-      } else {
-        p.oslot_b[mb] = p.oslot_f[mb];
-      }
-    } else {
-      --inflight;
-      kpool.release(p.kslot[mb]);
-      opool.release(p.oslot_b[mb]);
-    }
-  }
-  p.n_kslots = p.kslot_bytes ? kpool.count : 0;
-  p.n_oslots = p.oslot_bytes ? opool.count : 0;
-  p.n_host_slots = p.oslot_bytes ? hpool.count : 0;
+  assign_slots(p, tF, tB, tc);
 
   // backward working buffers
   const uint64_t hb = align256(T * h * es), fb = align256(T * f * es), qb = align256(T * 3 * h * es);

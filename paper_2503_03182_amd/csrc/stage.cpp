@@ -65,10 +65,15 @@ struct tps_stage {
   char* arena = nullptr;
   bool bpart_clean = false;   // the bias partial blocks are all zero (no layer backward cut short)
   char* host = nullptr;
-  hipStream_t cs = nullptr, xs = nullptr;
+  // cs: kernels; xs: device -> host copies; ps: host -> device copies (xs
+  // itself when the caller gives no prefetch stream)
+  hipStream_t cs = nullptr, xs = nullptr, ps = nullptr;
   int device = 0;
 
   std::vector<SlotEvent> oslot_ev;               // last release of each offload slot
+  std::vector<SlotEvent> offloaded_ev;           // [M] last device -> host copy of the mb issued (xs)
+  std::vector<SlotEvent> hslot_read_ev;          // [host slots] last prefetch out of the slot (ps)
+  std::vector<SlotEvent> lgrads_out_ev;          // [L] last flush of the layer's grads to host (xs)
   std::vector<std::vector<hipEvent_t>> ready_ev; // [M][L] H2D of (mb, layer) done
   std::vector<char> prefetched;
   hipEvent_t ev_tmp = nullptr;
@@ -222,6 +227,8 @@ int tps_stage::flush_grads(int e) {
   stats.d2h_bytes += p.gbytes;
   TPS_HIP(hipEventRecord(w.grads_out.ev, xs));
   w.grads_out.valid = true;
+  TPS_HIP(hipEventRecord(lgrads_out_ev[w.layer].ev, xs));
+  lgrads_out_ev[w.layer].valid = true;
   w.grads_live = false;
   return TPS_OK;
 }
@@ -244,14 +251,14 @@ int tps_stage::prefetch_layer(int l) {
     if (win[e].tick < win[victim].tick) victim = (int)e;
   WinEntry& w = win[victim];
   TPS_TRY(flush_grads(victim));
-  if (w.last_use.valid) TPS_HIP(hipStreamWaitEvent(xs, w.last_use.ev, 0));
+  if (w.last_use.valid) TPS_HIP(hipStreamWaitEvent(ps, w.last_use.ev, 0));
   w.layer = l;
   w.tick = ++tick;
   w.wt_valid = false;
   int e = victim;
-  TPS_HIP(hipMemcpyAsync(const_cast<char*>(params_of(l, &e)), lp[l], p.pbytes, hipMemcpyHostToDevice, xs));
+  TPS_HIP(hipMemcpyAsync(const_cast<char*>(params_of(l, &e)), lp[l], p.pbytes, hipMemcpyHostToDevice, ps));
   stats.h2d_bytes += p.pbytes;
-  TPS_HIP(hipEventRecord(w.param_ready.ev, xs));
+  TPS_HIP(hipEventRecord(w.param_ready.ev, ps));
   w.param_ready.valid = true;
   w.grads_live = false;
   return TPS_OK;
@@ -275,10 +282,12 @@ int tps_stage::ensure_layer(int l, bool for_backward, int* entry) {
     if (w.grads_out.valid) TPS_HIP(hipStreamWaitEvent(cs, w.grads_out.ev, 0));
     if (grads_touched[l]) {
       TPS_HIP(hipEventRecord(ev_tmp, cs));
-      TPS_HIP(hipStreamWaitEvent(xs, ev_tmp, 0));
-      TPS_HIP(hipMemcpyAsync(grads_of(l, e), lg[l], p.gbytes, hipMemcpyHostToDevice, xs));
+      TPS_HIP(hipStreamWaitEvent(ps, ev_tmp, 0));
+      // the host block holds this layer's sums once its last flush is done
+      if (lgrads_out_ev[l].valid) TPS_HIP(hipStreamWaitEvent(ps, lgrads_out_ev[l].ev, 0));
+      TPS_HIP(hipMemcpyAsync(grads_of(l, e), lg[l], p.gbytes, hipMemcpyHostToDevice, ps));
       stats.h2d_bytes += p.gbytes;
-      TPS_HIP(hipEventRecord(ev_tmp, xs));
+      TPS_HIP(hipEventRecord(ev_tmp, ps));
       TPS_HIP(hipStreamWaitEvent(cs, ev_tmp, 0));
     } else {
       TPS_HIP(fill_zero_launch(grads_of(l, e), p.gbytes, cs));
@@ -484,6 +493,9 @@ int tps_stage::d2h_layer(int l, int mb) {
   if (!any) return TPS_OK;
   TPS_HIP(hipEventRecord(ev_tmp, cs));
   TPS_HIP(hipStreamWaitEvent(xs, ev_tmp, 0));
+  // the host slot may still be read by the prefetch of its previous micro-batch
+  const SlotEvent& hs = hslot_read_ev[p.host_slot[mb]];
+  if (hs.valid) TPS_HIP(hipStreamWaitEvent(xs, hs.ev, 0));
   for (int t = 0; t < TPS_T_COUNT; ++t) {
     const size_t k = (size_t)l * TPS_T_COUNT + t;
     if (p.oslot_off[k] == kNone) continue;
@@ -491,6 +503,8 @@ int tps_stage::d2h_layer(int l, int mb) {
                            hipMemcpyDeviceToHost, xs));
     stats.d2h_bytes += p.tbytes[t];
   }
+  TPS_HIP(hipEventRecord(offloaded_ev[mb].ev, xs));
+  offloaded_ev[mb].valid = true;
   return TPS_OK;
 }
 
@@ -499,17 +513,21 @@ int tps_stage::d2h_layer(int l, int mb) {
 int tps_stage::prefetch_mb(int mb) {
   if (prefetched[mb]) return TPS_OK;
   const int slot = p.oslot_b[mb];
-  TPS_TRY(acquire_oslot(slot, xs));
+  TPS_TRY(acquire_oslot(slot, ps));
+  // the micro-batch's own offload must have reached the host
+  if (offloaded_ev[mb].valid) TPS_HIP(hipStreamWaitEvent(ps, offloaded_ev[mb].ev, 0));
   for (int l = p.L - 1; l >= 0; --l) {
     for (int t = 0; t < TPS_T_COUNT; ++t) {
       const size_t k = (size_t)l * TPS_T_COUNT + t;
       if (p.oslot_off[k] == kNone) continue;
       TPS_HIP(hipMemcpyAsync(oslot_base(slot) + p.oslot_off[k], host_base(mb) + p.oslot_off[k], p.tbytes[t],
-                             hipMemcpyHostToDevice, xs));
+                             hipMemcpyHostToDevice, ps));
       stats.h2d_bytes += p.tbytes[t];
     }
-    TPS_HIP(hipEventRecord(ready_ev[mb][l], xs));
+    TPS_HIP(hipEventRecord(ready_ev[mb][l], ps));
   }
+  TPS_HIP(hipEventRecord(hslot_read_ev[p.host_slot[mb]].ev, ps));
+  hslot_read_ev[p.host_slot[mb]].valid = true;
   prefetched[mb] = 1;
   return TPS_OK;
 }
@@ -636,16 +654,21 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
   st->host = static_cast<char*>(mem->host_arena);
   st->cs = static_cast<hipStream_t>(mem->compute_stream);
   st->xs = static_cast<hipStream_t>(mem->copy_stream);
-  if ((p.host_bytes || p.weights == TPS_W_STREAM) && (!st->xs || st->xs == st->cs)) {
+  st->ps = mem->prefetch_stream ? static_cast<hipStream_t>(mem->prefetch_stream) : st->xs;
+  if ((p.host_bytes || p.weights == TPS_W_STREAM) && (!st->xs || st->xs == st->cs || st->ps == st->cs)) {
     delete st;
-    return set_error(TPS_EINVAL, "offload and streamed weights need a copy stream distinct from the compute stream");
+    return set_error(TPS_EINVAL, "offload and streamed weights need copy streams distinct from the compute stream");
   }
   auto mkev = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
   hipError_t he = hipGetDevice(&st->device);
   if (he == hipSuccess) he = mkev(&st->ev_tmp);
   st->oslot_ev.resize(p.n_oslots);
-  for (auto& s : st->oslot_ev)
-    if (he == hipSuccess) he = mkev(&s.ev);
+  st->offloaded_ev.resize(p.M);
+  st->hslot_read_ev.resize(p.n_host_slots);
+  st->lgrads_out_ev.resize(p.L);
+  for (auto* v : {&st->oslot_ev, &st->offloaded_ev, &st->hslot_read_ev, &st->lgrads_out_ev})
+    for (auto& s : *v)
+      if (he == hipSuccess) he = mkev(&s.ev);
   st->ready_ev.assign(p.M, std::vector<hipEvent_t>(p.L, nullptr));
   for (int mb = 0; mb < p.M && he == hipSuccess; ++mb)
     if (p.host_slot[mb] >= 0)
@@ -867,6 +890,7 @@ extern "C" int tps_stage_sync(tps_stage* st) {
   if (!st) return set_error(TPS_EINVAL, "null stage");
   TPS_HIP(hipStreamSynchronize(st->cs));
   if (st->xs) TPS_HIP(hipStreamSynchronize(st->xs));
+  if (st->ps && st->ps != st->xs) TPS_HIP(hipStreamSynchronize(st->ps));
   return TPS_OK;
 }
 
@@ -907,9 +931,11 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
   if (!st) return TPS_OK;
   if (st->cs) (void)hipStreamSynchronize(st->cs);
   if (st->xs) (void)hipStreamSynchronize(st->xs);
+  if (st->ps && st->ps != st->xs) (void)hipStreamSynchronize(st->ps);
   if (st->ev_tmp) (void)hipEventDestroy(st->ev_tmp);
-  for (auto& s : st->oslot_ev)
-    if (s.ev) (void)hipEventDestroy(s.ev);
+  for (auto* v : {&st->oslot_ev, &st->offloaded_ev, &st->hslot_read_ev, &st->lgrads_out_ev})
+    for (auto& s : *v)
+      if (s.ev) (void)hipEventDestroy(s.ev);
   for (auto& v : st->ready_ev)
     for (auto e : v)
       if (e) (void)hipEventDestroy(e);

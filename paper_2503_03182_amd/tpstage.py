@@ -79,7 +79,7 @@ class Params(C.Structure):
 class Memory(C.Structure):
     _fields_ = [("device_arena", C.c_void_p), ("device_bytes", C.c_uint64),
                 ("host_arena", C.c_void_p), ("host_bytes", C.c_uint64),
-                ("compute_stream", C.c_void_p), ("copy_stream", C.c_void_p)]
+                ("compute_stream", C.c_void_p), ("copy_stream", C.c_void_p), ("prefetch_stream", C.c_void_p)]
 
 
 class KernelTime(C.Structure):
@@ -304,7 +304,7 @@ class Stage:
     laid out by param_layout()."""
 
     def __init__(self, cfg: StageConfig, layer_params, layer_grads, device="cuda",
-                 compute_stream=None, copy_stream=None):
+                 compute_stream=None, copy_stream=None, prefetch_stream=None):
         import torch
         self.cfg = cfg
         self.info = plan(cfg)
@@ -314,6 +314,7 @@ class Stage:
         self.host = HostBuffer(hb) if hb else None
         self.cs = compute_stream or torch.cuda.Stream(device=self.device)
         self.xs = copy_stream or torch.cuda.Stream(device=self.device)
+        self.ps = prefetch_stream or torch.cuda.Stream(device=self.device)
         self.layer_params, self.layer_grads = list(layer_params), list(layer_grads)
         L = cfg.n_layers
         self._pp = (C.c_void_p * L)(*[t.data_ptr() for t in self.layer_params])
@@ -321,7 +322,7 @@ class Stage:
         prm = Params(C.cast(self._pp, C.POINTER(C.c_void_p)), C.cast(self._gp, C.POINTER(C.c_void_p)))
         mem = Memory(self.arena.data_ptr(), self.arena.numel(),
                      self.host.data_ptr() if self.host is not None else None, hb,
-                     self.cs.cuda_stream, self.xs.cuda_stream)
+                     self.cs.cuda_stream, self.xs.cuda_stream, self.ps.cuda_stream)
         self._c = cfg.to_c()
         h = C.c_void_p()
         check(lib().tps_stage_init(C.byref(self._c), C.byref(prm), C.byref(mem), C.byref(h)))

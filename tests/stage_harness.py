@@ -79,14 +79,19 @@ def inputs(cfg):
     return xs, dys
 
 
-def run_gpu(cfg, xs=None, dys=None, iterations=1, group=False, params=None):
+def run_gpu(cfg, xs=None, dys=None, iterations=1, group=False, params=None, one_copy_stream=False):
     """Runs `iterations` iterations of the planned order; returns numpy results
-    of the last one: dict(ys, dxs, grads, stats, plan)."""
+    of the last one: dict(ys, dxs, grads, stats, plan).  one_copy_stream: both
+    host-link directions on one stream (no prefetch stream of their own)."""
     import torch
     if xs is None:
         xs, dys = inputs(cfg)
     blocks, grads, _ = params if params is not None else make_params(cfg)
-    st = T.Stage(cfg, blocks, grads)
+    if one_copy_stream:
+        xs_ = torch.cuda.Stream()
+        st = T.Stage(cfg, blocks, grads, copy_stream=xs_, prefetch_stream=xs_)
+    else:
+        st = T.Stage(cfg, blocks, grads)
     X = [to_dev(x, cfg.dtype) for x in xs]
     DY = [to_dev(d, cfg.dtype) for d in dys]
     Y = [torch.empty_like(x) for x in X]

@@ -66,6 +66,9 @@ def test_bf16_bitexact_across_policies_orders_and_groups():
     for name, cfg in variants.items():
         out = run_gpu(cfg)
         assert bit_equal(keep, out) == [], name
+    # offloads and prefetches sharing one copy stream
+    out = run_gpu(variants["offload_all"], one_copy_stream=True)
+    assert bit_equal(keep, out) == []
     # same stage, all forwards first: per-mb results do not depend on the order
     assert bit_equal(keep, run_gpu(_mid())) == []
     # layer-major group calls
@@ -83,6 +86,7 @@ def test_streamed_weights_bitexact_to_resident():
             out = run_gpu(cfg, group=group)
             assert bit_equal(resident, out) == [], (window, group)
             assert out["stats"]["h2d_bytes"] > 0 and out["stats"]["d2h_bytes"] > 0
+        assert bit_equal(resident, run_gpu(cfg, one_copy_stream=True)) == [], (window, "one copy stream")
 
 
 def test_repeat_iterations_reproduce():
@@ -90,6 +94,9 @@ def test_repeat_iterations_reproduce():
     one = run_gpu(cfg, iterations=1)
     three = run_gpu(cfg, iterations=3)
     assert bit_equal(one, three) == []
+    # host slots reused across iterations by offloads (copy stream) and
+    # prefetches (prefetch stream) in both orders
+    assert bit_equal(one, run_gpu(cfg, iterations=3, one_copy_stream=True)) == []
 
 
 def test_linearity_in_dy_bitwise():
