@@ -27,9 +27,10 @@ def _round(a, dtype):
 
 
 # ragged shapes take the generic path; tile-aligned ones (M, N multiples of
-# 128 or 256, K of 64) take the direct-to-LDS path at both tile sizes
+# 128 or 256, K of 64) take the direct-to-LDS path at both tile sizes, the
+# 128-row tiles in two K groups when the K tile count is even (384 x 256 x 512)
 GEMM_SHAPES = [(200, 264, 136), (1000, 520, 72), (64, 64, 8), (2072, 4104, 264),
-               (256, 384, 192), (4096, 2560, 128)]
+               (256, 384, 192), (4096, 2560, 128), (384, 256, 512)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
