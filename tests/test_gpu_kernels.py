@@ -169,11 +169,12 @@ ATTN_CASES = [  # (dtype, b, s, heads, d)
 
 
 # head dim 128: grids of 256 to 511 blocks of 128 rows take the forward with
-# the key tiles split in two parts per workgroup, of at least 512 such blocks
-# the forward without the split and the 32-row-per-wave backward; ragged
-# lengths throughout
+# the key tiles split in two parts per workgroup, smaller grids the same with
+# 64 rows per workgroup, at least 512 blocks the forward without splits; the
+# backward fuses dK/dV and dQ below 257 and above 1023 blocks; ragged lengths
+# throughout
 ATTN_BIG_CASES = [("bf16", 2, 130, 128, 128), ("bf16", 2, 520, 52, 128), ("bf16", 1, 1000, 40, 128),
-                  ("bf16", 1, 1500, 4, 128)]
+                  ("bf16", 1, 1500, 4, 128), ("bf16", 1, 2048, 4, 128), ("bf16", 3, 700, 2, 128)]
 
 
 @pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_CASES + ATTN_BIG_CASES)
