@@ -68,6 +68,11 @@ struct tps_stage {
   // cs: kernels; xs: device -> host copies; ps: host -> device copies (xs
   // itself when the caller gives no prefetch stream)
   hipStream_t cs = nullptr, xs = nullptr, ps = nullptr;
+  // gs: the layer backward's parameter-gradient kernels (weight GEMMs, column
+  // sums, finalize), forked from cs where their inputs are ready and joined
+  // back at the end of the layer; ks: the stream the next kernel goes to
+  hipStream_t gs = nullptr, ks = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   int device = 0;
 
   std::vector<SlotEvent> oslot_ev;               // last release of each offload slot
@@ -88,6 +93,7 @@ struct tps_stage {
     std::string name;
     double flops, bytes;
     hipEvent_t a, b;
+    hipStream_t on;
   };
   bool timing = false;
   std::string tprefix;
@@ -155,7 +161,7 @@ struct tps_stage {
     const GemmArgs ga{M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux, ldaux, epi, 0, 0};
     const int t = kbegin(gemm_kernel_name(p.dtype, layout, ga), 2.0 * M * N * K, bytes);
     const int rc = check_hip(gemm_launch(p.dtype, layout, epi, M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr,
-                                         aux, ldaux, cs),
+                                         aux, ldaux, ks),
                              "gemm");
     return rc ? rc : kend(t);
   }
@@ -213,7 +219,7 @@ int tps_stage::finalize_bias_grads(int l, float* G) {
   for (int r = 0; r <= Plan::BP_COUNT; ++r) m.c0[r] = (int)p.bpc[r];
   for (int r = 0; r < Plan::BP_COUNT; ++r) m.goff[r] = (int64_t)(p.goff[which[r]] / 4);
   const int k = kbegin("bias gradient finalize", 0.0, (double)p.bpart_segs * p.bpc[Plan::BP_COUNT] * 8.0);
-  TPS_HIP(colsum_finalize_launch(m, bpart(l), p.bpart_segs, p.bpc[Plan::BP_COUNT], G, cs));
+  TPS_HIP(colsum_finalize_launch(m, bpart(l), p.bpart_segs, p.bpc[Plan::BP_COUNT], G, ks));
   ++stats.kernels;
   return kend(k);
 }
@@ -315,14 +321,14 @@ int tps_stage::kbegin(const char* name, double flops, double bytes) {
       TPS_HIP(hipEventCreate(&ev[i]));
     }
   }
-  TPS_HIP(hipEventRecord(ev[0], cs));
-  tpending.push_back({name, flops, bytes, ev[0], ev[1]});
+  TPS_HIP(hipEventRecord(ev[0], ks));
+  tpending.push_back({name, flops, bytes, ev[0], ev[1], ks});
   return (int)tpending.size() - 1;
 }
 
 int tps_stage::kend(int idx) {
   if (idx < 0) return TPS_OK;
-  TPS_HIP(hipEventRecord(tpending[idx].b, cs));
+  TPS_HIP(hipEventRecord(tpending[idx].b, tpending[idx].on));
   return TPS_OK;
 }
 
@@ -414,6 +420,7 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
 // ---------------------------------------------------------------------------
 int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx) {
   const int T = p.T, h = p.h, f = p.f;
+  ks = cs;
   auto ptr = [&](int t) { return tensor(l, t, mb, true); };
   auto par = [&](int i) { return W + p.poff[i]; };
   auto grd = [&](int i) { return reinterpret_cast<float*>(reinterpret_cast<char*>(G) + p.goff[i]); };
@@ -440,9 +447,18 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   auto colsum = [&](const void* src, int cols, int range) -> int {
     ++stats.kernels;
     const int k = kbegin(cs_name, 0.0, (double)T * cols * es);
-    TPS_HIP(colsum_acc_launch(p.dtype, T, cols, src, cols, bp + p.bpc[range], bstride, cs));
+    TPS_HIP(colsum_acc_launch(p.dtype, T, cols, src, cols, bp + p.bpc[range], bstride, ks));
     return kend(k);
   };
+  // parameter-gradient kernels on gs once what cs issued so far is done;
+  // back to cs for the next input-gradient kernel
+  auto to_gs = [&]() -> int {
+    TPS_HIP(hipEventRecord(ev_fork, cs));
+    TPS_HIP(hipStreamWaitEvent(gs, ev_fork, 0));
+    ks = gs;
+    return TPS_OK;
+  };
+  auto to_cs = [&]() { ks = cs; };
   // beta's columns precede gamma's in the partial block
   auto lnbwd = [&](const void* dout, const void* xin, const float* st, int gi, int be_range, const void* res,
                    void* dst) -> int {
@@ -458,16 +474,26 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   const char* w1t = WT + p.wtoff[2];   // [h, f]
   const char* wot = WT + p.wtoff[1];   // [h, h]
   const char* wqt = WT + p.wtoff[0];   // [h, 3h]
-  TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_GELU_GRAD, T, f, h, dy, h, w2t, h, du, f, nullptr, nullptr, 0, u, f));
+  // The weight and bias gradients run on gs beside the input-gradient chain
+  // on cs (their inputs are only read from here on, and every buffer they
+  // read is rewritten only after the join at the end); the bias partials of
+  // gs and of the LayerNorm passes on cs are disjoint columns.
+  TPS_TRY(to_gs());
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f));
   TPS_TRY(colsum(dy, h, Plan::BP_2));
+  to_cs();
+  TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_GELU_GRAD, T, f, h, dy, h, w2t, h, du, f, nullptr, nullptr, 0, u, f));
+  TPS_TRY(to_gs());
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h));
   TPS_TRY(colsum(du, f, Plan::BP_1));
+  to_cs();
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, f, du, f, w1t, f, t1, h));
   TPS_TRY(lnbwd(t1, x1, ln2, TPS_P_G2, Plan::BP_BE2, dy, dx1));
   // attention block: x1 = x + o Wo^T + bo
+  TPS_TRY(to_gs());
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h));
   TPS_TRY(colsum(dx1, h, Plan::BP_O));
+  to_cs();
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, h, dx1, h, wot, h, t1, h));
   {
     ++stats.kernels;
@@ -475,11 +501,18 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
     TPS_HIP(attention_bwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, lse, t1, dqkv, dvec, cs));
     TPS_TRY(kend(k));
   }
+  TPS_TRY(to_gs());
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h));
   TPS_TRY(colsum(dqkv, 3 * h, Plan::BP_QKV));
+  to_cs();
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, 3 * h, dqkv, 3 * h, wqt, 3 * h, t1, h));
   TPS_TRY(lnbwd(t1, x, ln1, TPS_P_G1, Plan::BP_BE1, dx1, dx));
+  // finalize after both streams' column sums; cs continues once gs is done
+  TPS_TRY(to_gs());
   TPS_TRY(finalize_bias_grads(l, G));
+  to_cs();
+  TPS_HIP(hipEventRecord(ev_join, gs));
+  TPS_HIP(hipStreamWaitEvent(cs, ev_join, 0));
   bpart_clean = true;
   return TPS_OK;
 }
@@ -662,6 +695,10 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
   auto mkev = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
   hipError_t he = hipGetDevice(&st->device);
   if (he == hipSuccess) he = mkev(&st->ev_tmp);
+  if (he == hipSuccess) he = mkev(&st->ev_fork);
+  if (he == hipSuccess) he = mkev(&st->ev_join);
+  if (he == hipSuccess) he = hipStreamCreateWithFlags(&st->gs, hipStreamNonBlocking);   // default priority
+  st->ks = st->cs;
   st->oslot_ev.resize(p.n_oslots);
   st->offloaded_ev.resize(p.M);
   st->hslot_read_ev.resize(p.n_host_slots);
@@ -891,6 +928,7 @@ extern "C" int tps_stage_sync(tps_stage* st) {
   TPS_HIP(hipStreamSynchronize(st->cs));
   if (st->xs) TPS_HIP(hipStreamSynchronize(st->xs));
   if (st->ps && st->ps != st->xs) TPS_HIP(hipStreamSynchronize(st->ps));
+  if (st->gs) TPS_HIP(hipStreamSynchronize(st->gs));
   return TPS_OK;
 }
 
@@ -932,6 +970,12 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
   if (st->cs) (void)hipStreamSynchronize(st->cs);
   if (st->xs) (void)hipStreamSynchronize(st->xs);
   if (st->ps && st->ps != st->xs) (void)hipStreamSynchronize(st->ps);
+  if (st->gs) {
+    (void)hipStreamSynchronize(st->gs);
+    (void)hipStreamDestroy(st->gs);
+  }
+  if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
+  if (st->ev_join) (void)hipEventDestroy(st->ev_join);
   if (st->ev_tmp) (void)hipEventDestroy(st->ev_tmp);
   for (auto* v : {&st->oslot_ev, &st->offloaded_ev, &st->hslot_read_ev, &st->lgrads_out_ev})
     for (auto& s : *v)
