@@ -176,15 +176,28 @@ typedef struct tps_memory {
   void* host_arena;             /* pinned, >= plan.host_arena_bytes (may be NULL
                                    when that is 0)                              */
   uint64_t host_bytes;
-  void* compute_stream;         /* hipStream_t for kernels                      */
-  void* copy_stream;            /* hipStream_t for device -> host copies (and
-                                   for host -> device ones when prefetch_stream
-                                   is NULL)                                     */
+  void* compute_stream;         /* hipStream_t for kernels (NULL: the null
+                                   stream); the stage forks the backward's
+                                   parameter-gradient kernels onto a stream of
+                                   its own and joins them back at the end of
+                                   each layer backward                         */
+  void* copy_stream;            /* hipStream_t for device -> host copies, or
+                                   NULL: the stage creates its own             */
   void* prefetch_stream;        /* hipStream_t for host -> device copies, or
-                                   NULL; a stream of its own lets both link
-                                   directions run at once (the offloads of later
-                                   micro-batches under the prefetches of earlier
-                                   ones, Section 5)                             */
+                                   NULL: the stage creates its own; the same
+                                   stream as copy_stream puts both directions
+                                   on one stream.  Separate streams let both
+                                   link directions run at once (the offloads of
+                                   later micro-batches under the prefetches of
+                                   earlier ones, Section 5).  Streams the stage
+                                   creates each hold a hardware queue that no
+                                   other stream shares (a stream sharing a
+                                   queue with a copy stream waits behind its
+                                   copies) and synchronize with the null
+                                   stream.  Copy streams are used, and created,
+                                   only when the plan moves data over the host
+                                   link; a caller's copy stream must differ
+                                   from compute_stream                         */
 } tps_memory;
 
 typedef struct tps_stats {

@@ -14,6 +14,7 @@
 //  - streamed weights: a window of layer parameter blocks (and f32 gradient
 //    blocks) in the arena, brought in on the copy stream ahead of use.
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <cstring>
 #include <map>
@@ -40,6 +41,22 @@ namespace {
     if (_rc != TPS_OK) return _rc; \
   } while (0)
 
+// A stream the stage owns, on a hardware queue that no other stream shares.
+// The runtime multiplexes ordinary streams over a small pool of hardware
+// queues (GPU_MAX_HW_QUEUES, four by default, the default stream among
+// them); two streams on one queue run in submission order, so a kernel stream
+// that lands on the queue of a copy stream stalls behind every barrier the
+// copies put there.  A stream created with a CU mask gets a queue of its own
+// from the ROCm runtime; the mask here enables every CU.  Such streams are
+// blocking streams: they synchronize with the null stream.
+hipError_t queue_stream(int device, hipStream_t* s) {
+  int ncu = 0;
+  hipError_t e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, device);
+  if (e != hipSuccess) return e;
+  std::vector<uint32_t> mask((size_t)(ncu + 31) / 32, 0xFFFFFFFFu);
+  return hipExtStreamCreateWithCUMask(s, (uint32_t)mask.size(), mask.data());
+}
+
 struct SlotEvent {
   hipEvent_t ev = nullptr;
   bool valid = false;
@@ -65,9 +82,10 @@ struct tps_stage {
   char* arena = nullptr;
   bool bpart_clean = false;   // the bias partial blocks are all zero (no layer backward cut short)
   char* host = nullptr;
-  // cs: kernels; xs: device -> host copies; ps: host -> device copies (xs
-  // itself when the caller gives no prefetch stream)
+  // cs: kernels; xs: device -> host copies; ps: host -> device copies (the
+  // caller's, or the stage's own when it gives none: own_xs, own_ps)
   hipStream_t cs = nullptr, xs = nullptr, ps = nullptr;
+  bool own_xs = false, own_ps = false;
   // gs: the layer backward's parameter-gradient kernels (weight GEMMs, column
   // sums, finalize), forked from cs where their inputs are ready and joined
   // back at the end of the layer; ks: the stream the next kernel goes to
@@ -686,9 +704,9 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
   st->arena = static_cast<char*>(mem->device_arena);
   st->host = static_cast<char*>(mem->host_arena);
   st->cs = static_cast<hipStream_t>(mem->compute_stream);
-  st->xs = static_cast<hipStream_t>(mem->copy_stream);
-  st->ps = mem->prefetch_stream ? static_cast<hipStream_t>(mem->prefetch_stream) : st->xs;
-  if ((p.host_bytes || p.weights == TPS_W_STREAM) && (!st->xs || st->xs == st->cs || st->ps == st->cs)) {
+  const bool link = p.host_bytes || p.weights == TPS_W_STREAM;
+  if (link && ((mem->copy_stream && mem->copy_stream == mem->compute_stream) ||
+               (mem->prefetch_stream && mem->prefetch_stream == mem->compute_stream))) {
     delete st;
     return set_error(TPS_EINVAL, "offload and streamed weights need copy streams distinct from the compute stream");
   }
@@ -697,7 +715,13 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
   if (he == hipSuccess) he = mkev(&st->ev_tmp);
   if (he == hipSuccess) he = mkev(&st->ev_fork);
   if (he == hipSuccess) he = mkev(&st->ev_join);
-  if (he == hipSuccess) he = hipStreamCreateWithFlags(&st->gs, hipStreamNonBlocking);   // default priority
+  if (he == hipSuccess) he = queue_stream(st->device, &st->gs);
+  if (link) {
+    st->xs = static_cast<hipStream_t>(mem->copy_stream);
+    st->ps = static_cast<hipStream_t>(mem->prefetch_stream);
+    if (he == hipSuccess && !st->xs && (he = queue_stream(st->device, &st->xs)) == hipSuccess) st->own_xs = true;
+    if (he == hipSuccess && !st->ps && (he = queue_stream(st->device, &st->ps)) == hipSuccess) st->own_ps = true;
+  }
   st->ks = st->cs;
   st->oslot_ev.resize(p.n_oslots);
   st->offloaded_ev.resize(p.M);
@@ -719,7 +743,7 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
     }
   }
   if (he != hipSuccess) {
-    int r = check_hip(he, "tps_stage_init: event creation");
+    int r = check_hip(he, "tps_stage_init: stream and event creation");
     tps_stage_destroy(st);
     return r;
   }
@@ -974,6 +998,8 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
     (void)hipStreamSynchronize(st->gs);
     (void)hipStreamDestroy(st->gs);
   }
+  if (st->own_xs) (void)hipStreamDestroy(st->xs);
+  if (st->own_ps) (void)hipStreamDestroy(st->ps);
   if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
   if (st->ev_join) (void)hipEventDestroy(st->ev_join);
   if (st->ev_tmp) (void)hipEventDestroy(st->ev_tmp);

@@ -312,9 +312,9 @@ class Stage:
         self.arena = torch.empty(max(self.info["device_arena_bytes"], 256), dtype=torch.uint8, device=self.device)
         hb = self.info["host_arena_bytes"]
         self.host = HostBuffer(hb) if hb else None
+        # compute on a torch stream; copy streams default to the stage's own
         self.cs = compute_stream or torch.cuda.Stream(device=self.device)
-        self.xs = copy_stream or torch.cuda.Stream(device=self.device)
-        self.ps = prefetch_stream or torch.cuda.Stream(device=self.device)
+        self.xs, self.ps = copy_stream, prefetch_stream
         self.layer_params, self.layer_grads = list(layer_params), list(layer_grads)
         L = cfg.n_layers
         self._pp = (C.c_void_p * L)(*[t.data_ptr() for t in self.layer_params])
@@ -322,7 +322,7 @@ class Stage:
         prm = Params(C.cast(self._pp, C.POINTER(C.c_void_p)), C.cast(self._gp, C.POINTER(C.c_void_p)))
         mem = Memory(self.arena.data_ptr(), self.arena.numel(),
                      self.host.data_ptr() if self.host is not None else None, hb,
-                     self.cs.cuda_stream, self.xs.cuda_stream, self.ps.cuda_stream)
+                     self.cs.cuda_stream, _stream(self.xs), _stream(self.ps))
         self._c = cfg.to_c()
         h = C.c_void_p()
         check(lib().tps_stage_init(C.byref(self._c), C.byref(prm), C.byref(mem), C.byref(h)))

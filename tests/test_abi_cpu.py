@@ -204,6 +204,38 @@ def test_op_argument_errors_without_gpu():
     assert T.op_workspace_bytes(T.WS_ATTN_BWD, 256, 4) == 256 * 4 * 4
 
 
+def test_stage_init_argument_errors_without_gpu():
+    # the memory checks run before any device call: fake (never dereferenced)
+    # device addresses are enough to reach each of them
+    cfg = W.tiny("offload")
+    p = T.plan(cfg)
+    L = cfg.n_layers
+    blk = (C.c_void_p * L)(*([0x10000] * L))
+    gblk = (C.c_void_p * L)(*([0x20000] * L))
+    prm = T.Params(C.cast(blk, C.POINTER(C.c_void_p)), C.cast(gblk, C.POINTER(C.c_void_p)))
+    c = cfg.to_c()
+
+    def init(arena, nbytes, host, hbytes, cs, xs, ps):
+        h = C.c_void_p()
+        mem = T.Memory(arena, nbytes, host, hbytes, cs, xs, ps)
+        rc = T.lib().tps_stage_init(C.byref(c), C.byref(prm), C.byref(mem), C.byref(h))
+        assert not h.value
+        return rc, T.lib().tps_last_error().decode()
+
+    A, HB = p["device_arena_bytes"], p["host_arena_bytes"]
+    assert HB > 0
+    rc, msg = init(0x100000, A - 1, 0x200000, HB, 0x1, None, None)
+    assert rc == T.TPS_ENOMEM and "device arena" in msg
+    rc, msg = init(0x100080, A, 0x200000, HB, 0x1, None, None)
+    assert rc == T.TPS_EINVAL and "aligned" in msg
+    rc, msg = init(0x100000, A, 0x200000, HB - 1, 0x1, None, None)
+    assert rc == T.TPS_ENOMEM and "host arena" in msg
+    rc, msg = init(0x100000, A, 0x200000, HB, 0x1, 0x1, None)
+    assert rc == T.TPS_EINVAL and "distinct" in msg
+    rc, msg = init(0x100000, A, 0x200000, HB, 0x1, 0x2, 0x1)
+    assert rc == T.TPS_EINVAL and "distinct" in msg
+
+
 def test_param_layout_offsets():
     cfg = W.tiny()
     po, pb, go, gb = T.param_layout(cfg)
