@@ -406,16 +406,25 @@ int make_plan(const tps_config* c, Plan* out) {
 
   // backward working buffers
   const uint64_t hb = align256(T * h * es), fb = align256(T * f * es), qb = align256(T * 3 * h * es);
-  p.work.gA = 0;
-  p.work.gB = hb;
-  p.work.dx1 = 2 * hb;
-  p.work.t1 = 3 * hb;
-  p.work.du = 4 * hb;
-  p.work.dqkv = 4 * hb + fb;
-  p.work.dvec = p.work.dqkv + qb;
-  p.work.ws = p.work.dvec + align256((uint64_t)p.b * p.nh * p.s * 4);
-  p.ws_bytes = align256(4 * std::max(colsum_ws_elems(p.T, std::max(3 * p.h, p.f)), colsum_ws_elems(p.T, 2 * p.h)));
-  p.work_bytes = p.work.ws + p.ws_bytes;
+  p.defer_join = p.weights == TPS_W_RESIDENT && (p.granularity == TPS_GRAN_SEGMENT || p.n_replay_layers == 0);
+  {
+    uint64_t o = 0;
+    auto take = [&](uint64_t bytes) {
+      const uint64_t r = o;
+      o += bytes;
+      return r;
+    };
+    const int ng = p.defer_join ? 3 : 2, sets = p.defer_join ? 2 : 1;
+    for (int i = 0; i < 3; ++i) p.work.g[i] = i < ng ? take(hb) : p.work.g[0];
+    for (int k = 0; k < 2; ++k) {
+      p.work.dx1[k] = k < sets ? take(hb) : p.work.dx1[0];
+      p.work.du[k] = k < sets ? take(fb) : p.work.du[0];
+      p.work.dqkv[k] = k < sets ? take(qb) : p.work.dqkv[0];
+    }
+    p.work.t1 = take(hb);
+    p.work.dvec = take(align256((uint64_t)p.b * p.nh * p.s * 4));
+    p.work_bytes = o;
+  }
 
   {
     const int64_t H = (int64_t)h, F = (int64_t)f;

@@ -58,12 +58,20 @@ struct Plan {
   std::vector<uint32_t> replay_ops;   // [L] bit mask over FwdOp
   int n_replay_layers = 0;
 
-  // backward working buffers (offsets inside the work region)
+  // backward working buffers (offsets inside the work region): the running
+  // input gradient between layers (g, rotating), the layer's intermediate
+  // gradients (dx1, du, dqkv: one set per layer parity when defer_join),
+  // the attention output projection's input gradient (t1) and the
+  // attention backward's row dot products (dvec)
   struct Work {
-    uint64_t gA, gB, dx1, t1, du, dqkv, dvec, ws;
+    uint64_t g[3], dx1[2], du[2], dqkv[2], t1, dvec;
   } work{};
   uint64_t work_bytes = 0;
-  uint64_t ws_bytes = 0;
+  // the parameter-gradient kernels of a layer backward may still run while
+  // the next layer's input-gradient chain starts; the two streams join once
+  // per micro-batch (resident weights, and no replay between layer
+  // backwards, whose buffers the lagging kernels could still be reading)
+  bool defer_join = false;
 
   // per-layer f32 partial sums of the bias and LayerNorm parameter gradients:
   // [segments][bpart_cols] with column ranges (bpc[]) for b_qkv, b_o, b_1,

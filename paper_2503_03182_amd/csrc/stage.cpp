@@ -91,6 +91,10 @@ struct tps_stage {
   // back at the end of the layer; ks: the stream the next kernel goes to
   hipStream_t gs = nullptr, ks = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  // deferred joins: ev_gs[k] marks the end of the last parameter-gradient
+  // work that read the backward buffers of layer parity k
+  hipEvent_t ev_gs[2] = {nullptr, nullptr};
+  bool gs_pending[2] = {false, false};
   int device = 0;
 
   std::vector<SlotEvent> oslot_ev;               // last release of each offload slot
@@ -187,7 +191,14 @@ struct tps_stage {
     return p.dtype == TPS_BF16 ? bf16_name : f32_name;
   }
   int fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots);
-  int bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx);
+  int bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp, bool defer);
+  // cs waits for everything issued to gs so far
+  int join_gs() {
+    TPS_HIP(hipEventRecord(ev_join, gs));
+    TPS_HIP(hipStreamWaitEvent(cs, ev_join, 0));
+    gs_pending[0] = gs_pending[1] = false;
+    return TPS_OK;
+  }
   int forward_one(int mb, const void* x, void* y);
   int backward_one(int mb, const void* dy, void* dx);
   int prefetch_mb(int mb);
@@ -436,9 +447,17 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
 // ---------------------------------------------------------------------------
 // One layer backward; parameter gradients accumulate into G (f32).
 // ---------------------------------------------------------------------------
-int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx) {
+// wp: the set of intermediate-gradient buffers to use; defer: leave the
+// parameter-gradient kernels running on gs at the end (they are joined before
+// the buffers of set wp are written again, and once per micro-batch)
+int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp,
+                         bool defer) {
   const int T = p.T, h = p.h, f = p.f;
   ks = cs;
+  if (defer && gs_pending[wp]) {
+    TPS_HIP(hipStreamWaitEvent(cs, ev_gs[wp], 0));
+    gs_pending[wp] = false;
+  }
   auto ptr = [&](int t) { return tensor(l, t, mb, true); };
   auto par = [&](int i) { return W + p.poff[i]; };
   auto grd = [&](int i) { return reinterpret_cast<float*>(reinterpret_cast<char*>(G) + p.goff[i]); };
@@ -447,12 +466,11 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   const float* lse = static_cast<const float*>(ptr(TPS_T_LSE));
   const float* ln1 = static_cast<const float*>(ptr(TPS_T_LN1));
   const float* ln2 = static_cast<const float*>(ptr(TPS_T_LN2));
-  void* dx1 = work(p.work.dx1);
+  void* dx1 = work(p.work.dx1[wp]);
   void* t1 = work(p.work.t1);
-  void* du = work(p.work.du);
-  void* dqkv = work(p.work.dqkv);
+  void* du = work(p.work.du[wp]);
+  void* dqkv = work(p.work.dqkv[wp]);
   float* dvec = reinterpret_cast<float*>(work(p.work.dvec));
-  float* ws = reinterpret_cast<float*>(work(p.work.ws));
 
   const double es = p.esize;
   const char* cs_name = "column sums";
@@ -494,8 +512,8 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   const char* wqt = WT + p.wtoff[0];   // [h, 3h]
   // The weight and bias gradients run on gs beside the input-gradient chain
   // on cs (their inputs are only read from here on, and every buffer they
-  // read is rewritten only after the join at the end); the bias partials of
-  // gs and of the LayerNorm passes on cs are disjoint columns.
+  // read is rewritten only after a join); the bias partials of gs and of the
+  // LayerNorm passes on cs are disjoint columns.
   TPS_TRY(to_gs());
   TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f));
   TPS_TRY(colsum(dy, h, Plan::BP_2));
@@ -525,12 +543,17 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   to_cs();
   TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, h, 3 * h, dqkv, 3 * h, wqt, 3 * h, t1, h));
   TPS_TRY(lnbwd(t1, x, ln1, TPS_P_G1, Plan::BP_BE1, dx1, dx));
-  // finalize after both streams' column sums; cs continues once gs is done
+  // finalize after both streams' column sums; cs continues at once (defer)
+  // or once gs is done
   TPS_TRY(to_gs());
   TPS_TRY(finalize_bias_grads(l, G));
   to_cs();
-  TPS_HIP(hipEventRecord(ev_join, gs));
-  TPS_HIP(hipStreamWaitEvent(cs, ev_join, 0));
+  if (defer) {
+    TPS_HIP(hipEventRecord(ev_gs[wp], gs));
+    gs_pending[wp] = true;
+  } else {
+    TPS_TRY(join_gs());
+  }
   bpart_clean = true;
   return TPS_OK;
 }
@@ -647,9 +670,12 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
       }
     }
   }
+  // running input gradient: with deferred joins three buffers rotate, so the
+  // one layer l writes was last read two layers up (by kernels the wait at
+  // the start of its backward has joined), else two alternate
   const void* cur = dy;
-  char* gA = work(p.work.gA);
-  char* gB = work(p.work.gB);
+  char* gb[3] = {work(p.work.g[0]), work(p.work.g[1]), work(p.work.g[2])};
+  const bool defer = p.defer_join;
   for (int l = p.L - 1; l >= 0; --l) {
     int e = -1;
     TPS_TRY(ensure_layer(l, true, &e));
@@ -659,14 +685,17 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
       TPS_TRY(fwd_layer(l, mb, W, nullptr, p.replay_ops[l], true, true));
       ++stats.replays;
     }
-    void* out = (l == 0) ? dx : (cur == gA ? gB : gA);
-    TPS_TRY(bwd_layer(l, mb, W, wt_of(l, e), grads_of(l, e), cur, out));
+    void* out = (l == 0) ? dx : defer ? gb[(p.L - 1 - l) % 3] : (cur == gb[0] ? gb[1] : gb[0]);
+    TPS_TRY(bwd_layer(l, mb, W, wt_of(l, e), grads_of(l, e), cur, out, defer ? (l & 1) : 0, defer));
     if (e >= 0) {
       TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
       win[e].last_use.valid = true;
     }
     cur = out;
   }
+  // the lagging kernels read the caller's dy and the micro-batch's saved
+  // tensors: join before the slot and the buffers are handed back
+  if (defer) TPS_TRY(join_gs());
   if (p.oslot_bytes) TPS_TRY(release_oslot(p.oslot_b[mb], cs));
   return TPS_OK;
 }
@@ -713,8 +742,15 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
   auto mkev = [&](hipEvent_t* e) { return hipEventCreateWithFlags(e, hipEventDisableTiming); };
   hipError_t he = hipGetDevice(&st->device);
   if (he == hipSuccess) he = mkev(&st->ev_tmp);
-  if (he == hipSuccess) he = mkev(&st->ev_fork);
-  if (he == hipSuccess) he = mkev(&st->ev_join);
+  // fork and join events order kernels of two streams on this device: no
+  // system-scope fence (kernel completion already releases at device scope)
+  auto mkev_dev = [&](hipEvent_t* e) {
+    return hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventDisableSystemFence);
+  };
+  if (he == hipSuccess) he = mkev_dev(&st->ev_fork);
+  if (he == hipSuccess) he = mkev_dev(&st->ev_join);
+  for (auto& e : st->ev_gs)
+    if (he == hipSuccess) he = mkev_dev(&e);
   if (he == hipSuccess) he = queue_stream(st->device, &st->gs);
   if (link) {
     st->xs = static_cast<hipStream_t>(mem->copy_stream);
@@ -903,7 +939,7 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
     for (int l = 0; l < p.L; ++l) any |= p.replay_ops[l] != 0;
     if (any) return set_error(TPS_EINVAL, "segment replay shares one replay buffer: backward groups of more than one micro-batch need layer granularity");
   }
-  char* gA = st->work(p.work.gA);
+  char* gA = st->work(p.work.g[0]);
   for (int l = p.L - 1; l >= 0; --l) {
     int e = -1;
     TPS_TRY(st->ensure_layer(l, true, &e));
@@ -927,7 +963,7 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
       }
       // the running gradient of micro-batch i lives in dx[i] between layers
       const void* in = (l == p.L - 1) ? dy[i] : dx[i];
-      TPS_TRY(st->bwd_layer(l, mb, W, st->wt_of(l, e), st->grads_of(l, e), in, gA));
+      TPS_TRY(st->bwd_layer(l, mb, W, st->wt_of(l, e), st->grads_of(l, e), in, gA, 0, false));
       TPS_HIP(hipMemcpyAsync(dx[i], gA, p.tbytes[TPS_T_X], hipMemcpyDeviceToDevice, st->cs));
     }
     if (e >= 0) {
@@ -1002,6 +1038,8 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
   if (st->own_ps) (void)hipStreamDestroy(st->ps);
   if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
   if (st->ev_join) (void)hipEventDestroy(st->ev_join);
+  for (auto e : st->ev_gs)
+    if (e) (void)hipEventDestroy(e);
   if (st->ev_tmp) (void)hipEventDestroy(st->ev_tmp);
   for (auto* v : {&st->oslot_ev, &st->offloaded_ev, &st->hslot_read_ev, &st->lgrads_out_ev})
     for (auto& s : *v)
