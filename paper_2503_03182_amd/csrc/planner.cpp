@@ -407,6 +407,9 @@ int make_plan(const tps_config* c, Plan* out) {
   // backward working buffers
   const uint64_t hb = align256(T * h * es), fb = align256(T * f * es), qb = align256(T * 3 * h * es);
   p.defer_join = p.weights == TPS_W_RESIDENT && (p.granularity == TPS_GRAN_SEGMENT || p.n_replay_layers == 0);
+  p.replay_independent = true;
+  for (int l = 1; l < p.L; ++l)
+    if (p.policy[(size_t)l * TPS_T_COUNT + TPS_T_X] == TPS_RECOMPUTE) p.replay_independent = false;
   {
     uint64_t o = 0;
     auto take = [&](uint64_t bytes) {

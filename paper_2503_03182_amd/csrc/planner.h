@@ -72,6 +72,9 @@ struct Plan {
   // per micro-batch (resident weights, and no replay between layer
   // backwards, whose buffers the lagging kernels could still be reading)
   bool defer_join = false;
+  // no layer's replay reads another layer's replayed output (every layer
+  // input is kept or offloaded): the segment replay may run in any layer order
+  bool replay_independent = false;
 
   // per-layer f32 partial sums of the bias and LayerNorm parameter gradients:
   // [segments][bpart_cols] with column ranges (bpc[]) for b_qkv, b_o, b_1,

@@ -91,10 +91,14 @@ struct tps_stage {
   // back at the end of the layer; ks: the stream the next kernel goes to
   hipStream_t gs = nullptr, ks = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
-  // deferred joins: ev_gs[k] marks the end of the last parameter-gradient
-  // work that read the backward buffers of layer parity k
+  // deferred joins: layer backwards of an iteration are numbered in issue
+  // order (bstep); ev_gs[k] marks the end of the last parameter-gradient work
+  // of a layer backward with bstep parity k (layer gs_layer[k]), which read
+  // the buffers of set k; gs_pending[k]: cs has not waited for it yet
   hipEvent_t ev_gs[2] = {nullptr, nullptr};
   bool gs_pending[2] = {false, false};
+  int gs_layer[2] = {-1, -1};
+  int bstep = 0;
   int device = 0;
 
   std::vector<SlotEvent> oslot_ev;               // last release of each offload slot
@@ -192,6 +196,17 @@ struct tps_stage {
   }
   int fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots);
   int bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp, bool defer);
+  // cs waits for the lagging parameter-gradient kernels of layer l (and all
+  // gs work before them), if any are pending
+  int wait_gs_layer(int l) {
+    for (int k = 0; k < 2; ++k)
+      if (gs_pending[k] && gs_layer[k] == l) {
+        TPS_HIP(hipStreamWaitEvent(cs, ev_gs[k], 0));
+        gs_pending[k] = false;
+      }
+    return TPS_OK;
+  }
+  int join_if_pending() { return (gs_pending[0] || gs_pending[1]) ? join_gs() : TPS_OK; }
   // cs waits for everything issued to gs so far
   int join_gs() {
     TPS_HIP(hipEventRecord(ev_join, gs));
@@ -551,6 +566,7 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   if (defer) {
     TPS_HIP(hipEventRecord(ev_gs[wp], gs));
     gs_pending[wp] = true;
+    gs_layer[wp] = l;
   } else {
     TPS_TRY(join_gs());
   }
@@ -632,6 +648,9 @@ int tps_stage::check_op(int kind, int mb) {
 // ---------------------------------------------------------------------------
 int tps_stage::forward_one(int mb, const void* x, void* y) {
   const bool off = p.host_slot[mb] >= 0;
+  // a forward may reuse the saved-tensor slot of a micro-batch whose last
+  // parameter-gradient kernels are still running
+  TPS_TRY(join_if_pending());
   if (p.oslot_bytes) TPS_TRY(acquire_oslot(p.oslot_f[mb], cs));
   TPS_HIP(hipMemcpyAsync(tensor(0, TPS_T_X, mb, false), x, p.tbytes[TPS_T_X], hipMemcpyDeviceToDevice, cs));
   for (int l = 0; l < p.L; ++l) {
@@ -656,9 +675,16 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
     TPS_TRY(prefetch_mb(mb));
     for (int l = 0; l < p.L; ++l) TPS_HIP(hipStreamWaitEvent(cs, ready_ev[mb][l], 0));
   }
+  const bool defer = p.defer_join;
   if (p.granularity == TPS_GRAN_SEGMENT) {
-    for (int l = 0; l < p.L; ++l) {
+    // with deferred joins the previous micro-batch's last layer backwards may
+    // still read their replayed tensors: replay top-down where the layers are
+    // independent, so those layers come last, and wait for their kernels
+    const bool down = defer && p.replay_independent;
+    for (int i = 0; i < p.L; ++i) {
+      const int l = down ? p.L - 1 - i : i;
       if (!p.replay_ops[l]) continue;
+      if (defer) TPS_TRY(wait_gs_layer(l));
       int e = -1;
       TPS_TRY(ensure_layer(l, false, &e));
       void* yl = (l == p.L - 1) ? nullptr : tensor(l + 1, TPS_T_X, mb, true);
@@ -670,12 +696,12 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
       }
     }
   }
-  // running input gradient: with deferred joins three buffers rotate, so the
-  // one layer l writes was last read two layers up (by kernels the wait at
-  // the start of its backward has joined), else two alternate
+  // running input gradient: with deferred joins three buffers rotate over the
+  // iteration's layer backwards, so the one a layer backward writes was last
+  // read two layer backwards earlier (by kernels the wait at the start of
+  // bwd_layer has joined), else two alternate
   const void* cur = dy;
   char* gb[3] = {work(p.work.g[0]), work(p.work.g[1]), work(p.work.g[2])};
-  const bool defer = p.defer_join;
   for (int l = p.L - 1; l >= 0; --l) {
     int e = -1;
     TPS_TRY(ensure_layer(l, true, &e));
@@ -685,18 +711,22 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
       TPS_TRY(fwd_layer(l, mb, W, nullptr, p.replay_ops[l], true, true));
       ++stats.replays;
     }
-    void* out = (l == 0) ? dx : defer ? gb[(p.L - 1 - l) % 3] : (cur == gb[0] ? gb[1] : gb[0]);
-    TPS_TRY(bwd_layer(l, mb, W, wt_of(l, e), grads_of(l, e), cur, out, defer ? (l & 1) : 0, defer));
+    void* out = (l == 0) ? dx : defer ? gb[bstep % 3] : (cur == gb[0] ? gb[1] : gb[0]);
+    TPS_TRY(bwd_layer(l, mb, W, wt_of(l, e), grads_of(l, e), cur, out, defer ? (bstep & 1) : 0, defer));
+    ++bstep;
     if (e >= 0) {
       TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
       win[e].last_use.valid = true;
     }
     cur = out;
   }
-  // the lagging kernels read the caller's dy and the micro-batch's saved
-  // tensors: join before the slot and the buffers are handed back
-  if (defer) TPS_TRY(join_gs());
-  if (p.oslot_bytes) TPS_TRY(release_oslot(p.oslot_b[mb], cs));
+  // Pending now: the parameter-gradient kernels of the last two layer
+  // backwards (bottom layers), which read this micro-batch's saved tensors
+  // and, with fewer than three layers, the caller's dy.  Its staging slot is
+  // handed back on gs, after them; later forwards, the next replay of those
+  // layers and the end of the iteration wait for them.
+  if (defer && p.L < 3) TPS_TRY(join_gs());
+  if (p.oslot_bytes) TPS_TRY(release_oslot(p.oslot_b[mb], defer ? gs : cs));
   return TPS_OK;
 }
 
@@ -802,6 +832,9 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
   std::fill(st->prefetched.begin(), st->prefetched.end(), 0);
   st->stats = tps_stats{};
   const Plan& p = st->p;
+  // an iteration cut short may leave parameter-gradient kernels pending
+  TPS_TRY(st->join_if_pending());
+  st->bstep = 0;
   if (!st->bpart_clean) {
     // first iteration, or a layer backward was cut short by an error
     hipError_t e = fill_zero_launch(st->arena + p.off_bpart, (uint64_t)p.L * p.bpart_bytes, st->cs);
@@ -835,7 +868,11 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
 static int finish_op(tps_stage* st) {
   ++st->cursor;
   st->stats.ops_done = st->cursor;
-  if (st->cursor == (int)st->p.op_kind.size()) return st->flush_all_grads();
+  if (st->cursor == (int)st->p.op_kind.size()) {
+    // gradients complete in compute-stream order at the end of the iteration
+    TPS_TRY(st->join_if_pending());
+    return st->flush_all_grads();
+  }
   return TPS_OK;
 }
 
