@@ -181,6 +181,25 @@ __device__ __forceinline__ void read_frags(bf16x8 (&f)[NF], const FragAddr<ROWS,
   }
 }
 
+// Issue the LDS read(s) of fragment N alone of the wave's k-step KK.
+template <int ROWS, bool KC, int BK, int NF, int KSW, int KK, int N>
+__device__ __forceinline__ void read_frag(bf16x8 (&f)[NF], const FragAddr<ROWS, KC, BK, NF, KSW>& a,
+                                          uint32_t stage) {
+  static_assert(N < NF, "fragment index");
+  if constexpr (KC) {
+    constexpr int RS = BK * 64;   // bytes between row blocks of 32
+    f[N] = ds_b128<N * RS>(stage + a.base[KK]);
+  } else {
+    constexpr int ROWB = ROWS * 2;
+    typedef __attribute__((ext_vector_type(8))) short s16x8;
+    const uint32_t p = stage + a.base[N];
+    const s16x4 lo = ds_tr16<16 * KK * ROWB>(p);
+    const s16x4 hi = ds_tr16<16 * KK * ROWB + 4 * ROWB>(p);
+    s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    f[N] = *reinterpret_cast<bf16x8*>(&v);
+  }
+}
+
 }  // namespace gl
 
 // Epilogue through LDS: per 32-row strip, each wave parks its accumulators

@@ -10,8 +10,8 @@
 //    the stage of tile kt (whose fragments are all in registers by then) is
 //    refilled with tile kt+STAGES and the first fragments of tile kt+1 are
 //    read, both overlapping the last MFMAs of tile kt;
-//  * inside a tile the fragments of k-step ks+1 are read while the MFMAs of
-//    k-step ks run.
+//  * inside a tile the fragments of k-step ks+1 are read between the MFMAs of
+//    k-step ks (a few reads after each of its first MFMAs).
 // Waves own a (BM/WGM) x (BN/WGN) block of 32x32x16 MFMA tiles; the K loop of
 // every wave is sequential in steps of 16, so every output element sums its
 // products in the same order whatever the tile shape.
@@ -23,7 +23,6 @@ namespace tps {
 namespace gp {
 
 using gl::FragAddr;
-using gl::frag_reads;
 using gl::lds_barrier;
 using gl::lds_u32;
 using gl::pin;
@@ -185,8 +184,9 @@ void gemm_bf16_kernel(GemmArgs g) {
   fra.init(wm * WM, 0, lane);
   frb.init(wn * WN, 0, lane);
   const uint32_t lds0 = lds_u32(smem);
-  constexpr int RA = frag_reads<A_KC, TM>(), RB = frag_reads<B_KC, TN>();
-  static_assert(RA <= 15 && RB <= 15, "lgkmcnt range");
+  // the fragment buffers alternate per k-step, so the next tile's first
+  // k-step reads into the buffer k-step 0 uses
+  static_assert(KS % 2 == 0, "k-steps per tile must be even");
 
   const int nk = g.K / BK;
   // prologue: fill the ring
@@ -201,73 +201,58 @@ void gemm_bf16_kernel(GemmArgs g) {
   read_frags<BM, A_KC, BK, TM, KS, 0>(fa[0], fra, lds0);
   read_frags<BN, B_KC, BK, TN, KS, 0>(fb[0], frb, lds0 + A_BYTES);
 
-  // one K tile; REFILL: the stage is refilled with tile kt+STAGES (every tile
-  // but the last STAGES), which also fixes the number of tiles in flight
+  // One K tile; REFILL: the stage is refilled with tile kt+STAGES (every tile
+  // but the last STAGES), which also fixes the number of tiles in flight.
+  // The fragments of k-step kk+1 (of the next tile's first k-step in the
+  // last one) are read between the MFMAs of k-step kk, all within its first
+  // half, so LDS traffic spreads over the MFMA stream.
+  constexpr int NFR = TM + TN, NM = TM * TN;
+  constexpr int RPM = (NFR + NM / 2 - 1) / (NM / 2);   // fragment reads per MFMA
   auto k_tile = [&](int kt, auto refill_c) {
     constexpr bool REFILL = decltype(refill_c)::value;
     const int cur = kt % STAGES;
-    const uint32_t as = lds0 + cur * STAGE, bs = as + A_BYTES;
+    const uint32_t as = lds0 + cur * STAGE;
+    const uint32_t nst = lds0 + ((kt + 1) % STAGES) * STAGE;
     static_for<KS>([&](auto kc) {
       constexpr int kk = decltype(kc)::value, fc = kk & 1;
-      if constexpr (kk + 1 < KS) {
-        read_frags<BM, A_KC, BK, TM, KS, kk + 1>(fa[fc ^ 1], fra, as);
-        if constexpr (RA + RB <= 15) {
-          read_frags<BN, B_KC, BK, TN, KS, kk + 1>(fb[fc ^ 1], frb, bs);
-          wait_lgkm<RA + RB>();
-        } else {
-          wait_lgkm<RA>();
-          read_frags<BN, B_KC, BK, TN, KS, kk + 1>(fb[fc ^ 1], frb, bs);
-        }
+      constexpr bool LAST = kk + 1 == KS;
+      constexpr int NK = LAST ? 0 : kk + 1;   // k-step the reads are for
+      // the fragments of k-step kk were read during the previous k-step
+      wait_lgkm<0>();
 #pragma unroll
-        for (int i = 0; i < TM; ++i) pin(fa[fc][i]);
+      for (int i = 0; i < TM; ++i) pin(fa[fc][i]);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) pin(fb[fc][j]);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j) acc[i][j] = Mma<bf16>::run(fa[fc][i], fb[fc][j], acc[i][j]);
-        __builtin_amdgcn_sched_barrier(0);
-      } else {
-        // last k-step: every fragment of tile kt is in registers after this
-        // wait, so the stage can be handed back
-        wait_lgkm<0>();
-#pragma unroll
-        for (int i = 0; i < TM; ++i) pin(fa[fc][i]);
-#pragma unroll
-        for (int j = 0; j < TN; ++j) pin(fb[fc][j]);
-        // tile kt+1 has landed once the tiles after it are the only loads
-        // left (on the last tile: once nothing is left)
+      for (int j = 0; j < TN; ++j) pin(fb[fc][j]);
+      if constexpr (LAST) {
+        // tile kt+1 landed (all waves), tile kt's stage no longer read
         if constexpr (REFILL) wait_vm<(STAGES - 2) * LPT>();
         else wait_tiles<STAGES - 2, LPT>(max(0, min(STAGES - 2, nk - 2 - kt)));
-        // all waves: tile kt+1 visible, tile kt's stage no longer read
         lds_barrier();
-        // first fragments of tile kt+1 (after the last tile: in-bounds reads
-        // of a stale stage, never used)
-        const uint32_t nst = lds0 + ((kt + 1) % STAGES) * STAGE;
-        read_frags<BM, A_KC, BK, TM, KS, 0>(fa[fc ^ 1], fra, nst);
-        read_frags<BN, B_KC, BK, TN, KS, 0>(fb[fc ^ 1], frb, nst + A_BYTES);
-        // refill the stage of tile kt with tile kt+STAGES, one load per MFMA
-        static_for<TM * TN>([&](auto mc) {
-          constexpr int m = decltype(mc)::value, i = m / TN, j = m % TN;
-          acc[i][j] = Mma<bf16>::run(fa[fc][i], fb[fc][j], acc[i][j]);
-          if constexpr (REFILL) {
-            if constexpr (m < A_IPW) load_a(m, kt + STAGES, cur);
-            else if constexpr (m < LPT) load_b(m - A_IPW, kt + STAGES, cur);
-          }
-          __builtin_amdgcn_sched_barrier(0);
+      }
+      const uint32_t ra = LAST ? nst : as;
+      static_for<NM>([&](auto mc) {
+        constexpr int m = decltype(mc)::value, i = m / TN, j = m % TN;
+        acc[i][j] = Mma<bf16>::run(fa[fc][i], fb[fc][j], acc[i][j]);
+        static_for<RPM>([&](auto rc) {
+          constexpr int r = m * RPM + decltype(rc)::value;
+          if constexpr (r < TM) gl::read_frag<BM, A_KC, BK, TM, KS, NK, r>(fa[fc ^ 1], fra, ra);
+          else if constexpr (r < NFR) gl::read_frag<BN, B_KC, BK, TN, KS, NK, r - TM>(fb[fc ^ 1], frb, ra + A_BYTES);
         });
-        if constexpr (REFILL) {
-          static_for<(LPT > TM * TN ? LPT - TM * TN : 0)>([&](auto lc) {
-            constexpr int m = TM * TN + decltype(lc)::value;
-            if constexpr (m < A_IPW) load_a(m, kt + STAGES, cur);
-            else load_b(m - A_IPW, kt + STAGES, cur);
-          });
+        if constexpr (LAST && REFILL) {
+          if constexpr (m < A_IPW) load_a(m, kt + STAGES, cur);
+          else if constexpr (m < LPT) load_b(m - A_IPW, kt + STAGES, cur);
         }
         __builtin_amdgcn_sched_barrier(0);
+      });
+      if constexpr (LAST && REFILL) {
+        static_for<(LPT > NM ? LPT - NM : 0)>([&](auto lc) {
+          constexpr int m = NM + decltype(lc)::value;
+          if constexpr (m < A_IPW) load_a(m, kt + STAGES, cur);
+          else load_b(m - A_IPW, kt + STAGES, cur);
+        });
       }
+      __builtin_amdgcn_sched_barrier(0);
     });
-    // with an odd number of k-steps the fragment buffers would swap roles
-    static_assert(KS % 2 == 0, "k-steps per tile must be even");
   };
   int kt = 0;
   for (; kt < nk - STAGES; ++kt) k_tile(kt, std::true_type{});
