@@ -98,6 +98,31 @@ def test_replay_programs_and_recompute_flops():
     assert p["recompute_flops"] == pytest.approx((full + full - 2 * Tk * f * h) * cfg.n_micro)
 
 
+def test_backward_work_buffers():
+    # resident weights with a segment replay (or none): the parameter-gradient
+    # kernels lag, so the running input gradient rotates over three buffers and
+    # the intermediate gradients (dX1, dU, dQKV) have a set per layer parity;
+    # otherwise two gradient buffers and one set.  Plus t1 and the attention
+    # backward's row dot products.
+    def expect(cfg, lag):
+        es = 2 if cfg.dtype == "bf16" else 4
+        Tk, h, f = cfg.tokens, cfg.hidden, cfg.mlp
+        hb, fb, qb = _align(Tk * h * es), _align(Tk * f * es), _align(Tk * 3 * h * es)
+        dvec = _align(cfg.micro_batch * cfg.n_heads * cfg.seq * 4)
+        return (3 if lag else 2) * hb + (2 if lag else 1) * (hb + fb + qb) + hb + dvec
+
+    for name, lag in [("stage4_h2048", True), ("stage5_h5120_offload", True),
+                      ("stage4_seq8192_recompute", True), ("stage12_h8192_stream", False)]:
+        cfg = W.WORKLOADS[name]()
+        assert T.plan(cfg)["work_bytes"] == expect(cfg, lag), name
+    cfg = W.tiny("recompute")
+    cfg.granularity = T.GRAN_LAYER   # replays between layer backwards: no lag
+    cfg.policy = W.policy_layer_inputs(cfg.n_layers)
+    assert T.plan(cfg)["work_bytes"] == expect(cfg, False)
+    cfg.granularity = T.GRAN_SEGMENT
+    assert T.plan(cfg)["work_bytes"] == expect(cfg, True)
+
+
 def test_slots_follow_the_order():
     cfg = W.tiny("keep")
     cfg.inflight = 2
