@@ -99,6 +99,13 @@ struct tps_stage {
   bool gs_pending[2] = {false, false};
   int gs_layer[2] = {-1, -1};
   int bstep = 0;
+  // rs: replays of all but the first replayed layer of a segment run here,
+  // beside the backward chain on cs (lagging configuration with light,
+  // independent layer replays only); ev_replay[l] marks layer l's replay done
+  hipStream_t rs = nullptr;
+  hipEvent_t ev_rfork = nullptr;
+  std::vector<hipEvent_t> ev_replay;
+  std::vector<char> replay_on_rs;
   int device = 0;
 
   std::vector<SlotEvent> oslot_ev;               // last release of each offload slot
@@ -196,6 +203,13 @@ struct tps_stage {
   }
   int fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots);
   int bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp, bool defer);
+  // stream `on` waits for the lagging parameter-gradient kernels of layer l
+  // (and all gs work before them), if any are pending
+  int wait_gs_layer_on(int l, hipStream_t on) {
+    for (int k = 0; k < 2; ++k)
+      if (gs_pending[k] && gs_layer[k] == l) TPS_HIP(hipStreamWaitEvent(on, ev_gs[k], 0));
+    return TPS_OK;
+  }
   // cs waits for the lagging parameter-gradient kernels of layer l (and all
   // gs work before them), if any are pending
   int wait_gs_layer(int l) {
@@ -423,7 +437,7 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
     ++stats.kernels;
     const int k = kbegin(ln_name, 0.0, 2.0 * T * h * es);
     TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, x, par(TPS_P_G1), par(TPS_P_BE1), p.eps, a,
-                                 opt(TPS_T_LN1) ? ln1 : nullptr, opt(TPS_T_LN1) ? ln1 + T : nullptr, cs));
+                                 opt(TPS_T_LN1) ? ln1 : nullptr, opt(TPS_T_LN1) ? ln1 + T : nullptr, ks));
     TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_QKV))
@@ -433,7 +447,7 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
     const int k = kbegin(p.dtype == TPS_BF16 ? (p.d == 128 ? attention_fwd_v3_name(p.b, p.s, p.nh) : "tps::attn_fwd_v2_kernel<64>")
                                              : "tps::attn_fwd_kernel<float>",
                          2.0 * p.b * h * (double)p.s * (p.s + 1), 4.0 * T * h * es);
-    TPS_HIP(attention_fwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, opt(TPS_T_LSE) ? lse : nullptr, cs));
+    TPS_HIP(attention_fwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, opt(TPS_T_LSE) ? lse : nullptr, ks));
     TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_OPROJ))
@@ -442,7 +456,7 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
     ++stats.kernels;
     const int k = kbegin(ln_name, 0.0, 2.0 * T * h * es);
     TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, x1, par(TPS_P_G2), par(TPS_P_BE2), p.eps, c,
-                                 opt(TPS_T_LN2) ? ln2 : nullptr, opt(TPS_T_LN2) ? ln2 + T : nullptr, cs));
+                                 opt(TPS_T_LN2) ? ln2 : nullptr, opt(TPS_T_LN2) ? ln2 + T : nullptr, ks));
     TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_FC1))
@@ -451,7 +465,7 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
   if (ops & (1u << OP_GELU)) {
     ++stats.kernels;
     const int k = kbegin(tname("tps::gelu_kernel<__bf16>", "tps::gelu_kernel<float>"), 0.0, 2.0 * T * f * es);
-    TPS_HIP(gelu_launch(p.dtype, (int64_t)T * f, u, g, cs));
+    TPS_HIP(gelu_launch(p.dtype, (int64_t)T * f, u, g, ks));
     TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_FC2))
@@ -676,23 +690,57 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
     for (int l = 0; l < p.L; ++l) TPS_HIP(hipStreamWaitEvent(cs, ready_ev[mb][l], 0));
   }
   const bool defer = p.defer_join;
+  bool rs_forked = false;
+  // Replay of layer l (segment granularity).  With deferred joins the
+  // previous micro-batch's last layer backwards may still read its replayed
+  // tensors: wait for their kernels first.  side: on rs, starting where cs is
+  // now (this micro-batch's inputs and prefetched tensors in place), waited
+  // for by cs before the layer's backward.
+  auto replay = [&](int l, bool side) -> int {
+    if (side) {
+      if (!rs_forked) {
+        TPS_HIP(hipEventRecord(ev_rfork, cs));
+        TPS_HIP(hipStreamWaitEvent(rs, ev_rfork, 0));
+        rs_forked = true;
+      }
+      TPS_TRY(wait_gs_layer_on(l, rs));
+      ks = rs;
+    } else if (defer) {
+      TPS_TRY(wait_gs_layer(l));
+    }
+    int e = -1;
+    TPS_TRY(ensure_layer(l, false, &e));
+    void* yl = (l == p.L - 1) ? nullptr : tensor(l + 1, TPS_T_X, mb, true);
+    TPS_TRY(fwd_layer(l, mb, params_of(l, &e), yl, p.replay_ops[l], true, true));
+    if (side) {
+      TPS_HIP(hipEventRecord(ev_replay[l], rs));
+      replay_on_rs[l] = 1;
+      ks = cs;
+    }
+    ++stats.replays;
+    if (e >= 0) {
+      TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
+      win[e].last_use.valid = true;
+    }
+    return TPS_OK;
+  };
   if (p.granularity == TPS_GRAN_SEGMENT) {
-    // with deferred joins the previous micro-batch's last layer backwards may
-    // still read their replayed tensors: replay top-down where the layers are
-    // independent, so those layers come last, and wait for their kernels
-    const bool down = defer && p.replay_independent;
-    for (int i = 0; i < p.L; ++i) {
-      const int l = down ? p.L - 1 - i : i;
-      if (!p.replay_ops[l]) continue;
-      if (defer) TPS_TRY(wait_gs_layer(l));
-      int e = -1;
-      TPS_TRY(ensure_layer(l, false, &e));
-      void* yl = (l == p.L - 1) ? nullptr : tensor(l + 1, TPS_T_X, mb, true);
-      TPS_TRY(fwd_layer(l, mb, params_of(l, &e), yl, p.replay_ops[l], true, true));
-      ++stats.replays;
-      if (e >= 0) {
-        TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
-        win[e].last_use.valid = true;
+    if (rs) {
+      // the top replayed layer on cs, the lower ones on rs beside the
+      // backward of the layers above them
+      bool top = true;
+      for (int l = p.L - 1; l >= 0; --l) {
+        if (!p.replay_ops[l]) continue;
+        TPS_TRY(replay(l, !top));
+        top = false;
+      }
+    } else {
+      // top-down where the layers are independent, so the layers whose
+      // lagging kernels were issued last are replayed last
+      const bool down = defer && p.replay_independent;
+      for (int i = 0; i < p.L; ++i) {
+        const int l = down ? p.L - 1 - i : i;
+        if (p.replay_ops[l]) TPS_TRY(replay(l, false));
       }
     }
   }
@@ -710,6 +758,10 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
     if (p.granularity == TPS_GRAN_LAYER && p.replay_ops[l]) {
       TPS_TRY(fwd_layer(l, mb, W, nullptr, p.replay_ops[l], true, true));
       ++stats.replays;
+    }
+    if (rs && replay_on_rs[l]) {
+      TPS_HIP(hipStreamWaitEvent(cs, ev_replay[l], 0));
+      replay_on_rs[l] = 0;
     }
     void* out = (l == 0) ? dx : defer ? gb[bstep % 3] : (cur == gb[0] ? gb[1] : gb[0]);
     TPS_TRY(bwd_layer(l, mb, W, wt_of(l, e), grads_of(l, e), cur, out, defer ? (bstep & 1) : 0, defer));
@@ -781,6 +833,20 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
   if (he == hipSuccess) he = mkev_dev(&st->ev_join);
   for (auto& e : st->ev_gs)
     if (he == hipSuccess) he = mkev_dev(&e);
+  // a replay stream when replays are light (no GEMM in any layer's replay
+  // program) and independent across layers: full-layer replays beside the
+  // backward slowed it down (they compete for the CUs with its critical path)
+  bool light = true;
+  for (int l = 0; l < p.L; ++l)
+    light = light && !(p.replay_ops[l] & ((1u << OP_QKV) | (1u << OP_OPROJ) | (1u << OP_FC1) | (1u << OP_FC2)));
+  if (p.defer_join && p.granularity == TPS_GRAN_SEGMENT && p.replay_independent && p.n_replay_layers > 1 && light) {
+    if (he == hipSuccess) he = queue_stream(st->device, &st->rs);
+    if (he == hipSuccess) he = mkev_dev(&st->ev_rfork);
+    st->ev_replay.assign(p.L, nullptr);
+    st->replay_on_rs.assign(p.L, 0);
+    for (auto& e : st->ev_replay)
+      if (he == hipSuccess) he = mkev_dev(&e);
+  }
   if (he == hipSuccess) he = queue_stream(st->device, &st->gs);
   if (link) {
     st->xs = static_cast<hipStream_t>(mem->copy_stream);
@@ -1026,6 +1092,7 @@ extern "C" int tps_stage_sync(tps_stage* st) {
   if (st->xs) TPS_HIP(hipStreamSynchronize(st->xs));
   if (st->ps && st->ps != st->xs) TPS_HIP(hipStreamSynchronize(st->ps));
   if (st->gs) TPS_HIP(hipStreamSynchronize(st->gs));
+  if (st->rs) TPS_HIP(hipStreamSynchronize(st->rs));
   return TPS_OK;
 }
 
@@ -1076,6 +1143,13 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
   if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
   if (st->ev_join) (void)hipEventDestroy(st->ev_join);
   for (auto e : st->ev_gs)
+    if (e) (void)hipEventDestroy(e);
+  if (st->rs) {
+    (void)hipStreamSynchronize(st->rs);
+    (void)hipStreamDestroy(st->rs);
+  }
+  if (st->ev_rfork) (void)hipEventDestroy(st->ev_rfork);
+  for (auto e : st->ev_replay)
     if (e) (void)hipEventDestroy(e);
   if (st->ev_tmp) (void)hipEventDestroy(st->ev_tmp);
   for (auto* v : {&st->oslot_ev, &st->offloaded_ev, &st->hslot_read_ev, &st->lgrads_out_ev})
