@@ -245,28 +245,43 @@ void attn_fwd_kernel(const T* __restrict__ qkv, T* __restrict__ o, float* __rest
 
 // ---------------------------------------------------------------------------
 // Backward preprocessing: Dv[b, n, q] = sum_d do[q, n*D + d] * o[q, n*D + d].
+// LPR lanes per (row, head) read 16 contiguous bytes of each operand (a wave
+// covers 64 / LPR whole head rows: fully coalesced), multiply-add them in
+// element order and sum across the LPR lanes with a fixed xor butterfly (every
+// lane of the group ends with the same value).
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ void attn_bwd_dot_kernel(const T* __restrict__ o, const T* __restrict__ dout,
                                     float* __restrict__ dvec, int b, int s, int nh) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // over rows * heads
-  const int64_t total = (int64_t)b * s * nh;
-  if (i >= total) return;
-  const int n = (int)(i % nh);
-  const int64_t row = i / nh;
-  const int H = nh * D;
   constexpr int VEC = 16 / sizeof(T);
-  const T* po = o + row * H + n * D;
-  const T* pd = dout + row * H + n * D;
+  constexpr int LPR = D / VEC;
+  static_assert(LPR <= kWave && kWave % LPR == 0 && (LPR & (LPR - 1)) == 0, "lanes per head row");
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t i = t / LPR;                              // (row, head) index
+  const int c = (int)(t % LPR) * VEC;
+  const int64_t total = (int64_t)b * s * nh;
+  const bool ok = i < total;                              // uniform over the lane group
+  const int n = ok ? (int)(i % nh) : 0;
+  const int64_t row = ok ? i / nh : 0;
+  const int64_t off = row * (int64_t)nh * D + (int64_t)n * D + c;
   float acc = 0.f;
-#pragma unroll 4
-  for (int c = 0; c < D; c += VEC) {
-    const Vec16<T> a = load16(po + c), g = load16(pd + c);
+  if (ok) {
+    const Vec16<T> a = load16(o + off), g = load16(dout + off);
 #pragma unroll
-    for (int t = 0; t < VEC; ++t) acc += to_f32(a.get(t)) * to_f32(g.get(t));
+    for (int e = 0; e < VEC; ++e) acc += to_f32(a.get(e)) * to_f32(g.get(e));
   }
-  const int ib = (int)(row / s), qpos = (int)(row % s);
-  dvec[((int64_t)ib * nh + n) * s + qpos] = acc;
+#pragma unroll
+  for (int m = 1; m < LPR; m <<= 1) acc += __shfl_xor(acc, m, kWave);
+  if (ok && c == 0) dvec[((row / s) * nh + n) * s + row % s] = acc;
+}
+
+template <typename T, int D>
+static hipError_t dot_launch(int b, int s, int nh, const void* o, const void* dout, float* dvec, hipStream_t st) {
+  constexpr int LPR = D * (int)sizeof(T) / 16;
+  const int64_t threads = (int64_t)b * s * nh * LPR;
+  hipLaunchKernelGGL((attn_bwd_dot_kernel<T, D>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+                     static_cast<const T*>(o), static_cast<const T*>(dout), dvec, b, s, nh);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -523,10 +538,7 @@ template <typename T, int D>
 static hipError_t bwd_launch(int b, int s, int nh, const void* qkv, const void* o, const float* lse,
                              const void* dout, void* dqkv, float* dvec, hipStream_t st) {
   const float scale = 1.0f / sqrtf((float)D);
-  const int64_t rows_heads = (int64_t)b * s * nh;
-  hipLaunchKernelGGL((attn_bwd_dot_kernel<T, D>), dim3((unsigned)((rows_heads + 255) / 256)), dim3(256), 0, st,
-                     static_cast<const T*>(o), static_cast<const T*>(dout), dvec, b, s, nh);
-  hipError_t e = hipGetLastError();
+  hipError_t e = dot_launch<T, D>(b, s, nh, o, dout, dvec, st);
   if (e != hipSuccess) return e;
   const int nkb = (s + 127) / 128;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, D>), dim3(nkb * nh * b), dim3(256), 0, st,
@@ -554,14 +566,8 @@ hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const vo
                                 const float* lse, const void* dout, void* dqkv, float* dvec,
                                 hipStream_t st) {
   if (dtype == TPS_BF16) {
-    const int64_t rows_heads = (int64_t)b * s * nh;
-    if (d == 128)
-      hipLaunchKernelGGL((attn_bwd_dot_kernel<bf16, 128>), dim3((unsigned)((rows_heads + 255) / 256)), dim3(256), 0, st,
-                         static_cast<const bf16*>(o), static_cast<const bf16*>(dout), dvec, b, s, nh);
-    else
-      hipLaunchKernelGGL((attn_bwd_dot_kernel<bf16, 64>), dim3((unsigned)((rows_heads + 255) / 256)), dim3(256), 0, st,
-                         static_cast<const bf16*>(o), static_cast<const bf16*>(dout), dvec, b, s, nh);
-    const hipError_t e = hipGetLastError();
+    const hipError_t e = d == 128 ? dot_launch<bf16, 128>(b, s, nh, o, dout, dvec, st)
+                                  : dot_launch<bf16, 64>(b, s, nh, o, dout, dvec, st);
     if (e != hipSuccess) return e;
     if (d == 128) return attention_bwd_v3_launch(b, s, nh, d, qkv, lse, dout, dqkv, dvec, st);
     return attention_bwd_v2_launch(b, s, nh, d, qkv, lse, dout, dqkv, dvec, st);
