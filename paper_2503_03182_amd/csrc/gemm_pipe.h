@@ -287,6 +287,7 @@ static hipError_t launch_pipe(GemmArgs g, hipStream_t stream) {
     }
   } else if constexpr (LAYOUT == TPS_GEMM_NN) {
     if (g.epi == TPS_EPI_GELU_GRAD) return launch_pipe_epi<LAYOUT, BM, BN, TPS_EPI_GELU_GRAD>(g, stream);
+    if (g.epi == TPS_EPI_BIAS_RESID) return launch_pipe_epi<LAYOUT, BM, BN, TPS_EPI_BIAS_RESID>(g, stream);
     return launch_pipe_epi<LAYOUT, BM, BN, TPS_EPI_STORE>(g, stream);
   } else {
     if (g.epi == TPS_EPI_ACC_F32) return launch_pipe_epi<LAYOUT, BM, BN, TPS_EPI_ACC_F32>(g, stream);

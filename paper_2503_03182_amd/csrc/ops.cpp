@@ -131,7 +131,7 @@ static bool v2_epilogue(int layout, int epi) {
   if (layout == TPS_GEMM_NT)
     return epi == TPS_EPI_STORE || epi == TPS_EPI_BIAS || epi == TPS_EPI_BIAS_RESID || epi == TPS_EPI_BIAS_GELU ||
            epi == TPS_EPI_GELU_GRAD;
-  if (layout == TPS_GEMM_NN) return epi == TPS_EPI_STORE || epi == TPS_EPI_GELU_GRAD;
+  if (layout == TPS_GEMM_NN) return epi == TPS_EPI_STORE || epi == TPS_EPI_GELU_GRAD || epi == TPS_EPI_BIAS_RESID;
   return epi == TPS_EPI_STORE || epi == TPS_EPI_ACC_F32;
 }
 

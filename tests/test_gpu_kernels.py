@@ -94,6 +94,11 @@ def test_gemm_epilogues(dtype, shape):
     torch.cuda.synchronize()
     ref = (A.astype(np.float64) @ B2.astype(np.float64)) * ora.gelu_grad(U.astype(np.float64))
     assert rel_l2(to_np(out), ref) < TOL[dtype]
+    # BIAS_RESID (NN): C = A B + bias + R
+    T.op_gemm(DT[dtype], T.GEMM_NN, T.EPI_BIAS_RESID, M, N, K, dA, K, to_dev(B2, dtype), N, out, N, bias=dbias,
+              resid=dR, ldr=N)
+    torch.cuda.synchronize()
+    assert rel_l2(to_np(out), A.astype(np.float64) @ B2.astype(np.float64) + bias + R) < TOL[dtype]
     # ACC_F32 (TN): C32 += A^T B over K rows
     A3 = _t(27, (K, M), dtype)
     B3 = _t(28, (K, N), dtype)
