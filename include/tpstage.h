@@ -178,9 +178,11 @@ typedef struct tps_memory {
   uint64_t host_bytes;
   void* compute_stream;         /* hipStream_t for kernels (NULL: the null
                                    stream); the stage forks the backward's
-                                   parameter-gradient kernels onto a stream of
-                                   its own and joins them back at the end of
-                                   each layer backward                         */
+                                   parameter-gradient kernels (and light
+                                   segment replays) onto streams of its own
+                                   and joins them back before anything on this
+                                   stream reads their results, and at the end
+                                   of each forward and of the iteration       */
   void* copy_stream;            /* hipStream_t for device -> host copies, or
                                    NULL: the stage creates its own             */
   void* prefetch_stream;        /* hipStream_t for host -> device copies, or

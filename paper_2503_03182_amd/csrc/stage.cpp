@@ -1,5 +1,6 @@
 // Stage executor: runs F(mb) and B(mb) in the planned order on the caller's
-// compute stream, with
+// compute stream (the backward's parameter-gradient kernels on a stream of
+// its own, light segment replays of lower layers on another), with
 //  - the recompute engine: the replay program of each layer re-runs the same
 //    forward kernels with the same launch shapes, so regenerated tensors are
 //    bit-identical to the ones the forward produced; SEGMENT granularity
@@ -275,7 +276,8 @@ int tps_stage::refresh_wt(int l, int e) {
 }
 
 // Adds the layer's bias / LayerNorm partial sums of one micro-batch to its
-// gradient block G (on the compute stream) and clears them.
+// gradient block G (on the current kernel stream, the parameter-gradient
+// stream in a layer backward) and clears them.
 int tps_stage::finalize_bias_grads(int l, float* G) {
   static const int which[Plan::BP_COUNT] = {TPS_P_B_QKV, TPS_P_B_O, TPS_P_B_1, TPS_P_B_2,
                                             TPS_P_BE1,   TPS_P_G1,  TPS_P_BE2, TPS_P_G2};
@@ -372,8 +374,8 @@ int tps_stage::ensure_layer(int l, bool for_backward, int* entry) {
 }
 
 // ---------------------------------------------------------------------------
-// Kernel timing: events recorded on the compute stream around selected
-// launches, resolved when the totals are read.
+// Kernel timing: events recorded on the stream each selected launch goes to
+// (the current kernel stream), resolved when the totals are read.
 // ---------------------------------------------------------------------------
 int tps_stage::kbegin(const char* name, double flops, double bytes) {
   if (!timing || strncmp(name, tprefix.c_str(), tprefix.size()) != 0) return -1;
