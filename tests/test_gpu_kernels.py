@@ -179,7 +179,8 @@ ATTN_CASES = [  # (dtype, b, s, heads, d)
 # backward fuses dK/dV and dQ below 257 and above 1023 blocks; ragged lengths
 # throughout
 ATTN_BIG_CASES = [("bf16", 2, 130, 128, 128), ("bf16", 2, 520, 52, 128), ("bf16", 1, 1000, 40, 128),
-                  ("bf16", 1, 1500, 4, 128), ("bf16", 1, 2048, 4, 128), ("bf16", 3, 700, 2, 128)]
+                  ("bf16", 1, 1500, 4, 128), ("bf16", 1, 2048, 4, 128), ("bf16", 3, 700, 2, 128),
+                  ("bf16", 1, 2048, 16, 128), ("bf16", 1, 1100, 30, 128)]
 
 
 @pytest.mark.parametrize("dtype,b,s,nh,d", ATTN_CASES + ATTN_BIG_CASES)
