@@ -241,8 +241,11 @@ int tps_plan(const tps_config* cfg, tps_plan_info* out);
 int tps_stage_init(const tps_config* cfg, const tps_params* params,
                    const tps_memory* mem, tps_stage** out);
 
-/* Start an iteration: resets the order cursor; zero_grads != 0 enqueues a
- * zero fill of every gradient block on the compute stream. */
+/* Start an iteration: resets the order cursor; zero_grads != 0 restarts the
+ * gradients from zero: with resident weights the iteration's first backward
+ * contribution to each gradient tensor writes it instead of adding to it (the
+ * bytes between tensors in a block are left as they are), with streamed
+ * weights the host blocks are cleared as each layer is first used. */
 int tps_stage_begin_iteration(tps_stage* st, int zero_grads);
 
 /* F(mb): x, y are [b, s, h] device buffers in storage dtype. */

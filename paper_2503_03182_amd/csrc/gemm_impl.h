@@ -212,7 +212,7 @@ void gemm_kernel(GemmArgs g) {
         const float v = acc[i][j][r];
         if (epi == TPS_EPI_ACC_F32) {
           float* c = static_cast<float*>(g.C) + (int64_t)row * g.ldc + col;
-          *c = *c + v;
+          *c = (g.overwrite ? 0.f : *c) + v;
         } else {
           T* c = static_cast<T*>(g.C) + (int64_t)row * g.ldc + col;
           float out;

@@ -240,9 +240,14 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[T
     for (int q = 0; q < P; ++q) {
       const int64_t row = row0 + i * 32 + q * RPP;
       if constexpr (EPI == TPS_EPI_ACC_F32) {
-        const f32x4* c = reinterpret_cast<const f32x4*>(static_cast<const float*>(g.C) + row * g.ldc + col);
-        in.c0[q] = c[0];
-        in.c1[q] = c[1];
+        if (g.overwrite) {
+          in.c0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+          in.c1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        } else {
+          const f32x4* c = reinterpret_cast<const f32x4*>(static_cast<const float*>(g.C) + row * g.ldc + col);
+          in.c0[q] = c[0];
+          in.c1[q] = c[1];
+        }
       } else if constexpr (EPI == TPS_EPI_BIAS_RESID) {
         in.v[q] = load16(static_cast<const bf16*>(g.resid) + row * g.ldr + col);
       } else if constexpr (EPI == TPS_EPI_GELU_GRAD) {

@@ -17,6 +17,7 @@ struct GemmArgs {
   void* aux; int64_t ldaux;
   int epi;
   int tiles_m, tiles_n;
+  int overwrite;   // TPS_EPI_ACC_F32 only: C = A^T B instead of C += A^T B
 };
 
 // Tile shape of a GEMM launch.  Depends on the shape only (never on timing)
@@ -47,7 +48,7 @@ hipError_t gemm_launch_tn(int dtype, GemmArgs g, hipStream_t stream);
 hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, const void* A,
                        int64_t lda, const void* B, int64_t ldb, void* C, int64_t ldc,
                        const void* bias, const void* resid, int64_t ldr, void* aux, int64_t ldaux,
-                       hipStream_t stream);
+                       hipStream_t stream, int overwrite = 0);
 
 hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, void* o,
                                 float* lse, hipStream_t st);
@@ -102,8 +103,9 @@ hipError_t layernorm_bwd_acc_launch(int dtype, int rows, int cols, const void* d
                                     const float* mean, const float* rstd, const void* gamma, const void* resid,
                                     void* dx, float* part_dbeta, int64_t k_stride, int64_t seg_stride,
                                     hipStream_t st);
+// grads (+)= the sum of the segments' partials (overwrite: =), partials cleared
 hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_t seg_stride, float* grads,
-                                  hipStream_t st);
+                                  hipStream_t st, int overwrite = 0);
 hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st);
 hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st);
 // out[c][r] = in[r][c] for in [rows, cols]; rows and cols multiples of 8

@@ -358,7 +358,8 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restri
 // m.goff[r]) in ascending segment order, adds them to that vector and clears
 // the partials.
 __global__ __launch_bounds__(256) void colsum_finalize_kernel(ColMap m, float* __restrict__ part, int segs,
-                                                              int64_t seg_stride, float* __restrict__ grads) {
+                                                              int64_t seg_stride, float* __restrict__ grads,
+                                                              int overwrite) {
   const int c = blockIdx.x * 256 + threadIdx.x;
   if (c >= m.c0[m.n]) return;
   int r = 0;
@@ -372,7 +373,8 @@ __global__ __launch_bounds__(256) void colsum_finalize_kernel(ColMap m, float* _
     if (i < segs) acc += v[i];
   for (int i = 16; i < segs; ++i) acc += part[(int64_t)i * seg_stride + c];
   for (int i = 0; i < segs; ++i) part[(int64_t)i * seg_stride + c] = 0.f;
-  grads[m.goff[r] + (c - m.c0[r])] += acc;
+  float* gp = grads + m.goff[r] + (c - m.c0[r]);
+  *gp = (overwrite ? 0.f : *gp) + acc;
 }
 
 template <typename T>
@@ -489,11 +491,11 @@ hipError_t colsum_acc_launch(int dtype, int rows, int cols, const void* x, int64
 }
 
 hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_t seg_stride, float* grads,
-                                  hipStream_t st) {
+                                  hipStream_t st, int overwrite) {
   const int cols = m.c0[m.n];
   if (cols == 0) return hipSuccess;
   hipLaunchKernelGGL(colsum_finalize_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, m, part, segs, seg_stride,
-                     grads);
+                     grads, overwrite);
   return hipGetLastError();
 }
 

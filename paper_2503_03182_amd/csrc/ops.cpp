@@ -188,9 +188,9 @@ const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g) {
 
 hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, const void* A, int64_t lda,
                        const void* B, int64_t ldb, void* C, int64_t ldc, const void* bias, const void* resid,
-                       int64_t ldr, void* aux, int64_t ldaux, hipStream_t stream) {
+                       int64_t ldr, void* aux, int64_t ldaux, hipStream_t stream, int overwrite) {
   if (M == 0 || N == 0) return hipSuccess;
-  GemmArgs g{M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux, ldaux, epi, 0, 0};
+  GemmArgs g{M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux, ldaux, epi, 0, 0, overwrite};
   if (layout == TPS_GEMM_NT) return gemm_launch_nt(dtype, g, stream);
   if (layout == TPS_GEMM_NN) return gemm_launch_nn(dtype, g, stream);
   return gemm_launch_tn(dtype, g, stream);

@@ -107,6 +107,10 @@ struct tps_stage {
   bool gs_pending[2] = {false, false};
   int gs_layer[2] = {-1, -1};
   int bstep = 0;
+  // grads_fresh[l]: layer l's gradient block counts as zero (requested by
+  // begin_iteration and not yet written): its next layer backward writes the
+  // gradients instead of adding to them, so no zero fill is needed
+  std::vector<char> grads_fresh;
   // rs: replays of all but the first replayed layer of a segment run here,
   // beside the backward chain on cs (lagging configuration with light,
   // independent layer replays only); ev_replay[l] marks layer l's replay done
@@ -189,20 +193,20 @@ struct tps_stage {
   int prefetch_layer(int l);
   int flush_grads(int entry);
   int flush_all_grads();
-  int finalize_bias_grads(int l, float* G);
+  int finalize_bias_grads(int l, float* G, bool overwrite);
 
   // --- compute ----------------------------------------------------------------
   int gemm(int layout, int epi, int M, int N, int K, const void* A, int64_t lda, const void* B, int64_t ldb,
            void* C, int64_t ldc, const void* bias = nullptr, const void* resid = nullptr, int64_t ldr = 0,
-           void* aux = nullptr, int64_t ldaux = 0) {
+           void* aux = nullptr, int64_t ldaux = 0, bool overwrite = false) {
     ++stats.kernels;
     const double es = p.esize;
     const double bytes = ((double)M * K + (double)N * K) * es +
-                         (epi == TPS_EPI_ACC_F32 ? 8.0 * M * N : (double)M * N * es);
-    const GemmArgs ga{M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux, ldaux, epi, 0, 0};
+                         (epi == TPS_EPI_ACC_F32 ? (overwrite ? 4.0 : 8.0) * M * N : (double)M * N * es);
+    const GemmArgs ga{M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr, aux, ldaux, epi, 0, 0, overwrite};
     const int t = kbegin(gemm_kernel_name(p.dtype, layout, ga), 2.0 * M * N * K, bytes);
     const int rc = check_hip(gemm_launch(p.dtype, layout, epi, M, N, K, A, lda, B, ldb, C, ldc, bias, resid, ldr,
-                                         aux, ldaux, ks),
+                                         aux, ldaux, ks, overwrite),
                              "gemm");
     return rc ? rc : kend(t);
   }
@@ -275,10 +279,10 @@ int tps_stage::refresh_wt(int l, int e) {
   return TPS_OK;
 }
 
-// Adds the layer's bias / LayerNorm partial sums of one micro-batch to its
-// gradient block G (on the current kernel stream, the parameter-gradient
-// stream in a layer backward) and clears them.
-int tps_stage::finalize_bias_grads(int l, float* G) {
+// Adds (overwrite: writes) the layer's bias / LayerNorm partial sums of one
+// micro-batch to its gradient block G (on the current kernel stream, the
+// parameter-gradient stream in a layer backward) and clears them.
+int tps_stage::finalize_bias_grads(int l, float* G, bool overwrite) {
   static const int which[Plan::BP_COUNT] = {TPS_P_B_QKV, TPS_P_B_O, TPS_P_B_1, TPS_P_B_2,
                                             TPS_P_BE1,   TPS_P_G1,  TPS_P_BE2, TPS_P_G2};
   ColMap m{};
@@ -286,7 +290,7 @@ int tps_stage::finalize_bias_grads(int l, float* G) {
   for (int r = 0; r <= Plan::BP_COUNT; ++r) m.c0[r] = (int)p.bpc[r];
   for (int r = 0; r < Plan::BP_COUNT; ++r) m.goff[r] = (int64_t)(p.goff[which[r]] / 4);
   const int k = kbegin("bias gradient finalize", 0.0, (double)p.bpart_segs * p.bpc[Plan::BP_COUNT] * 8.0);
-  TPS_HIP(colsum_finalize_launch(m, bpart(l), p.bpart_segs, p.bpc[Plan::BP_COUNT], G, ks));
+  TPS_HIP(colsum_finalize_launch(m, bpart(l), p.bpart_segs, p.bpc[Plan::BP_COUNT], G, ks, overwrite ? 1 : 0));
   ++stats.kernels;
   return kend(k);
 }
@@ -499,6 +503,8 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
                          bool defer) {
   const int T = p.T, h = p.h, f = p.f;
   ks = cs;
+  const bool fresh = grads_fresh[l] != 0;
+  grads_fresh[l] = 0;
   if (defer && gs_pending[wp]) {
     TPS_HIP(hipStreamWaitEvent(cs, ev_gs[wp], 0));
     gs_pending[wp] = false;
@@ -567,19 +573,22 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   // read is rewritten only after a join); the bias partials of gs and of the
   // LayerNorm passes on cs are disjoint columns.
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f, nullptr, nullptr, 0, nullptr,
+               0, fresh));
   TPS_TRY(colsum(dy, h, Plan::BP_2));
   to_cs();
   TPS_TRY(ingrad(TPS_EPI_GELU_GRAD, f, h, dy, TPS_P_W_2, w2t, du, u));
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h, nullptr, nullptr, 0, nullptr,
+               0, fresh));
   TPS_TRY(colsum(du, f, Plan::BP_1));
   to_cs();
   TPS_TRY(ingrad(TPS_EPI_STORE, h, f, du, TPS_P_W_1, w1t, t1, nullptr));
   TPS_TRY(lnbwd(t1, x1, ln2, TPS_P_G2, Plan::BP_BE2, dy, dx1));
   // attention block: x1 = x + o Wo^T + bo
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h, nullptr, nullptr, 0, nullptr,
+               0, fresh));
   TPS_TRY(colsum(dx1, h, Plan::BP_O));
   to_cs();
   TPS_TRY(ingrad(TPS_EPI_STORE, h, h, dx1, TPS_P_W_O, wot, t1, nullptr));
@@ -590,7 +599,8 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
     TPS_TRY(kend(k));
   }
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h, nullptr, nullptr, 0,
+               nullptr, 0, fresh));
   TPS_TRY(colsum(dqkv, 3 * h, Plan::BP_QKV));
   to_cs();
   TPS_TRY(ingrad(TPS_EPI_STORE, h, 3 * h, dqkv, TPS_P_W_QKV, wqt, t1, nullptr));
@@ -598,7 +608,7 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   // finalize after both streams' column sums; cs continues at once (defer)
   // or once gs is done
   TPS_TRY(to_gs());
-  TPS_TRY(finalize_bias_grads(l, G));
+  TPS_TRY(finalize_bias_grads(l, G, fresh));
   to_cs();
   if (defer) {
     TPS_HIP(hipEventRecord(ev_gs[wp], gs));
@@ -906,6 +916,7 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
   st->b_done.assign(p.M, 0);
   st->prefetched.assign(p.M, 0);
   st->grads_touched.assign(p.L, 0);
+  st->grads_fresh.assign(p.L, 0);
   *out = st;
   return TPS_OK;
 }
@@ -937,13 +948,8 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
     if (rc) return rc;
     std::fill(st->grads_touched.begin(), st->grads_touched.end(), zero_grads ? 0 : 1);
   } else {
-    if (zero_grads) {
-      for (int l = 0; l < p.L; ++l) {
-        hipError_t e = fill_zero_launch(st->lg[l], p.gbytes, st->cs);
-        if (e != hipSuccess) return check_hip(e, "zero grads");
-        ++st->stats.kernels;
-      }
-    }
+    // the first layer backward of the iteration writes each gradient tensor
+    if (zero_grads) std::fill(st->grads_fresh.begin(), st->grads_fresh.end(), 1);
     // parameters may have changed since the last iteration
     for (int l = 0; l < p.L; ++l) {
       int rc = st->refresh_wt(l, -1);
