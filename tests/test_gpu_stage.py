@@ -99,6 +99,38 @@ def test_repeat_iterations_reproduce():
     assert bit_equal(one, run_gpu(cfg, iterations=3, one_copy_stream=True)) == []
 
 
+def test_gradient_accumulation_across_iterations():
+    """zero_grads=False adds the iteration's gradients to the blocks; a later
+    zero_grads=True restarts them (bit-identical to a fresh first iteration)."""
+    import torch
+    from stage_harness import make_params, read_grads, to_dev
+    for weights in (T.W_RESIDENT, T.W_STREAM):
+        cfg = _mid(weights=weights, window=2) if weights == T.W_STREAM else _mid()
+        xs, dys = inputs(cfg)
+        blocks, grads, _ = make_params(cfg)
+        st = T.Stage(cfg, blocks, grads)
+        X = [to_dev(x, cfg.dtype) for x in xs]
+        DY = [to_dev(d, cfg.dtype) for d in dys]
+        Y = [torch.empty_like(x) for x in X]
+        DX = [torch.empty_like(x) for x in X]
+        snaps = []
+        for zero in (True, False, True):
+            st.begin_iteration(zero_grads=zero)
+            for k, mb in cfg.order():
+                if k == "F":
+                    st.forward(mb, X[mb], Y[mb])
+                else:
+                    st.backward(mb, DY[mb], DX[mb])
+            st.sync()
+            snaps.append(read_grads(cfg, grads))
+        st.close()
+        for l in range(cfg.n_layers):
+            for name, g1 in snaps[0][l].items():
+                g2 = snaps[1][l][name]
+                assert np.linalg.norm(g2 - 2 * g1) <= 1e-5 * np.linalg.norm(g1), (weights, l, name)
+                assert np.array_equal(snaps[2][l][name], g1), (weights, l, name)
+
+
 def test_linearity_in_dy_bitwise():
     cfg = _mid(policy=W.policy_selective(3))
     xs, dys = inputs(cfg)
