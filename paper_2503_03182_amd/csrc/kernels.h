@@ -35,7 +35,7 @@ GemmTile gemm_select_tile(int dtype, int layout, const GemmArgs& g);
 struct V3Config {
   int wgm, wgn, bk, stages;
 };
-constexpr V3Config v3_config(bool big) { return big ? V3Config{2, 4, 64, 2} : V3Config{2, 2, 64, 3}; }
+constexpr V3Config v3_config(bool big) { return big ? V3Config{2, 4, 64, 2} : V3Config{2, 2, 64, 4}; }
 // Demangled name of the kernel instantiation a launch uses (as profilers
 // print it), e.g. "tps::gemm_bf16_kernel<0, 256, 256, 2, 4, 64, 2, 1>".
 const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g);
