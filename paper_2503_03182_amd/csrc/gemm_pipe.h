@@ -107,6 +107,7 @@ void gemm_bf16_kernel(GemmArgs g) {
   constexpr int NW = WGM * WGN, NT = 64 * NW;
   constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 32, TN = WN / 32;
   constexpr int KS = BK / 16;
+  constexpr bool TWO_AHEAD = NW == 4 && KS == 4;
   constexpr bool A_KC = (LAYOUT != TPS_GEMM_TN);
   constexpr bool B_KC = (LAYOUT == TPS_GEMM_NT);
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2, STAGE = A_BYTES + B_BYTES;
@@ -197,6 +198,73 @@ void gemm_bf16_kernel(GemmArgs g) {
   wait_tiles<STAGES - 1, LPT>(min(STAGES, nk) - 1);
   lds_barrier();
 
+  constexpr int NFR = TM + TN, NM = TM * TN;
+  constexpr int RPM = (NFR + NM / 2 - 1) / (NM / 2);   // fragment reads per MFMA
+  int kt = 0;
+  if constexpr (TWO_AHEAD) {
+    // One wave per SIMD: the fragments of k-step kk + 2 are read during k-step
+    // kk (one buffer per k-step of the tile), so a read has two k-steps of
+    // MFMAs to land.  The tile barrier moves to k-step KS - 2, whose reads are
+    // the first of tile kt + 1: there the wave waits until every fragment of
+    // tile kt is in registers, so after the barrier the stage of tile kt is
+    // refilled while the last two k-steps run from registers.
+    constexpr int R = gl::frag_reads<A_KC, TM>() + gl::frag_reads<B_KC, TN>();   // LDS reads per k-step
+    static_assert(R <= 15, "lgkmcnt range");
+    bf16x8 fa[KS][TM], fb[KS][TN];
+    read_frags<BM, A_KC, BK, TM, KS, 0>(fa[0], fra, lds0);
+    read_frags<BN, B_KC, BK, TN, KS, 0>(fb[0], frb, lds0 + A_BYTES);
+    read_frags<BM, A_KC, BK, TM, KS, 1>(fa[1], fra, lds0);
+    read_frags<BN, B_KC, BK, TN, KS, 1>(fb[1], frb, lds0 + A_BYTES);
+    auto k_tile2 = [&](int kt, auto refill_c) {
+      constexpr bool REFILL = decltype(refill_c)::value;
+      const int cur = kt % STAGES;
+      const uint32_t as = lds0 + cur * STAGE;
+      const uint32_t nst = lds0 + ((kt + 1) % STAGES) * STAGE;
+      static_for<KS>([&](auto kc) {
+        constexpr int kk = decltype(kc)::value;
+        constexpr int NK = (kk + 2) % KS;     // k-step the reads are for
+        constexpr bool NEXT = kk + 2 >= KS;   // ... of tile kt + 1
+        constexpr bool BAR = kk + 2 == KS;
+        if constexpr (BAR) {
+          wait_lgkm<0>();
+          if constexpr (REFILL) wait_vm<(STAGES - 2) * LPT>();
+          else wait_tiles<STAGES - 2, LPT>(max(0, min(STAGES - 2, nk - 2 - kt)));
+          lds_barrier();
+        } else {
+          wait_lgkm<R>();   // the reads of k-step kk + 1 may still be in flight
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i) pin(fa[kk][i]);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) pin(fb[kk][j]);
+        const uint32_t ra = NEXT ? nst : as;
+        static_for<NM>([&](auto mc) {
+          constexpr int m = decltype(mc)::value, i = m / TN, j = m % TN;
+          acc[i][j] = Mma<bf16>::run(fa[kk][i], fb[kk][j], acc[i][j]);
+          static_for<RPM>([&](auto rc) {
+            constexpr int r = m * RPM + decltype(rc)::value;
+            if constexpr (r < TM) gl::read_frag<BM, A_KC, BK, TM, KS, NK, r>(fa[NK], fra, ra);
+            else if constexpr (r < NFR) gl::read_frag<BN, B_KC, BK, TN, KS, NK, r - TM>(fb[NK], frb, ra + A_BYTES);
+          });
+          if constexpr (BAR && REFILL) {
+            if constexpr (m < A_IPW) load_a(m, kt + STAGES, cur);
+            else if constexpr (m < LPT) load_b(m - A_IPW, kt + STAGES, cur);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        });
+        if constexpr (BAR && REFILL) {
+          static_for<(LPT > NM ? LPT - NM : 0)>([&](auto lc) {
+            constexpr int m = NM + decltype(lc)::value;
+            if constexpr (m < A_IPW) load_a(m, kt + STAGES, cur);
+            else load_b(m - A_IPW, kt + STAGES, cur);
+          });
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
+    for (; kt < nk - STAGES; ++kt) k_tile2(kt, std::true_type{});
+    for (; kt < nk; ++kt) k_tile2(kt, std::false_type{});
+  } else {
   bf16x8 fa[2][TM], fb[2][TN];
   read_frags<BM, A_KC, BK, TM, KS, 0>(fa[0], fra, lds0);
   read_frags<BN, B_KC, BK, TN, KS, 0>(fb[0], frb, lds0 + A_BYTES);
@@ -206,8 +274,6 @@ void gemm_bf16_kernel(GemmArgs g) {
   // The fragments of k-step kk+1 (of the next tile's first k-step in the
   // last one) are read between the MFMAs of k-step kk, all within its first
   // half, so LDS traffic spreads over the MFMA stream.
-  constexpr int NFR = TM + TN, NM = TM * TN;
-  constexpr int RPM = (NFR + NM / 2 - 1) / (NM / 2);   // fragment reads per MFMA
   auto k_tile = [&](int kt, auto refill_c) {
     constexpr bool REFILL = decltype(refill_c)::value;
     const int cur = kt % STAGES;
@@ -254,9 +320,9 @@ void gemm_bf16_kernel(GemmArgs g) {
       __builtin_amdgcn_sched_barrier(0);
     });
   };
-  int kt = 0;
   for (; kt < nk - STAGES; ++kt) k_tile(kt, std::true_type{});
   for (; kt < nk; ++kt) k_tile(kt, std::false_type{});
+  }
   wait_vm<0>();
   wait_lgkm<0>();
   __syncthreads();   // LDS is reused below
