@@ -27,10 +27,13 @@ def _round(a, dtype):
 
 
 # ragged shapes take the generic path; tile-aligned ones (M, N multiples of
-# 128 or 256, K of 64) take the direct-to-LDS path at both tile sizes, the
-# 128-row tiles in two K groups when the K tile count is even (384 x 256 x 512)
+# 128 or 256, K of 64) take the direct-to-LDS path at both tile sizes: 256 x
+# 256 tiles (2-stage ring) at 1 and 2 K tiles, 128 x 128 tiles (4-stage ring,
+# fragments read two k-steps ahead) at 1, 2, 3, 4, 5 and 8 K tiles, so the
+# ring's fill, refill and drain each meet short and long loops
 GEMM_SHAPES = [(200, 264, 136), (1000, 520, 72), (64, 64, 8), (2072, 4104, 264),
-               (256, 384, 192), (4096, 2560, 128), (384, 256, 512)]
+               (256, 384, 192), (4096, 2560, 128), (384, 256, 512), (128, 128, 64), (256, 128, 128),
+               (128, 256, 256), (384, 128, 320), (4096, 2560, 64)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
