@@ -162,7 +162,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU's share of the stage; --gpus {args.gpus} is not supported "
-              f"(multi-GPU runs are outside this build)", file=sys.stderr)
+              f"(the library runs one GPU per process and has no multi-GPU path)", file=sys.stderr)
         sys.exit(2)
 
     import torch
