@@ -106,44 +106,73 @@ def build_stage(cfg):
     return blocks, grads, xs, dys, ys, dxs
 
 
-def cpu_baseline(cfg, unit_flops, budget_s):
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, budget_s):
     """The oracle as it stands, on one (layer, micro-batch) unit of the
-    workload (forward, the policy's recompute, backward), repeated while the
-    budget lasts."""
+    workload (forward, the policy's recompute, backward) at the workload's
+    widths, repeated while the budget lasts.  Where one unit at the full
+    sequence length would take far longer than the budget, the sample keeps
+    the widths and shortens the sequence by powers of two; TFLOP/s is taken
+    over the sample's own algorithmic flops (same formulas as the GPU
+    number)."""
+    import dataclasses
+
     import numpy as np
     from oracle import decoder_stage as ora
     from paper_2503_03182_amd import synth
+    from paper_2503_03182_amd import tpstage as T
     try:
         from threadpoolctl import threadpool_info
         threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
+    pol1 = None if cfg.policy is None else [cfg.policy[0]]
+    unit_cfg = dataclasses.replace(cfg, n_layers=1, n_micro=1, policy=pol1, weights=T.W_RESIDENT,
+                                   offload_auto=False, offload_mb_mask=0, ops=None, inflight=0)
+    # a sample of at most ~4 TFLOP (~15 s at the 0.28 TFLOP/s measured on the box's host)
+    while unit_cfg.seq > 128:
+        info = T.plan(unit_cfg)
+        if info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"] <= 4e12:
+            break
+        unit_cfg = dataclasses.replace(unit_cfg, seq=unit_cfg.seq // 2)
+    info = T.plan(unit_cfg)
+    unit_flops = info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]
     params = [{k: v.astype(np.float64) for k, v in synth.layer_params(0, cfg.hidden, cfg.mlp, cfg.dtype).items()}]
-    x = [synth.stage_input(0, cfg.tokens, cfg.hidden, cfg.dtype).astype(np.float64)]
-    dy = [synth.output_grad(0, cfg.tokens, cfg.hidden, cfg.dtype).astype(np.float64)]
-    policy = None if cfg.policy is None else [cfg.policy[0]]
-    if policy is not None:
-        policy = [{k: (v if v != 2 else 0) for k, v in policy[0].items()}]   # offload is a copy on the CPU
+    x = [synth.stage_input(0, unit_cfg.tokens, cfg.hidden, cfg.dtype).astype(np.float64)]
+    dy = [synth.output_grad(0, unit_cfg.tokens, cfg.hidden, cfg.dtype).astype(np.float64)]
+    policy = None if pol1 is None else [{k: (v if v != T.OFFLOAD else T.KEEP) for k, v in pol1[0].items()}]
     times = []
     t_end = time.perf_counter() + budget_s
     while len(times) < 3 and (not times or time.perf_counter() < t_end):
         t0 = time.perf_counter()
-        ora.run_stage(params, x, dy, cfg.n_heads, cfg.micro_batch, cfg.seq, cfg.ln_eps, policy=policy)
+        ora.run_stage(params, x, dy, cfg.n_heads, unit_cfg.micro_batch, unit_cfg.seq, cfg.ln_eps, policy=policy)
         times.append(time.perf_counter() - t0)
     med = statistics.median(times)
+    ncpu = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
     return {"value": round(unit_flops / med / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"one layer x one micro-batch unit of the workload (forward, the policy's recompute, "
-                      f"backward) in float64 numpy, median of {len(times)} run(s), {med:.2f} s each; "
-                      f"TFLOP/s over the same algorithmic flop count as the GPU number"}
+            "kind": "oracle", "nproc": ncpu, "cpu_model": cpu_model(),
+            "sample": f"one layer x one micro-batch at the workload's widths and policy, seq "
+                      f"{unit_cfg.seq} (workload {cfg.seq}), {unit_flops / 1e12:.3f} TFLOP of forward, "
+                      f"recompute and backward, in float64 numpy on {int(threads)} BLAS threads; median of "
+                      f"{len(times)} run(s), {med:.2f} s each; TFLOP/s over the sample's own algorithmic flops"}
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="stage4_h2048")
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: 5 for the hidden-8192 "
+                    "streamed workload, 20 otherwise)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default: 2, resp. 3)")
+    ap.add_argument("--workload", default="stage12_h8192_stream")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -170,12 +199,23 @@ def main():
     from paper_2503_03182_amd import tpstage as T
 
     cfg = configs.WORKLOADS[args.workload]()
+    long_step = cfg.hidden >= 8192
+    if args.steps is None:
+        args.steps = 5 if long_step else 20
+    if args.warmup is None:
+        args.warmup = 2 if long_step else 3
     info = T.plan(cfg)
+    # the whole run on a stream of its own: the stage computes on it, and
+    # nothing synchronizes implicitly with the library's copy streams
+    run_stream = torch.cuda.Stream()
+    torch.cuda.set_stream(run_stream)
     free0, total = torch.cuda.mem_get_info()
     torch.cuda.reset_peak_memory_stats()
     log(f"[bench] workload {args.workload}: building parameters and inputs")
     blocks, grads, xs, dys, ys, dxs = build_stage(cfg)
+    torch.cuda.synchronize()
     stage = T.Stage(cfg, blocks, grads)
+    assert stage.cs.cuda_stream == run_stream.cuda_stream
     order = cfg.order()
     step_flops = info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]
 
@@ -220,6 +260,7 @@ def main():
     stage.sync()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    link = stage.stats()   # bytes the last timed iteration moved over the host link
     dom = [r for r in stage.kernel_times() if r["name"] == dominant][0]
     stage.time_kernels(None)
     free1, _ = torch.cuda.mem_get_info()
@@ -271,6 +312,12 @@ def main():
             "launches": dom["launches"],
             "avg_launch_us": round(dom["ms"] * 1e3 / max(dom["launches"], 1), 2),
         },
+        "host_link": {
+            "h2d_gb_per_step": round(link["h2d_bytes"] / 1e9, 3),
+            "d2h_gb_per_step": round(link["d2h_bytes"] / 1e9, 3),
+            "h2d_gbs_over_step": round(link["h2d_bytes"] / (ms_per_step * 1e-3) / 1e9, 2),
+            "d2h_gbs_over_step": round(link["d2h_bytes"] / (ms_per_step * 1e-3) / 1e9, 2),
+        },
         "kernels_per_step": [
             {"name": r["name"], "launches": r["launches"], "ms": round(r["ms"], 3),
              "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 1) if r["flops"] else None,
@@ -282,8 +329,7 @@ def main():
     stage.close()
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample")
-        unit = (info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]) / (cfg.n_layers * cfg.n_micro)
-        out["cpu_baseline"] = cpu_baseline(cfg, unit, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

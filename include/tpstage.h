@@ -119,7 +119,8 @@ typedef struct tps_config {
   int32_t offload_auto;         /* 1: ignore offload_mb_mask and pick victims
                                    by slack (see tps_plan)                     */
   int32_t weights;              /* TPS_W_RESIDENT or TPS_W_STREAM               */
-  int32_t window;               /* streamed layers resident at once (>= 2)      */
+  int32_t window;               /* streamed layers resident at once,
+                                   2..max(2, n_layers)                          */
   int32_t recompute_granularity;/* TPS_GRAN_LAYER or TPS_GRAN_SEGMENT           */
   int32_t n_ops;                /* 0: default order from `inflight`             */
   const int32_t* ops;           /* n_ops pairs (TPS_OP_F|TPS_OP_B, mb)          */
@@ -245,7 +246,13 @@ int tps_stage_init(const tps_config* cfg, const tps_params* params,
  * gradients from zero: with resident weights the iteration's first backward
  * contribution to each gradient tensor writes it instead of adding to it (the
  * bytes between tensors in a block are left as they are), with streamed
- * weights the host blocks are cleared as each layer is first used. */
+ * weights the host blocks are cleared as each layer is first used.
+ * Parameters may change between iterations (an optimizer step): resident
+ * weights get their transposed copies rebuilt here, and streamed weights are
+ * brought in again from the host blocks for every layer (no layer runs on a
+ * copy made in an earlier iteration).  With streamed weights the caller
+ * changes the pinned host blocks, or reads the host gradient blocks, only
+ * after tps_stage_sync() has followed the iteration's last op. */
 int tps_stage_begin_iteration(tps_stage* st, int zero_grads);
 
 /* F(mb): x, y are [b, s, h] device buffers in storage dtype. */
@@ -263,8 +270,17 @@ int tps_stage_forward_group(tps_stage* st, int mb0, int n, const void* const* x,
 int tps_stage_backward_group(tps_stage* st, int mb0, int n, const void* const* dy,
                              void* const* dx);
 
-/* Wait for both streams; reports asynchronous faults as TPS_EHIP. */
+/* Wait for every stream of the stage (compute, parameter-gradient, replay
+ * and copy streams); reports asynchronous faults as TPS_EHIP. */
 int tps_stage_sync(tps_stage* st);
+
+/* The same wait with a deadline: returns TPS_OK once every stream of the
+ * stage is idle, TPS_EHIP if a stream reports a fault, and TPS_ETIMEOUT
+ * (naming a busy stream) if work is still pending after timeout_ms
+ * milliseconds (0 = just test).  A timeout leaves the work running: the
+ * stage stays usable and a later sync completes it.  TPS_EINVAL for a
+ * negative timeout. */
+int tps_stage_sync_for(tps_stage* st, double timeout_ms);
 
 int tps_stage_stats(const tps_stage* st, tps_stats* out);
 

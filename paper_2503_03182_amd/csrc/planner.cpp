@@ -271,7 +271,9 @@ int make_plan(const tps_config* c, Plan* out) {
   p.weights = c->weights;
   if (p.weights != TPS_W_RESIDENT && p.weights != TPS_W_STREAM) return inval("weights");
   p.window = c->window;
-  if (p.weights == TPS_W_STREAM && (p.window < 2 || p.window > p.L)) return inval("window must be in 2..n_layers");
+  // a window of two serves a single layer too (one entry stays unused)
+  if (p.weights == TPS_W_STREAM && (p.window < 2 || p.window > (p.L < 2 ? 2 : p.L)))
+    return inval("window must be in 2..max(2, n_layers)");
   p.granularity = c->recompute_granularity;
   if (p.granularity != TPS_GRAN_LAYER && p.granularity != TPS_GRAN_SEGMENT) return inval("recompute_granularity");
   p.lookahead = c->lookahead;

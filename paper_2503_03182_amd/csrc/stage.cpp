@@ -17,9 +17,11 @@
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 
+#include <chrono>
 #include <cstring>
 #include <map>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "errors.h"
@@ -190,6 +192,8 @@ struct tps_stage {
   }
   int refresh_wt(int l, int entry);
   int ensure_layer(int l, bool for_backward, int* entry);
+  int touch(int entry);
+  int invalidate_window();
   int prefetch_layer(int l);
   int flush_grads(int entry);
   int flush_all_grads();
@@ -338,6 +342,32 @@ int tps_stage::prefetch_layer(int l) {
   TPS_HIP(hipEventRecord(w.param_ready.ev, ps));
   w.param_ready.valid = true;
   w.grads_live = false;
+  return TPS_OK;
+}
+
+// Marks the window entry's last compute use (cs): an eviction's H2D into
+// the entry waits for it.  Every kernel sequence that reads an entry's
+// parameters, transposes or gradients is followed by one.
+int tps_stage::touch(int e) {
+  if (e < 0) return TPS_OK;
+  TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
+  win[e].last_use.valid = true;
+  return TPS_OK;
+}
+
+// Drops every window entry at an iteration boundary: the caller may have
+// changed the host parameter blocks since the last iteration, so no layer
+// may run on parameters (or transposed copies) brought in before.  The
+// entries keep their last-use and grads-out events, which the next H2D and
+// the next gradient fill of the entry still wait for.
+int tps_stage::invalidate_window() {
+  for (auto& w : win) {
+    w.layer = -1;
+    w.wt_valid = false;
+    w.grads_live = false;
+    w.param_ready.valid = false;
+    w.tick = 0;
+  }
   return TPS_OK;
 }
 
@@ -706,10 +736,7 @@ int tps_stage::forward_one(int mb, const void* x, void* y) {
     TPS_TRY(prefetch_layer(l + 1));
     void* yl = (l == p.L - 1) ? y : tensor(l + 1, TPS_T_X, mb, false);
     TPS_TRY(fwd_layer(l, mb, params_of(l, &e), yl, 0xFFu & ~(1u << OP_GELU), false, false));
-    if (e >= 0) {
-      TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
-      win[e].last_use.valid = true;
-    }
+    TPS_TRY(touch(e));
     if (off) TPS_TRY(d2h_layer(l, mb));
   }
   if (off) TPS_TRY(release_oslot(p.oslot_f[mb], xs));
@@ -751,10 +778,7 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
       ks = cs;
     }
     ++stats.replays;
-    if (e >= 0) {
-      TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
-      win[e].last_use.valid = true;
-    }
+    TPS_TRY(touch(e));
     return TPS_OK;
   };
   if (p.granularity == TPS_GRAN_SEGMENT) {
@@ -799,10 +823,7 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
     void* out = (l == 0) ? dx : defer ? gb[bstep % 3] : (cur == gb[0] ? gb[1] : gb[0]);
     TPS_TRY(bwd_layer(l, mb, W, wt_of(l, e), grads_of(l, e), cur, out, defer ? (bstep & 1) : 0, defer));
     ++bstep;
-    if (e >= 0) {
-      TPS_HIP(hipEventRecord(win[e].last_use.ev, cs));
-      win[e].last_use.valid = true;
-    }
+    TPS_TRY(touch(e));
     cur = out;
   }
   // Pending now: the parameter-gradient kernels of the last two layer
@@ -946,6 +967,10 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
     // host gradients of the previous iteration must be complete before reuse
     int rc = st->flush_all_grads();
     if (rc) return rc;
+    // parameters may have changed since the last iteration: every layer is
+    // brought in again (and its transposed copies rebuilt)
+    rc = st->invalidate_window();
+    if (rc) return rc;
     std::fill(st->grads_touched.begin(), st->grads_touched.end(), zero_grads ? 0 : 1);
   } else {
     // the first layer backward of the iteration writes each gradient tensor
@@ -1007,6 +1032,9 @@ extern "C" int tps_stage_forward_group(tps_stage* st, int mb0, int n, const void
     if (!x[i] || !y[i]) return set_error(TPS_EINVAL, "forward group: null buffer");
   }
   TPS_TRY(st->check_op(TPS_OP_F, mb0));
+  // a preceding per-micro-batch backward may have left parameter-gradient
+  // kernels running that still read slots and buffers this group rewrites
+  TPS_TRY(st->join_if_pending());
   if (n > 1)
     for (int l = 1; l < p.L; ++l)
       if (p.pol(l, TPS_T_X) == TPS_RECOMPUTE)
@@ -1027,10 +1055,7 @@ extern "C" int tps_stage_forward_group(tps_stage* st, int mb0, int n, const void
       TPS_TRY(st->fwd_layer(l, mb, st->params_of(l, &e), yl, 0xFFu & ~(1u << OP_GELU), false, false));
       if (p.host_slot[mb] >= 0) TPS_TRY(st->d2h_layer(l, mb));
     }
-    if (e >= 0) {
-      TPS_HIP(hipEventRecord(st->win[e].last_use.ev, st->cs));
-      st->win[e].last_use.valid = true;
-    }
+    TPS_TRY(st->touch(e));
   }
   for (int i = 0; i < n; ++i) {
     const int mb = mb0 + i;
@@ -1055,6 +1080,15 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
     if (!dy[i] || !dx[i]) return set_error(TPS_EINVAL, "backward group: null buffer");
   }
   TPS_TRY(st->check_op(TPS_OP_B, mb0));
+  if (p.granularity == TPS_GRAN_SEGMENT && n > 1) {
+    bool any = false;
+    for (int l = 0; l < p.L; ++l) any |= p.replay_ops[l] != 0;
+    if (any) return set_error(TPS_EINVAL, "segment replay shares one replay buffer: backward groups of more than one micro-batch need layer granularity");
+  }
+  // the layer backwards below write work set 0 and the running-gradient
+  // buffer, which lagging parameter-gradient kernels of a preceding
+  // per-micro-batch backward may still read
+  TPS_TRY(st->join_if_pending());
   for (int i = 0; i < n; ++i) TPS_TRY(st->run_prefetches(st->cursor + i));
   // gradients flow per micro-batch through ping-pong buffers; keep one pair
   // per group member in the caller's dx buffers: dx[i] holds the running
@@ -1066,10 +1100,20 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
       for (int l = 0; l < p.L; ++l) TPS_HIP(hipStreamWaitEvent(st->cs, st->ready_ev[mb][l], 0));
     }
   }
-  if (p.granularity == TPS_GRAN_SEGMENT && n > 1) {
-    bool any = false;
-    for (int l = 0; l < p.L; ++l) any |= p.replay_ops[l] != 0;
-    if (any) return set_error(TPS_EINVAL, "segment replay shares one replay buffer: backward groups of more than one micro-batch need layer granularity");
+  // segment granularity (one micro-batch, checked above): the whole replay
+  // runs before the first layer backward, each layer on its own window entry
+  // (with streamed weights a replay may evict the entry of another layer, so
+  // no entry is bound across it)
+  if (p.granularity == TPS_GRAN_SEGMENT) {
+    for (int r = 0; r < p.L; ++r) {
+      if (!p.replay_ops[r]) continue;
+      int er = -1;
+      TPS_TRY(st->ensure_layer(r, false, &er));
+      void* yl = (r == p.L - 1) ? nullptr : st->tensor(r + 1, TPS_T_X, mb0, true);
+      TPS_TRY(st->fwd_layer(r, mb0, st->params_of(r, &er), yl, p.replay_ops[r], true, true));
+      TPS_TRY(st->touch(er));
+      ++st->stats.replays;
+    }
   }
   char* gA = st->work(p.work.g[0]);
   for (int l = p.L - 1; l >= 0; --l) {
@@ -1079,16 +1123,6 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
     const char* W = st->params_of(l, &e);
     for (int i = 0; i < n; ++i) {
       const int mb = mb0 + i;
-      if (p.granularity == TPS_GRAN_SEGMENT && l == p.L - 1) {
-        for (int r = 0; r < p.L; ++r) {
-          if (!p.replay_ops[r]) continue;
-          int er = -1;
-          TPS_TRY(st->ensure_layer(r, false, &er));
-          void* yl = (r == p.L - 1) ? nullptr : st->tensor(r + 1, TPS_T_X, mb, true);
-          TPS_TRY(st->fwd_layer(r, mb, st->params_of(r, &er), yl, p.replay_ops[r], true, true));
-          ++st->stats.replays;
-        }
-      }
       if (p.granularity == TPS_GRAN_LAYER && p.replay_ops[l]) {
         TPS_TRY(st->fwd_layer(l, mb, W, nullptr, p.replay_ops[l], true, true));
         ++st->stats.replays;
@@ -1098,10 +1132,7 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
       TPS_TRY(st->bwd_layer(l, mb, W, st->wt_of(l, e), st->grads_of(l, e), in, gA, 0, false));
       TPS_HIP(hipMemcpyAsync(dx[i], gA, p.tbytes[TPS_T_X], hipMemcpyDeviceToDevice, st->cs));
     }
-    if (e >= 0) {
-      TPS_HIP(hipEventRecord(st->win[e].last_use.ev, st->cs));
-      st->win[e].last_use.valid = true;
-    }
+    TPS_TRY(st->touch(e));
   }
   for (int i = 0; i < n; ++i) {
     const int mb = mb0 + i;
@@ -1123,6 +1154,41 @@ extern "C" int tps_stage_sync(tps_stage* st) {
   if (st->gs) TPS_HIP(hipStreamSynchronize(st->gs));
   if (st->rs) TPS_HIP(hipStreamSynchronize(st->rs));
   return TPS_OK;
+}
+
+// Bounded wait: polls every stream of the stage until all are idle, a
+// stream reports an error, or the deadline passes.
+extern "C" int tps_stage_sync_for(tps_stage* st, double timeout_ms) {
+  clear_error();
+  if (!st) return set_error(TPS_EINVAL, "null stage");
+  if (!(timeout_ms >= 0.0)) return set_error(TPS_EINVAL, "tps_stage_sync_for: negative or NaN timeout");
+  struct Named {
+    hipStream_t s;
+    const char* name;
+  };
+  std::vector<Named> streams = {{st->cs, "compute"}};
+  if (st->gs) streams.push_back({st->gs, "parameter-gradient"});
+  if (st->rs) streams.push_back({st->rs, "replay"});
+  if (st->xs) streams.push_back({st->xs, "device-to-host copy"});
+  if (st->ps && st->ps != st->xs) streams.push_back({st->ps, "host-to-device copy"});
+  const auto t0 = std::chrono::steady_clock::now();
+  for (;;) {
+    const char* busy = nullptr;
+    for (const Named& n : streams) {
+      const hipError_t e = hipStreamQuery(n.s);
+      if (e == hipErrorNotReady) {
+        if (!busy) busy = n.name;
+        continue;
+      }
+      if (e != hipSuccess) return check_hip(e, "tps_stage_sync_for");
+    }
+    if (!busy) return TPS_OK;
+    const double ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+    if (ms >= timeout_ms)
+      return set_error(TPS_ETIMEOUT, std::string("tps_stage_sync_for: the ") + busy + " stream still has work after " +
+                                         std::to_string(timeout_ms) + " ms");
+    std::this_thread::sleep_for(std::chrono::microseconds(50));
+  }
 }
 
 extern "C" int tps_stage_stats(const tps_stage* st, tps_stats* out) {

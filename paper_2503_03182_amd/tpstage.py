@@ -98,7 +98,7 @@ _lib = None
 EXPORTED = (
     "tps_param_layout", "tps_plan", "tps_stage_init", "tps_stage_begin_iteration",
     "tps_stage_forward", "tps_stage_backward", "tps_stage_forward_group",
-    "tps_stage_backward_group", "tps_stage_sync", "tps_stage_stats", "tps_stage_destroy",
+    "tps_stage_backward_group", "tps_stage_sync", "tps_stage_sync_for", "tps_stage_stats", "tps_stage_destroy",
     "tps_last_error", "tps_op_gemm", "tps_op_layernorm_fwd", "tps_op_layernorm_bwd",
     "tps_op_attention_fwd", "tps_op_attention_bwd", "tps_op_colsum", "tps_op_gelu",
     "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
@@ -129,6 +129,7 @@ def lib() -> C.CDLL:
         L.tps_stage_forward_group.argtypes = [vp, i32, i32, C.POINTER(vp), C.POINTER(vp)]
         L.tps_stage_backward_group.argtypes = [vp, i32, i32, C.POINTER(vp), C.POINTER(vp)]
         L.tps_stage_sync.argtypes = [vp]
+        L.tps_stage_sync_for.argtypes = [vp, C.c_double]
         L.tps_stage_stats.argtypes = [vp, C.POINTER(Stats)]
         L.tps_stage_destroy.argtypes = [vp]
         L.tps_stage_time_kernels.argtypes = [vp, C.c_char_p]
@@ -301,7 +302,19 @@ class Stage:
     """One pipeline stage on one GPU.  The device arena is a torch allocation
     and the pinned host arena a HostBuffer, both sized by the plan; parameter
     and f32 gradient blocks are byte buffers (torch tensors or HostBuffers)
-    laid out by param_layout()."""
+    laid out by param_layout().
+
+    Stream order: the stage's kernels run on its compute stream `cs`: the
+    given one, else the stream current at construction unless that is the
+    device's default (null) stream, else a private stream.  Every call that
+    enqueues work first makes `cs` wait for the caller's current stream (so
+    inputs and parameters written there are complete) and afterwards makes
+    the caller's current stream wait for `cs` (so outputs are complete, and
+    buffers freed there are not reused while the stage still reads them).
+    When the two are the same stream no event is needed.  Work on the
+    default stream synchronizes with the copy and side streams the library
+    creates, so callers that want calls to overlap the library's copies run
+    under a `torch.cuda.stream(...)` of their own."""
 
     def __init__(self, cfg: StageConfig, layer_params, layer_grads, device="cuda",
                  compute_stream=None, copy_stream=None, prefetch_stream=None):
@@ -313,7 +326,10 @@ class Stage:
         hb = self.info["host_arena_bytes"]
         self.host = HostBuffer(hb) if hb else None
         # compute on a torch stream; copy streams default to the stage's own
-        self.cs = compute_stream or torch.cuda.Stream(device=self.device)
+        if compute_stream is None:
+            cur = torch.cuda.current_stream(self.device)
+            compute_stream = cur if cur.cuda_stream != 0 else torch.cuda.Stream(device=self.device)
+        self.cs = compute_stream
         self.xs, self.ps = copy_stream, prefetch_stream
         self.layer_params, self.layer_grads = list(layer_params), list(layer_grads)
         L = cfg.n_layers
@@ -328,29 +344,52 @@ class Stage:
         check(lib().tps_stage_init(C.byref(self._c), C.byref(prm), C.byref(mem), C.byref(h)))
         self.handle = h
 
+    def _ordered(self, fn, *args) -> None:
+        """Runs one enqueuing call between the two stream waits described in
+        the class docstring."""
+        import torch
+        cur = torch.cuda.current_stream(self.device)
+        same = cur.cuda_stream == self.cs.cuda_stream
+        if not same:
+            self.cs.wait_stream(cur)
+        try:
+            check(fn(*args))
+        finally:
+            if not same:
+                cur.wait_stream(self.cs)
+
     def begin_iteration(self, zero_grads: bool = True) -> None:
-        check(lib().tps_stage_begin_iteration(self.handle, int(zero_grads)))
+        self._ordered(lib().tps_stage_begin_iteration, self.handle, int(zero_grads))
 
     def forward(self, mb: int, x, y) -> None:
-        check(lib().tps_stage_forward(self.handle, mb, x.data_ptr(), y.data_ptr()))
+        self._ordered(lib().tps_stage_forward, self.handle, mb, x.data_ptr(), y.data_ptr())
 
     def backward(self, mb: int, dy, dx) -> None:
-        check(lib().tps_stage_backward(self.handle, mb, dy.data_ptr(), dx.data_ptr()))
+        self._ordered(lib().tps_stage_backward, self.handle, mb, dy.data_ptr(), dx.data_ptr())
 
     def forward_group(self, mb0: int, xs, ys) -> None:
         n = len(xs)
         a = (C.c_void_p * n)(*[t.data_ptr() for t in xs])
         b = (C.c_void_p * n)(*[t.data_ptr() for t in ys])
-        check(lib().tps_stage_forward_group(self.handle, mb0, n, a, b))
+        self._ordered(lib().tps_stage_forward_group, self.handle, mb0, n, a, b)
 
     def backward_group(self, mb0: int, dys, dxs) -> None:
         n = len(dys)
         a = (C.c_void_p * n)(*[t.data_ptr() for t in dys])
         b = (C.c_void_p * n)(*[t.data_ptr() for t in dxs])
-        check(lib().tps_stage_backward_group(self.handle, mb0, n, a, b))
+        self._ordered(lib().tps_stage_backward_group, self.handle, mb0, n, a, b)
 
     def sync(self) -> None:
         check(lib().tps_stage_sync(self.handle))
+
+    def sync_for(self, timeout_ms: float) -> int:
+        """Bounded wait: TPS_OK when every stream of the stage is idle,
+        TPS_ETIMEOUT if work is still pending after timeout_ms (the work keeps
+        running); raises on other errors."""
+        rc = lib().tps_stage_sync_for(self.handle, float(timeout_ms))
+        if rc not in (TPS_OK, TPS_ETIMEOUT):
+            check(rc)
+        return rc
 
     def stats(self) -> dict:
         s = Stats()

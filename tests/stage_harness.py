@@ -79,7 +79,41 @@ def inputs(cfg):
     return xs, dys
 
 
-def run_gpu(cfg, xs=None, dys=None, iterations=1, group=False, params=None, one_copy_stream=False):
+def drive_iteration(st, cfg, X, DY, Y, DX, group=False, calls=None):
+    """One iteration of the planned order through the C ABI.  group: each run
+    of consecutive micro-batches with the same task kind is one group call.
+    calls: explicit [(kind, [mbs], as_group)] (kind "F" or "B"), for mixing
+    per-micro-batch and group calls."""
+    st.begin_iteration(zero_grads=True)
+    if calls is None:
+        calls = []
+        if group:
+            for k, mb0, n in cfg.groups():
+                calls.append((k, list(range(mb0, mb0 + n)), True))
+        else:
+            calls = [(k, [mb], False) for k, mb in cfg.order()]
+    for k, mbs, as_group in calls:
+        if as_group:
+            if k == "F":
+                st.forward_group(mbs[0], [X[m] for m in mbs], [Y[m] for m in mbs])
+            else:
+                st.backward_group(mbs[0], [DY[m] for m in mbs], [DX[m] for m in mbs])
+        else:
+            for mb in mbs:
+                if k == "F":
+                    st.forward(mb, X[mb], Y[mb])
+                else:
+                    st.backward(mb, DY[mb], DX[mb])
+
+
+def results(cfg, st, Y, DX, grads):
+    """numpy copies of the outputs and gradient blocks (waits for the stage)."""
+    st.sync()
+    return dict(ys=[to_np(y) for y in Y], dxs=[to_np(d) for d in DX], grads=read_grads(cfg, grads),
+                stats=st.stats(), plan=st.info)
+
+
+def run_gpu(cfg, xs=None, dys=None, iterations=1, group=False, params=None, one_copy_stream=False, calls=None):
     """Runs `iterations` iterations of the planned order; returns numpy results
     of the last one: dict(ys, dxs, grads, stats, plan).  one_copy_stream: both
     host-link directions on one stream (no prefetch stream of their own)."""
@@ -98,27 +132,7 @@ def run_gpu(cfg, xs=None, dys=None, iterations=1, group=False, params=None, one_
     DX = [torch.empty_like(x) for x in X]
     torch.cuda.synchronize()
     for _ in range(iterations):
-        st.begin_iteration(zero_grads=True)
-        order = cfg.order()
-        if group:
-            i = 0
-            while i < len(order):
-                k = order[i][0]
-                j = i
-                while j < len(order) and order[j][0] == k and order[j][1] == order[i][1] + (j - i):
-                    j += 1
-                mbs = [order[t][1] for t in range(i, j)]
-                if k == "F":
-                    st.forward_group(mbs[0], [X[m] for m in mbs], [Y[m] for m in mbs])
-                else:
-                    st.backward_group(mbs[0], [DY[m] for m in mbs], [DX[m] for m in mbs])
-                i = j
-        else:
-            for k, mb in order:
-                if k == "F":
-                    st.forward(mb, X[mb], Y[mb])
-                else:
-                    st.backward(mb, DY[mb], DX[mb])
+        drive_iteration(st, cfg, X, DY, Y, DX, group=group, calls=calls)
         st.sync()
     out = dict(ys=[to_np(y) for y in Y], dxs=[to_np(d) for d in DX], grads=read_grads(cfg, grads),
                stats=st.stats(), plan=st.info)
@@ -137,16 +151,61 @@ def run_oracle(cfg, xs=None, dys=None, ora_params=None):
                          cfg.n_heads, cfg.micro_batch, cfg.seq, cfg.ln_eps)
 
 
-def compare(gpu, ref, tol):
-    """Worst rel-L2 over y, dx of every micro-batch and every parameter grad."""
-    worst = {}
+def tile_excess(a, b, tol, tile=256) -> float:
+    """Per-tile bound beside the per-tensor rel-L2: for every tile (256 x 256
+    of a matrix, 256 elements of a vector) the error norm must stay within
+    tol times the larger of the tile's own reference norm and its fair share
+    of the tensor's reference norm (||ref|| * sqrt(tile size / size)).
+    Returns the worst ratio error / bound (<= 1 passes): a single tile
+    carrying a large error fails even when the whole tensor's rel-L2 passes."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    if a.ndim == 1:
+        a, b = a[None, :], b[None, :]
+    a = a.reshape(-1, a.shape[-1])
+    b = b.reshape(-1, b.shape[-1])
+    rows, cols = b.shape
+    tr = tile if rows > 1 else 1
+    total = float(np.linalg.norm(b))
+    n = b.size
+    worst = 0.0
+    for r0 in range(0, rows, tr):
+        for c0 in range(0, cols, tile):
+            rb = b[r0:r0 + tr, c0:c0 + tile]
+            ra = a[r0:r0 + tr, c0:c0 + tile]
+            err = float(np.linalg.norm(ra - rb))
+            bound = tol * max(float(np.linalg.norm(rb)), total * np.sqrt(rb.size / n), 1e-30)
+            worst = max(worst, err / bound)
+    return worst
+
+
+def assert_close(got, ref, tol, what=""):
+    """Parity bar of one tensor: rel-L2 below tol and every tile within the
+    per-tile bound of tile_excess."""
+    r = rel_l2(got, ref)
+    assert r < tol, f"{what} rel-L2 {r:.3g} >= {tol:g}"
+    t = tile_excess(got, ref, tol)
+    assert t <= 1.0, f"{what} worst tile at {t:.3g} x its bound (tol {tol:g})"
+
+
+def compare(gpu, ref, tol, tiles=True):
+    """Worst rel-L2 over y, dx of every micro-batch and every parameter grad;
+    with tiles, also the per-tile bound of tile_excess (reported as
+    "<name>@tile", failing above 1)."""
+    worst, tile_worst = {}, {}
+    pairs = []
     for mb in range(len(ref["ys"])):
-        worst[f"y{mb}"] = rel_l2(gpu["ys"][mb], ref["ys"][mb])
-        worst[f"dx{mb}"] = rel_l2(gpu["dxs"][mb], ref["dxs"][mb])
+        pairs.append((f"y{mb}", gpu["ys"][mb], ref["ys"][mb]))
+        pairs.append((f"dx{mb}", gpu["dxs"][mb], ref["dxs"][mb]))
     for l, g in enumerate(ref["grads"]):
         for k, v in g.items():
-            worst[f"L{l}.{k}"] = rel_l2(gpu["grads"][l][k], v)
+            pairs.append((f"L{l}.{k}", gpu["grads"][l][k], v))
+    for name, a, b in pairs:
+        worst[name] = rel_l2(a, b)
+        if tiles:
+            tile_worst[name] = tile_excess(a, b, tol)
     bad = {k: v for k, v in worst.items() if not v <= tol}
+    bad.update({f"{k}@tile": v for k, v in tile_worst.items() if not v <= 1.0})
     return worst, bad
 
 

@@ -157,3 +157,40 @@ def test_h5120_one_layer_matches_oracle():
     worst, bad = compare(gpu, ref, BF16_TOL)
     print("worst rel-L2", max(worst.values()), flush=True)
     assert not bad, bad
+
+
+@pytest.mark.timeout(1500)
+def test_seq8192_one_layer_recompute_matches_oracle():
+    """One full-width layer at sequence 8192 (hidden 4096, 32 heads, MLP
+    16384) with the full-layer recompute policy and launch configuration of
+    the long-sequence workload (segment replay of everything but the layer
+    input), one micro-batch, against the float64 oracle."""
+    cfg = dataclasses.replace(W.stage4_seq8192_recompute(), n_layers=1, n_micro=1)
+    cfg.policy = cfg.policy[:1]
+    print("seq 8192, hidden 4096, one layer, one micro-batch: GPU run", flush=True)
+    gpu = run_gpu(cfg)
+    assert gpu["stats"]["replays"] == 1
+    print("oracle run", flush=True)
+    ref = run_oracle(cfg)
+    worst, bad = compare(gpu, ref, BF16_TOL)
+    print("worst rel-L2", max(worst.values()), flush=True)
+    assert not bad, bad
+
+
+@pytest.mark.timeout(1500)
+def test_h8192_one_streamed_layer_matches_oracle():
+    """One full-width layer of the hidden-8192 workload (64 heads, MLP 32768,
+    seq 4096) in its launch configuration: weights streamed in from pinned
+    host memory and f32 gradients streamed out, layer-input recompute at
+    layer granularity, driven by group calls; one micro-batch, against the
+    float64 oracle."""
+    cfg = dataclasses.replace(W.stage12_h8192_stream(), n_layers=1, n_micro=1, window=2)
+    cfg.policy = cfg.policy[:1]
+    print("hidden 8192, seq 4096, one streamed layer, one micro-batch: GPU run", flush=True)
+    gpu = run_gpu(cfg, group=True)
+    assert gpu["stats"]["h2d_bytes"] > 0 and gpu["stats"]["d2h_bytes"] > 0
+    print("oracle run", flush=True)
+    ref = run_oracle(cfg)
+    worst, bad = compare(gpu, ref, BF16_TOL)
+    print("worst rel-L2", max(worst.values()), flush=True)
+    assert not bad, bad

@@ -9,7 +9,7 @@ from oracle import decoder_stage as ora
 from paper_2503_03182_amd import synth
 from paper_2503_03182_amd import tpstage as T
 
-from stage_harness import rel_l2, to_dev, to_np
+from stage_harness import assert_close, rel_l2, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -53,7 +53,7 @@ def test_gemm_store(dtype, layout, shape):
     dC = torch.full((M, N), float("nan"), device="cuda").to(dA.dtype)
     T.op_gemm(DT[dtype], layout, T.EPI_STORE, M, N, K, dA, a_shape[1], dB, b_shape[1], dC, N)
     torch.cuda.synchronize()
-    assert rel_l2(to_np(dC), ref) < TOL[dtype]
+    assert_close(to_np(dC), ref, TOL[dtype])
 
 
 @pytest.mark.parametrize("dtype,shape", [("f32", (296, 392, 200)), ("bf16", (296, 392, 200)),
@@ -71,17 +71,17 @@ def test_gemm_epilogues(dtype, shape):
     # BIAS
     T.op_gemm(DT[dtype], T.GEMM_NT, T.EPI_BIAS, M, N, K, dA, K, dB, K, out, N, bias=dbias)
     torch.cuda.synchronize()
-    assert rel_l2(to_np(out), acc + bias) < TOL[dtype]
+    assert_close(to_np(out), acc + bias, TOL[dtype])
     # BIAS_RESID
     T.op_gemm(DT[dtype], T.GEMM_NT, T.EPI_BIAS_RESID, M, N, K, dA, K, dB, K, out, N, bias=dbias, resid=dR, ldr=N)
     torch.cuda.synchronize()
-    assert rel_l2(to_np(out), acc + bias + R) < TOL[dtype]
+    assert_close(to_np(out), acc + bias + R, TOL[dtype])
     # BIAS_GELU: u = round(acc + b) kept, g = round(GeLU(u))
     u = torch.empty_like(out)
     T.op_gemm(DT[dtype], T.GEMM_NT, T.EPI_BIAS_GELU, M, N, K, dA, K, dB, K, out, N, bias=dbias, aux=u, ldaux=N)
     torch.cuda.synchronize()
-    assert rel_l2(to_np(u), acc + bias) < TOL[dtype]
-    assert rel_l2(to_np(out), ora.gelu(to_np(u))) < TOL[dtype]
+    assert_close(to_np(u), acc + bias, TOL[dtype])
+    assert_close(to_np(out), ora.gelu(to_np(u)), TOL[dtype])
     # and without keeping u the GeLU output is bitwise the same
     out2 = torch.empty_like(out)
     T.op_gemm(DT[dtype], T.GEMM_NT, T.EPI_BIAS_GELU, M, N, K, dA, K, dB, K, out2, N, bias=dbias)
@@ -94,12 +94,12 @@ def test_gemm_epilogues(dtype, shape):
               aux=to_dev(U, dtype), ldaux=N)
     torch.cuda.synchronize()
     ref = (A.astype(np.float64) @ B2.astype(np.float64)) * ora.gelu_grad(U.astype(np.float64))
-    assert rel_l2(to_np(out), ref) < TOL[dtype]
+    assert_close(to_np(out), ref, TOL[dtype])
     # BIAS_RESID (NN): C = A B + bias + R
     T.op_gemm(DT[dtype], T.GEMM_NN, T.EPI_BIAS_RESID, M, N, K, dA, K, to_dev(B2, dtype), N, out, N, bias=dbias,
               resid=dR, ldr=N)
     torch.cuda.synchronize()
-    assert rel_l2(to_np(out), A.astype(np.float64) @ B2.astype(np.float64) + bias + R) < TOL[dtype]
+    assert_close(to_np(out), A.astype(np.float64) @ B2.astype(np.float64) + bias + R, TOL[dtype])
     # ACC_F32 (TN): C32 += A^T B over K rows
     A3 = _t(27, (K, M), dtype)
     B3 = _t(28, (K, N), dtype)
@@ -108,7 +108,7 @@ def test_gemm_epilogues(dtype, shape):
     T.op_gemm(DT[dtype], T.GEMM_TN, T.EPI_ACC_F32, M, N, K, to_dev(A3, dtype), M, to_dev(B3, dtype), N, C32, N)
     torch.cuda.synchronize()
     ref = C0.astype(np.float64) + A3.astype(np.float64).T @ B3.astype(np.float64)
-    assert rel_l2(C32.cpu().numpy(), ref) < 2e-6
+    assert_close(C32.cpu().numpy(), ref, 2e-6)
 
 
 def test_gemm_leading_dimensions_and_deterministic():
@@ -127,7 +127,7 @@ def test_gemm_leading_dimensions_and_deterministic():
         outs.append(C)
     torch.cuda.synchronize()
     assert torch.equal(outs[0], outs[1])
-    assert rel_l2(to_np(outs[0]), A.astype(np.float64) @ B.astype(np.float64).T) < TOL["bf16"]
+    assert_close(to_np(outs[0]), A.astype(np.float64) @ B.astype(np.float64).T, TOL["bf16"])
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -156,12 +156,12 @@ def test_layernorm_fwd_bwd(dtype, rows, cols):
     ws = torch.empty(T.op_workspace_bytes(T.WS_COLSUM, rows, 2 * cols) // 4, device="cuda")
     T.op_layernorm_bwd(DT[dtype], rows, cols, dD, dX, mean, rstd, dG, dR, dxo, dg, dbb, ws)
     torch.cuda.synchronize()
-    assert rel_l2(to_np(out), ref) < TOL[dtype]
+    assert_close(to_np(out), ref, TOL[dtype])
     assert np.allclose(mean.cpu().numpy(), mu, rtol=1e-5, atol=1e-5)
     assert np.allclose(rstd.cpu().numpy(), rs, rtol=1e-4)
-    assert rel_l2(to_np(dxo), dx_ref) < TOL[dtype]
-    assert rel_l2(dg.cpu().numpy() - 0.25, dg_ref) < 1e-5
-    assert rel_l2(dbb.cpu().numpy() + 0.5, db_ref) < 1e-5
+    assert_close(to_np(dxo), dx_ref, TOL[dtype])
+    assert_close(dg.cpu().numpy() - 0.25, dg_ref, 1e-5)
+    assert_close(dbb.cpu().numpy() + 0.5, db_ref, 1e-5)
 
 
 ATTN_CASES = [  # (dtype, b, s, heads, d)
@@ -196,7 +196,7 @@ def test_attention_fwd(dtype, b, s, nh, d):
     lse = torch.full((b, nh, s), float("nan"), device="cuda")
     T.op_attention_fwd(DT[dtype], b, s, nh, d, dq, o, lse)
     torch.cuda.synchronize()
-    assert rel_l2(to_np(o), o_ref) < (2e-5 if dtype == "f32" else 1e-2)
+    assert_close(to_np(o), o_ref, (2e-5 if dtype == "f32" else 1e-2))
     assert np.abs(lse.cpu().numpy() - lse_ref).max() < (1e-4 if dtype == "f32" else 2e-2)
 
 
@@ -224,7 +224,7 @@ def test_attention_bwd(dtype, b, s, nh, d):
             # degenerate case (one key: dS = P (dP - D) vanishes exactly)
             assert np.abs(got[:, sl]).max() < 1e-5, name
         else:
-            assert rel_l2(got[:, sl], dqkv_ref[:, sl]) < tol, name
+            assert_close(got[:, sl], dqkv_ref[:, sl], tol, name)
 
 
 def test_attention_deterministic_and_causal_bitwise():
@@ -265,5 +265,5 @@ def test_colsum_and_gelu(dtype):
     T.op_gelu(DT[dtype], u.size, to_dev(u, dtype), g)
     torch.cuda.synchronize()
     ref = x[:, cols:].astype(np.float64).sum(axis=0) + 1.5
-    assert rel_l2(out.cpu().numpy(), ref) < 1e-6
-    assert rel_l2(to_np(g), ora.gelu(u.astype(np.float64))) < TOL[dtype]
+    assert_close(out.cpu().numpy(), ref, 1e-6)
+    assert_close(to_np(g), ora.gelu(u.astype(np.float64)), TOL[dtype])

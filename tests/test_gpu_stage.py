@@ -11,7 +11,7 @@ import pytest
 from paper_2503_03182_amd import configs as W
 from paper_2503_03182_amd import tpstage as T
 
-from stage_harness import bit_equal, compare, inputs, run_gpu, run_oracle
+from stage_harness import bit_equal, compare, inputs, read_grads, run_gpu, run_oracle, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -220,3 +220,153 @@ def test_full_shape_stage4_h2048_two_microbatches_matches_oracle():
     worst, bad = compare(gpu, ref, BF16_TOL)
     print("worst rel-L2", max(worst.values()), flush=True)
     assert not bad, bad
+
+
+def _streamed(window, granularity, policy=None, **kw):
+    L = 4
+    return _mid(n_layers=L, policy=policy or W.policy_layer_inputs(L), granularity=granularity,
+                weights=T.W_STREAM, window=window, **kw)
+
+
+def test_streamed_weights_match_oracle():
+    """Weights streamed in and f32 gradients streamed out (window < layers)
+    against the oracle, through per-micro-batch calls and group calls, at
+    both recompute granularities (segment granularity in groups of one
+    micro-batch: inflight 1 makes the order F0 B0 F1 B1 F2 B2)."""
+    L = 4
+    ref = run_oracle(_mid(n_layers=L))
+    cases = [
+        ("per-mb, segment, window 2", _streamed(2, T.GRAN_SEGMENT), False),
+        ("per-mb, layer, window 3", _streamed(3, T.GRAN_LAYER), False),
+        ("group, layer, window 2", _streamed(2, T.GRAN_LAYER), True),
+        ("groups of one, segment, window 2", _streamed(2, T.GRAN_SEGMENT, inflight=1), True),
+        ("groups of one, selective segment, window 3",
+         _streamed(3, T.GRAN_SEGMENT, policy=W.policy_selective(L), inflight=1), True),
+    ]
+    for name, cfg, group in cases:
+        print(name, flush=True)
+        out = run_gpu(cfg, group=group)
+        worst, bad = compare(out, ref, BF16_TOL)
+        assert not bad, (name, bad)
+        assert out["stats"]["h2d_bytes"] > 0 and out["stats"]["d2h_bytes"] > 0, name
+
+
+def _permuted_blocks(blocks):
+    """New parameters for every layer: layer l takes the values of layer L-1-l."""
+    return [b.clone() for b in reversed(blocks)]
+
+
+def test_parameters_changed_between_iterations():
+    """An optimizer step between iterations (here: the layers' parameter
+    blocks permuted in place) must reach every layer of the next iteration:
+    the second iteration of one stage equals, bitwise, a fresh stage built on
+    the new parameters, for resident weights and for a streamed window whose
+    entries survive the iteration boundary."""
+    import torch
+    from stage_harness import drive_iteration, make_params, results, to_dev
+    variants = [("resident", _mid(n_layers=4, policy=W.policy_selective(4)), False),
+                ("streamed, layer, window 2", _streamed(2, T.GRAN_LAYER), True),
+                ("streamed, segment, window 3", _streamed(3, T.GRAN_SEGMENT), False)]
+    for name, cfg, group in variants:
+        print(name, flush=True)
+        xs, dys = inputs(cfg)
+        blocks, grads, _ = make_params(cfg)
+        new_blocks = _permuted_blocks(blocks)
+        X = [to_dev(x, cfg.dtype) for x in xs]
+        DY = [to_dev(d, cfg.dtype) for d in dys]
+        Y = [torch.empty_like(x) for x in X]
+        DX = [torch.empty_like(x) for x in X]
+        torch.cuda.synchronize()
+        st = T.Stage(cfg, blocks, grads)
+        drive_iteration(st, cfg, X, DY, Y, DX, group=group)
+        st.sync()
+        for b, nb in zip(blocks, new_blocks):
+            b.copy_(nb)
+        torch.cuda.synchronize()
+        drive_iteration(st, cfg, X, DY, Y, DX, group=group)
+        second = results(cfg, st, Y, DX, grads)
+        st.close()
+        fb, fg, _ = make_params(cfg)
+        for b, nb in zip(fb, new_blocks):
+            b.copy_(nb)
+        torch.cuda.synchronize()
+        fresh = run_gpu(cfg, xs, dys, group=group, params=(fb, fg, None))
+        assert bit_equal(second, fresh) == [], name
+
+
+def test_group_calls_after_per_microbatch_calls_bitexact():
+    """Group calls that follow per-micro-batch calls in one iteration (the
+    per-micro-batch backward leaves its last parameter-gradient kernels
+    running): bit-exact to the same iteration made of per-micro-batch calls
+    only."""
+    keep_order = [("F", 0), ("F", 1), ("F", 2), ("B", 0), ("B", 1), ("B", 2)]
+    ref = run_gpu(_mid(ops=keep_order))
+    mixed = run_gpu(_mid(ops=keep_order), calls=[("F", [0, 1, 2], False), ("B", [0], False), ("B", [1, 2], True)])
+    assert bit_equal(ref, mixed) == []
+    order2 = [("F", 0), ("B", 0), ("F", 1), ("F", 2), ("B", 1), ("B", 2)]
+    mixed2 = run_gpu(_mid(ops=order2), calls=[("F", [0], False), ("B", [0], False), ("F", [1, 2], True),
+                                              ("B", [1, 2], False)])
+    assert bit_equal(ref, mixed2) == []
+    # the same with the selective policy (segment replays; groups of one)
+    sel = _mid(ops=keep_order, policy=W.policy_selective(3))
+    ref_sel = run_gpu(sel)
+    mixed_sel = run_gpu(sel, calls=[("F", [0, 1], False), ("F", [2], True), ("B", [0], False), ("B", [1], True),
+                                    ("B", [2], False)])
+    assert bit_equal(ref_sel, mixed_sel) == []
+
+
+def test_stream_ordering_without_explicit_synchronize():
+    """The binding orders the stage after the caller's current stream and the
+    caller after the stage: inputs written by a late kernel on the caller's
+    stream just before each call are the ones the stage reads, and outputs
+    read on the caller's stream are complete, with no torch.cuda.synchronize().
+    Both with the caller on a stream of its own (the stage then runs on it)
+    and on the default stream (the stage on a private stream)."""
+    import torch
+    from stage_harness import drive_iteration, make_params, results, to_dev
+    cfg = _mid(policy=W.policy_selective(3))
+    ref = run_gpu(cfg)
+    xs, dys = inputs(cfg)
+    torch.cuda.synchronize()
+    for own_stream in (True, False):
+        s = torch.cuda.Stream() if own_stream else torch.cuda.default_stream()
+        with torch.cuda.stream(s):
+            blocks, grads, _ = make_params(cfg)
+            st = T.Stage(cfg, blocks, grads)
+            assert (st.cs.cuda_stream == s.cuda_stream) == own_stream
+            X = [torch.zeros(cfg.tokens, cfg.hidden, device="cuda", dtype=torch.bfloat16) for _ in xs]
+            DY = [torch.zeros_like(x) for x in X]
+            Y = [torch.empty_like(x) for x in X]
+            DX = [torch.empty_like(x) for x in X]
+            srcX = [to_dev(x, cfg.dtype) for x in xs]
+            srcDY = [to_dev(d, cfg.dtype) for d in dys]
+            # a spin kernel delays the input writes on the caller's stream
+            torch.cuda._sleep(50_000_000)
+            for a, b in zip(X + DY, srcX + srcDY):
+                a.copy_(b)
+            drive_iteration(st, cfg, X, DY, Y, DX)
+            out = dict(ys=[to_np(y) for y in Y], dxs=[to_np(d) for d in DX], grads=read_grads(cfg, grads))
+        st.close()
+        assert bit_equal(ref, out) == [], own_stream
+
+
+def test_sync_for_times_out_and_recovers():
+    """tps_stage_sync_for returns TPS_ETIMEOUT while the compute stream is
+    still busy (a bounded spin kernel holds it), and TPS_OK once the work is
+    done; the stage stays usable."""
+    import torch
+    from stage_harness import make_params
+    cfg = W.tiny()
+    blocks, grads, _ = make_params(cfg)
+    st = T.Stage(cfg, blocks, grads)
+    torch.cuda.synchronize()
+    assert st.sync_for(0) == T.TPS_OK
+    with torch.cuda.stream(st.cs):
+        torch.cuda._sleep(200_000_000)
+    assert st.sync_for(1.0) == T.TPS_ETIMEOUT
+    assert "compute stream still has work" in T.lib().tps_last_error().decode()
+    assert st.sync_for(120_000.0) == T.TPS_OK
+    with pytest.raises(T.TpsError) as e:
+        st.sync_for(-1.0)
+    assert e.value.code == T.TPS_EINVAL
+    st.close()
