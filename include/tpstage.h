@@ -90,8 +90,10 @@ enum { TPS_W_RESIDENT = 0, TPS_W_STREAM = 1 };
  * the micro-batch before its backward starts (block-wise T-Recomp). */
 enum { TPS_GRAN_LAYER = 0, TPS_GRAN_SEGMENT = 1 };
 
-/* op kinds in the planned order */
-enum { TPS_OP_F = 0, TPS_OP_B = 1 };
+/* op kinds in the planned order (TPS_OP_R: a recompute task of the T-Pipe
+ * schedule, reported by tps_tpipe_schedule; a stage runs the recompute of a
+ * micro-batch at the start of its backward) */
+enum { TPS_OP_F = 0, TPS_OP_B = 1, TPS_OP_R = 2 };
 
 /* parameter order inside one layer's packed parameter / gradient block */
 enum {
@@ -308,6 +310,60 @@ int tps_stage_destroy(tps_stage* st);
  * system cannot pin that much. */
 int tps_host_alloc(uint64_t bytes, void** out);
 int tps_host_free(void* p);
+
+/* T-Pipe two-chunk pipeline schedule and unit-time simulator (host only, no
+ * GPU needed).  Paper: Section 4.1 "T-Pipe Schedule" and the appendix
+ * "Theoretical Analysis of T-Pipe" (two chunks per stage, chunk 1 the
+ * shallow layer block s, chunk 2 the deep block p + s; forward 1 T_unit and
+ * backward 2 T_unit per chunk and stage); Section 4.2 "Addressing the
+ * Concerns" and the appendices on the delay rounds and on T-Recomp
+ * (block-wise recompute of chunk 1 as a task of its own, 1 T_unit, before
+ * that chunk's backward; chunk 2 delayed by k rounds).
+ *
+ * Each stage runs its tasks in the T-Pipe order (rounds of F chunk 1,
+ * B chunk 2, F chunk 2, B chunk 1); the simulator starts every task as soon
+ * as its stage is free and its dependencies have finished.  Activation
+ * blocks (m_a / 2p each) are held from the start of a chunk's forward to the
+ * start of its backward on the stage; a recomputed chunk holds none and its
+ * regenerated activations take one buffer block from the recompute to the
+ * end of the backward. */
+typedef struct tps_tpipe_config {
+  int32_t stages;               /* p, 1..256                                    */
+  int32_t micro;                /* m micro-batches per mini-batch, 1..4096      */
+  int32_t t_recomp;             /* 1: block-wise T-Recomp of chunk 1            */
+  int32_t delay;                /* chunk-2 delay rounds k, or -1: the smallest k
+                                   that reaches the shortest makespan          */
+} tps_tpipe_config;
+
+typedef struct tps_tpipe_task {
+  int32_t kind;                 /* TPS_OP_F, TPS_OP_B or TPS_OP_R               */
+  int32_t chunk;                /* 1 (shallow) or 2 (deep)                      */
+  int32_t mb;                   /* micro-batch                                  */
+  int32_t start, end;           /* simulated time, T_unit                       */
+} tps_tpipe_task;
+
+typedef struct tps_tpipe_result {
+  int32_t delay;                /* k used                                       */
+  int32_t makespan;             /* whole pipeline, T_unit                       */
+  int32_t busy;                 /* busy time of one stage, T_unit               */
+  double bubble_ratio;          /* (makespan - busy) / makespan                 */
+  int32_t peak_blocks_chunk1;   /* at the requested stage, blocks of m_a / 2p   */
+  int32_t peak_blocks_chunk2;
+  int32_t peak_buffer_blocks;   /* recompute buffer (T-Recomp)                  */
+  int32_t peak_blocks;          /* all three together at the requested stage   */
+  int32_t max_stage_peak_blocks;/* the largest peak_blocks over all stages      */
+  int32_t life_chunk1;          /* start of forward to start of backward of the
+                                   middle micro-batch on the requested stage   */
+  int32_t life_chunk2;
+} tps_tpipe_result;
+
+/* Simulates the schedule and writes the requested stage's tasks in execution
+ * order (at most max_tasks of them; *n_tasks receives the count: 4m, or 5m
+ * with T-Recomp) and the summary.  Splitting the list by chunk gives the F/B
+ * order of each chunk's layers (tps_config.ops, recompute tasks folded into
+ * the backward that follows them).  TPS_EINVAL for out-of-range arguments. */
+int tps_tpipe_schedule(const tps_tpipe_config* cfg, int32_t stage, tps_tpipe_task* tasks,
+                       int32_t max_tasks, int32_t* n_tasks, tps_tpipe_result* out);
 
 /* Thread-local message of the last failing call ("" if none). */
 const char* tps_last_error(void);
