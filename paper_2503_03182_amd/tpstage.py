@@ -23,7 +23,7 @@ TENSORS = ("x", "a", "qkv", "o", "lse", "x1", "c", "u", "g", "ln1", "ln2")
 T_INDEX = {n: i for i, n in enumerate(TENSORS)}
 W_RESIDENT, W_STREAM = 0, 1
 GRAN_LAYER, GRAN_SEGMENT = 0, 1
-OP_F, OP_B = 0, 1
+OP_F, OP_B, OP_R = 0, 1, 2
 PARAMS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "g1", "be1", "g2", "be2")
 GEMM_NT, GEMM_NN, GEMM_TN = 0, 1, 2
 EPI_STORE, EPI_BIAS, EPI_BIAS_RESID, EPI_BIAS_GELU, EPI_GELU_GRAD, EPI_ACC_F32 = range(6)
@@ -87,6 +87,22 @@ class KernelTime(C.Structure):
                 ("flops", C.c_double), ("bytes", C.c_double)]
 
 
+class TPipeConfig(C.Structure):
+    _fields_ = [("stages", C.c_int32), ("micro", C.c_int32), ("t_recomp", C.c_int32), ("delay", C.c_int32)]
+
+
+class TPipeTask(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("chunk", C.c_int32), ("mb", C.c_int32), ("start", C.c_int32),
+                ("end", C.c_int32)]
+
+
+class TPipeResult(C.Structure):
+    _fields_ = [("delay", C.c_int32), ("makespan", C.c_int32), ("busy", C.c_int32), ("bubble_ratio", C.c_double),
+                ("peak_blocks_chunk1", C.c_int32), ("peak_blocks_chunk2", C.c_int32),
+                ("peak_buffer_blocks", C.c_int32), ("peak_blocks", C.c_int32),
+                ("max_stage_peak_blocks", C.c_int32), ("life_chunk1", C.c_int32), ("life_chunk2", C.c_int32)]
+
+
 class Stats(C.Structure):
     _fields_ = [("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("kernels", C.c_uint64),
                 ("replays", C.c_uint64), ("ops_done", C.c_int32)]
@@ -102,7 +118,7 @@ EXPORTED = (
     "tps_last_error", "tps_op_gemm", "tps_op_layernorm_fwd", "tps_op_layernorm_bwd",
     "tps_op_attention_fwd", "tps_op_attention_bwd", "tps_op_colsum", "tps_op_gelu",
     "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
-    "tps_host_alloc", "tps_host_free",
+    "tps_host_alloc", "tps_host_free", "tps_tpipe_schedule",
 )
 
 
@@ -145,6 +161,8 @@ def lib() -> C.CDLL:
         L.tps_op_workspace_bytes.restype = u64
         L.tps_host_alloc.argtypes = [u64, C.POINTER(vp)]
         L.tps_host_free.argtypes = [vp]
+        L.tps_tpipe_schedule.argtypes = [C.POINTER(TPipeConfig), i32, C.POINTER(TPipeTask), i32,
+                                         C.POINTER(C.c_int32), C.POINTER(TPipeResult)]
         _lib = L
     return _lib
 
@@ -295,6 +313,38 @@ def param_layout(cfg: StageConfig):
     c = cfg.to_c()
     check(lib().tps_param_layout(C.byref(c), po, C.byref(pb), go, C.byref(gb)))
     return list(po), pb.value, list(go), gb.value
+
+
+# --- T-Pipe schedule -------------------------------------------------------------
+def tpipe_schedule(stages: int, micro: int, stage: int = 0, t_recomp: bool = False, delay: int = -1):
+    """The T-Pipe two-chunk schedule of `stages` pipeline stages over `micro`
+    micro-batches, simulated in T_unit (tps_tpipe_schedule).  Returns
+    (summary dict, tasks of `stage` in execution order as
+    (kind "F"|"B"|"R", chunk 1|2, mb, start, end))."""
+    cfg = TPipeConfig(stages, micro, int(t_recomp), delay)
+    res = TPipeResult()
+    n = C.c_int32()
+    check(lib().tps_tpipe_schedule(C.byref(cfg), stage, None, 0, C.byref(n), C.byref(res)))
+    arr = (TPipeTask * max(n.value, 1))()
+    check(lib().tps_tpipe_schedule(C.byref(cfg), stage, arr, n.value, C.byref(n), C.byref(res)))
+    names = {OP_F: "F", OP_B: "B", OP_R: "R"}
+    tasks = [(names[t.kind], t.chunk, t.mb, t.start, t.end) for t in arr[:n.value]]
+    return {k: getattr(res, k) for k, _ in TPipeResult._fields_}, tasks
+
+
+def chunk_orders(tasks):
+    """Splits a stage's T-Pipe task list into the F/B order of each chunk's
+    layers (StageConfig.ops form: [("F"|"B", mb)]); a recompute task is run by
+    the chunk's backward that follows it.  Also returns the interleaved call
+    sequence [(chunk, "F"|"B", mb)]."""
+    orders = {1: [], 2: []}
+    calls = []
+    for kind, chunk, mb, _, _ in tasks:
+        if kind == "R":
+            continue
+        orders[chunk].append((kind, mb))
+        calls.append((chunk, kind, mb))
+    return orders[1], orders[2], calls
 
 
 # --- stage ---------------------------------------------------------------------

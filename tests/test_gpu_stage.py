@@ -370,3 +370,47 @@ def test_sync_for_times_out_and_recovers():
         st.sync_for(-1.0)
     assert e.value.code == T.TPS_EINVAL
     st.close()
+
+
+def test_tpipe_stage_orders_bitexact_to_default():
+    """One stage of a 4-stage T-Pipe with T-Recomp over 8 micro-batches, as
+    the simulator orders it: chunk 1 (full recompute from the chunk input,
+    replayed as one block before each backward) and chunk 2 (every tensor
+    kept) are two stage objects on one stream, called in the stage's
+    interleaved order.  Each is bit-exact to the same chunk run alone in the
+    default order (all forwards first), and the planner holds fewer
+    checkpoint slots for chunk 2 under the T-Pipe order."""
+    import torch
+    from stage_harness import make_params, results, to_dev
+    _, tasks = T.tpipe_schedule(4, 8, stage=1, t_recomp=True)
+    o1, o2, calls = T.chunk_orders(tasks)
+    c1 = _mid(n_layers=2, n_micro=8, policy=W.policy_all(2, T.RECOMPUTE), granularity=T.GRAN_SEGMENT, ops=o1)
+    c2 = _mid(n_layers=2, n_micro=8, ops=o2)
+    ref1 = run_gpu(dataclasses.replace(c1, ops=None))
+    ref2 = run_gpu(dataclasses.replace(c2, ops=None))
+    assert T.plan(c2)["n_slots"] < T.plan(dataclasses.replace(c2, ops=None))["n_slots"]
+    xs, dys = inputs(c1)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        stages, io = {}, {}
+        for ch, cfg in ((1, c1), (2, c2)):
+            blocks, grads, _ = make_params(cfg)
+            st = T.Stage(cfg, blocks, grads)
+            X = [to_dev(x, cfg.dtype) for x in xs]
+            DY = [to_dev(d, cfg.dtype) for d in dys]
+            io[ch] = (X, DY, [torch.empty_like(x) for x in X], [torch.empty_like(x) for x in X], grads, cfg)
+            stages[ch] = st
+            st.begin_iteration(zero_grads=True)
+        for ch, kind, mb in calls:
+            X, DY, Y, DX, _, _ = io[ch]
+            if kind == "F":
+                stages[ch].forward(mb, X[mb], Y[mb])
+            else:
+                stages[ch].backward(mb, DY[mb], DX[mb])
+        outs = {}
+        for ch in (1, 2):
+            X, DY, Y, DX, grads, cfg = io[ch]
+            outs[ch] = results(cfg, stages[ch], Y, DX, grads)
+            stages[ch].close()
+    assert bit_equal(ref1, outs[1]) == []
+    assert bit_equal(ref2, outs[2]) == []
