@@ -86,6 +86,16 @@ def stage12_h8192_stream(n_micro: int = 8) -> StageConfig:
                        weights=W_STREAM, window=3, layer_major=True)
 
 
+def stage12_h8192_stream_m20() -> StageConfig:
+    """The hidden-8192 streamed workload with 20 micro-batches in flight
+    (same layers, shapes and policy): every tensor kept would need more than
+    the 288 GB of one MI355X (activations of 20 x 12 layer-micro-batch units
+    plus bf16 weights and f32 gradients), while layer-input recompute and
+    streamed weights and gradients keep the stage's peak a small fraction of
+    it."""
+    return stage12_h8192_stream(n_micro=20)
+
+
 WORKLOADS = {
     "tiny": tiny,
     "stage4_h2048": stage4_h2048,
@@ -93,4 +103,5 @@ WORKLOADS = {
     "stage5_h5120_resident": stage5_h5120_resident,
     "stage4_seq8192_recompute": stage4_seq8192_recompute,
     "stage12_h8192_stream": stage12_h8192_stream,
+    "stage12_h8192_stream_m20": stage12_h8192_stream_m20,
 }

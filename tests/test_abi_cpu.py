@@ -272,3 +272,22 @@ def test_param_layout_offsets():
         off = _align(off + 4 * n)
     assert pb == off
     assert gb == pb   # f32 storage: same layout as the gradients
+
+
+def test_oversubscribed_stage_exceeds_hbm_only_when_kept():
+    """The hidden-8192 streamed stage with 20 micro-batches in flight: keeping
+    every tensor (activations at the in-flight peak, bf16 weights and f32
+    gradients of all 12 layers) would need more than the 288 GB of HBM of one
+    MI355X, while the planned peak with layer-input recompute and streamed
+    weights and gradients stays far below it."""
+    from paper_2503_03182_amd import configs as W
+    cfg = W.stage12_h8192_stream_m20()
+    info = T.plan(cfg)
+    L = cfg.n_layers
+    keep_all = info["keep_all_bytes"] + L * (info["param_bytes"] + info["grad_bytes"])
+    assert keep_all > 288e9
+    assert info["predicted_peak_bytes"] < 0.2 * 288e9
+    # the same stage at 8 micro-batches fits either way (the workload's
+    # premise needs the larger in-flight count)
+    info8 = T.plan(W.stage12_h8192_stream())
+    assert info8["keep_all_bytes"] + L * (info8["param_bytes"] + info8["grad_bytes"]) < 288e9
