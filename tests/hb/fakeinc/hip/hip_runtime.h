@@ -1,0 +1,54 @@
+// Host-only stand-in for the HIP runtime API used by the stage executor, for
+// the happens-before checker build (tests/hb).  No GPU code: streams and
+// events are records of a vector-clock model, kernel launches and copies are
+// recorded as memory accesses (hb_runtime.cpp, hb_kernels.cpp).
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+typedef enum hipError_t {
+  hipSuccess = 0,
+  hipErrorInvalidValue = 1,
+  hipErrorNotReady = 600,
+  hipErrorUnknown = 999
+} hipError_t;
+
+struct HbStream;
+struct HbEvent;
+typedef HbStream* hipStream_t;
+typedef HbEvent* hipEvent_t;
+
+typedef enum hipMemcpyKind {
+  hipMemcpyHostToHost = 0,
+  hipMemcpyHostToDevice = 1,
+  hipMemcpyDeviceToHost = 2,
+  hipMemcpyDeviceToDevice = 3,
+  hipMemcpyDefault = 4
+} hipMemcpyKind;
+
+typedef enum hipDeviceAttribute_t { hipDeviceAttributeMultiprocessorCount = 1 } hipDeviceAttribute_t;
+
+#define hipEventDefault 0x0u
+#define hipEventDisableTiming 0x2u
+#define hipEventDisableSystemFence 0x20000000u
+#define hipHostMallocDefault 0x0u
+#define hipStreamNonBlocking 0x1u
+
+hipError_t hipGetDevice(int* dev);
+hipError_t hipDeviceGetAttribute(int* v, hipDeviceAttribute_t a, int dev);
+hipError_t hipEventCreate(hipEvent_t* e);
+hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned flags);
+hipError_t hipEventDestroy(hipEvent_t e);
+hipError_t hipEventRecord(hipEvent_t e, hipStream_t s);
+hipError_t hipEventSynchronize(hipEvent_t e);
+hipError_t hipEventElapsedTime(float* ms, hipEvent_t a, hipEvent_t b);
+hipError_t hipStreamWaitEvent(hipStream_t s, hipEvent_t e, unsigned flags);
+hipError_t hipStreamSynchronize(hipStream_t s);
+hipError_t hipStreamQuery(hipStream_t s);
+hipError_t hipStreamDestroy(hipStream_t s);
+hipError_t hipStreamCreateWithFlags(hipStream_t* s, unsigned flags);
+hipError_t hipMemcpyAsync(void* dst, const void* src, size_t bytes, hipMemcpyKind kind, hipStream_t s);
+hipError_t hipHostMalloc(void** p, size_t bytes, unsigned flags);
+hipError_t hipHostFree(void* p);
+hipError_t hipGetLastError(void);
+const char* hipGetErrorString(hipError_t e);

@@ -1,0 +1,183 @@
+// Kernel launchers of the stage library (csrc/kernels.h) for the
+// happens-before checker build: each records the byte ranges its kernels
+// read and write, from the operand shapes and layouts documented in
+// csrc/kernels.h and include/tpstage_ops.h, and computes nothing.
+#include <cstdint>
+#include <string>
+
+#include "hb.h"
+#include "kernels.h"
+#include "ws.h"
+
+namespace {
+
+uint64_t U(const void* p) { return reinterpret_cast<uint64_t>(p); }
+
+// rows x row_bytes at stride `stride` bytes
+void add2d(HbRanges& v, const void* p, int64_t rows, int64_t row_bytes, int64_t stride) {
+  if (!p || rows <= 0 || row_bytes <= 0) return;
+  if (stride == row_bytes) {
+    v.push_back({U(p), U(p) + (uint64_t)(rows * row_bytes)});
+    return;
+  }
+  for (int64_t r = 0; r < rows; ++r) v.push_back({U(p) + (uint64_t)(r * stride), U(p) + (uint64_t)(r * stride + row_bytes)});
+}
+
+void add1d(HbRanges& v, const void* p, int64_t bytes) {
+  if (p && bytes > 0) v.push_back({U(p), U(p) + (uint64_t)bytes});
+}
+
+int64_t esz(int dtype) { return dtype == TPS_BF16 ? 2 : 4; }
+
+}  // namespace
+
+namespace tps {
+
+GemmTile gemm_select_tile(int, int, const GemmArgs&) { return {128, 128, 32, 0}; }
+const char* gemm_kernel_name(int, int, const GemmArgs&) { return "gemm"; }
+const char* attention_fwd_v3_name(int, int, int) { return "attention forward"; }
+
+hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, const void* A, int64_t lda, const void* B,
+                       int64_t ldb, void* C, int64_t ldc, const void* bias, const void* resid, int64_t ldr, void* aux,
+                       int64_t ldaux, hipStream_t stream, int overwrite) {
+  const int64_t e = esz(dtype);
+  HbRanges rd, wr;
+  if (layout == TPS_GEMM_TN) add2d(rd, A, K, M * e, lda * e);
+  else add2d(rd, A, M, K * e, lda * e);
+  if (layout == TPS_GEMM_NT) add2d(rd, B, N, K * e, ldb * e);
+  else add2d(rd, B, K, N * e, ldb * e);
+  const int64_t ce = epi == TPS_EPI_ACC_F32 ? 4 : e;
+  if (epi == TPS_EPI_ACC_F32 && !overwrite) add2d(rd, C, M, N * ce, ldc * ce);
+  add2d(wr, C, M, N * ce, ldc * ce);
+  if (epi == TPS_EPI_BIAS || epi == TPS_EPI_BIAS_RESID || epi == TPS_EPI_BIAS_GELU) add1d(rd, bias, N * e);
+  if (epi == TPS_EPI_BIAS_RESID) add2d(rd, resid, M, N * e, ldr * e);
+  if (epi == TPS_EPI_BIAS_GELU) add2d(wr, aux, M, N * e, ldaux * e);
+  if (epi == TPS_EPI_GELU_GRAD) add2d(rd, aux, M, N * e, ldaux * e);
+  hb_op(stream, ("gemm layout " + std::to_string(layout) + " epilogue " + std::to_string(epi)).c_str(), rd, wr);
+  return hipSuccess;
+}
+
+hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
+                                hipStream_t st) {
+  const int64_t e = esz(dtype), T = (int64_t)b * s, h = (int64_t)nh * d;
+  HbRanges rd, wr;
+  add1d(rd, qkv, T * 3 * h * e);
+  add1d(wr, o, T * h * e);
+  add1d(wr, lse, T * nh * 4);
+  hb_op(st, "attention forward", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, const void* o, const float* lse,
+                                const void* dout, void* dqkv, float* dvec, hipStream_t st) {
+  const int64_t e = esz(dtype), T = (int64_t)b * s, h = (int64_t)nh * d;
+  HbRanges rd, wr, rd2;
+  add1d(rd, o, T * h * e);
+  add1d(rd, dout, T * h * e);
+  add1d(wr, dvec, T * nh * 4);
+  hb_op(st, "attention backward row dots", rd, wr);
+  add1d(rd2, qkv, T * 3 * h * e);
+  add1d(rd2, lse, T * nh * 4);
+  add1d(rd2, dout, T * h * e);
+  add1d(rd2, dvec, T * nh * 4);
+  HbRanges wr2;
+  add1d(wr2, dqkv, T * 3 * h * e);
+  hb_op(st, "attention backward", rd2, wr2);
+  return hipSuccess;
+}
+
+hipError_t layernorm_fwd_launch(int dtype, int rows, int cols, const void* x, const void* gamma, const void* beta,
+                                float, void* out, float* mean, float* rstd, hipStream_t st) {
+  const int64_t e = esz(dtype);
+  HbRanges rd, wr;
+  add1d(rd, x, (int64_t)rows * cols * e);
+  add1d(rd, gamma, cols * e);
+  add1d(rd, beta, cols * e);
+  add1d(wr, out, (int64_t)rows * cols * e);
+  add1d(wr, mean, rows * 4);
+  add1d(wr, rstd, rows * 4);
+  hb_op(st, "layernorm forward", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t layernorm_bwd_acc_launch(int dtype, int rows, int cols, const void* dout, const void* x, const float* mean,
+                                    const float* rstd, const void* gamma, const void* resid, void* dx,
+                                    float* part_dbeta, int64_t k_stride, int64_t seg_stride, hipStream_t st) {
+  const int64_t e = esz(dtype);
+  HbRanges rd, wr;
+  add1d(rd, dout, (int64_t)rows * cols * e);
+  add1d(rd, x, (int64_t)rows * cols * e);
+  add1d(rd, mean, rows * 4);
+  add1d(rd, rstd, rows * 4);
+  add1d(rd, gamma, cols * e);
+  add1d(rd, resid, (int64_t)rows * cols * e);
+  add1d(wr, dx, (int64_t)rows * cols * e);
+  const int64_t segs = colsum_segments(rows);
+  for (int64_t sgi = 0; sgi < segs; ++sgi) {
+    for (int64_t off : {(int64_t)0, k_stride}) {
+      const float* p = part_dbeta + sgi * seg_stride + off;
+      add1d(rd, p, cols * 4);
+      add1d(wr, p, cols * 4);
+    }
+  }
+  hb_op(st, "layernorm backward", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t colsum_acc_launch(int dtype, int rows, int cols, const void* x, int64_t ldx, float* part, int64_t seg_stride,
+                             hipStream_t st) {
+  const int64_t e = esz(dtype);
+  HbRanges rd, wr;
+  add2d(rd, x, rows, cols * e, ldx * e);
+  const int64_t segs = colsum_segments(rows);
+  for (int64_t sgi = 0; sgi < segs; ++sgi) {
+    add1d(rd, part + sgi * seg_stride, cols * 4);
+    add1d(wr, part + sgi * seg_stride, cols * 4);
+  }
+  hb_op(st, "column sums", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_t seg_stride, float* grads,
+                                  hipStream_t st, int overwrite) {
+  HbRanges rd, wr;
+  for (int sgi = 0; sgi < segs; ++sgi) {
+    add1d(rd, part + sgi * seg_stride + m.c0[0], (int64_t)(m.c0[m.n] - m.c0[0]) * 4);
+    add1d(wr, part + sgi * seg_stride + m.c0[0], (int64_t)(m.c0[m.n] - m.c0[0]) * 4);
+  }
+  for (int r = 0; r < m.n; ++r) {
+    float* g = grads + m.goff[r];
+    const int64_t n = m.c0[r + 1] - m.c0[r];
+    if (!overwrite) add1d(rd, g, n * 4);
+    add1d(wr, g, n * 4);
+  }
+  hb_op(st, "bias gradient finalize", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st) {
+  HbRanges rd, wr;
+  add1d(rd, u, n * esz(dtype));
+  add1d(wr, g, n * esz(dtype));
+  hb_op(st, "gelu", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st) {
+  HbRanges none, wr;
+  add1d(wr, p, (int64_t)bytes);
+  hb_op(st, "fill zero", none, wr);
+  return hipSuccess;
+}
+
+hipError_t transpose_launch(int dtype, int rows, int cols, const void* in, int64_t ldi, void* out, int64_t ldo,
+                            hipStream_t st) {
+  const int64_t e = esz(dtype);
+  HbRanges rd, wr;
+  add2d(rd, in, rows, cols * e, ldi * e);
+  add2d(wr, out, cols, rows * e, ldo * e);
+  hb_op(st, "transpose", rd, wr);
+  return hipSuccess;
+}
+
+}  // namespace tps
