@@ -81,6 +81,22 @@ int tps_op_attention_bwd(int dtype, int b, int s, int n_heads, int head_dim,
                          const void* d_o, void* dqkv, float* workspace,
                          void* stream);
 
+/* Allocation-free variant of tps_op_attention_bwd, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid allocation): same arguments without the workspace
+ * and bitwise the same result.  Its row-dot workspace is a fixed device
+ * array of the library (4 MiB per GPU, held until the process ends), so
+ * b * s * n_heads must not exceed tps_op_attention_bwd_noalloc_max_rows()
+ * (TPS_EINVAL otherwise, before anything is launched).  Calls allocate
+ * nothing (the first call on a device only looks up the array's address).
+ * All calls on one GPU share that GPU's array: calls that overlap in time on
+ * one GPU (different streams without ordering between them, or host threads)
+ * race; calls ordered on one stream do not. */
+int tps_op_attention_bwd_noalloc(int dtype, int b, int s, int n_heads, int head_dim,
+                                 const void* qkv, const void* o, const float* lse,
+                                 const void* d_o, void* dqkv, void* stream);
+int64_t tps_op_attention_bwd_noalloc_max_rows(void);
+
 /* out[c] += sum_r x[r, c] over x[rows, cols] (leading dimension ldx), f32,
  * fixed order.  workspace: tps_op_workspace_bytes(TPS_WS_COLSUM, rows, cols). */
 int tps_op_colsum(int dtype, int rows, int cols, const void* x, int64_t ldx,

@@ -118,7 +118,8 @@ EXPORTED = (
     "tps_last_error", "tps_op_gemm", "tps_op_layernorm_fwd", "tps_op_layernorm_bwd",
     "tps_op_attention_fwd", "tps_op_attention_bwd", "tps_op_colsum", "tps_op_gelu",
     "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
-    "tps_host_alloc", "tps_host_free", "tps_tpipe_schedule",
+    "tps_host_alloc", "tps_host_free", "tps_tpipe_schedule", "tps_op_attention_bwd_noalloc",
+    "tps_op_attention_bwd_noalloc_max_rows",
 )
 
 
@@ -155,6 +156,9 @@ def lib() -> C.CDLL:
         L.tps_op_layernorm_bwd.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.tps_op_attention_fwd.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp]
         L.tps_op_attention_bwd.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+        L.tps_op_attention_bwd_noalloc.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
+        L.tps_op_attention_bwd_noalloc_max_rows.argtypes = []
+        L.tps_op_attention_bwd_noalloc_max_rows.restype = i64
         L.tps_op_colsum.argtypes = [i32, i32, i32, vp, i64, vp, vp, vp]
         L.tps_op_gelu.argtypes = [i32, i64, vp, vp, vp]
         L.tps_op_workspace_bytes.argtypes = [i32, i64, i64]
@@ -504,6 +508,11 @@ def op_attention_fwd(dtype, b, s, nh, d, qkv, o, lse, stream=None):
 def op_attention_bwd(dtype, b, s, nh, d, qkv, o, lse, do, dqkv, ws, stream=None):
     check(lib().tps_op_attention_bwd(dtype, b, s, nh, d, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(do), _ptr(dqkv),
                                      _ptr(ws), _stream(stream)))
+
+
+def op_attention_bwd_noalloc(dtype, b, s, nh, d, qkv, o, lse, do, dqkv, stream=None):
+    check(lib().tps_op_attention_bwd_noalloc(dtype, b, s, nh, d, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(do),
+                                             _ptr(dqkv), _stream(stream)))
 
 
 def op_colsum(dtype, rows, cols, x, ldx, out, ws, stream=None):
