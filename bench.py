@@ -33,15 +33,28 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    """sha256 over the HIP/C++ sources of the library (sorted by name)."""
+# Sources each kernel family is compiled from (device code and the headers it
+# includes); counters recorded for a kernel stay valid while these are unchanged.
+KERNEL_SOURCES = {
+    "tps::gemm_bf16_kernel": ("gemm_pipe.h", "gemm_lds.h", "gemm_impl.h", "gemm_nt.hip", "gemm_nn.hip",
+                              "gemm_tn.hip", "tps_device.h", "kernels.h"),
+    "tps::attn": ("attention.hip", "attention_fwd.hip", "attention_bwd.hip", "attn_tiles.h", "tps_device.h",
+                  "kernels.h"),
+}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    """sha256 over the sources `kernel` is built from (every library source
+    for a kernel outside the known families)."""
     import hashlib
     csrc = os.path.join(ROOT, "paper_2503_03182_amd", "csrc")
+    names = next((v for k, v in KERNEL_SOURCES.items() if kernel.startswith(k)), None)
+    if names is None:
+        names = [n for n in os.listdir(csrc) if n.endswith((".hip", ".h", ".cpp"))]
     h = hashlib.sha256()
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h", ".cpp")):
-            h.update(name.encode())
-            h.update(open(os.path.join(csrc, name), "rb").read())
+    for name in sorted(names):
+        h.update(name.encode())
+        h.update(open(os.path.join(csrc, name), "rb").read())
     return h.hexdigest()
 
 
@@ -52,7 +65,7 @@ def measured_traffic(workload: str, kernel: str):
     if not os.path.exists(path):
         return None
     rec = dict(line.rstrip("\n").split("\t", 1) for line in open(path) if "\t" in line)
-    if rec.get("kernel") != kernel or rec.get("source_sha256") != kernel_source_hash():
+    if rec.get("kernel") != kernel or rec.get("source_sha256") != kernel_source_hash(kernel):
         return None
     return float(rec["bytes_per_launch"])
 
@@ -166,6 +179,69 @@ def cpu_baseline(cfg, budget_s):
                       f"{len(times)} run(s), {med:.2f} s each; TFLOP/s over the sample's own algorithmic flops"}
 
 
+def standalone_gemms(cfg, reps: int = 10) -> list:
+    """Every GEMM of one (layer, micro-batch) unit of the workload launched
+    alone through the op-level C ABI (same kernels, layouts, epilogues and
+    tile choices as in the stage), each timed with HIP events over `reps`
+    launches on an otherwise idle GPU: the kernels' stand-alone rates beside
+    their in-stage rates."""
+    import torch
+    from paper_2503_03182_amd import tpstage as T
+    Tk, h, f = cfg.tokens, cfg.hidden, cfg.mlp
+    nn = lambda K: K >= 12288   # the stage's layout choice for long contractions
+    td = torch.bfloat16
+    dev = "cuda"
+
+    def t(r, c):
+        return (torch.randn(r, c, device=dev) * 0.05).to(td)
+
+    shapes = [
+        ("QKV forward", T.GEMM_NT, T.EPI_BIAS, Tk, 3 * h, h),
+        ("out-proj forward", T.GEMM_NT, T.EPI_BIAS_RESID, Tk, h, h),
+        ("FC1 forward (GeLU)", T.GEMM_NT, T.EPI_BIAS_GELU, Tk, f, h),
+        ("FC2 forward", T.GEMM_NN if (nn(f) and cfg.weights == T.W_RESIDENT) else T.GEMM_NT, T.EPI_BIAS_RESID,
+         Tk, h, f),
+        ("dgelu input grad (FC2)", T.GEMM_NN if nn(h) else T.GEMM_NT, T.EPI_GELU_GRAD, Tk, f, h),
+        ("FC1 input grad", T.GEMM_NN if nn(f) else T.GEMM_NT, T.EPI_STORE, Tk, h, f),
+        ("out-proj input grad", T.GEMM_NN if nn(h) else T.GEMM_NT, T.EPI_STORE, Tk, h, h),
+        ("QKV input grad", T.GEMM_NN if nn(3 * h) else T.GEMM_NT, T.EPI_STORE, Tk, h, 3 * h),
+        ("W2 weight grad", T.GEMM_TN, T.EPI_ACC_F32, h, f, Tk),
+        ("W1 weight grad", T.GEMM_TN, T.EPI_ACC_F32, f, h, Tk),
+        ("Wo weight grad", T.GEMM_TN, T.EPI_ACC_F32, h, h, Tk),
+        ("Wqkv weight grad", T.GEMM_TN, T.EPI_ACC_F32, 3 * h, h, Tk),
+    ]
+    out = []
+    for name, layout, epi, M, N, K in shapes:
+        a = t(K, M) if layout == T.GEMM_TN else t(M, K)
+        b = t(N, K) if layout == T.GEMM_NT else t(K, N)
+        lda = M if layout == T.GEMM_TN else K
+        ldb = K if layout == T.GEMM_NT else N
+        c = torch.zeros(M, N, device=dev, dtype=torch.float32 if epi == T.EPI_ACC_F32 else td)
+        bias = t(1, N).reshape(-1) if epi in (T.EPI_BIAS, T.EPI_BIAS_RESID, T.EPI_BIAS_GELU) else None
+        resid = t(M, N) if epi == T.EPI_BIAS_RESID else None
+        aux = t(M, N) if epi in (T.EPI_BIAS_GELU, T.EPI_GELU_GRAD) else None
+        s = torch.cuda.current_stream()
+
+        def launch():
+            T.op_gemm(T.TPS_BF16, layout, epi, M, N, K, a, lda, b, ldb, c, N, bias=bias, resid=resid,
+                      ldr=N if resid is not None else 0, aux=aux, ldaux=N if aux is not None else 0, stream=s)
+        launch()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            launch()
+        e1.record(s)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        fl = 2.0 * M * N * K
+        out.append({"gemm": name, "layout": ["NT", "NN", "TN"][layout], "M": M, "N": N, "K": K,
+                    "us": round(us, 1), "tflops": round(fl / (us * 1e-6) / 1e12, 1),
+                    "frac_bf16_peak": round(fl / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)})
+        del a, b, c, bias, resid, aux
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -177,7 +253,15 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 512 MiB device-to-device copy (reference for HBM byte counters)")
+    ap.add_argument("--standalone-gemms", action="store_true",
+                    help="time every GEMM of one (layer, micro-batch) unit of the workload alone and exit")
     args = ap.parse_args()
+    if args.standalone_gemms:
+        import torch
+        from paper_2503_03182_amd import configs
+        cfg = configs.WORKLOADS[args.workload]()
+        print(json.dumps({"workload": args.workload, "standalone_gemms": standalone_gemms(cfg)}), flush=True)
+        return
     if args.copy_calibration:
         import torch
         n = 512 << 20

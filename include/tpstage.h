@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TPS_ABI_VERSION 1
+#define TPS_ABI_VERSION 2
 #define TPS_MAX_MICRO 64
 
 /* return codes */
@@ -89,6 +89,12 @@ enum { TPS_W_RESIDENT = 0, TPS_W_STREAM = 1 };
  * (layer-grouped); SEGMENT replays every recomputed tensor of the stage for
  * the micro-batch before its backward starts (block-wise T-Recomp). */
 enum { TPS_GRAN_LAYER = 0, TPS_GRAN_SEGMENT = 1 };
+
+/* format of the streamed parameter blocks in host memory (T-Offload's
+ * weight reload): the storage dtype, or FP8 E4M3 codes with one f32 scale per
+ * matrix row (the four weight matrices; vectors stay in the storage dtype),
+ * expanded on the device to the storage dtype as bf16(decode(q) * scale). */
+enum { TPS_Q_NONE = 0, TPS_Q_FP8_ROW = 1 };
 
 /* op kinds in the planned order (TPS_OP_R: a recompute task of the T-Pipe
  * schedule, reported by tps_tpipe_schedule; a stage runs the recompute of a
@@ -133,6 +139,10 @@ typedef struct tps_config {
   float tflops_hint;            /* sustained TFLOP/s for victim choice          */
   int32_t lookahead;            /* prefetch an offloaded mb this many ops before
                                    its backward (>= 1)                          */
+  int32_t weights_quant;        /* TPS_Q_NONE, or TPS_Q_FP8_ROW (streamed bf16
+                                   weights only): the host parameter blocks are
+                                   in the quantized layout of
+                                   tps_param_layout_q                           */
 } tps_config;
 
 typedef struct tps_plan_info {
@@ -230,6 +240,14 @@ typedef struct tps_stage tps_stage;
 int tps_param_layout(const tps_config* cfg, uint64_t param_offsets[TPS_P_COUNT],
                      uint64_t* param_bytes, uint64_t grad_offsets[TPS_P_COUNT],
                      uint64_t* grad_bytes);
+
+/* Layout of one layer's quantized host parameter block (TPS_Q_FP8_ROW):
+ * byte offsets of the TPS_P_COUNT tensors (uint8 E4M3 codes [rows][cols] for
+ * W_qkv, W_o, W_1, W_2; storage dtype for the vectors) and of the f32 row
+ * scales of the four matrices (in the order W_qkv, W_o, W_1, W_2), each
+ * 256-byte aligned, and the block size. */
+int tps_param_layout_q(const tps_config* cfg, uint64_t offsets[TPS_P_COUNT], uint64_t scale_offsets[4],
+                       uint64_t* bytes);
 
 /* Host only, no GPU needed.  Validates the config, resolves the op order and
  * the policy closure, assigns checkpoint slots over the order, lays out the
@@ -364,6 +382,52 @@ typedef struct tps_tpipe_result {
  * the backward that follows them).  TPS_EINVAL for out-of-range arguments. */
 int tps_tpipe_schedule(const tps_tpipe_config* cfg, int32_t stage, tps_tpipe_task* tasks,
                        int32_t max_tasks, int32_t* n_tasks, tps_tpipe_result* out);
+
+/* AdamW hyper-parameters of the host optimizer update. */
+typedef struct tps_adamw {
+  float lr;                     /* learning rate (>= 0)                         */
+  float beta1, beta2;           /* moment decay rates in [0, 1)                 */
+  float eps;                    /* added to sqrt of the second moment (>= 0)    */
+  float weight_decay;           /* decoupled weight decay (>= 0)                */
+} tps_adamw;
+
+/* T-Offload's host-side model-state update of one layer (paper, Section 5:
+ * gradients offloaded after the layer's last backward, optimizer update on
+ * the CPU, weights reloaded in quantized form).  All arrays are host memory:
+ * master, m, v and grad are f32 in the layout of the layer's gradient block
+ * (tps_param_layout's gradient offsets).  With step >= 1 one AdamW step is
+ * applied in place to master, m and v:
+ *   m = b1 m + (1 - b1) g,  v = b2 v + (1 - b2) g^2,
+ *   w = w - lr (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps) - lr wd w;
+ * with step == 0 nothing is updated (m, v, grad and opt may be NULL).  Then
+ * params_out receives the layer's parameter block as the device will load
+ * it: quant == TPS_Q_NONE in the storage dtype (tps_param_layout, bf16
+ * rounded to nearest even), TPS_Q_FP8_ROW in the quantized layout of
+ * tps_param_layout_q (matrix rows as E4M3 codes of w / scale with
+ * scale = max|row| / 448 in f32, nearest code, ties to an even mantissa,
+ * saturating at 448; vectors in bf16).  Runs on n_threads host threads
+ * (0: one per hardware thread) and returns when done.  TPS_EINVAL for bad
+ * arguments. */
+int tps_host_adamw_layer(const tps_config* cfg, const tps_adamw* opt, int32_t step, float* master, float* m,
+                         float* v, const float* grad, void* params_out, int32_t quant, int32_t n_threads);
+
+/* Turns on the model-state half of T-Offload for a stage with streamed
+ * weights (paper, Section 5): in every iteration, once all backwards have
+ * passed layer l, its f32 gradient block goes to the host and a host thread
+ * of the stage applies one AdamW step (tps_host_adamw_layer semantics, step
+ * numbers first_step, first_step + 1, ... per layer, n_threads threads) to
+ * the layer's master weights and moments and rewrites the layer's pinned
+ * parameter block (storage dtype, or the quantized layout when the config
+ * has weights_quant); the update overlaps the backward of the layers below,
+ * and the layer's next load waits for it.  master, m, v: [n_layers] pinned or
+ * pageable host f32 blocks in the gradient-block layout (master initialised
+ * to the weights, m and v to zero), owned by the caller and not touched by
+ * the caller while updates may run (until tps_stage_sync returns, which also
+ * waits for the updates and reports their errors).  Call between iterations;
+ * iterations should start with zero_grads set.  TPS_EINVAL without streamed
+ * weights or with bad arguments, TPS_ESTATE if already set. */
+int tps_stage_set_optimizer(tps_stage* st, const tps_adamw* opt, float* const* master, float* const* m,
+                            float* const* v, int32_t first_step, int32_t n_threads);
 
 /* Thread-local message of the last failing call ("" if none). */
 const char* tps_last_error(void);

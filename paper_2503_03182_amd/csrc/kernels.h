@@ -108,6 +108,10 @@ hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_
                                   hipStream_t st, int overwrite = 0);
 hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st);
 hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st);
+// out (bf16) [rows][cols] = bf16(decode_e4m3(q[r][c]) * scale[r]); cols % 8 == 0,
+// q 8-byte and out 16-byte aligned
+hipError_t dequant_fp8_rows_launch(const void* q, const float* scale, int64_t rows, int64_t cols, void* out,
+                                   hipStream_t st);
 // out[c][r] = in[r][c] for in [rows, cols]; rows and cols multiples of 8
 hipError_t transpose_launch(int dtype, int rows, int cols, const void* in, int64_t ldi, void* out, int64_t ldo,
                             hipStream_t st);

@@ -278,6 +278,10 @@ int make_plan(const tps_config* c, Plan* out) {
   if (p.granularity != TPS_GRAN_LAYER && p.granularity != TPS_GRAN_SEGMENT) return inval("recompute_granularity");
   p.lookahead = c->lookahead;
   if (p.lookahead < 1) return inval("lookahead must be >= 1");
+  p.quant = c->weights_quant;
+  if (p.quant != TPS_Q_NONE && p.quant != TPS_Q_FP8_ROW) return inval("weights_quant");
+  if (p.quant == TPS_Q_FP8_ROW && (p.weights != TPS_W_STREAM || p.dtype != TPS_BF16))
+    return inval("quantized weight reload needs streamed bf16 weights");
 
   // policy
   p.policy.assign((size_t)p.L * TPS_T_COUNT, TPS_KEEP);
@@ -312,6 +316,21 @@ int make_plan(const tps_config* c, Plan* out) {
       p.goff[i] = go; go = align256(go + elems[i] * 4);
     }
     p.pbytes = po; p.gbytes = go;
+    // quantized block: matrices as one byte per element, their f32 row
+    // scales after the vectors
+    const bool is_mat[TPS_P_COUNT] = {true, false, true, false, true, false, true, false, false, false, false, false};
+    const uint64_t rows[4] = {3 * h, h, f, h};
+    uint64_t qo = 0;
+    for (int i = 0; i < TPS_P_COUNT; ++i) {
+      p.qoff[i] = qo;
+      qo = align256(qo + elems[i] * (is_mat[i] ? 1 : es));
+    }
+    for (int k = 0; k < 4; ++k) {
+      p.qsoff[k] = qo;
+      qo = align256(qo + rows[k] * 4);
+    }
+    p.qbytes = qo;
+    p.hpbytes = p.quant == TPS_Q_FP8_ROW ? p.qbytes : p.pbytes;
   }
 
   // layouts: checkpoint slot, host slot, replay buffer
@@ -440,7 +459,11 @@ int make_plan(const tps_config* c, Plan* out) {
     p.bpart_bytes = align256((uint64_t)p.bpart_segs * p.bpc[Plan::BP_COUNT] * 4);
   }
 
-  p.wwin_bytes = p.weights == TPS_W_STREAM ? (uint64_t)p.window * (p.pbytes + p.gbytes) : 0;
+  // streamed window entry: parameter block, f32 gradient block, and with a
+  // quantized reload the staging area its codes land in
+  p.wwin_bytes = p.weights == TPS_W_STREAM
+                     ? (uint64_t)p.window * (p.pbytes + p.gbytes + (p.quant ? align256(p.qbytes) : 0))
+                     : 0;
   {
     const uint64_t mats[4] = {3 * h * h, h * h, f * h, h * f};
     uint64_t o = 0;
@@ -467,7 +490,7 @@ int make_plan(const tps_config* c, Plan* out) {
   p.h2d_bytes = (uint64_t)n_off * p.oslot_bytes;
   p.d2h_bytes = (uint64_t)n_off * p.oslot_bytes;
   if (p.weights == TPS_W_STREAM) {
-    p.h2d_bytes += 2ull * p.L * p.pbytes;
+    p.h2d_bytes += 2ull * p.L * p.hpbytes;
     p.d2h_bytes += (uint64_t)p.L * p.gbytes;
   }
   uint64_t per_mb_all = 0;
@@ -517,6 +540,20 @@ extern "C" int tps_plan(const tps_config* cfg, tps_plan_info* out) {
   const int rc = tps::make_plan(cfg, &p);
   if (rc) return rc;
   tps::fill_plan_info(p, out);
+  return TPS_OK;
+}
+
+extern "C" int tps_param_layout_q(const tps_config* cfg, uint64_t offsets[TPS_P_COUNT], uint64_t scale_offsets[4],
+                                  uint64_t* bytes) {
+  tps::clear_error();
+  tps::Plan p;
+  const int rc = tps::make_plan(cfg, &p);
+  if (rc) return rc;
+  for (int i = 0; i < TPS_P_COUNT; ++i)
+    if (offsets) offsets[i] = p.qoff[i];
+  for (int k = 0; k < 4; ++k)
+    if (scale_offsets) scale_offsets[k] = p.qsoff[k];
+  if (bytes) *bytes = p.qbytes;
   return TPS_OK;
 }
 

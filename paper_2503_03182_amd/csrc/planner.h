@@ -32,6 +32,11 @@ struct Plan {
   uint64_t tbytes[TPS_T_COUNT] = {};  // bytes of each tensor of one (layer, mb)
   uint64_t poff[TPS_P_COUNT] = {}, pbytes = 0;   // packed parameter block
   uint64_t goff[TPS_P_COUNT] = {}, gbytes = 0;   // packed f32 gradient block
+  // quantized host parameter block (weights_quant == TPS_Q_FP8_ROW): codes or
+  // storage-dtype vectors at qoff, f32 row scales of the four matrices at qsoff
+  int quant = TPS_Q_NONE;
+  uint64_t qoff[TPS_P_COUNT] = {}, qsoff[4] = {}, qbytes = 0;
+  uint64_t hpbytes = 0;   // bytes of one host parameter block (pbytes or qbytes)
 
   // Checkpoint slots of one micro-batch, in two parts:
   //  - resident part: KEEP tensors of every layer, held from F(mb) to B(mb);
@@ -119,5 +124,10 @@ int make_plan(const tps_config* cfg, Plan* out);
 double op_flops(const Plan& p, int op);
 
 void fill_plan_info(const Plan& p, tps_plan_info* info);
+
+// One host AdamW step of a layer and its parameter block for the device
+// (tps_host_adamw_layer, on an existing plan).
+int host_adamw(const Plan& p, const tps_adamw* opt, int32_t step, float* master, float* m, float* v,
+               const float* grad, void* params_out, int32_t quant, int32_t n_threads);
 
 }  // namespace tps

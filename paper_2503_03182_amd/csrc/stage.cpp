@@ -18,8 +18,11 @@
 #include <hip/hip_ext.h>
 
 #include <chrono>
+#include <condition_variable>
 #include <cstring>
+#include <deque>
 #include <map>
+#include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
@@ -58,6 +61,24 @@ hipError_t queue_stream(int device, hipStream_t* s) {
   if (e != hipSuccess) return e;
   std::vector<uint32_t> mask((size_t)(ncu + 31) / 32, 0xFFFFFFFFu);
   return hipExtStreamCreateWithCUMask(s, (uint32_t)mask.size(), mask.data());
+}
+
+// Device-to-host copy issued as a pitched (2D) copy of 4 MiB rows plus one
+// row for the remainder.  With the framework's runtime initialised first, a
+// plain device-to-host copy runs as a copy kernel on every CU for its whole
+// duration (tens of milliseconds per gradient block, beside the GEMMs); the
+// pitched form runs on the copy engines.
+hipError_t d2h_async(void* dst, const void* src, size_t bytes, hipStream_t s) {
+  constexpr size_t W = size_t(4) << 20;
+  const size_t rows = bytes / W, tail = bytes - rows * W;
+  if (rows) {
+    const hipError_t e = hipMemcpy2DAsync(dst, W, src, W, W, rows, hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return e;
+  }
+  if (tail)
+    return hipMemcpy2DAsync(static_cast<char*>(dst) + rows * W, tail, static_cast<const char*>(src) + rows * W, tail,
+                            tail, 1, hipMemcpyDeviceToHost, s);
+  return hipSuccess;
 }
 
 // Products with a long contraction take the weight operand in its [K][N]
@@ -135,6 +156,31 @@ struct tps_stage {
   std::vector<char> grads_touched;  // [L] this iteration
   uint64_t tick = 0;
 
+  // T-Offload of model state: the host optimizer update of each layer, run
+  // by a worker thread once the layer's final gradients of the iteration are
+  // on the host; the layer's next load waits for it
+  struct HostOpt {
+    bool on = false;
+    tps_adamw hp{};
+    int threads = 0;
+    std::vector<float*> master, m, v;
+    std::vector<int> step;           // step number of the layer's next update
+    std::vector<int> bpass;          // layer backwards this iteration
+    std::vector<hipEvent_t> final_ev;   // final gradient flush of the layer (copy stream)
+    std::vector<char> pending;       // update queued or running
+    std::deque<int> queue;
+    std::mutex mu;
+    std::condition_variable cv;
+    std::thread worker;
+    bool stop = false;
+    int rc = TPS_OK;
+    std::string err;
+  } hopt;
+  int opt_after_backward(int l, int passes);
+  int wait_layer_update(int l);
+  int wait_all_updates();
+  void opt_worker();
+
   // kernel timing (measurement only)
   struct TimedLaunch {
     std::string name;
@@ -187,6 +233,9 @@ struct tps_stage {
   // --- parameters (resident or streamed window) ------------------------------
   const char* params_of(int l, int* entry);
   float* grads_of(int l, int entry);
+  uint64_t entry_bytes() const { return p.pbytes + p.gbytes + (p.quant ? ((p.qbytes + 255) & ~uint64_t(255)) : 0); }
+  char* qstage_of(int entry);
+  int load_params(int l, int entry);
   char* wt_of(int l, int entry) const {
     return arena + p.off_wt + (uint64_t)(p.weights == TPS_W_STREAM ? entry : l) * p.wt_bytes;
   }
@@ -260,12 +309,48 @@ struct tps_stage {
 // ---------------------------------------------------------------------------
 const char* tps_stage::params_of(int l, int* entry) {
   if (p.weights == TPS_W_RESIDENT) return lp[l];
-  return arena + p.off_wwin + (uint64_t)(*entry) * (p.pbytes + p.gbytes);
+  return arena + p.off_wwin + (uint64_t)(*entry) * entry_bytes();
 }
 
 float* tps_stage::grads_of(int l, int entry) {
   if (p.weights == TPS_W_RESIDENT) return lg[l];
-  return reinterpret_cast<float*>(arena + p.off_wwin + (uint64_t)entry * (p.pbytes + p.gbytes) + p.pbytes);
+  return reinterpret_cast<float*>(arena + p.off_wwin + (uint64_t)entry * entry_bytes() + p.pbytes);
+}
+
+// Staging area of a window entry for a quantized parameter block.
+char* tps_stage::qstage_of(int entry) {
+  return arena + p.off_wwin + (uint64_t)entry * entry_bytes() + p.pbytes + p.gbytes;
+}
+
+// Brings layer l's parameter block from its host block into window entry e on
+// the prefetch stream: a plain copy, or the quantized block into the entry's
+// staging area followed by its expansion to the storage dtype (matrices from
+// E4M3 codes and row scales, vectors copied as they are).
+int tps_stage::load_params(int l, int e) {
+  int ent = e;
+  char* dst = const_cast<char*>(params_of(l, &ent));
+  if (p.quant != TPS_Q_FP8_ROW) {
+    TPS_HIP(hipMemcpyAsync(dst, lp[l], p.pbytes, hipMemcpyHostToDevice, ps));
+    stats.h2d_bytes += p.pbytes;
+    return TPS_OK;
+  }
+  char* q = qstage_of(e);
+  TPS_HIP(hipMemcpyAsync(q, lp[l], p.qbytes, hipMemcpyHostToDevice, ps));
+  stats.h2d_bytes += p.qbytes;
+  const int64_t h = p.h, f = p.f;
+  const int mats[4] = {TPS_P_W_QKV, TPS_P_W_O, TPS_P_W_1, TPS_P_W_2};
+  const int64_t rows[4] = {3 * h, h, f, h}, cols[4] = {h, h, h, f};
+  for (int k = 0; k < 4; ++k) {
+    TPS_HIP(dequant_fp8_rows_launch(q + p.qoff[mats[k]], reinterpret_cast<const float*>(q + p.qsoff[k]), rows[k],
+                                    cols[k], dst + p.poff[mats[k]], ps));
+    ++stats.kernels;
+  }
+  const int vecs[8] = {TPS_P_B_QKV, TPS_P_B_O, TPS_P_B_1, TPS_P_B_2, TPS_P_G1, TPS_P_BE1, TPS_P_G2, TPS_P_BE2};
+  const int64_t len[8] = {3 * h, h, f, h, h, h, h, h};
+  for (int k = 0; k < 8; ++k)
+    TPS_HIP(hipMemcpyAsync(dst + p.poff[vecs[k]], q + p.qoff[vecs[k]], (size_t)len[k] * p.esize,
+                           hipMemcpyDeviceToDevice, ps));
+  return TPS_OK;
 }
 
 // Transposed copies of the four weight matrices (operands of the input-
@@ -304,7 +389,7 @@ int tps_stage::flush_grads(int e) {
   if (w.layer < 0 || !w.grads_live) return TPS_OK;
   TPS_HIP(hipEventRecord(ev_tmp, cs));
   TPS_HIP(hipStreamWaitEvent(xs, ev_tmp, 0));
-  TPS_HIP(hipMemcpyAsync(lg[w.layer], grads_of(w.layer, e), p.gbytes, hipMemcpyDeviceToHost, xs));
+  TPS_HIP(d2h_async(lg[w.layer], grads_of(w.layer, e), p.gbytes, xs));
   stats.d2h_bytes += p.gbytes;
   TPS_HIP(hipEventRecord(w.grads_out.ev, xs));
   w.grads_out.valid = true;
@@ -336,9 +421,8 @@ int tps_stage::prefetch_layer(int l) {
   w.layer = l;
   w.tick = ++tick;
   w.wt_valid = false;
-  int e = victim;
-  TPS_HIP(hipMemcpyAsync(const_cast<char*>(params_of(l, &e)), lp[l], p.pbytes, hipMemcpyHostToDevice, ps));
-  stats.h2d_bytes += p.pbytes;
+  TPS_TRY(wait_layer_update(l));
+  TPS_TRY(load_params(l, victim));
   TPS_HIP(hipEventRecord(w.param_ready.ev, ps));
   w.param_ready.valid = true;
   w.grads_live = false;
@@ -369,6 +453,84 @@ int tps_stage::invalidate_window() {
     w.tick = 0;
   }
   return TPS_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Host optimizer (T-Offload of model state, Section 5): once every backward
+// of the iteration has passed layer l, its gradient block is flushed to the
+// host and a worker thread, after that copy has completed, applies one AdamW
+// step to the layer's f32 master weights and moments and rewrites the pinned
+// parameter block the next iteration loads (storage dtype or quantized).
+// ---------------------------------------------------------------------------
+int tps_stage::opt_after_backward(int l, int passes) {
+  if (!hopt.on) return TPS_OK;
+  hopt.bpass[l] += passes;
+  if (hopt.bpass[l] < p.M) return TPS_OK;
+  for (size_t e = 0; e < win.size(); ++e)
+    if (win[e].layer == l) TPS_TRY(flush_grads((int)e));
+  TPS_HIP(hipEventRecord(hopt.final_ev[l], xs));
+  {
+    std::lock_guard<std::mutex> lock(hopt.mu);
+    hopt.pending[l] = 1;
+    hopt.queue.push_back(l);
+  }
+  hopt.cv.notify_all();
+  return TPS_OK;
+}
+
+int tps_stage::wait_layer_update(int l) {
+  if (!hopt.on) return TPS_OK;
+  std::unique_lock<std::mutex> lock(hopt.mu);
+  hopt.cv.wait(lock, [&] { return !hopt.pending[l]; });
+  if (hopt.rc != TPS_OK) return set_error(hopt.rc, "host optimizer: " + hopt.err);
+  return TPS_OK;
+}
+
+int tps_stage::wait_all_updates() {
+  if (!hopt.on) return TPS_OK;
+  std::unique_lock<std::mutex> lock(hopt.mu);
+  hopt.cv.wait(lock, [&] {
+    for (char c : hopt.pending)
+      if (c) return false;
+    return true;
+  });
+  if (hopt.rc != TPS_OK) return set_error(hopt.rc, "host optimizer: " + hopt.err);
+  return TPS_OK;
+}
+
+void tps_stage::opt_worker() {
+  (void)hipSetDevice(device);
+  for (;;) {
+    int l;
+    {
+      std::unique_lock<std::mutex> lock(hopt.mu);
+      hopt.cv.wait(lock, [&] { return hopt.stop || !hopt.queue.empty(); });
+      if (hopt.queue.empty()) return;
+      l = hopt.queue.front();
+      hopt.queue.pop_front();
+    }
+    int rc = TPS_OK;
+    std::string err;
+    const hipError_t he = hipEventSynchronize(hopt.final_ev[l]);
+    if (he != hipSuccess) {
+      rc = TPS_EHIP;
+      err = std::string("waiting for the gradients of layer ") + std::to_string(l) + ": " + hipGetErrorString(he);
+    } else {
+      rc = host_adamw(p, &hopt.hp, hopt.step[l], hopt.master[l], hopt.m[l], hopt.v[l], lg[l], lp[l], p.quant,
+                      hopt.threads);
+      if (rc != TPS_OK) err = last_error();
+    }
+    {
+      std::lock_guard<std::mutex> lock(hopt.mu);
+      ++hopt.step[l];
+      hopt.pending[l] = 0;
+      if (rc != TPS_OK && hopt.rc == TPS_OK) {
+        hopt.rc = rc;
+        hopt.err = err;
+      }
+    }
+    hopt.cv.notify_all();
+  }
 }
 
 int tps_stage::ensure_layer(int l, bool for_backward, int* entry) {
@@ -666,8 +828,7 @@ int tps_stage::d2h_layer(int l, int mb) {
   for (int t = 0; t < TPS_T_COUNT; ++t) {
     const size_t k = (size_t)l * TPS_T_COUNT + t;
     if (p.oslot_off[k] == kNone) continue;
-    TPS_HIP(hipMemcpyAsync(host_base(mb) + p.oslot_off[k], oslot_base(p.oslot_f[mb]) + p.oslot_off[k], p.tbytes[t],
-                           hipMemcpyDeviceToHost, xs));
+    TPS_HIP(d2h_async(host_base(mb) + p.oslot_off[k], oslot_base(p.oslot_f[mb]) + p.oslot_off[k], p.tbytes[t], xs));
     stats.d2h_bytes += p.tbytes[t];
   }
   TPS_HIP(hipEventRecord(offloaded_ev[mb].ev, xs));
@@ -824,6 +985,7 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
     TPS_TRY(bwd_layer(l, mb, W, wt_of(l, e), grads_of(l, e), cur, out, defer ? (bstep & 1) : 0, defer));
     ++bstep;
     TPS_TRY(touch(e));
+    TPS_TRY(opt_after_backward(l, 1));
     cur = out;
   }
   // Pending now: the parameter-gradient kernels of the last two layer
@@ -953,6 +1115,7 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
   std::fill(st->prefetched.begin(), st->prefetched.end(), 0);
   st->stats = tps_stats{};
   const Plan& p = st->p;
+  std::fill(st->hopt.bpass.begin(), st->hopt.bpass.end(), 0);
   // an iteration cut short may leave parameter-gradient kernels pending
   TPS_TRY(st->join_if_pending());
   st->bstep = 0;
@@ -1133,6 +1296,7 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
       TPS_HIP(hipMemcpyAsync(dx[i], gA, p.tbytes[TPS_T_X], hipMemcpyDeviceToDevice, st->cs));
     }
     TPS_TRY(st->touch(e));
+    TPS_TRY(st->opt_after_backward(l, n));
   }
   for (int i = 0; i < n; ++i) {
     const int mb = mb0 + i;
@@ -1153,6 +1317,37 @@ extern "C" int tps_stage_sync(tps_stage* st) {
   if (st->ps && st->ps != st->xs) TPS_HIP(hipStreamSynchronize(st->ps));
   if (st->gs) TPS_HIP(hipStreamSynchronize(st->gs));
   if (st->rs) TPS_HIP(hipStreamSynchronize(st->rs));
+  return st->wait_all_updates();
+}
+
+extern "C" int tps_stage_set_optimizer(tps_stage* st, const tps_adamw* opt, float* const* master, float* const* m,
+                                       float* const* v, int32_t first_step, int32_t n_threads) {
+  clear_error();
+  if (!st || !opt || !master || !m || !v) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: null argument");
+  const Plan& p = st->p;
+  if (p.weights != TPS_W_STREAM) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: needs streamed weights");
+  if (st->hopt.on) return set_error(TPS_ESTATE, "tps_stage_set_optimizer: already set");
+  if (st->in_iteration && st->cursor != 0 && st->cursor < (int)p.op_kind.size())
+    return set_error(TPS_ESTATE, "tps_stage_set_optimizer: inside an iteration");
+  if (first_step < 1) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: first_step must be >= 1");
+  if (!(opt->lr >= 0.f && opt->beta1 >= 0.f && opt->beta1 < 1.f && opt->beta2 >= 0.f && opt->beta2 < 1.f &&
+        opt->eps >= 0.f && opt->weight_decay >= 0.f))
+    return set_error(TPS_EINVAL, "tps_stage_set_optimizer: hyper-parameters out of range");
+  for (int l = 0; l < p.L; ++l)
+    if (!master[l] || !m[l] || !v[l]) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: null layer block");
+  auto& h = st->hopt;
+  h.hp = *opt;
+  h.threads = n_threads;
+  h.master.assign(master, master + p.L);
+  h.m.assign(m, m + p.L);
+  h.v.assign(v, v + p.L);
+  h.step.assign(p.L, first_step);
+  h.bpass.assign(p.L, 0);
+  h.pending.assign(p.L, 0);
+  h.final_ev.assign(p.L, nullptr);
+  for (auto& e : h.final_ev) TPS_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  h.on = true;
+  h.worker = std::thread([st] { st->opt_worker(); });
   return TPS_OK;
 }
 
@@ -1226,6 +1421,16 @@ extern "C" int tps_stage_kernel_times(tps_stage* st, tps_kernel_time* out, int m
 extern "C" int tps_stage_destroy(tps_stage* st) {
   clear_error();
   if (!st) return TPS_OK;
+  if (st->hopt.worker.joinable()) {
+    {
+      std::lock_guard<std::mutex> lock(st->hopt.mu);
+      st->hopt.stop = true;
+    }
+    st->hopt.cv.notify_all();
+    st->hopt.worker.join();
+  }
+  for (auto e : st->hopt.final_ev)
+    if (e) (void)hipEventDestroy(e);
   if (st->cs) (void)hipStreamSynchronize(st->cs);
   if (st->xs) (void)hipStreamSynchronize(st->xs);
   if (st->ps && st->ps != st->xs) (void)hipStreamSynchronize(st->ps);

@@ -15,13 +15,14 @@ from typing import Optional, Sequence
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpstage.so")
 
 # --- constants (mirror tpstage.h) ------------------------------------------
-TPS_ABI_VERSION = 1
+TPS_ABI_VERSION = 2
 TPS_OK, TPS_EINVAL, TPS_ENOMEM, TPS_EORDER, TPS_EHIP, TPS_ETIMEOUT, TPS_ESTATE = 0, -1, -2, -3, -4, -5, -6
 TPS_F32, TPS_BF16 = 0, 1
 KEEP, RECOMPUTE, OFFLOAD = 0, 1, 2
 TENSORS = ("x", "a", "qkv", "o", "lse", "x1", "c", "u", "g", "ln1", "ln2")
 T_INDEX = {n: i for i, n in enumerate(TENSORS)}
 W_RESIDENT, W_STREAM = 0, 1
+Q_NONE, Q_FP8_ROW = 0, 1
 GRAN_LAYER, GRAN_SEGMENT = 0, 1
 OP_F, OP_B, OP_R = 0, 1, 2
 PARAMS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "g1", "be1", "g2", "be2")
@@ -49,7 +50,7 @@ class Config(C.Structure):
         ("offload_auto", C.c_int32), ("weights", C.c_int32), ("window", C.c_int32),
         ("recompute_granularity", C.c_int32), ("n_ops", C.c_int32), ("ops", C.POINTER(C.c_int32)),
         ("inflight", C.c_int32), ("link_gbps_hint", C.c_float), ("tflops_hint", C.c_float),
-        ("lookahead", C.c_int32),
+        ("lookahead", C.c_int32), ("weights_quant", C.c_int32),
     ]
 
 
@@ -103,6 +104,11 @@ class TPipeResult(C.Structure):
                 ("max_stage_peak_blocks", C.c_int32), ("life_chunk1", C.c_int32), ("life_chunk2", C.c_int32)]
 
 
+class AdamW(C.Structure):
+    _fields_ = [("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float),
+                ("weight_decay", C.c_float)]
+
+
 class Stats(C.Structure):
     _fields_ = [("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("kernels", C.c_uint64),
                 ("replays", C.c_uint64), ("ops_done", C.c_int32)]
@@ -119,7 +125,7 @@ EXPORTED = (
     "tps_op_attention_fwd", "tps_op_attention_bwd", "tps_op_colsum", "tps_op_gelu",
     "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
     "tps_host_alloc", "tps_host_free", "tps_tpipe_schedule", "tps_op_attention_bwd_noalloc",
-    "tps_op_attention_bwd_noalloc_max_rows",
+    "tps_op_attention_bwd_noalloc_max_rows", "tps_param_layout_q", "tps_host_adamw_layer",
 )
 
 
@@ -165,6 +171,9 @@ def lib() -> C.CDLL:
         L.tps_op_workspace_bytes.restype = u64
         L.tps_host_alloc.argtypes = [u64, C.POINTER(vp)]
         L.tps_host_free.argtypes = [vp]
+        L.tps_param_layout_q.argtypes = [C.POINTER(Config), C.POINTER(C.c_uint64), C.POINTER(C.c_uint64),
+                                         C.POINTER(C.c_uint64)]
+        L.tps_host_adamw_layer.argtypes = [C.POINTER(Config), C.POINTER(AdamW), i32, vp, vp, vp, vp, vp, i32, i32]
         L.tps_tpipe_schedule.argtypes = [C.POINTER(TPipeConfig), i32, C.POINTER(TPipeTask), i32,
                                          C.POINTER(C.c_int32), C.POINTER(TPipeResult)]
         _lib = L
@@ -232,6 +241,7 @@ class StageConfig:
     link_gbps_hint: float = 50.0
     tflops_hint: float = 1000.0
     lookahead: int = 1
+    weights_quant: int = Q_NONE
     # drive the planned order with layer-major group calls (each run of
     # consecutive F (or B) tasks is one tps_stage_forward_group / _backward_group)
     layer_major: bool = False
@@ -285,6 +295,7 @@ class StageConfig:
         c.inflight = self.inflight
         c.link_gbps_hint, c.tflops_hint = self.link_gbps_hint, self.tflops_hint
         c.lookahead = self.lookahead
+        c.weights_quant = self.weights_quant
         return c
 
     def order(self) -> list:
@@ -317,6 +328,34 @@ def param_layout(cfg: StageConfig):
     c = cfg.to_c()
     check(lib().tps_param_layout(C.byref(c), po, C.byref(pb), go, C.byref(gb)))
     return list(po), pb.value, list(go), gb.value
+
+
+def param_layout_q(cfg: StageConfig):
+    """(offsets of the 12 tensors, offsets of the 4 matrices' row scales, bytes)
+    of one layer's quantized host parameter block."""
+    qo = (C.c_uint64 * len(PARAMS))()
+    so = (C.c_uint64 * 4)()
+    nb = C.c_uint64()
+    c = cfg.to_c()
+    check(lib().tps_param_layout_q(C.byref(c), qo, so, C.byref(nb)))
+    return list(qo), list(so), nb.value
+
+
+def host_adamw_layer(cfg: StageConfig, step: int, master, m, v, grad, params_out, quant: int = Q_NONE,
+                     lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0, n_threads: int = 0) -> None:
+    """tps_host_adamw_layer on host buffers (anything with data_ptr(), or
+    numpy arrays): one AdamW step of a layer (step >= 1; 0 = only write
+    params_out) and its parameter block for the device."""
+    def ptr(a):
+        if a is None:
+            return None
+        if hasattr(a, "data_ptr"):
+            return a.data_ptr()
+        return a.ctypes.data
+    opt = AdamW(lr, beta1, beta2, eps, weight_decay)
+    c = cfg.to_c()
+    check(lib().tps_host_adamw_layer(C.byref(c), C.byref(opt), step, ptr(master), ptr(m), ptr(v), ptr(grad),
+                                     ptr(params_out), quant, n_threads))
 
 
 # --- T-Pipe schedule -------------------------------------------------------------

@@ -170,6 +170,16 @@ hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st) {
   return hipSuccess;
 }
 
+hipError_t dequant_fp8_rows_launch(const void* q, const float* scale, int64_t rows, int64_t cols, void* out,
+                                   hipStream_t st) {
+  HbRanges rd, wr;
+  add1d(rd, q, rows * cols);
+  add1d(rd, scale, rows * 4);
+  add1d(wr, out, rows * cols * 2);
+  hb_op(st, "dequantize weights", rd, wr);
+  return hipSuccess;
+}
+
 hipError_t transpose_launch(int dtype, int rows, int cols, const void* in, int64_t ldi, void* out, int64_t ldo,
                             hipStream_t st) {
   const int64_t e = esz(dtype);

@@ -303,6 +303,19 @@ hipError_t hipMemcpyAsync(void* dst, const void* src, size_t bytes, hipMemcpyKin
   hb_op(s, name, HbRanges{{r, r + bytes}}, HbRanges{{d, d + bytes}});
   return hipSuccess;
 }
+hipError_t hipMemcpy2DAsync(void* dst, size_t dpitch, const void* src, size_t spitch, size_t width, size_t height,
+                            hipMemcpyKind kind, hipStream_t s) {
+  const char* name = kind == hipMemcpyDeviceToHost ? "pitched copy device->host"
+                     : kind == hipMemcpyHostToDevice ? "pitched copy host->device" : "pitched copy device->device";
+  HbRanges rd, wr;
+  const uint64_t d = reinterpret_cast<uint64_t>(dst), r = reinterpret_cast<uint64_t>(src);
+  for (size_t i = 0; i < height; ++i) {
+    rd.push_back({r + i * spitch, r + i * spitch + width});
+    wr.push_back({d + i * dpitch, d + i * dpitch + width});
+  }
+  hb_op(s, name, rd, wr);
+  return hipSuccess;
+}
 hipError_t hipHostMalloc(void** p, size_t bytes, unsigned) {
   *p = malloc(bytes ? bytes : 1);
   return *p ? hipSuccess : hipErrorInvalidValue;
