@@ -22,9 +22,9 @@ _lib = None
 
 def build() -> str:
     os.makedirs(os.path.dirname(OUT), exist_ok=True)
-    srcs = [os.path.join(CSRC, n) for n in ("stage.cpp", "planner.cpp", "errors.cpp")]
+    srcs = [os.path.join(CSRC, n) for n in ("stage.cpp", "planner.cpp", "errors.cpp", "host_optim.cpp")]
     srcs += [os.path.join(HERE, n) for n in ("hb_runtime.cpp", "hb_kernels.cpp")]
-    cmd = ["g++", "-std=c++17", "-O1", "-fPIC", "-shared", "-I", os.path.join(HERE, "fakeinc"), "-I", HERE,
+    cmd = ["g++", "-std=c++17", "-O1", "-fPIC", "-shared", "-pthread", "-I", os.path.join(HERE, "fakeinc"), "-I", HERE,
            "-I", os.path.join(ROOT, "include"), "-I", CSRC, *srcs, "-o", OUT + ".tmp"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode:

@@ -35,6 +35,7 @@ typedef enum hipDeviceAttribute_t { hipDeviceAttributeMultiprocessorCount = 1 } 
 #define hipStreamNonBlocking 0x1u
 
 hipError_t hipGetDevice(int* dev);
+hipError_t hipSetDevice(int dev);
 hipError_t hipDeviceGetAttribute(int* v, hipDeviceAttribute_t a, int dev);
 hipError_t hipEventCreate(hipEvent_t* e);
 hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned flags);

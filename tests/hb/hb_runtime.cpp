@@ -246,6 +246,7 @@ hipError_t hipGetDevice(int* dev) {
   *dev = 0;
   return hipSuccess;
 }
+hipError_t hipSetDevice(int) { return hipSuccess; }
 hipError_t hipDeviceGetAttribute(int* v, hipDeviceAttribute_t, int) {
   *v = 256;
   return hipSuccess;

@@ -85,6 +85,16 @@ def test_streamed_weights_race_free():
                     assert _run(cfg, iterations=3, group=group) == 0, (window, gran, inflight, group, D.report())
 
 
+def test_quantized_weight_reload_race_free():
+    """Streamed weights reloaded as FP8 codes with row scales: the staging area
+    of a window entry and its expansion into the entry's parameter block."""
+    for window in (2, 3):
+        cfg = _mid(n_layers=4, policy=W.policy_layer_inputs(4), granularity=T.GRAN_LAYER, weights=T.W_STREAM,
+                   window=window, weights_quant=T.Q_FP8_ROW)
+        for group in (False, True):
+            assert _run(cfg, iterations=3, group=group) == 0, (window, group, D.report())
+
+
 def test_mixed_per_microbatch_and_group_calls_race_free():
     keep_order = [("F", 0), ("F", 1), ("F", 2), ("B", 0), ("B", 1), ("B", 2)]
     assert _run(_mid(ops=keep_order), calls=[("F", [0, 1, 2], False), ("B", [0], False), ("B", [1, 2], True)]) == 0, \
