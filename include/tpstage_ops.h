@@ -102,6 +102,13 @@ int64_t tps_op_attention_bwd_noalloc_max_rows(void);
 int tps_op_colsum(int dtype, int rows, int cols, const void* x, int64_t ldx,
                   float* out, float* workspace, void* stream);
 
+/* Expansion of an FP8 E4M3 weight matrix with one f32 scale per row (the
+ * quantized weight reload of streamed layers, tpstage.h TPS_Q_FP8_ROW):
+ * out[r][c] = bf16(decode(q[r][c]) * scale[r]), f32 product rounded to
+ * nearest even.  q: rows * cols bytes (8-byte aligned), out: bf16 (16-byte
+ * aligned), cols a multiple of 8. */
+int tps_op_dequant_fp8_rows(int64_t rows, int64_t cols, const void* q, const float* scale, void* out, void* stream);
+
 /* g[i] = round(GeLU(u[i])) for n elements. */
 int tps_op_gelu(int dtype, int64_t n, const void* u, void* g, void* stream);
 

@@ -119,6 +119,16 @@ extern "C" int tps_op_gelu(int dtype, int64_t n, const void* u, void* g, void* s
   return check_hip(gelu_launch(dtype, n, u, g, (hipStream_t)stream), "gelu launch");
 }
 
+extern "C" int tps_op_dequant_fp8_rows(int64_t rows, int64_t cols, const void* q, const float* scale, void* out,
+                                       void* stream) {
+  clear_error();
+  if (rows < 0 || cols <= 0 || cols % 8) return bad("dequant: cols must be a positive multiple of 8");
+  if (rows == 0) return TPS_OK;
+  if (!q || !scale || !out) return bad("dequant: null pointer");
+  if ((reinterpret_cast<uintptr_t>(q) & 7u) || !aligned16(out)) return bad("dequant: alignment");
+  return check_hip(dequant_fp8_rows_launch(q, scale, rows, cols, out, (hipStream_t)stream), "dequant launch");
+}
+
 extern "C" uint64_t tps_op_workspace_bytes(int kind, int64_t rows, int64_t cols) {
   if (kind == TPS_WS_COLSUM) return colsum_ws_bytes(rows, cols);
   if (kind == TPS_WS_ATTN_BWD) return (uint64_t)(rows * cols * 4);  // rows = b*s, cols = heads

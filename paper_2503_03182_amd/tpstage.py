@@ -126,7 +126,7 @@ EXPORTED = (
     "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
     "tps_host_alloc", "tps_host_free", "tps_tpipe_schedule", "tps_op_attention_bwd_noalloc",
     "tps_op_attention_bwd_noalloc_max_rows", "tps_param_layout_q", "tps_host_adamw_layer",
-    "tps_stage_set_optimizer",
+    "tps_stage_set_optimizer", "tps_op_dequant_fp8_rows",
 )
 
 
@@ -166,6 +166,7 @@ def lib() -> C.CDLL:
         L.tps_op_attention_bwd_noalloc.argtypes = [i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
         L.tps_op_attention_bwd_noalloc_max_rows.argtypes = []
         L.tps_op_attention_bwd_noalloc_max_rows.restype = i64
+        L.tps_op_dequant_fp8_rows.argtypes = [i64, i64, vp, vp, vp, vp]
         L.tps_op_colsum.argtypes = [i32, i32, i32, vp, i64, vp, vp, vp]
         L.tps_op_gelu.argtypes = [i32, i64, vp, vp, vp]
         L.tps_op_workspace_bytes.argtypes = [i32, i64, i64]
@@ -570,6 +571,10 @@ def op_attention_bwd(dtype, b, s, nh, d, qkv, o, lse, do, dqkv, ws, stream=None)
 def op_attention_bwd_noalloc(dtype, b, s, nh, d, qkv, o, lse, do, dqkv, stream=None):
     check(lib().tps_op_attention_bwd_noalloc(dtype, b, s, nh, d, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(do),
                                              _ptr(dqkv), _stream(stream)))
+
+
+def op_dequant_fp8_rows(rows, cols, q, scale, out, stream=None):
+    check(lib().tps_op_dequant_fp8_rows(rows, cols, _ptr(q), _ptr(scale), _ptr(out), _stream(stream)))
 
 
 def op_colsum(dtype, rows, cols, x, ldx, out, ws, stream=None):

@@ -1,0 +1,173 @@
+"""T-Offload of model state on the GPU, through the C ABI: quantized weight
+reload (FP8 E4M3 codes with row scales expanded on the device) and the host
+AdamW update of every streamed layer between iterations, against the
+oracle: the oracle runs the same iterations with its own float64 AdamW and
+the weights the device computes with (bf16 of the f32 master, or
+bf16(decode(q) * scale) of the oracle's quantization of it)."""
+import numpy as np
+import pytest
+
+from oracle import model_state as ms
+from paper_2503_03182_amd import configs as W
+from paper_2503_03182_amd import synth
+from paper_2503_03182_amd import tpstage as T
+from stage_harness import compare, drive_iteration, inputs, read_grads, results, run_oracle, to_dev, to_np
+
+pytestmark = pytest.mark.gpu
+BF16_TOL = 2e-2
+MATS = ("w_qkv", "w_o", "w_1", "w_2")
+# eps large against the gradients keeps the update linear in them, so the
+# bf16-level gradient differences of the two sides stay small in the update
+HP = dict(lr=0.05, beta1=0.9, beta2=0.95, eps=1.0, weight_decay=0.1)
+
+
+def test_dequant_kernel_bitexact():
+    import torch
+    rng = np.random.default_rng(3)
+    rows, cols = 300, 520
+    codes = rng.integers(0, 256, size=(rows, cols)).astype(np.uint8)
+    codes[(codes & 0x7F) == 0x7F] = 0x12          # no NaN codes
+    scale = (rng.random(rows).astype(np.float32) * 0.01 + 1e-4).astype(np.float32)
+    q = torch.from_numpy(codes).cuda()
+    s = torch.from_numpy(scale).cuda()
+    out = torch.empty(rows, cols, dtype=torch.bfloat16, device="cuda")
+    T.op_dequant_fp8_rows(rows, cols, q, s, out)
+    torch.cuda.synchronize()
+    ref = synth.round_to_storage(ms.dequantize_rows(codes, scale).astype(np.float32), "bf16")
+    got = out.float().cpu().numpy()
+    assert np.array_equal(got, ref)
+
+
+def _cfg(quant, **kw):
+    L = 3
+    base = dict(n_layers=L, hidden=512, n_heads=4, mlp=2048, seq=200, micro_batch=2, n_micro=3, dtype="bf16",
+                policy=W.policy_layer_inputs(L), granularity=T.GRAN_LAYER, weights=T.W_STREAM, window=2,
+                weights_quant=quant)
+    base.update(kw)
+    return T.StageConfig(**base)
+
+
+def _master_blocks(cfg):
+    """Per-layer f32 master blocks in the gradient layout from the synthetic
+    parameters."""
+    po, pb, go, gb = T.param_layout(cfg)
+    out = []
+    for l in range(cfg.n_layers):
+        vals = synth.layer_params(l, cfg.hidden, cfg.mlp, "f32")
+        blk = np.zeros(gb // 4, dtype=np.float32)
+        for i, n in enumerate(T.PARAMS):
+            v = vals[n].reshape(-1).astype(np.float32)
+            blk[go[i] // 4: go[i] // 4 + v.size] = v
+        out.append(blk)
+    return out
+
+
+def _unpack(cfg, blk):
+    po, pb, go, gb = T.param_layout(cfg)
+    shapes = synth.param_shapes(cfg.hidden, cfg.mlp)
+    return {n: blk[go[i] // 4: go[i] // 4 + int(np.prod(shapes[n]))].reshape(shapes[n]).astype(np.float64)
+            for i, n in enumerate(T.PARAMS)}
+
+
+def _device_weights(cfg, master32: dict) -> dict:
+    """The weights the device computes with, from f32 master values."""
+    out = {}
+    for n, w in master32.items():
+        w32 = np.asarray(w, dtype=np.float32)
+        if cfg.weights_quant == T.Q_FP8_ROW and n in MATS:
+            q, s = ms.quantize_rows(w32)
+            w32 = ms.dequantize_rows(q, s).astype(np.float32)
+        out[n] = synth.round_to_storage(w32, "bf16").astype(np.float64)
+    return out
+
+
+def _host_param_blocks(cfg, masters):
+    import torch
+    nbytes = T.param_layout_q(cfg)[2] if cfg.weights_quant == T.Q_FP8_ROW else T.param_layout(cfg)[1]
+    blocks = []
+    for mblk in masters:
+        hb = torch.zeros(nbytes, dtype=torch.uint8, pin_memory=True)
+        T.host_adamw_layer(cfg, 0, mblk, None, None, None, hb, quant=cfg.weights_quant)
+        blocks.append(hb)
+    return blocks
+
+
+@pytest.mark.parametrize("quant", [T.Q_NONE, T.Q_FP8_ROW])
+def test_reloaded_weights_match_oracle(quant):
+    import torch
+    for group in (False, True):
+        cfg = _cfg(quant)
+        masters = _master_blocks(cfg)
+        blocks = _host_param_blocks(cfg, masters)
+        gb = T.param_layout(cfg)[3]
+        grads = [torch.zeros(gb, dtype=torch.uint8, pin_memory=True) for _ in range(cfg.n_layers)]
+        xs, dys = inputs(cfg)
+        st = T.Stage(cfg, blocks, grads)
+        X = [to_dev(x, cfg.dtype) for x in xs]
+        DY = [to_dev(d, cfg.dtype) for d in dys]
+        Y = [torch.empty_like(x) for x in X]
+        DX = [torch.empty_like(x) for x in X]
+        drive_iteration(st, cfg, X, DY, Y, DX, group=group)
+        out = results(cfg, st, Y, DX, grads)
+        st.close()
+        ora_params = [_device_weights(cfg, {n: v.astype(np.float32) for n, v in _unpack(cfg, m).items()})
+                      for m in masters]
+        ref = run_oracle(cfg, xs, dys, ora_params=ora_params)
+        worst, bad = compare(out, ref, BF16_TOL)
+        assert not bad, (quant, group, bad)
+
+
+@pytest.mark.parametrize("quant", [T.Q_NONE, T.Q_FP8_ROW])
+@pytest.mark.parametrize("group", [False, True])
+def test_host_optimizer_iterations_match_oracle(quant, group):
+    """Two iterations with the stage's host AdamW between them: the second
+    iteration runs on the updated (and reloaded) weights and matches the
+    oracle's second iteration; the master weights after both updates match
+    the oracle's."""
+    import torch
+    cfg = _cfg(quant)
+    L = cfg.n_layers
+    masters = _master_blocks(cfg)
+    m0 = [np.zeros_like(b) for b in masters]
+    v0 = [np.zeros_like(b) for b in masters]
+    start = [_unpack(cfg, b) for b in masters]
+    blocks = _host_param_blocks(cfg, masters)
+    gb = T.param_layout(cfg)[3]
+    grads = [torch.zeros(gb, dtype=torch.uint8, pin_memory=True) for _ in range(L)]
+    xs, dys = inputs(cfg)
+    st = T.Stage(cfg, blocks, grads)
+    st.set_optimizer(masters, m0, v0, first_step=1, n_threads=4, **HP)
+    X = [to_dev(x, cfg.dtype) for x in xs]
+    DY = [to_dev(d, cfg.dtype) for d in dys]
+    Y = [torch.empty_like(x) for x in X]
+    DX = [torch.empty_like(x) for x in X]
+    drive_iteration(st, cfg, X, DY, Y, DX, group=group)
+    first = results(cfg, st, Y, DX, grads)
+    drive_iteration(st, cfg, X, DY, Y, DX, group=group)
+    second = results(cfg, st, Y, DX, grads)
+    st.close()
+    # the oracle: iteration 1 on the starting weights, AdamW, iteration 2
+    w = [{n: v.copy() for n, v in s.items()} for s in start]
+    mo = [{n: np.zeros_like(v) for n, v in s.items()} for s in start]
+    vo = [{n: np.zeros_like(v) for n, v in s.items()} for s in start]
+    refs = []
+    for step in (1, 2):
+        ora_params = [_device_weights(cfg, {n: v.astype(np.float32) for n, v in wl.items()}) for wl in w]
+        ref = run_oracle(cfg, xs, dys, ora_params=ora_params)
+        refs.append(ref)
+        for l in range(L):
+            for n in T.PARAMS:
+                w[l][n], mo[l][n], vo[l][n] = ms.adamw_step(w[l][n], mo[l][n], vo[l][n], ref["grads"][l][n], step, **HP)
+    for it, (got, ref) in enumerate(((first, refs[0]), (second, refs[1]))):
+        worst, bad = compare(got, ref, BF16_TOL)
+        assert not bad, (quant, group, it, bad)
+    # the update reached the device: the second iteration's output moved
+    assert any(np.linalg.norm(second["ys"][mb] - first["ys"][mb]) > 1e-2 * np.linalg.norm(first["ys"][mb])
+               for mb in range(cfg.n_micro))
+    # master weights after two steps: the updates agree with the oracle's
+    for l in range(L):
+        got = _unpack(cfg, masters[l])
+        for n in T.PARAMS:
+            du, dr = got[n] - start[l][n], w[l][n] - start[l][n]
+            rel = np.linalg.norm(du - dr) / max(np.linalg.norm(dr), 1e-30)
+            assert rel < 3e-2, (quant, group, l, n, rel)
