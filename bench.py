@@ -374,6 +374,8 @@ def main():
             "policy": configs.WORKLOADS[args.workload].__doc__.split(";")[-1].strip().rstrip("."),
             "order": ("layer-major: one forward group and one backward group over all micro-batches"
                       if cfg.layer_major else "all forwards, then all backwards (in-flight = micro-batches)"),
+            "parameter_gradients": ("inline on the compute stream" if info["wgrad_inline"]
+                                    else "on a stream of their own beside the input-gradient chain"),
             "parallelism": "one GPU",
         },
         "pct_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TPS_ABI_VERSION 2
+#define TPS_ABI_VERSION 3
 #define TPS_MAX_MICRO 64
 
 /* return codes */
@@ -96,6 +96,15 @@ enum { TPS_GRAN_LAYER = 0, TPS_GRAN_SEGMENT = 1 };
  * expanded on the device to the storage dtype as bf16(decode(q) * scale). */
 enum { TPS_Q_NONE = 0, TPS_Q_FP8_ROW = 1 };
 
+/* where a layer backward's parameter-gradient kernels (weight-gradient GEMMs,
+ * bias and LayerNorm column sums) run: SIDE forks them onto a stream of the
+ * stage's own, beside the input-gradient chain on the compute stream; INLINE
+ * issues them on the compute stream in the same order; AUTO picks INLINE when
+ * a micro-batch has 4096 tokens or more (there every kernel of the chain fills
+ * the chip, and two concurrent GEMMs slow each other more than the overlap
+ * gains), else SIDE.  Results are bit-identical either way. */
+enum { TPS_WGRAD_AUTO = 0, TPS_WGRAD_SIDE = 1, TPS_WGRAD_INLINE = 2 };
+
 /* op kinds in the planned order (TPS_OP_R: a recompute task of the T-Pipe
  * schedule, reported by tps_tpipe_schedule; a stage runs the recompute of a
  * micro-batch at the start of its backward) */
@@ -143,6 +152,7 @@ typedef struct tps_config {
                                    weights only): the host parameter blocks are
                                    in the quantized layout of
                                    tps_param_layout_q                           */
+  int32_t wgrad_stream;         /* TPS_WGRAD_AUTO, _SIDE or _INLINE             */
 } tps_config;
 
 typedef struct tps_plan_info {
@@ -171,6 +181,7 @@ typedef struct tps_plan_info {
   double recompute_flops;       /* extra forward work the policy implies         */
   uint64_t h2d_bytes;           /* host-link traffic per iteration               */
   uint64_t d2h_bytes;
+  int32_t wgrad_inline;         /* 1: parameter gradients on the compute stream */
 } tps_plan_info;
 
 typedef struct tps_params {
@@ -258,7 +269,14 @@ int tps_param_layout_q(const tps_config* cfg, uint64_t offsets[TPS_P_COUNT], uin
 int tps_plan(const tps_config* cfg, tps_plan_info* out);
 
 /* Create a stage.  Copies the config and policy; keeps the pointers of
- * params and mem.  Launches nothing. */
+ * params and mem.  Launches nothing.
+ * Debug: with the environment variable TPS_POISON set (and not "0") when the
+ * stage is created, memory whose contents are dead by the stage's protocol is
+ * filled with all-ones bytes (NaN in f32 and bf16) as it is handed back: a
+ * staging slot after its copy to host or its micro-batch's backward, the
+ * checkpoint slot and the replay buffer after each backward, the transposed
+ * weights of an evicted window entry.  Results are unchanged unless a read
+ * escapes the protocol; each fill costs one kernel. */
 int tps_stage_init(const tps_config* cfg, const tps_params* params,
                    const tps_memory* mem, tps_stage** out);
 

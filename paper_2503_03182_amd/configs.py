@@ -52,12 +52,13 @@ def stage4_h2048() -> StageConfig:
 def stage5_h5120_offload() -> StageConfig:
     """5 layers, hidden 5120, 40 heads, MLP 20480, causal seq 2048, micro-batch 1,
     16 micro-batches in flight, bf16; every activation offloadable: the planner
-    offloads the micro-batches (by slack) whose copies over a 50 GB/s link
-    lower the device peak without lengthening the round, and prefetches them
-    before their backward."""
+    offloads the micro-batches (by slack) whose copies over the host link (55
+    GB/s, measured per direction on MI355X) lower the device peak without
+    lengthening the round, and prefetches each three ops before its backward
+    (late enough that it returns after the peak has passed)."""
     return StageConfig(n_layers=5, hidden=5120, n_heads=40, mlp=20480, seq=2048, micro_batch=1, n_micro=16,
-                       dtype="bf16", policy=policy_all(5, OFFLOAD), offload_auto=True, lookahead=4,
-                       link_gbps_hint=50.0, tflops_hint=1000.0)
+                       dtype="bf16", policy=policy_all(5, OFFLOAD), offload_auto=True, lookahead=3,
+                       link_gbps_hint=55.0, tflops_hint=1000.0)
 
 
 def stage5_h5120_resident() -> StageConfig:

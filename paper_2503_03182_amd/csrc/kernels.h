@@ -108,6 +108,8 @@ hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_
                                   hipStream_t st, int overwrite = 0);
 hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st);
 hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st);
+// every byte of p[0, bytes) set to value
+hipError_t fill_bytes_launch(void* p, uint64_t bytes, uint8_t value, hipStream_t st);
 // out (bf16) [rows][cols] = bf16(decode_e4m3(q[r][c]) * scale[r]); cols % 8 == 0,
 // q 8-byte and out 16-byte aligned
 hipError_t dequant_fp8_rows_launch(const void* q, const float* scale, int64_t rows, int64_t cols, void* out,

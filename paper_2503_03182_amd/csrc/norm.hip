@@ -419,11 +419,12 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in
   }
 }
 
-__global__ __launch_bounds__(256) void fill_zero_kernel(u32x4* p, uint64_t n16, uint8_t* tail, uint32_t ntail) {
+__global__ __launch_bounds__(256) void fill_bytes_kernel(u32x4* p, uint64_t n16, uint8_t* tail, uint32_t ntail,
+                                                         uint32_t word) {
   const uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x;
   const uint64_t stride = (uint64_t)gridDim.x * 256;
-  for (uint64_t k = i; k < n16; k += stride) p[k] = u32x4{0u, 0u, 0u, 0u};
-  if (i < ntail) tail[i] = 0;
+  for (uint64_t k = i; k < n16; k += stride) p[k] = u32x4{word, word, word, word};
+  if (i < ntail) tail[i] = (uint8_t)word;
 }
 
 // Per-row kernels are instantiated for NC 16-byte chunks per thread.
@@ -581,16 +582,18 @@ hipError_t transpose_launch(int dtype, int rows, int cols, const void* in, int64
   return hipGetLastError();
 }
 
-hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st) {
+hipError_t fill_bytes_launch(void* p, uint64_t bytes, uint8_t value, hipStream_t st) {
   if (bytes == 0) return hipSuccess;
   const uint64_t n16 = bytes / 16;
   const uint32_t ntail = (uint32_t)(bytes % 16);
   uint64_t blocks = (n16 + 255) / 256;
   if (blocks < 1) blocks = 1;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st, (u32x4*)p, n16,
-                     (uint8_t*)p + n16 * 16, ntail);
+  hipLaunchKernelGGL(fill_bytes_kernel, dim3((unsigned)blocks), dim3(256), 0, st, (u32x4*)p, n16,
+                     (uint8_t*)p + n16 * 16, ntail, 0x01010101u * value);
   return hipGetLastError();
 }
+
+hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st) { return fill_bytes_launch(p, bytes, 0, st); }
 
 }  // namespace tps

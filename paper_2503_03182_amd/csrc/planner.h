@@ -35,6 +35,7 @@ struct Plan {
   // quantized host parameter block (weights_quant == TPS_Q_FP8_ROW): codes or
   // storage-dtype vectors at qoff, f32 row scales of the four matrices at qsoff
   int quant = TPS_Q_NONE;
+  bool wgrad_inline = false;   // parameter-gradient kernels on the compute stream
   uint64_t qoff[TPS_P_COUNT] = {}, qsoff[4] = {}, qbytes = 0;
   uint64_t hpbytes = 0;   // bytes of one host parameter block (pbytes or qbytes)
 

@@ -19,6 +19,7 @@
 
 #include <chrono>
 #include <condition_variable>
+#include <cstdlib>
 #include <cstring>
 #include <deque>
 #include <map>
@@ -119,7 +120,9 @@ struct tps_stage {
   bool own_xs = false, own_ps = false;
   // gs: the layer backward's parameter-gradient kernels (weight GEMMs, column
   // sums, finalize), forked from cs where their inputs are ready and joined
-  // back at the end of the layer; ks: the stream the next kernel goes to
+  // back at the end of the layer (gs is cs itself when the plan issues them
+  // inline: the forks and joins are then no-ops); ks: the stream the next
+  // kernel goes to
   hipStream_t gs = nullptr, ks = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   // deferred joins: layer backwards of an iteration are numbered in issue
@@ -220,7 +223,27 @@ struct tps_stage {
   float* bpart(int l) const { return reinterpret_cast<float*>(arena + p.off_bpart + (uint64_t)l * p.bpart_bytes); }
 
   // --- events ---------------------------------------------------------------
+  // TPS_POISON: memory whose contents the protocol declares dead (a staging
+  // slot handed back, a checkpoint slot and the replay buffer after the
+  // micro-batch's backward, the transposed weights of an evicted window
+  // entry) is filled with all-ones bytes, a NaN in f32 and bf16, so a read
+  // that should not happen shows in the results
+  bool poison = false;
+  int poison_fill(void* ptr, uint64_t bytes, hipStream_t on) {
+    if (poison && bytes) TPS_HIP(fill_bytes_launch(ptr, bytes, 0xFF, on));
+    return TPS_OK;
+  }
+  // after the backward of micro-batch mb: its checkpoint slot and the replay
+  // buffer, once the parameter-gradient kernels that read them are done
+  int poison_after_backward(int mb) {
+    if (!poison) return TPS_OK;
+    TPS_TRY(join_if_pending());
+    if (p.kslot_bytes) TPS_TRY(poison_fill(kslot_base(mb), p.kslot_bytes, cs));
+    TPS_TRY(poison_fill(arena + p.off_replay, p.replay_bytes, cs));
+    return TPS_OK;
+  }
   int release_oslot(int slot, hipStream_t on) {
+    TPS_TRY(poison_fill(oslot_base(slot), p.oslot_bytes, on));
     TPS_HIP(hipEventRecord(oslot_ev[slot].ev, on));
     oslot_ev[slot].valid = true;
     return TPS_OK;
@@ -418,6 +441,7 @@ int tps_stage::prefetch_layer(int l) {
   WinEntry& w = win[victim];
   TPS_TRY(flush_grads(victim));
   if (w.last_use.valid) TPS_HIP(hipStreamWaitEvent(ps, w.last_use.ev, 0));
+  if (p.wt_bytes) TPS_TRY(poison_fill(wt_of(l, victim), p.wt_bytes, ps));
   w.layer = l;
   w.tick = ++tick;
   w.wt_valid = false;
@@ -995,7 +1019,7 @@ int tps_stage::backward_one(int mb, const void* dy, void* dx) {
   // layers and the end of the iteration wait for them.
   if (defer && p.L < 3) TPS_TRY(join_gs());
   if (p.oslot_bytes) TPS_TRY(release_oslot(p.oslot_b[mb], defer ? gs : cs));
-  return TPS_OK;
+  return poison_after_backward(mb);
 }
 
 // ---------------------------------------------------------------------------
@@ -1011,6 +1035,10 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
   int rc = make_plan(cfg, &st->p);
   if (rc) { delete st; return rc; }
   const Plan& p = st->p;
+  {
+    const char* ev = std::getenv("TPS_POISON");
+    st->poison = ev && *ev && std::strcmp(ev, "0") != 0;
+  }
   if (!params->layer_params || !params->layer_grads) { delete st; return set_error(TPS_EINVAL, "tps_stage_init: params"); }
   for (int l = 0; l < p.L; ++l) {
     if (!params->layer_params[l] || !params->layer_grads[l]) { delete st; return set_error(TPS_EINVAL, "tps_stage_init: null layer block"); }
@@ -1063,7 +1091,9 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
     for (auto& e : st->ev_replay)
       if (he == hipSuccess) he = mkev_dev(&e);
   }
-  if (he == hipSuccess) he = queue_stream(st->device, &st->gs);
+  // parameter-gradient kernels: a stream of their own, or the compute stream
+  if (p.wgrad_inline) st->gs = st->cs;
+  else if (he == hipSuccess) he = queue_stream(st->device, &st->gs);
   if (link) {
     st->xs = static_cast<hipStream_t>(mem->copy_stream);
     st->ps = static_cast<hipStream_t>(mem->prefetch_stream);
@@ -1301,6 +1331,7 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
   for (int i = 0; i < n; ++i) {
     const int mb = mb0 + i;
     if (p.oslot_bytes) TPS_TRY(st->release_oslot(p.oslot_b[mb], st->cs));
+    TPS_TRY(st->poison_after_backward(mb));
     st->b_done[mb] = 1;
     ++st->cursor;
   }
@@ -1362,7 +1393,7 @@ extern "C" int tps_stage_sync_for(tps_stage* st, double timeout_ms) {
     const char* name;
   };
   std::vector<Named> streams = {{st->cs, "compute"}};
-  if (st->gs) streams.push_back({st->gs, "parameter-gradient"});
+  if (st->gs && st->gs != st->cs) streams.push_back({st->gs, "parameter-gradient"});
   if (st->rs) streams.push_back({st->rs, "replay"});
   if (st->xs) streams.push_back({st->xs, "device-to-host copy"});
   if (st->ps && st->ps != st->xs) streams.push_back({st->ps, "host-to-device copy"});
@@ -1434,7 +1465,7 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
   if (st->cs) (void)hipStreamSynchronize(st->cs);
   if (st->xs) (void)hipStreamSynchronize(st->xs);
   if (st->ps && st->ps != st->xs) (void)hipStreamSynchronize(st->ps);
-  if (st->gs) {
+  if (st->gs && st->gs != st->cs) {
     (void)hipStreamSynchronize(st->gs);
     (void)hipStreamDestroy(st->gs);
   }

@@ -15,7 +15,7 @@ from typing import Optional, Sequence
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpstage.so")
 
 # --- constants (mirror tpstage.h) ------------------------------------------
-TPS_ABI_VERSION = 2
+TPS_ABI_VERSION = 3
 TPS_OK, TPS_EINVAL, TPS_ENOMEM, TPS_EORDER, TPS_EHIP, TPS_ETIMEOUT, TPS_ESTATE = 0, -1, -2, -3, -4, -5, -6
 TPS_F32, TPS_BF16 = 0, 1
 KEEP, RECOMPUTE, OFFLOAD = 0, 1, 2
@@ -23,6 +23,7 @@ TENSORS = ("x", "a", "qkv", "o", "lse", "x1", "c", "u", "g", "ln1", "ln2")
 T_INDEX = {n: i for i, n in enumerate(TENSORS)}
 W_RESIDENT, W_STREAM = 0, 1
 Q_NONE, Q_FP8_ROW = 0, 1
+WGRAD_AUTO, WGRAD_SIDE, WGRAD_INLINE = 0, 1, 2
 GRAN_LAYER, GRAN_SEGMENT = 0, 1
 OP_F, OP_B, OP_R = 0, 1, 2
 PARAMS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "g1", "be1", "g2", "be2")
@@ -50,7 +51,7 @@ class Config(C.Structure):
         ("offload_auto", C.c_int32), ("weights", C.c_int32), ("window", C.c_int32),
         ("recompute_granularity", C.c_int32), ("n_ops", C.c_int32), ("ops", C.POINTER(C.c_int32)),
         ("inflight", C.c_int32), ("link_gbps_hint", C.c_float), ("tflops_hint", C.c_float),
-        ("lookahead", C.c_int32), ("weights_quant", C.c_int32),
+        ("lookahead", C.c_int32), ("weights_quant", C.c_int32), ("wgrad_stream", C.c_int32),
     ]
 
 
@@ -66,7 +67,7 @@ class PlanInfo(C.Structure):
         ("predicted_peak_bytes", C.c_uint64), ("offload_mb_mask", C.c_uint64),
         ("n_offload_mbs", C.c_int32), ("n_replay_layers", C.c_int32),
         ("fwd_flops", C.c_double), ("bwd_flops", C.c_double), ("recompute_flops", C.c_double),
-        ("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64),
+        ("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("wgrad_inline", C.c_int32),
     ]
 
     def as_dict(self) -> dict:
@@ -246,6 +247,7 @@ class StageConfig:
     tflops_hint: float = 1000.0
     lookahead: int = 1
     weights_quant: int = Q_NONE
+    wgrad_stream: int = WGRAD_AUTO
     # drive the planned order with layer-major group calls (each run of
     # consecutive F (or B) tasks is one tps_stage_forward_group / _backward_group)
     layer_major: bool = False
@@ -300,6 +302,7 @@ class StageConfig:
         c.link_gbps_hint, c.tflops_hint = self.link_gbps_hint, self.tflops_hint
         c.lookahead = self.lookahead
         c.weights_quant = self.weights_quant
+        c.wgrad_stream = self.wgrad_stream
         return c
 
     def order(self) -> list:

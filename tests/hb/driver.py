@@ -22,14 +22,15 @@ _lib = None
 
 def build() -> str:
     os.makedirs(os.path.dirname(OUT), exist_ok=True)
+    tmp = f"{OUT}.{os.getpid()}.tmp"   # parallel test workers build side by side
     srcs = [os.path.join(CSRC, n) for n in ("stage.cpp", "planner.cpp", "errors.cpp", "host_optim.cpp")]
     srcs += [os.path.join(HERE, n) for n in ("hb_runtime.cpp", "hb_kernels.cpp")]
     cmd = ["g++", "-std=c++17", "-O1", "-fPIC", "-shared", "-pthread", "-I", os.path.join(HERE, "fakeinc"), "-I", HERE,
-           "-I", os.path.join(ROOT, "include"), "-I", CSRC, *srcs, "-o", OUT + ".tmp"]
+           "-I", os.path.join(ROOT, "include"), "-I", CSRC, *srcs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode:
         raise RuntimeError("checker build failed:\n" + r.stderr)
-    os.replace(OUT + ".tmp", OUT)
+    os.replace(tmp, OUT)
     return OUT
 
 
@@ -201,3 +202,11 @@ def races() -> int:
 
 def report() -> str:
     return lib().tps_hb_report().decode()
+
+
+def count_ops(name: str) -> int:
+    """Operations recorded so far (since the library was loaded) with this name."""
+    f = lib().tps_hb_count_ops
+    f.restype = C.c_int64
+    f.argtypes = [C.c_char_p]
+    return f(name.encode())

@@ -163,12 +163,14 @@ hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t
   return hipSuccess;
 }
 
-hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st) {
+hipError_t fill_bytes_launch(void* p, uint64_t bytes, uint8_t value, hipStream_t st) {
   HbRanges none, wr;
   add1d(wr, p, (int64_t)bytes);
-  hb_op(st, "fill zero", none, wr);
+  hb_op(st, value ? "fill" : "fill zero", none, wr);
   return hipSuccess;
 }
+
+hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st) { return fill_bytes_launch(p, bytes, 0, st); }
 
 hipError_t dequant_fp8_rows_launch(const void* q, const float* scale, int64_t rows, int64_t cols, void* out,
                                    hipStream_t st) {

@@ -239,6 +239,11 @@ const char* tps_hb_report(void) {
 int64_t tps_hb_waits(void) { return S().waits; }
 void tps_hb_drop_wait(int64_t n) { S().drop_wait = n; }
 uint64_t tps_hb_ops(void) { return S().ops.size() - 1; }
+int64_t tps_hb_count_ops(const char* name) {
+  int64_t n = 0;
+  for (auto& o : S().ops) n += o.name == name;
+  return n;
+}
 }
 
 // --- stand-in HIP runtime ------------------------------------------------------

@@ -291,3 +291,19 @@ def test_oversubscribed_stage_exceeds_hbm_only_when_kept():
     # premise needs the larger in-flight count)
     info8 = T.plan(W.stage12_h8192_stream())
     assert info8["keep_all_bytes"] + L * (info8["param_bytes"] + info8["grad_bytes"]) < 288e9
+
+
+def test_wgrad_stream_choice():
+    """AUTO issues the parameter-gradient kernels inline from 4096 tokens per
+    micro-batch on; SIDE and INLINE force either arrangement; other values are
+    rejected."""
+    import dataclasses
+    small, large = W.stage4_h2048(), W.stage12_h8192_stream()
+    assert small.tokens < 4096 <= large.tokens
+    assert T.plan(small)["wgrad_inline"] == 0
+    assert T.plan(large)["wgrad_inline"] == 1
+    assert T.plan(W.stage4_seq8192_recompute())["wgrad_inline"] == 1
+    assert T.plan(dataclasses.replace(small, wgrad_stream=T.WGRAD_INLINE))["wgrad_inline"] == 1
+    assert T.plan(dataclasses.replace(large, wgrad_stream=T.WGRAD_SIDE))["wgrad_inline"] == 0
+    with pytest.raises(T.TpsError):
+        T.plan(dataclasses.replace(small, wgrad_stream=3))

@@ -89,6 +89,46 @@ def test_streamed_weights_bitexact_to_resident():
         assert bit_equal(resident, run_gpu(cfg, one_copy_stream=True)) == [], (window, "one copy stream")
 
 
+def test_wgrad_inline_bitexact_to_side_stream():
+    """Parameter-gradient kernels inline on the compute stream give the same
+    bits as on their own stream (same kernels, same accumulation order)."""
+    L = 4
+    order = [("F", 0), ("F", 1), ("B", 0), ("F", 2), ("B", 1), ("B", 2)]
+    cases = {
+        "keep": (_mid(n_layers=L, ops=order), False),
+        "selective": (_mid(n_layers=L, policy=W.policy_selective(L)), False),
+        "offload": (_mid(n_layers=L, ops=order, policy=W.policy_all(L, T.OFFLOAD), offload_mb_mask=0b101), False),
+        "streamed_groups": (_mid(n_layers=L, policy=W.policy_layer_inputs(L), granularity=T.GRAN_LAYER,
+                                 weights=T.W_STREAM, window=2), True),
+    }
+    for name, (cfg, group) in cases.items():
+        side = run_gpu(dataclasses.replace(cfg, wgrad_stream=T.WGRAD_SIDE), group=group)
+        inline = run_gpu(dataclasses.replace(cfg, wgrad_stream=T.WGRAD_INLINE), group=group)
+        assert bit_equal(side, inline) == [], name
+
+
+def test_poison_leaves_results_unchanged(monkeypatch):
+    """TPS_POISON fills dead slots, replay buffers and evicted transposes with
+    NaN as they are handed back; no read escapes the protocol, so the results
+    stay bit-identical."""
+    L = 4
+    order = [("F", 0), ("F", 1), ("B", 0), ("F", 2), ("B", 1), ("B", 2)]
+    cases = {
+        "selective": (_mid(n_layers=L, ops=order, policy=W.policy_selective(L)), False),
+        "offload": (_mid(n_layers=L, ops=order, policy=W.policy_all(L, T.OFFLOAD), offload_mb_mask=0b101,
+                         lookahead=2), False),
+        "segment": (_mid(n_layers=L, policy=W.policy_layer_inputs(L), granularity=T.GRAN_SEGMENT), False),
+        "streamed_groups": (_mid(n_layers=L, policy=W.policy_layer_inputs(L), granularity=T.GRAN_LAYER,
+                                 weights=T.W_STREAM, window=2), True),
+    }
+    plain = {name: run_gpu(cfg, group=group, iterations=2) for name, (cfg, group) in cases.items()}
+    monkeypatch.setenv("TPS_POISON", "1")
+    for name, (cfg, group) in cases.items():
+        for mode in (T.WGRAD_SIDE, T.WGRAD_INLINE):
+            out = run_gpu(dataclasses.replace(cfg, wgrad_stream=mode), group=group, iterations=2)
+            assert bit_equal(plain[name], out) == [], (name, mode)
+
+
 def test_repeat_iterations_reproduce():
     cfg = _mid(policy=W.policy_all(3, T.OFFLOAD), offload_mb_mask=0b011, inflight=2)
     one = run_gpu(cfg, iterations=1)

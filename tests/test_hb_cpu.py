@@ -95,6 +95,46 @@ def test_quantized_weight_reload_race_free():
             assert _run(cfg, iterations=3, group=group) == 0, (window, group, D.report())
 
 
+def test_wgrad_arrangements_race_free():
+    """Parameter-gradient kernels on their own stream and inline on the
+    compute stream, for both call styles and the replay-stream and streamed
+    configurations."""
+    L = 4
+    cfgs = [_mid(n_layers=L), _mid(n_layers=L, policy=W.policy_selective(L)),
+            _mid(n_layers=L, policy=W.policy_all(L, T.OFFLOAD), offload_mb_mask=0b101),
+            _mid(n_layers=L, policy=W.policy_layer_inputs(L), granularity=T.GRAN_LAYER, weights=T.W_STREAM, window=2)]
+    for i, base in enumerate(cfgs):
+        for mode in (T.WGRAD_SIDE, T.WGRAD_INLINE):
+            cfg = dataclasses.replace(base, wgrad_stream=mode)
+            for group in ((False, True) if base.granularity == T.GRAN_LAYER else (False,)):
+                assert _run(cfg, iterations=2, group=group) == 0, (i, mode, group, D.report())
+
+
+def test_poison_fills_race_free(monkeypatch):
+    """With TPS_POISON the dead memory is filled as it is handed back; every
+    fill is ordered after the last reader of that memory and before its next
+    writer (a fill that raced would itself be reported)."""
+    monkeypatch.setenv("TPS_POISON", "1")
+    L = 4
+    cfgs = [(_mid(n_layers=L, policy=W.policy_selective(L)), False),
+            (_mid(n_layers=L, policy=W.policy_all(L, T.OFFLOAD), offload_mb_mask=0b101, lookahead=2), False),
+            (_mid(n_layers=L, policy=W.policy_layer_inputs(L), granularity=T.GRAN_SEGMENT), False),
+            (_mid(n_layers=L, policy=W.policy_layer_inputs(L), granularity=T.GRAN_LAYER, weights=T.W_STREAM,
+                  window=2), True),
+            (_mid(n_layers=L, policy=W.policy_layer_inputs(L), granularity=T.GRAN_LAYER, weights=T.W_STREAM,
+                  window=3, weights_quant=T.Q_FP8_ROW), False)]
+    for i, (base, group) in enumerate(cfgs):
+        for mode in (T.WGRAD_SIDE, T.WGRAD_INLINE):
+            before = D.count_ops("fill")
+            assert _run(dataclasses.replace(base, wgrad_stream=mode), iterations=2, group=group) == 0, \
+                (i, mode, D.report())
+            assert D.count_ops("fill") > before, (i, mode)
+    monkeypatch.delenv("TPS_POISON")
+    before = D.count_ops("fill")
+    assert _run(cfgs[1][0]) == 0
+    assert D.count_ops("fill") == before
+
+
 def test_mixed_per_microbatch_and_group_calls_race_free():
     keep_order = [("F", 0), ("F", 1), ("F", 2), ("B", 0), ("B", 1), ("B", 2)]
     assert _run(_mid(ops=keep_order), calls=[("F", [0, 1, 2], False), ("B", [0], False), ("B", [1, 2], True)]) == 0, \
@@ -155,7 +195,9 @@ def test_checker_reports_left_out_waits():
     c2 = dataclasses.replace(W.stage4_h2048(), n_micro=4)
     n, det = _dropped_wait_detection(c2)
     assert n > 100 and det >= 0.95 * n, (n, det)
-    c5 = dataclasses.replace(W.stage12_h8192_stream(), n_layers=4, n_micro=4)
+    # (the side-stream arrangement: inline, the parameter-gradient waits are
+    # on the compute stream itself and leave nothing to detect)
+    c5 = dataclasses.replace(W.stage12_h8192_stream(), n_layers=4, n_micro=4, wgrad_stream=T.WGRAD_SIDE)
     c5.policy = c5.policy[:4]
     n, det = _dropped_wait_detection(c5, group=True)
     assert n > 100 and det >= 0.9 * n, (n, det)
