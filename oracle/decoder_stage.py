@@ -241,7 +241,7 @@ def _deep_copy(v):
 
 
 def run_stage(params, xs, dys, n_heads, b, s, eps=1e-5, policy=None,
-              offload_mbs=(), order=None):
+              offload_mbs=(), order=None, layer=None):
     """Forward and backward of the whole stage for every micro-batch.
 
     params : list (one per layer) of dicts keyed by PARAM_NAMES (float64)
@@ -256,9 +256,17 @@ def run_stage(params, xs, dys, n_heads, b, s, eps=1e-5, policy=None,
     order  : op list of ("F", mb) / ("B", mb); default: all forwards, then
              all backwards in ascending micro-batch order.
 
+    layer  : None (the GPT layer of this module) or dict(forward=, backward=,
+             output=) with the signatures of layer_forward, layer_backward
+             and _layer_output, for another layer kind run by the same
+             stage logic.
+
     Returns dict(ys=[...], dxs=[...], grads=[per-layer dicts]) where grads
     are summed over micro-batches in the order the backwards run.
     """
+    fwd = layer["forward"] if layer else layer_forward
+    bwd = layer["backward"] if layer else layer_backward
+    out = layer["output"] if layer else _layer_output
     L = len(params)
     M = len(xs)
     if order is None:
@@ -284,7 +292,7 @@ def run_stage(params, xs, dys, n_heads, b, s, eps=1e-5, policy=None,
             h = np.asarray(xs[mb], dtype=np.float64)
             stage_inputs[mb] = h
             for l in range(L):
-                h_next, sv = layer_forward(params[l], h, b, s, n_heads, eps)
+                h_next, sv = fwd(params[l], h, b, s, n_heads, eps)
                 kept = {}
                 for name in TENSORS:
                     m = mode(l, name, mb)
@@ -316,14 +324,13 @@ def run_stage(params, xs, dys, n_heads, b, s, eps=1e-5, policy=None,
                 elif l == 0:
                     x_in = stage_inputs[mb]
                 else:
-                    x_in = _layer_output(params[l - 1], full[l - 1], b, s,
-                                         n_heads, eps)
-                _, sv = layer_forward(params[l], x_in, b, s, n_heads, eps)
+                    x_in = out(params[l - 1], full[l - 1], b, s, n_heads, eps)
+                _, sv = fwd(params[l], x_in, b, s, n_heads, eps)
                 for n in missing:
                     full[l][n] = sv[n]
             g = np.asarray(dys[mb], dtype=np.float64)
             for l in reversed(range(L)):
-                g, gr = layer_backward(params[l], full[l], g, b, s, n_heads)
+                g, gr = bwd(params[l], full[l], g, b, s, n_heads)
                 for k in gr:
                     grads[l][k] += gr[k]
             dxs[mb] = g

@@ -34,6 +34,14 @@ def param_shapes(h: int, f: int) -> dict:
     }
 
 
+def llama_param_shapes(h: int, n_heads: int, n_kv: int, f: int) -> dict:
+    """LLAMA-style layer: packed q | k | v projection with n_kv key/value
+    heads, packed gate | up projection, no biases, RMSNorm gains only."""
+    d = h // n_heads
+    return {"w_qkv": ((n_heads + 2 * n_kv) * d, h), "w_o": (h, h), "w_1": (2 * f, h), "w_2": (h, f),
+            "g1": (h,), "g2": (h,)}
+
+
 def _rng(seed: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(seed))
 
@@ -64,6 +72,19 @@ def layer_params(layer: int, h: int, f: int, dtype: str) -> dict:
     out = {}
     for tid, (name, shape) in enumerate(param_shapes(h, f).items()):
         r = _rng(1000 + 16 * layer + tid)
+        v = r.standard_normal(shape, dtype=np.float32) * np.float32(0.02)
+        if name in ("g1", "g2"):
+            v = v + np.float32(1.0)
+        out[name] = round_to_storage(v, dtype)
+    return out
+
+
+def llama_layer_params(layer: int, h: int, n_heads: int, n_kv: int, f: int, dtype: str) -> dict:
+    """LLAMA-style layer parameters, same recipe (a tensor's seed uses its
+    GPT-layer id: w_qkv 0, w_o 2, w_1 4, w_2 6, g1 8, g2 10)."""
+    out = {}
+    for name, shape in llama_param_shapes(h, n_heads, n_kv, f).items():
+        r = _rng(1000 + 16 * layer + PARAM_ORDER.index(name))
         v = r.standard_normal(shape, dtype=np.float32) * np.float32(0.02)
         if name in ("g1", "g2"):
             v = v + np.float32(1.0)
