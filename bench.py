@@ -78,7 +78,10 @@ def build_stage(cfg):
     td = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     es = 2 if cfg.dtype == "bf16" else 4
     blocks, grads = [], []
-    shapes = synth.param_shapes(cfg.hidden, cfg.mlp)
+    llama = cfg.arch == T.ARCH_LLAMA
+    nkv = cfg.n_kv_heads or cfg.n_heads
+    shapes = (synth.llama_param_shapes(cfg.hidden, cfg.n_heads, nkv, cfg.mlp) if llama
+              else synth.param_shapes(cfg.hidden, cfg.mlp))
     for l in range(cfg.n_layers):
         blk = torch.zeros(pb, dtype=torch.uint8, device="cuda")
         if cfg.weights == T.W_STREAM:
@@ -88,6 +91,8 @@ def build_stage(cfg):
             # depend on them, and it avoids drawing ~10^10 values on the CPU)
             gen = torch.Generator(device="cuda").manual_seed(1000 + 16 * l)
             for i, name in enumerate(T.PARAMS):
+                if name not in shapes:
+                    continue
                 n = 1
                 for d in shapes[name]:
                     n *= d
@@ -103,8 +108,11 @@ def build_stage(cfg):
             g = T.HostBuffer(gb)
             g.numpy()[:] = 0
         else:
-            vals = synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype)
+            vals = (synth.llama_layer_params(l, cfg.hidden, cfg.n_heads, nkv, cfg.mlp, cfg.dtype) if llama
+                    else synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype))
             for i, name in enumerate(T.PARAMS):
+                if name not in vals:
+                    continue
                 v = torch.from_numpy(vals[name].reshape(-1)).to("cuda").to(td)
                 blk[po[i]:po[i] + v.numel() * es].view(td).copy_(v)
             g = torch.zeros(gb, dtype=torch.uint8, device="cuda")
@@ -159,7 +167,11 @@ def cpu_baseline(cfg, budget_s):
         unit_cfg = dataclasses.replace(unit_cfg, seq=unit_cfg.seq // 2)
     info = T.plan(unit_cfg)
     unit_flops = info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]
-    params = [{k: v.astype(np.float64) for k, v in synth.layer_params(0, cfg.hidden, cfg.mlp, cfg.dtype).items()}]
+    llama = cfg.arch == T.ARCH_LLAMA
+    nkv = cfg.n_kv_heads or cfg.n_heads
+    vals = (synth.llama_layer_params(0, cfg.hidden, cfg.n_heads, nkv, cfg.mlp, cfg.dtype) if llama
+            else synth.layer_params(0, cfg.hidden, cfg.mlp, cfg.dtype))
+    params = [{k: v.astype(np.float64) for k, v in vals.items()}]
     x = [synth.stage_input(0, unit_cfg.tokens, cfg.hidden, cfg.dtype).astype(np.float64)]
     dy = [synth.output_grad(0, unit_cfg.tokens, cfg.hidden, cfg.dtype).astype(np.float64)]
     policy = None if pol1 is None else [{k: (v if v != T.OFFLOAD else T.KEEP) for k, v in pol1[0].items()}]
@@ -167,7 +179,12 @@ def cpu_baseline(cfg, budget_s):
     t_end = time.perf_counter() + budget_s
     while len(times) < 3 and (not times or time.perf_counter() < t_end):
         t0 = time.perf_counter()
-        ora.run_stage(params, x, dy, cfg.n_heads, unit_cfg.micro_batch, unit_cfg.seq, cfg.ln_eps, policy=policy)
+        if llama:
+            from oracle import llama_stage
+            llama_stage.run_stage(params, x, dy, cfg.n_heads, nkv, unit_cfg.micro_batch, unit_cfg.seq, cfg.ln_eps,
+                                  cfg.rope_base, policy=policy)
+        else:
+            ora.run_stage(params, x, dy, cfg.n_heads, unit_cfg.micro_batch, unit_cfg.seq, cfg.ln_eps, policy=policy)
         times.append(time.perf_counter() - t0)
     med = statistics.median(times)
     ncpu = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
@@ -369,7 +386,10 @@ def main():
         "data": "synthetic: seeded N(0,0.02) weights, N(0,1) stage inputs and output gradients",
         "config": {
             "workload": args.workload,
-            "layers": cfg.n_layers, "hidden": cfg.hidden, "heads": cfg.n_heads, "mlp": cfg.mlp,
+            "layer": "LLAMA-style (RMSNorm, rotary, grouped-query attention, SwiGLU)" if cfg.arch == T.ARCH_LLAMA
+                     else "GPT pre-LN (LayerNorm, biases, GeLU)",
+            "layers": cfg.n_layers, "hidden": cfg.hidden, "heads": cfg.n_heads,
+            "kv_heads": cfg.n_kv_heads or cfg.n_heads, "mlp": cfg.mlp,
             "seq": cfg.seq, "micro_batch": cfg.micro_batch, "micro_batches": cfg.n_micro,
             "policy": configs.WORKLOADS[args.workload].__doc__.split(";")[-1].strip().rstrip("."),
             "order": ("layer-major: one forward group and one backward group over all micro-batches"

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TPS_ABI_VERSION 3
+#define TPS_ABI_VERSION 4
 #define TPS_MAX_MICRO 64
 
 /* return codes */
@@ -105,6 +105,22 @@ enum { TPS_Q_NONE = 0, TPS_Q_FP8_ROW = 1 };
  * gains), else SIDE.  Results are bit-identical either way. */
 enum { TPS_WGRAD_AUTO = 0, TPS_WGRAD_SIDE = 1, TPS_WGRAD_INLINE = 2 };
 
+/* layer kind.  GPT: the pre-LN decoder layer above (LayerNorm, biases, GeLU
+ * MLP, multi-head attention).  LLAMA: the LLAMA-style layer of the paper's
+ * LLAMA2-70B workload (Section 6.1, "Workloads"; architecture from the public
+ * LLAMA-2 description): RMSNorm (gains only, eps inside the root), no
+ * biases, rotary position embedding of q and k (pairs (i, i + d/2) of each
+ * head turned by pos * rope_base^(-2i/d)), grouped-query attention with
+ * n_kv_heads key/value heads (query head n reads key/value head
+ * n / (n_heads / n_kv_heads)), and a SwiGLU MLP g = SiLU(gate) * up with the
+ * gate and up projections packed in one [2f, h] matrix (gate rows first).
+ * LLAMA needs bf16 storage and head dim 128.  Tensor shapes under LLAMA:
+ * QKV [T, (n_heads + 2 n_kv_heads) d] stored after the rotation, U [T, 2f]
+ * (gate | up), G [T, f], LN1/LN2 [T] f32 (the reciprocal RMS); parameter
+ * blocks hold W_QKV [(n_heads + 2 n_kv_heads) d, h], W_O, W_1 [2f, h], W_2,
+ * G1, G2, and the bias / shift slots are empty (zero bytes). */
+enum { TPS_ARCH_GPT = 0, TPS_ARCH_LLAMA = 1 };
+
 /* op kinds in the planned order (TPS_OP_R: a recompute task of the T-Pipe
  * schedule, reported by tps_tpipe_schedule; a stage runs the recompute of a
  * micro-batch at the start of its backward) */
@@ -153,6 +169,10 @@ typedef struct tps_config {
                                    in the quantized layout of
                                    tps_param_layout_q                           */
   int32_t wgrad_stream;         /* TPS_WGRAD_AUTO, _SIDE or _INLINE             */
+  int32_t arch;                 /* TPS_ARCH_GPT or TPS_ARCH_LLAMA               */
+  int32_t n_kv_heads;           /* LLAMA: key/value heads, dividing n_heads (0:
+                                   n_heads); GPT: 0 or n_heads                  */
+  float rope_base;              /* LLAMA: rotary base (0: 10000)                */
 } tps_config;
 
 typedef struct tps_plan_info {

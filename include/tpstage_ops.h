@@ -112,6 +112,56 @@ int tps_op_dequant_fp8_rows(int64_t rows, int64_t cols, const void* q, const flo
 /* g[i] = round(GeLU(u[i])) for n elements. */
 int tps_op_gelu(int dtype, int64_t n, const void* u, void* g, void* stream);
 
+/* LLAMA-style layer kernels (the layer the paper's evaluation runs as
+ * LLAMA2-70B, Section 6.1 "Workloads"; architecture from the public LLAMA-2
+ * description).
+ *
+ * RMSNorm over rows of x[rows, cols]: out = x * rstd * gamma with
+ * rstd = 1/sqrt(mean(x^2) + eps) in f32 ([rows] f32, written when non-NULL).
+ * cols <= 16384. */
+int tps_op_rmsnorm_fwd(int dtype, int rows, int cols, const void* x, const void* gamma, float eps, void* out,
+                       float* rstd, void* stream);
+
+/* RMSNorm backward: with zhat = x rstd and g = dout * gamma,
+ *   dx = resid_grad + rstd (g - zhat mean(g zhat))   (resid_grad may be NULL)
+ * and, when dgamma is non-NULL, dgamma += sum_rows dout * zhat (f32, fixed
+ * order).  workspace: tps_op_workspace_bytes(TPS_WS_COLSUM, rows, cols). */
+int tps_op_rmsnorm_bwd(int dtype, int rows, int cols, const void* dout, const void* x, const float* rstd,
+                       const void* gamma, const void* resid_grad, void* dx, float* dgamma, float* workspace,
+                       void* stream);
+
+/* Rotary position embedding, in place, bf16: for each of `rows` rows
+ * (position row % s) and each of the first n_rot heads of d columns (d a
+ * multiple of 16, ld a multiple of 8), the pair (x_i, x_{i+d/2}), i < d/2,
+ * turns by +angle (inverse != 0: -angle, the gradient's transposed rotation),
+ * angle = pos * base^(-2i/d).  table: caller's [2 s d/2] f32 workspace,
+ * filled with cos and sin (evaluated in double, rounded once) before use. */
+int tps_op_rope(void* x, int64_t ld, int rows, int s, int n_rot, int d, float base, int inverse, float* table,
+                void* stream);
+
+/* SwiGLU, bf16: g[r, j] = SiLU(u[r, j]) * u[r, f + j] for u [rows, 2f]
+ * (gate | up), SiLU(z) = z / (1 + exp(-z)); f a multiple of 8. */
+int tps_op_swiglu_fwd(int rows, int f, const void* u, void* g, void* stream);
+
+/* SwiGLU backward: du[r, j] = dg * up * sigma(gate) (1 + gate (1 - sigma(gate))),
+ * du[r, f + j] = dg * SiLU(gate), from dg [rows, f] and u [rows, 2f]. */
+int tps_op_swiglu_bwd(int rows, int f, const void* dg, const void* u, void* du, void* stream);
+
+/* Causal grouped-query attention, bf16, head dim 128: qkv [b*s, (n_heads +
+ * 2 n_kv) 128] holds q of n_heads heads, then k and v of n_kv heads
+ * (n_heads a multiple of n_kv); query head n attends with key/value head
+ * n / (n_heads / n_kv).  o [b*s, n_heads 128], lse [b, n_heads, s] f32. */
+int tps_op_attention_gqa_fwd(int b, int s, int n_heads, int n_kv, const void* qkv, void* o, float* lse,
+                             void* stream);
+
+/* Its backward: dqkv (layout of qkv) from qkv, o, lse and do; the key/value
+ * gradient of a head is the sum over its query heads in ascending order.
+ * workspace: tps_op_workspace_bytes(TPS_WS_ATTN_BWD, b*s, n_heads) bytes;
+ * kv_workspace: b*s * 2 * n_heads * 128 bf16 when n_kv < n_heads (may be NULL
+ * when n_kv == n_heads). */
+int tps_op_attention_gqa_bwd(int b, int s, int n_heads, int n_kv, const void* qkv, const void* o, const float* lse,
+                             const void* d_o, void* dqkv, float* workspace, void* kv_workspace, void* stream);
+
 enum { TPS_WS_COLSUM = 0, TPS_WS_ATTN_BWD = 1 };
 uint64_t tps_op_workspace_bytes(int kind, int64_t rows, int64_t cols);
 

@@ -1,11 +1,12 @@
 """The stage workloads (shapes and policies) used by tests and the bench.
 
-Every workload is one pipeline stage of GPT pre-LN decoder layers run
-micro-batch by micro-batch; names say what the workload is.
+Every workload is one pipeline stage of decoder layers (GPT pre-LN, or
+LLAMA-style for the llama* workloads) run micro-batch by micro-batch; names
+say what the workload is.
 """
 from __future__ import annotations
 
-from .tpstage import (GRAN_LAYER, GRAN_SEGMENT, KEEP, OFFLOAD, RECOMPUTE, TENSORS, W_RESIDENT,
+from .tpstage import (ARCH_LLAMA, GRAN_LAYER, GRAN_SEGMENT, KEEP, OFFLOAD, RECOMPUTE, TENSORS, W_RESIDENT,
                       W_STREAM, StageConfig)
 
 
@@ -97,6 +98,27 @@ def stage12_h8192_stream_m20() -> StageConfig:
     return stage12_h8192_stream(n_micro=20)
 
 
+def llama12_h8192_stream() -> StageConfig:
+    """12 LLAMA-style layers at the LLAMA2-70B widths: hidden 8192, 64 query
+    heads and 8 key/value heads of 128, SwiGLU MLP 28672 (gate and up
+    packed), causal seq 4096, micro-batch 1, 8 micro-batches, bf16; weights
+    and f32 grads streamed from pinned host per layer, run as layer-major
+    groups; activations recomputed from layer inputs."""
+    return StageConfig(n_layers=12, hidden=8192, n_heads=64, mlp=28672, seq=4096, micro_batch=1, n_micro=8,
+                       dtype="bf16", policy=policy_layer_inputs(12), granularity=GRAN_LAYER, weights=W_STREAM,
+                       window=3, layer_major=True, arch=ARCH_LLAMA, n_kv_heads=8)
+
+
+def llama4_h4096() -> StageConfig:
+    """4 LLAMA-style layers, hidden 4096, 32 query heads and 8 key/value heads
+    of 128, SwiGLU MLP 14336, causal seq 4096, micro-batch 1, 8
+    micro-batches, bf16, resident weights; selective recompute of the
+    attention and SwiGLU outputs."""
+    return StageConfig(n_layers=4, hidden=4096, n_heads=32, mlp=14336, seq=4096, micro_batch=1, n_micro=8,
+                       dtype="bf16", policy=policy_selective(4), granularity=GRAN_SEGMENT, arch=ARCH_LLAMA,
+                       n_kv_heads=8)
+
+
 WORKLOADS = {
     "tiny": tiny,
     "stage4_h2048": stage4_h2048,
@@ -105,4 +127,6 @@ WORKLOADS = {
     "stage4_seq8192_recompute": stage4_seq8192_recompute,
     "stage12_h8192_stream": stage12_h8192_stream,
     "stage12_h8192_stream_m20": stage12_h8192_stream_m20,
+    "llama4_h4096": llama4_h4096,
+    "llama12_h8192_stream": llama12_h8192_stream,
 }

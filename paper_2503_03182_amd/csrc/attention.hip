@@ -553,23 +553,25 @@ static hipError_t bwd_launch(int b, int s, int nh, const void* qkv, const void* 
   return hipGetLastError();
 }
 
-hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, void* o,
+hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int nkv, int d, const void* qkv, void* o,
                                 float* lse, hipStream_t st) {
+  if (nkv != nh && !(dtype == TPS_BF16 && d == 128)) return hipErrorInvalidValue;
   if (dtype == TPS_BF16) {
-    if (d == 128) return attention_fwd_v3_launch(b, s, nh, d, qkv, o, lse, st);
+    if (d == 128) return attention_fwd_v3_launch(b, s, nh, nkv, d, qkv, o, lse, st);
     return attention_fwd_v2_launch(b, s, nh, d, qkv, o, lse, st);
   }
   return d == 64 ? fwd_launch<float, 64>(b, s, nh, qkv, o, lse, st) : fwd_launch<float, 128>(b, s, nh, qkv, o, lse, st);
 }
 
-hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, const void* o,
-                                const float* lse, const void* dout, void* dqkv, float* dvec,
+hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int nkv, int d, const void* qkv, const void* o,
+                                const float* lse, const void* dout, void* dqkv, float* dvec, void* kv_ws,
                                 hipStream_t st) {
+  if (nkv != nh && !(dtype == TPS_BF16 && d == 128)) return hipErrorInvalidValue;
   if (dtype == TPS_BF16) {
     const hipError_t e = d == 128 ? dot_launch<bf16, 128>(b, s, nh, o, dout, dvec, st)
                                   : dot_launch<bf16, 64>(b, s, nh, o, dout, dvec, st);
     if (e != hipSuccess) return e;
-    if (d == 128) return attention_bwd_v3_launch(b, s, nh, d, qkv, lse, dout, dqkv, dvec, st);
+    if (d == 128) return attention_bwd_v3_launch(b, s, nh, nkv, d, qkv, lse, dout, dqkv, dvec, kv_ws, st);
     return attention_bwd_v2_launch(b, s, nh, d, qkv, lse, dout, dqkv, dvec, st);
   }
   return d == 64 ? bwd_launch<float, 64>(b, s, nh, qkv, o, lse, dout, dqkv, dvec, st)

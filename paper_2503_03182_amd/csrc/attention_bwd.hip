@@ -43,19 +43,30 @@ constexpr int kDkdvLds = 2 * (2 * TILE + 2 * kVecBytes);
 // LDS of a dQ block: a ring of two stages of K, V
 constexpr int kDqLds = 2 * (2 * TILE);
 
-// dK, dV of key block kb (32 KW keys) of one (batch, head); smem holds
-// kDkdvLds bytes.
+// Where dK/dV blocks write: with one key/value head per query head into
+// dqkv's k and v blocks; with grouped heads (nkv < nh) into a workspace
+// [T][2 nh d] of per-query-head gradients (dK of head n at column n d, dV at
+// nh d + n d) that gqa_fold sums per key/value head.
+struct KvOut {
+  bf16* p;        // rows of dK | dV
+  int64_t ld;     // row stride
+  int dk0, dv0;   // column of query head 0's dK and dV
+};
+
+// dK, dV of key block kb (32 KW keys) of one (batch, query head); smem holds
+// kDkdvLds bytes.  qkv rows: q of nh heads | k, v of nkv heads.
 template <int KW>
 __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
                                            const float* __restrict__ lse, const float* __restrict__ dvec,
-                                           bf16* __restrict__ dqkv, int b, int s, int nh, float scale, int kb,
+                                           KvOut ko, int b, int s, int nh, int nkv, float scale, int kb,
                                            int head, int batch, char* smem) {
   constexpr int VEC = kVecBytes;
   constexpr int STAGE = 2 * TILE + 2 * VEC;    // Q, dO, lse, D
   constexpr int BKEY = 32 * KW;                // keys per workgroup
 
-  const int H = nh * D;
-  const int64_t ld = 3 * (int64_t)H;
+  const int H = nh * D, HK = nkv * D;
+  const int64_t ld = (int64_t)H + 2 * HK;
+  const int kvh = head / (nh / nkv);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
@@ -67,11 +78,11 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
   // K^T and V^T fragments (B operands): lane holds key's d = 16 ks + 8 g .. +8
   bf16x8 kf[D / 16], vf[D / 16];
   {
-    const bf16* krow = base + (int64_t)min(key, s - 1) * ld + H + head * D + 8 * g;
+    const bf16* krow = base + (int64_t)min(key, s - 1) * ld + H + kvh * D + 8 * g;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
       kf[ks] = load_frag_settled(krow + 16 * ks);
-      vf[ks] = load_frag_settled(krow + H + 16 * ks);
+      vf[ks] = load_frag_settled(krow + HK + 16 * ks);
     }
   }
   // query tiles from the one holding this workgroup's first key to the end
@@ -233,7 +244,7 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
 
   // ---- store: lane holds dK^T / dV^T [32 mt + acc_row(j, l)][key]
   if (key < s) {
-    bf16* row = dqkv + ((int64_t)batch * s + key) * ld + head * D;
+    bf16* row = ko.p + ((int64_t)batch * s + key) * ko.ld + head * D;
 #pragma unroll
     for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
@@ -246,8 +257,8 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
           wv[j] = (bf16)dv[mt][4 * j4 + j];
         }
         const int c = 32 * mt + acc_row(4 * j4, lane);
-        *reinterpret_cast<bf16x4*>(row + H + c) = wk;
-        *reinterpret_cast<bf16x4*>(row + 2 * H + c) = wv;
+        *reinterpret_cast<bf16x4*>(row + ko.dk0 + c) = wk;
+        *reinterpret_cast<bf16x4*>(row + ko.dv0 + c) = wv;
       }
   }
 }
@@ -255,13 +266,12 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
 template <int KW>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * KW, 64 * KW), amdgpu_waves_per_eu(1, 1)))
 void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
-                             const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
-                             int b, int s, int nh, float scale) {
+                             const float* __restrict__ lse, const float* __restrict__ dvec, KvOut ko,
+                             int b, int s, int nh, int nkv, float scale) {
   __shared__ __attribute__((aligned(1024))) char smem[kDkdvLds];
   const int idx = blockIdx.x;
   // first key blocks carry the most queries
-  dkdv_block<KW>(qkv, dout, lse, dvec, dqkv, b, s, nh, scale, idx / (nh * b), idx % nh, (idx / nh) % b,
-                        smem);
+  dkdv_block<KW>(qkv, dout, lse, dvec, ko, b, s, nh, nkv, scale, idx / (nh * b), idx % nh, (idx / nh) % b, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -272,13 +282,14 @@ void attn_bwd_dkdv_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restric
 template <int QW>
 __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
                                          const float* __restrict__ lse, const float* __restrict__ dvec,
-                                         bf16* __restrict__ dqkv, int b, int s, int nh, float scale, int qb, int head,
-                                         int batch, char* smem) {
+                                         bf16* __restrict__ dqkv, int b, int s, int nh, int nkv, float scale, int qb,
+                                         int head, int batch, char* smem) {
   constexpr int STAGE = 2 * TILE;   // K, V
   constexpr int BQ = 32 * QW;       // queries per workgroup
 
-  const int H = nh * D;
-  const int64_t ld = 3 * (int64_t)H;
+  const int H = nh * D, HK = nkv * D;
+  const int64_t ld = (int64_t)H + 2 * HK;
+  const int kvh = head / (nh / nkv);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 5;
@@ -307,8 +318,8 @@ __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf1
   const int wave_last = min(q0 + 31, s - 1) / BT;
 
   TileSrcN<QW> ksrc, vsrc;
-  ksrc.init(base + H + head * D, ld, s, slice, lane);
-  vsrc.init(base + 2 * H + head * D, ld, s, slice, lane);
+  ksrc.init(base + H + kvh * D, ld, s, slice, lane);
+  vsrc.init(base + H + HK + kvh * D, ld, s, slice, lane);
   char* const ring = smem;
   auto load_tile = [&](int t, int st) {
     ksrc.load(t * BT, ring + st * STAGE);
@@ -437,13 +448,13 @@ template <int QW>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * QW, 64 * QW), amdgpu_waves_per_eu(1, 1)))
 void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout,
                            const float* __restrict__ lse, const float* __restrict__ dvec, bf16* __restrict__ dqkv,
-                           int b, int s, int nh, float scale) {
+                           int b, int s, int nh, int nkv, float scale) {
   __shared__ __attribute__((aligned(1024))) char smem[kDqLds];
   const int idx = blockIdx.x;
   const int nqb = (s + 32 * QW - 1) / (32 * QW);
   // heaviest blocks first
-  dq_block<QW>(qkv, dout, lse, dvec, dqkv, b, s, nh, scale, nqb - 1 - idx / (nh * b), idx % nh,
-                      (idx / nh) % b, smem);
+  dq_block<QW>(qkv, dout, lse, dvec, dqkv, b, s, nh, nkv, scale, nqb - 1 - idx / (nh * b), idx % nh,
+               (idx / nh) % b, smem);
 }
 
 // dK, dV of key block j and then dQ of query block j (128 rows each): with n
@@ -453,37 +464,44 @@ void attn_bwd_dq_v3_kernel(const bf16* __restrict__ qkv, const bf16* __restrict_
 // causal triangle is balanced without splitting any block).
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void attn_bwd_fused_kernel(const bf16* __restrict__ qkv, const bf16* __restrict__ dout, const float* __restrict__ lse,
-                           const float* __restrict__ dvec, bf16* __restrict__ dqkv, int b, int s, int nh,
-                           float scale) {
+                           const float* __restrict__ dvec, bf16* __restrict__ dqkv, KvOut ko, int b, int s, int nh,
+                           int nkv, float scale) {
   __shared__ __attribute__((aligned(1024))) char smem[kDkdvLds > kDqLds ? kDkdvLds : kDqLds];
   const int idx = blockIdx.x;
   const int j = idx / (nh * b), head = idx % nh, batch = (idx / nh) % b;
-  dkdv_block<4>(qkv, dout, lse, dvec, dqkv, b, s, nh, scale, j, head, batch, smem);
+  dkdv_block<4>(qkv, dout, lse, dvec, ko, b, s, nh, nkv, scale, j, head, batch, smem);
   __syncthreads();   // the LDS ring is reused
-  dq_block<4>(qkv, dout, lse, dvec, dqkv, b, s, nh, scale, j, head, batch, smem);
+  dq_block<4>(qkv, dout, lse, dvec, dqkv, b, s, nh, nkv, scale, j, head, batch, smem);
 }
 
-hipError_t attention_bwd_v3_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
-                                   void* dqkv, const float* dvec, hipStream_t st) {
-  if (d != D) return hipErrorInvalidValue;
+hipError_t attention_bwd_v3_launch(int b, int s, int nh, int nkv, int d, const void* qkv, const float* lse,
+                                   const void* dout, void* dqkv, const float* dvec, void* kv_ws, hipStream_t st) {
+  if (d != D || nkv <= 0 || nh % nkv != 0) return hipErrorInvalidValue;
+  if (nkv != nh && kv_ws == nullptr) return hipErrorInvalidValue;
   const float scale = 1.0f / sqrtf((float)d);
   const bf16* x = (const bf16*)qkv;
   const bf16* dy = (const bf16*)dout;
   bf16* dx = (bf16*)dqkv;
+  const int H = nh * D;
+  const KvOut ko = nkv == nh ? KvOut{dx, 3 * (int64_t)H, H, 2 * H} : KvOut{(bf16*)kv_ws, 2 * (int64_t)H, 0, H};
   // Fused workgroups all take the same time, so they pack the CUs well when
   // there is at most one per CU or many per CU; in between, the two kernels
   // (heaviest blocks first) fill the last round better.
   const int n128 = (s + 127) / 128 * nh * b;
   if (n128 <= 256 || n128 >= 1024) {
-    hipLaunchKernelGGL(attn_bwd_fused_kernel, dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh, scale);
-    return hipGetLastError();
+    hipLaunchKernelGGL(attn_bwd_fused_kernel, dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, ko, b, s, nh, nkv,
+                       scale);
+  } else {
+    hipLaunchKernelGGL((attn_bwd_dkdv_v3_kernel<4>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, ko, b, s, nh,
+                       nkv, scale);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_bwd_dq_v3_kernel<4>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh, nkv,
+                       scale);
   }
-  hipLaunchKernelGGL((attn_bwd_dkdv_v3_kernel<4>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh,
-                     scale);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_bwd_dq_v3_kernel<4>), dim3(n128), dim3(256), 0, st, x, dy, lse, dvec, dx, b, s, nh, scale);
-  return hipGetLastError();
+  if (e != hipSuccess || nkv == nh) return e;
+  return gqa_fold_launch(kv_ws, dqkv, b * s, nh, nkv, d, st);
 }
 
 }  // namespace tps

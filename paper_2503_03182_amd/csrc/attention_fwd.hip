@@ -43,18 +43,21 @@ template <int QW, int PARTS>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * QW * PARTS, 64 * QW * PARTS),
                           amdgpu_waves_per_eu(QW / 2, QW / 2)))
 void attn_fwd_sk_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, float* __restrict__ lse, int b, int s,
-                        int nh, float scale) {
+                        int nh, float scale, int nkv) {
   constexpr int BQ = 32 * QW;        // queries per workgroup
   constexpr int STAGE = 2 * TILE;    // K and V
   constexpr int RING = 2 * STAGE;    // one key part's two stages
   static_assert(PARTS == 1 || PARTS == 2, "key parts");
   __shared__ __attribute__((aligned(1024))) char smem[PARTS * RING];
 
-  const int H = nh * D;
-  const int64_t ld = 3 * (int64_t)H;
+  // qkv rows: q of nh heads | k, v of nkv heads; query head n reads
+  // key/value head n / (nh / nkv) (nkv == nh: plain multi-head)
+  const int H = nh * D, HK = nkv * D;
+  const int64_t ld = (int64_t)H + 2 * HK;
   const int nqb = (s + BQ - 1) / BQ;
   const int idx = blockIdx.x;
   const int head = idx % nh;
+  const int kvh = head / (nh / nkv);
   const int batch = (idx / nh) % b;
   const int qb = nqb - 1 - idx / (nh * b);   // heaviest blocks first
   const int lane = threadIdx.x & 63;
@@ -82,8 +85,8 @@ void attn_fwd_sk_kernel(const bf16* __restrict__ qkv, bf16* __restrict__ o, floa
   }
 
   TileSrcN<QW> ksrc, vsrc;
-  ksrc.init(base + H + head * D, ld, s, slice, lane);
-  vsrc.init(base + 2 * H + head * D, ld, s, slice, lane);
+  ksrc.init(base + H + kvh * D, ld, s, slice, lane);
+  vsrc.init(base + H + HK + kvh * D, ld, s, slice, lane);
   char* const ring = smem + part * RING;
   auto load_tile = [&](int t, int st) {
     ksrc.load(t * BT, ring + st * STAGE);
@@ -283,8 +286,9 @@ const char* attention_fwd_v3_name(int b, int s, int nh) {
                              : "tps::attn_fwd_sk_kernel<2, 2>";
 }
 
-hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse, hipStream_t st) {
-  if (d != D) return hipErrorInvalidValue;
+hipError_t attention_fwd_v3_launch(int b, int s, int nh, int nkv, int d, const void* qkv, void* o, float* lse,
+                                   hipStream_t st) {
+  if (d != D || nkv <= 0 || nh % nkv != 0) return hipErrorInvalidValue;
   const float scale = 1.0f / sqrtf((float)d);
   // 128 queries per workgroup: with two resident workgroups per CU when the
   // grid fills the chip twice over, else with the key tiles split in two
@@ -293,12 +297,12 @@ hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv,
   const int n128 = (s + 127) / 128 * nh * b;
   const bf16* x = (const bf16*)qkv;
   if (n128 >= kFwdNoSplit) {
-    hipLaunchKernelGGL((attn_fwd_sk_kernel<4, 1>), dim3(n128), dim3(256), 0, st, x, (bf16*)o, lse, b, s, nh, scale);
+    hipLaunchKernelGGL((attn_fwd_sk_kernel<4, 1>), dim3(n128), dim3(256), 0, st, x, (bf16*)o, lse, b, s, nh, scale, nkv);
   } else if (n128 >= kFwdWide) {
-    hipLaunchKernelGGL((attn_fwd_sk_kernel<4, 2>), dim3(n128), dim3(512), 0, st, x, (bf16*)o, lse, b, s, nh, scale);
+    hipLaunchKernelGGL((attn_fwd_sk_kernel<4, 2>), dim3(n128), dim3(512), 0, st, x, (bf16*)o, lse, b, s, nh, scale, nkv);
   } else {
     hipLaunchKernelGGL((attn_fwd_sk_kernel<2, 2>), dim3((s + 63) / 64 * nh * b), dim3(256), 0, st, x, (bf16*)o, lse,
-                       b, s, nh, scale);
+                       b, s, nh, scale, nkv);
   }
   return hipGetLastError();
 }

@@ -110,17 +110,15 @@ int host_adamw(const Plan& p, const tps_adamw* opt, int32_t step, float* master,
     A.wd_c = opt->lr * opt->weight_decay;
   }
   const int threads = n_threads > 0 ? n_threads : std::max(1u, std::thread::hardware_concurrency());
-  const int64_t h = p.h, f = p.f;
-  const int64_t rows[TPS_P_COUNT] = {3 * h, 1, h, 1, f, 1, h, 1, 1, 1, 1, 1};
-  const int64_t cols[TPS_P_COUNT] = {h, 3 * h, h, h, h, f, f, h, h, h, h, h};
   const int mat_slot[TPS_P_COUNT] = {0, -1, 1, -1, 2, -1, 3, -1, -1, -1, -1, -1};
   char* out = static_cast<char*>(params_out);
   for (int i = 0; i < TPS_P_COUNT; ++i) {
+    if (p.prow[i] == 0) continue;   // a parameter the layer kind does not have
     float* W = master + p.goff[i] / 4;
     float* M = m ? m + p.goff[i] / 4 : nullptr;
     float* V = v ? v + p.goff[i] / 4 : nullptr;
     const float* G = grad ? grad + p.goff[i] / 4 : nullptr;
-    const int64_t R = rows[i], Cn = cols[i];
+    const int64_t R = p.prow[i], Cn = p.pcol[i];
     const bool q8 = quant == TPS_Q_FP8_ROW && mat_slot[i] >= 0;
     // rows are the unit of work (a matrix row is quantized with its own scale)
     const int64_t units = R, per = Cn;

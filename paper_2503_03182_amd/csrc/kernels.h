@@ -50,11 +50,14 @@ hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, cons
                        const void* bias, const void* resid, int64_t ldr, void* aux, int64_t ldaux,
                        hipStream_t stream, int overwrite = 0);
 
-hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, void* o,
+// qkv rows: q of nh heads | k, v of nkv heads (nkv == nh: plain multi-head;
+// nkv < nh, grouped query heads, bf16 with head dim 128 only)
+hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int nkv, int d, const void* qkv, void* o,
                                 float* lse, hipStream_t st);
-// dvec: [b, nh, s] f32 scratch
-hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, const void* o,
-                                const float* lse, const void* dout, void* dqkv, float* dvec,
+// dvec: [b, nh, s] f32 scratch; kv_ws: [b s, 2 nh d] scratch of the
+// per-query-head dK, dV when nkv < nh (else unused, may be null)
+hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int nkv, int d, const void* qkv, const void* o,
+                                const float* lse, const void* dout, void* dqkv, float* dvec, void* kv_ws,
                                 hipStream_t st);
 
 // bf16 kernels on 16x16x32 MFMAs with paired causal blocks (attention_v2.hip)
@@ -63,12 +66,12 @@ hipError_t attention_fwd_v2_launch(int b, int s, int nh, int d, const void* qkv,
 // bf16, head dim 128: 32 queries per wave on 32x32x16 MFMAs, key tiles split
 // in two parts per workgroup on small grids (attention_fwd.hip); the name of
 // the kernel instance a shape launches
-hipError_t attention_fwd_v3_launch(int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
+hipError_t attention_fwd_v3_launch(int b, int s, int nh, int nkv, int d, const void* qkv, void* o, float* lse,
                                    hipStream_t st);
 const char* attention_fwd_v3_name(int b, int s, int nh);
 // bf16, head dim 128: dK/dV by 32-key waves, dQ by 32-query waves (attention_bwd.hip)
-hipError_t attention_bwd_v3_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
-                                   void* dqkv, const float* dvec, hipStream_t st);
+hipError_t attention_bwd_v3_launch(int b, int s, int nh, int nkv, int d, const void* qkv, const float* lse,
+                                   const void* dout, void* dqkv, const float* dvec, void* kv_ws, hipStream_t st);
 hipError_t attention_bwd_v2_launch(int b, int s, int nh, int d, const void* qkv, const float* lse, const void* dout,
                                    void* dqkv, const float* dvec, hipStream_t st);
 
@@ -108,6 +111,31 @@ hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_
                                   hipStream_t st, int overwrite = 0);
 hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st);
 hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st);
+// RMSNorm (no centring, no shift): out = x * rstd * gamma, rstd per row
+hipError_t rmsnorm_fwd_launch(int dtype, int rows, int cols, const void* x, const void* gamma, float eps, void* out,
+                              float* rstd, hipStream_t st);
+// dx = resid + RMSNorm^T(dout); dgamma (optional, added to) via ws as in
+// layernorm_bwd_launch
+hipError_t rmsnorm_bwd_launch(int dtype, int rows, int cols, const void* dout, const void* x, const float* rstd,
+                              const void* gamma, const void* resid, void* dx, float* dgamma, float* ws,
+                              hipStream_t st);
+// same, with the per-segment dgamma sums added into a partial block
+hipError_t rmsnorm_bwd_acc_launch(int dtype, int rows, int cols, const void* dout, const void* x, const float* rstd,
+                                  const void* gamma, const void* resid, void* dx, float* part_dgamma,
+                                  int64_t seg_stride, hipStream_t st);
+// LLAMA-style element-wise kernels (llama.hip), bf16
+// table [2][s][d/2] f32: cos, then sin, of pos * base^(-2i/d)
+hipError_t rope_table_launch(int s, int d, float base, float* table, hipStream_t st);
+// in place: columns [0, n_rot d) of each of rows rows (position row % s),
+// pairs (i, i + d/2) of every head turned by +angle (inverse: -angle)
+hipError_t rope_launch(void* x, int64_t ld, int rows, int s, int n_rot, int d, const float* table, int inverse,
+                       hipStream_t st);
+// g [rows, f] = SiLU(u[:, :f]) * u[:, f:] for u [rows, 2f]
+hipError_t swiglu_launch(int rows, int f, const void* u, void* g, hipStream_t st);
+// du [rows, 2f] from dg [rows, f] and u [rows, 2f]
+hipError_t swiglu_bwd_launch(int rows, int f, const void* dg, const void* u, void* du, hipStream_t st);
+// dqkv's k and v blocks = per key/value head sums of ws [rows, 2 nh d]
+hipError_t gqa_fold_launch(const void* ws, void* dqkv, int rows, int nh, int nkv, int d, hipStream_t st);
 // every byte of p[0, bytes) set to value
 hipError_t fill_bytes_launch(void* p, uint64_t bytes, uint8_t value, hipStream_t st);
 // out (bf16) [rows][cols] = bf16(decode_e4m3(q[r][c]) * scale[r]); cols % 8 == 0,

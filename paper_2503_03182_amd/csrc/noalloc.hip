@@ -69,7 +69,7 @@ extern "C" int tps_op_attention_bwd_noalloc(int dtype, int b, int s, int n_heads
   float* ws = nullptr;
   const int rc = scratch_for_current_device(&ws);
   if (rc != TPS_OK) return rc;
-  return check_hip(attention_bwd_launch(dtype, b, s, n_heads, head_dim, qkv, o, lse, d_o, dqkv, ws,
-                                        static_cast<hipStream_t>(stream)),
+  return check_hip(attention_bwd_launch(dtype, b, s, n_heads, n_heads, head_dim, qkv, o, lse, d_o, dqkv, ws,
+                                        nullptr, static_cast<hipStream_t>(stream)),
                    "attention_bwd_noalloc launch");
 }

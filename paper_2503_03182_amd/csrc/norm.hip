@@ -20,7 +20,8 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return ((red[0] + red[1]) + red[2]) + red[3];
 }
 
-template <typename T, int NC>
+// RMS: no centring and no shift (mean taken as 0, beta unused)
+template <typename T, int NC, bool RMS = false>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const T* __restrict__ x, const T* __restrict__ gamma,
                                                      const T* __restrict__ beta, float eps, T* __restrict__ out,
                                                      float* __restrict__ mean, float* __restrict__ rstd,
@@ -45,7 +46,7 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const T* __restrict__ x, co
 #pragma unroll
     for (int i = 0; i < VEC; ++i) s += v[c][i];
   }
-  const float mu = block_sum(s, red) / (float)cols;
+  const float mu = RMS ? 0.f : block_sum(s, red) / (float)cols;
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
@@ -65,10 +66,15 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const T* __restrict__ x, co
   for (int c = 0; c < NC; ++c) {
     const int col = (threadIdx.x + c * 256) * VEC;
     if (col < cols) {
-      const Vec16<T> g = load16(gamma + col), b = load16(beta + col);
+      const Vec16<T> g = load16(gamma + col);
+      Vec16<T> b;
+      if constexpr (!RMS) b = load16(beta + col);
       Vec16<T> o;
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) o.set(i, from_f32<T>((v[c][i] - mu) * rs * to_f32(g.get(i)) + to_f32(b.get(i))));
+      for (int i = 0; i < VEC; ++i) {
+        const float n = (v[c][i] - mu) * rs * to_f32(g.get(i));
+        o.set(i, from_f32<T>(RMS ? n : n + to_f32(b.get(i))));
+      }
       store16(orow + col, o);
     }
   }
@@ -78,7 +84,7 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const T* __restrict__ x, co
   }
 }
 
-template <typename T, int NC>
+template <typename T, int NC, bool RMS = false>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dout, const T* __restrict__ x,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
                                                      const T* __restrict__ gamma, const T* __restrict__ resid,
@@ -86,7 +92,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dout,
   constexpr int VEC = 16 / sizeof(T);
   __shared__ float red[4];
   const int row = blockIdx.x;
-  const float mu = mean[row], rs = rstd[row];
+  const float mu = RMS ? 0.f : mean[row], rs = rstd[row];
   const T* xr = x + (int64_t)row * cols;
   const T* dr = dout + (int64_t)row * cols;
   float zh[NC][VEC], gv[NC][VEC];
@@ -108,7 +114,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dout,
       for (int i = 0; i < VEC; ++i) zh[c][i] = gv[c][i] = 0.f;
     }
   }
-  const float m1 = block_sum(s1, red) / (float)cols;
+  const float m1 = RMS ? 0.f : block_sum(s1, red) / (float)cols;
   const float m2 = block_sum(s2, red) / (float)cols;
   T* o = dx + (int64_t)row * cols;
   const T* rr = resid ? resid + (int64_t)row * cols : nullptr;
@@ -133,7 +139,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dout,
 // Wave-per-row LayerNorm for rows of NV * 512 bf16 (lane l holds the 8-column
 // chunks l, l + 64, ...): reductions are wave butterflies only, four rows per
 // 256-thread workgroup.
-template <int NV>
+template <int NV, bool RMS = false>
 __global__ __launch_bounds__(256) void ln_fwd_wave_kernel(const bf16* __restrict__ x, const bf16* __restrict__ gamma,
                                                           const bf16* __restrict__ beta, float eps,
                                                           bf16* __restrict__ out, float* __restrict__ mean,
@@ -146,11 +152,13 @@ __global__ __launch_bounds__(256) void ln_fwd_wave_kernel(const bf16* __restrict
 #pragma unroll
   for (int c = 0; c < NV; ++c) xv[c] = load16(xr + (c * 64 + lane) * 8);
   float s = 0.f;
+  if constexpr (!RMS) {
 #pragma unroll
-  for (int c = 0; c < NV; ++c)
+    for (int c = 0; c < NV; ++c)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) s += to_f32(xv[c].get(i));
-  const float mu = wave_sum(s) / (float)cols;
+      for (int i = 0; i < 8; ++i) s += to_f32(xv[c].get(i));
+  }
+  const float mu = RMS ? 0.f : wave_sum(s) / (float)cols;
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < NV; ++c)
@@ -164,11 +172,15 @@ __global__ __launch_bounds__(256) void ln_fwd_wave_kernel(const bf16* __restrict
 #pragma unroll
   for (int c = 0; c < NV; ++c) {
     const int col = (c * 64 + lane) * 8;
-    const Vec16<bf16> g = load16(gamma + col), b = load16(beta + col);
+    const Vec16<bf16> g = load16(gamma + col);
+    Vec16<bf16> b;
+    if constexpr (!RMS) b = load16(beta + col);
     Vec16<bf16> o;
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      o.set(i, from_f32<bf16>((to_f32(xv[c].get(i)) - mu) * rs * to_f32(g.get(i)) + to_f32(b.get(i))));
+    for (int i = 0; i < 8; ++i) {
+      const float n = (to_f32(xv[c].get(i)) - mu) * rs * to_f32(g.get(i));
+      o.set(i, from_f32<bf16>(RMS ? n : n + to_f32(b.get(i))));
+    }
     store16(orow + col, o);
   }
   if (lane == 0) {
@@ -177,7 +189,7 @@ __global__ __launch_bounds__(256) void ln_fwd_wave_kernel(const bf16* __restrict
   }
 }
 
-template <int NV>
+template <int NV, bool RMS = false>
 __global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict__ dout, const bf16* __restrict__ x,
                                                           const float* __restrict__ mean,
                                                           const float* __restrict__ rstd,
@@ -187,7 +199,7 @@ __global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
-  const float mu = mean[row], rs = rstd[row];
+  const float mu = RMS ? 0.f : mean[row], rs = rstd[row];
   const bf16* xr = x + (int64_t)row * cols;
   const bf16* dr = dout + (int64_t)row * cols;
   Vec16<bf16> xv[NV], dv[NV], rv[NV];
@@ -209,7 +221,7 @@ __global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict
       s2 += gv * ((to_f32(xv[c].get(i)) - mu) * rs);
     }
   }
-  const float m1 = wave_sum(s1) / (float)cols;
+  const float m1 = RMS ? 0.f : wave_sum(s1) / (float)cols;
   const float m2 = wave_sum(s2) / (float)cols;
   bf16* o = dx + (int64_t)row * cols;
 #pragma unroll
@@ -231,17 +243,17 @@ __global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict
 
 // Wave-per-row launch for bf16 rows of a multiple of 512 columns (up to 8192);
 // returns false when the shape needs the block-per-row kernels.
-#define TPS_WAVE_ROW_DISPATCH(KERNEL, rows, cols, st, ...)                                          \
+#define TPS_WAVE_ROW_DISPATCH(KERNEL, FLAG, rows, cols, st, ...)                                       \
   ([&]() -> bool {                                                                                  \
     if ((cols) % 512 != 0 || (cols) > 8192) return false;                                            \
     const dim3 grid_(((rows) + 3) / 4), block_(256);                                                 \
     switch ((cols) / 512) {                                                                          \
-      case 1: hipLaunchKernelGGL((KERNEL<1>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
-      case 2: hipLaunchKernelGGL((KERNEL<2>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
-      case 4: hipLaunchKernelGGL((KERNEL<4>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
-      case 8: hipLaunchKernelGGL((KERNEL<8>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
-      case 10: hipLaunchKernelGGL((KERNEL<10>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break; \
-      case 16: hipLaunchKernelGGL((KERNEL<16>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break; \
+      case 1: hipLaunchKernelGGL((KERNEL<1, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
+      case 2: hipLaunchKernelGGL((KERNEL<2, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
+      case 4: hipLaunchKernelGGL((KERNEL<4, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
+      case 8: hipLaunchKernelGGL((KERNEL<8, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break;   \
+      case 10: hipLaunchKernelGGL((KERNEL<10, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break; \
+      case 16: hipLaunchKernelGGL((KERNEL<16, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols); break; \
       default: return false;                                                                         \
     }                                                                                                \
     return true;                                                                                     \
@@ -255,7 +267,8 @@ __global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict
 // dst[segment * seg_stride + k * k_stride + c], stored (ACC false) or added
 // to what is there (ACC true: one owner per element, so calls in stream order
 // accumulate in a fixed order).
-template <typename T, bool LN, bool ACC>
+// MODE 2 (RMS): one output, sum dout * x * rstd (no centring).
+template <typename T, int MODE, bool ACC>
 __global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ x, int64_t ldx,
                                                           const T* __restrict__ xin, const float* __restrict__ mean,
                                                           const float* __restrict__ rstd, float* __restrict__ dst,
@@ -263,6 +276,7 @@ __global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ 
                                                           int seg_rows) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int COLS = 8 * VEC;                 // columns per block
+  constexpr bool LN = MODE == 1, ZH = MODE != 0;
   __shared__ float red[LN ? 2 : 1][32][COLS + 1];
   const int cc = threadIdx.x & 7, rl = threadIdx.x >> 3;
   const int col = blockIdx.x * COLS + cc * VEC;
@@ -282,9 +296,9 @@ __global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ 
         const int ru = r + 32 * u;
         if (ru < r1) {
           v[u] = load16(x + (int64_t)ru * ldx + col);
-          if constexpr (LN) {
+          if constexpr (ZH) {
             xv[u] = load16(xin + (int64_t)ru * cols + col);
-            mu[u] = mean[ru];
+            mu[u] = LN ? mean[ru] : 0.f;
             rs[u] = rstd[ru];
           }
         }
@@ -299,6 +313,9 @@ __global__ __launch_bounds__(256) void colsum_part_kernel(const T* __restrict__ 
               a[i] += d;
               z[i] += d * ((to_f32(xv[u].get(i)) - mu[u]) * rs[u]);
             }
+          } else if constexpr (ZH) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) a[i] += to_f32(v[u].get(i)) * (to_f32(xv[u].get(i)) * rs[u]);
           } else {
 #pragma unroll
             for (int i = 0; i < VEC; ++i) a[i] += to_f32(v[u].get(i));
@@ -428,35 +445,39 @@ __global__ __launch_bounds__(256) void fill_bytes_kernel(u32x4* p, uint64_t n16,
 }
 
 // Per-row kernels are instantiated for NC 16-byte chunks per thread.
-#define TPS_ROW_DISPATCH(KERNEL, T, rows, cols, st, ...)                                        \
+#define TPS_ROW_DISPATCH(KERNEL, T, FLAG, rows, cols, st, ...)                                     \
   do {                                                                                           \
     constexpr int VEC_ = 16 / sizeof(T);                                                         \
     const int nc_ = (cols + 256 * VEC_ - 1) / (256 * VEC_);                                      \
     dim3 grid_(rows), block_(256);                                                               \
-    if (nc_ <= 1) hipLaunchKernelGGL((KERNEL<T, 1>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);       \
-    else if (nc_ <= 2) hipLaunchKernelGGL((KERNEL<T, 2>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
-    else if (nc_ <= 4) hipLaunchKernelGGL((KERNEL<T, 4>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
-    else if (nc_ <= 8) hipLaunchKernelGGL((KERNEL<T, 8>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
-    else hipLaunchKernelGGL((KERNEL<T, 16>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);               \
+    if (nc_ <= 1) hipLaunchKernelGGL((KERNEL<T, 1, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);       \
+    else if (nc_ <= 2) hipLaunchKernelGGL((KERNEL<T, 2, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
+    else if (nc_ <= 4) hipLaunchKernelGGL((KERNEL<T, 4, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
+    else if (nc_ <= 8) hipLaunchKernelGGL((KERNEL<T, 8, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);  \
+    else hipLaunchKernelGGL((KERNEL<T, 16, FLAG>), grid_, block_, 0, st, __VA_ARGS__, rows, cols);               \
   } while (0)
 
 template <typename T>
 hipError_t colsum_typed(int rows, int cols, const void* x, int64_t ldx, const void* xin, const float* mean,
-                        const float* rstd, float* out0, float* out1, float* ws, bool ln, hipStream_t st) {
+                        const float* rstd, float* out0, float* out1, float* ws, int mode, hipStream_t st) {
   constexpr int VEC = 16 / sizeof(T);
   const int seg = (int)colsum_seg_rows(rows);
   const int parts = (int)colsum_segments(rows);
   dim3 grid((cols + 8 * VEC - 1) / (8 * VEC), parts);
-  const int64_t nk = ln ? 2 : 1;
-  if (ln)
-    hipLaunchKernelGGL((colsum_part_kernel<T, true, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
-                       static_cast<const T*>(xin), mean, rstd, ws, nk * cols, (int64_t)cols, rows, cols, seg);
+  const int64_t nk = mode == 1 ? 2 : 1;
+  const T* xi = static_cast<const T*>(mode ? xin : nullptr);
+  if (mode == 1)
+    hipLaunchKernelGGL((colsum_part_kernel<T, 1, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx, xi,
+                       mean, rstd, ws, nk * cols, (int64_t)cols, rows, cols, seg);
+  else if (mode == 2)
+    hipLaunchKernelGGL((colsum_part_kernel<T, 2, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx, xi,
+                       mean, rstd, ws, nk * cols, (int64_t)cols, rows, cols, seg);
   else
-    hipLaunchKernelGGL((colsum_part_kernel<T, false, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
-                       static_cast<const T*>(nullptr), mean, rstd, ws, nk * cols, (int64_t)cols, rows, cols, seg);
+    hipLaunchKernelGGL((colsum_part_kernel<T, 0, false>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx, xi,
+                       mean, rstd, ws, nk * cols, (int64_t)cols, rows, cols, seg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, ws, parts, ln ? 2 : 1,
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, ws, parts, (int)nk,
                      cols, out0, out1);
   return hipGetLastError();
 }
@@ -464,18 +485,22 @@ hipError_t colsum_typed(int rows, int cols, const void* x, int64_t ldx, const vo
 // Pass 1 only, accumulating into a caller's partial block.
 template <typename T>
 hipError_t colsum_acc_typed(int rows, int cols, const void* x, int64_t ldx, const void* xin, const float* mean,
-                            const float* rstd, float* part0, int64_t k_stride, int64_t seg_stride, bool ln,
+                            const float* rstd, float* part0, int64_t k_stride, int64_t seg_stride, int mode,
                             hipStream_t st) {
   constexpr int VEC = 16 / sizeof(T);
   const int seg = (int)colsum_seg_rows(rows);
   const int parts = (int)colsum_segments(rows);
   dim3 grid((cols + 8 * VEC - 1) / (8 * VEC), parts);
-  if (ln)
-    hipLaunchKernelGGL((colsum_part_kernel<T, true, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
-                       static_cast<const T*>(xin), mean, rstd, part0, seg_stride, k_stride, rows, cols, seg);
+  const T* xi = static_cast<const T*>(mode ? xin : nullptr);
+  if (mode == 1)
+    hipLaunchKernelGGL((colsum_part_kernel<T, 1, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx, xi,
+                       mean, rstd, part0, seg_stride, k_stride, rows, cols, seg);
+  else if (mode == 2)
+    hipLaunchKernelGGL((colsum_part_kernel<T, 2, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx, xi,
+                       mean, rstd, part0, seg_stride, k_stride, rows, cols, seg);
   else
-    hipLaunchKernelGGL((colsum_part_kernel<T, false, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx,
-                       static_cast<const T*>(nullptr), mean, rstd, part0, seg_stride, k_stride, rows, cols, seg);
+    hipLaunchKernelGGL((colsum_part_kernel<T, 0, true>), grid, dim3(256), 0, st, static_cast<const T*>(x), ldx, xi,
+                       mean, rstd, part0, seg_stride, k_stride, rows, cols, seg);
   return hipGetLastError();
 }
 
@@ -487,8 +512,8 @@ hipError_t colsum_acc_launch(int dtype, int rows, int cols, const void* x, int64
                              int64_t seg_stride, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   if (dtype == TPS_BF16)
-    return colsum_acc_typed<bf16>(rows, cols, x, ldx, nullptr, nullptr, nullptr, part, 0, seg_stride, false, st);
-  return colsum_acc_typed<float>(rows, cols, x, ldx, nullptr, nullptr, nullptr, part, 0, seg_stride, false, st);
+    return colsum_acc_typed<bf16>(rows, cols, x, ldx, nullptr, nullptr, nullptr, part, 0, seg_stride, 0, st);
+  return colsum_acc_typed<float>(rows, cols, x, ldx, nullptr, nullptr, nullptr, part, 0, seg_stride, 0, st);
 }
 
 hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_t seg_stride, float* grads,
@@ -505,12 +530,12 @@ hipError_t layernorm_fwd_launch(int dtype, int rows, int cols, const void* x, co
                                 hipStream_t st) {
   if (rows == 0) return hipSuccess;
   if (dtype == TPS_BF16) {
-    if (!TPS_WAVE_ROW_DISPATCH(ln_fwd_wave_kernel, rows, cols, st, (const bf16*)x, (const bf16*)gamma,
+    if (!TPS_WAVE_ROW_DISPATCH(ln_fwd_wave_kernel, false, rows, cols, st, (const bf16*)x, (const bf16*)gamma,
                                (const bf16*)beta, eps, (bf16*)out, mean, rstd))
-      TPS_ROW_DISPATCH(ln_fwd_kernel, bf16, rows, cols, st, (const bf16*)x, (const bf16*)gamma, (const bf16*)beta,
+      TPS_ROW_DISPATCH(ln_fwd_kernel, bf16, false, rows, cols, st, (const bf16*)x, (const bf16*)gamma, (const bf16*)beta,
                        eps, (bf16*)out, mean, rstd);
   } else
-    TPS_ROW_DISPATCH(ln_fwd_kernel, float, rows, cols, st, (const float*)x, (const float*)gamma,
+    TPS_ROW_DISPATCH(ln_fwd_kernel, float, false, rows, cols, st, (const float*)x, (const float*)gamma,
                      (const float*)beta, eps, (float*)out, mean, rstd);
   return hipGetLastError();
 }
@@ -521,19 +546,19 @@ hipError_t layernorm_bwd_launch(int dtype, int rows, int cols, const void* dout,
                                 float* ws, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   if (dtype == TPS_BF16) {
-    if (!TPS_WAVE_ROW_DISPATCH(ln_bwd_wave_kernel, rows, cols, st, (const bf16*)dout, (const bf16*)x, mean, rstd,
+    if (!TPS_WAVE_ROW_DISPATCH(ln_bwd_wave_kernel, false, rows, cols, st, (const bf16*)dout, (const bf16*)x, mean, rstd,
                                (const bf16*)gamma, (const bf16*)resid, (bf16*)dx))
-      TPS_ROW_DISPATCH(ln_bwd_kernel, bf16, rows, cols, st, (const bf16*)dout, (const bf16*)x, mean, rstd,
+      TPS_ROW_DISPATCH(ln_bwd_kernel, bf16, false, rows, cols, st, (const bf16*)dout, (const bf16*)x, mean, rstd,
                        (const bf16*)gamma, (const bf16*)resid, (bf16*)dx);
   } else
-    TPS_ROW_DISPATCH(ln_bwd_kernel, float, rows, cols, st, (const float*)dout, (const float*)x, mean, rstd,
+    TPS_ROW_DISPATCH(ln_bwd_kernel, float, false, rows, cols, st, (const float*)dout, (const float*)x, mean, rstd,
                      (const float*)gamma, (const float*)resid, (float*)dx);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || (dgamma == nullptr && dbeta == nullptr)) return e;
   // dbeta = sum dout (k = 0), dgamma = sum dout * zhat (k = 1)
   if (dtype == TPS_BF16)
-    return colsum_typed<bf16>(rows, cols, dout, cols, x, mean, rstd, dbeta, dgamma, ws, true, st);
-  return colsum_typed<float>(rows, cols, dout, cols, x, mean, rstd, dbeta, dgamma, ws, true, st);
+    return colsum_typed<bf16>(rows, cols, dout, cols, x, mean, rstd, dbeta, dgamma, ws, 1, st);
+  return colsum_typed<float>(rows, cols, dout, cols, x, mean, rstd, dbeta, dgamma, ws, 1, st);
 }
 
 hipError_t layernorm_bwd_acc_launch(int dtype, int rows, int cols, const void* dout, const void* x,
@@ -545,16 +570,16 @@ hipError_t layernorm_bwd_acc_launch(int dtype, int rows, int cols, const void* d
                                       nullptr, st);
   if (e != hipSuccess) return e;
   if (dtype == TPS_BF16)
-    return colsum_acc_typed<bf16>(rows, cols, dout, cols, x, mean, rstd, part_dbeta, k_stride, seg_stride, true, st);
-  return colsum_acc_typed<float>(rows, cols, dout, cols, x, mean, rstd, part_dbeta, k_stride, seg_stride, true, st);
+    return colsum_acc_typed<bf16>(rows, cols, dout, cols, x, mean, rstd, part_dbeta, k_stride, seg_stride, 1, st);
+  return colsum_acc_typed<float>(rows, cols, dout, cols, x, mean, rstd, part_dbeta, k_stride, seg_stride, 1, st);
 }
 
 hipError_t colsum_launch(int dtype, int rows, int cols, const void* x, int64_t ldx, float* out,
                          float* ws, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   if (dtype == TPS_BF16)
-    return colsum_typed<bf16>(rows, cols, x, ldx, nullptr, nullptr, nullptr, out, nullptr, ws, false, st);
-  return colsum_typed<float>(rows, cols, x, ldx, nullptr, nullptr, nullptr, out, nullptr, ws, false, st);
+    return colsum_typed<bf16>(rows, cols, x, ldx, nullptr, nullptr, nullptr, out, nullptr, ws, 0, st);
+  return colsum_typed<float>(rows, cols, x, ldx, nullptr, nullptr, nullptr, out, nullptr, ws, 0, st);
 }
 
 hipError_t gelu_launch(int dtype, int64_t n, const void* u, void* g, hipStream_t st) {
@@ -580,6 +605,57 @@ hipError_t transpose_launch(int dtype, int rows, int cols, const void* in, int64
     hipLaunchKernelGGL((transpose_kernel<float>), grid, dim3(256), 0, st, (const float*)in, ldi, (float*)out, ldo, rows,
                        cols);
   return hipGetLastError();
+}
+
+hipError_t rmsnorm_fwd_launch(int dtype, int rows, int cols, const void* x, const void* gamma, float eps, void* out,
+                              float* rstd, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  if (dtype == TPS_BF16) {
+    if (!TPS_WAVE_ROW_DISPATCH(ln_fwd_wave_kernel, true, rows, cols, st, (const bf16*)x, (const bf16*)gamma,
+                               (const bf16*)nullptr, eps, (bf16*)out, (float*)nullptr, rstd))
+      TPS_ROW_DISPATCH(ln_fwd_kernel, bf16, true, rows, cols, st, (const bf16*)x, (const bf16*)gamma,
+                       (const bf16*)nullptr, eps, (bf16*)out, (float*)nullptr, rstd);
+  } else
+    TPS_ROW_DISPATCH(ln_fwd_kernel, float, true, rows, cols, st, (const float*)x, (const float*)gamma,
+                     (const float*)nullptr, eps, (float*)out, (float*)nullptr, rstd);
+  return hipGetLastError();
+}
+
+namespace {
+hipError_t rms_bwd_rows(int dtype, int rows, int cols, const void* dout, const void* x, const float* rstd,
+                        const void* gamma, const void* resid, void* dx, hipStream_t st) {
+  if (dtype == TPS_BF16) {
+    if (!TPS_WAVE_ROW_DISPATCH(ln_bwd_wave_kernel, true, rows, cols, st, (const bf16*)dout, (const bf16*)x,
+                               (const float*)nullptr, rstd, (const bf16*)gamma, (const bf16*)resid, (bf16*)dx))
+      TPS_ROW_DISPATCH(ln_bwd_kernel, bf16, true, rows, cols, st, (const bf16*)dout, (const bf16*)x,
+                       (const float*)nullptr, rstd, (const bf16*)gamma, (const bf16*)resid, (bf16*)dx);
+  } else
+    TPS_ROW_DISPATCH(ln_bwd_kernel, float, true, rows, cols, st, (const float*)dout, (const float*)x,
+                     (const float*)nullptr, rstd, (const float*)gamma, (const float*)resid, (float*)dx);
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t rmsnorm_bwd_launch(int dtype, int rows, int cols, const void* dout, const void* x, const float* rstd,
+                              const void* gamma, const void* resid, void* dx, float* dgamma, float* ws,
+                              hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  const hipError_t e = rms_bwd_rows(dtype, rows, cols, dout, x, rstd, gamma, resid, dx, st);
+  if (e != hipSuccess || dgamma == nullptr) return e;
+  if (dtype == TPS_BF16)
+    return colsum_typed<bf16>(rows, cols, dout, cols, x, nullptr, rstd, dgamma, nullptr, ws, 2, st);
+  return colsum_typed<float>(rows, cols, dout, cols, x, nullptr, rstd, dgamma, nullptr, ws, 2, st);
+}
+
+hipError_t rmsnorm_bwd_acc_launch(int dtype, int rows, int cols, const void* dout, const void* x, const float* rstd,
+                                  const void* gamma, const void* resid, void* dx, float* part_dgamma,
+                                  int64_t seg_stride, hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  const hipError_t e = rms_bwd_rows(dtype, rows, cols, dout, x, rstd, gamma, resid, dx, st);
+  if (e != hipSuccess) return e;
+  if (dtype == TPS_BF16)
+    return colsum_acc_typed<bf16>(rows, cols, dout, cols, x, nullptr, rstd, part_dgamma, 0, seg_stride, 2, st);
+  return colsum_acc_typed<float>(rows, cols, dout, cols, x, nullptr, rstd, part_dgamma, 0, seg_stride, 2, st);
 }
 
 hipError_t fill_bytes_launch(void* p, uint64_t bytes, uint8_t value, hipStream_t st) {

@@ -81,7 +81,7 @@ extern "C" int tps_op_attention_fwd(int dtype, int b, int s, int n_heads, int he
   if (b < 0 || s < 0 || n_heads <= 0) return bad("attention: shape");
   if (b == 0 || s == 0) return TPS_OK;
   if (!qkv || !o || !aligned16(qkv)) return bad("attention: qkv/o");
-  return check_hip(attention_fwd_launch(dtype, b, s, n_heads, head_dim, qkv, o, lse, (hipStream_t)stream),
+  return check_hip(attention_fwd_launch(dtype, b, s, n_heads, n_heads, head_dim, qkv, o, lse, (hipStream_t)stream),
                    "attention_fwd launch");
 }
 
@@ -95,9 +95,89 @@ extern "C" int tps_op_attention_bwd(int dtype, int b, int s, int n_heads, int he
   if (b == 0 || s == 0) return TPS_OK;
   if (!qkv || !o || !lse || !d_o || !dqkv || !workspace) return bad("attention_bwd: null pointer");
   if (!aligned16(qkv) || !aligned16(o) || !aligned16(d_o)) return bad("attention_bwd: alignment");
-  return check_hip(attention_bwd_launch(dtype, b, s, n_heads, head_dim, qkv, o, lse, d_o, dqkv, workspace,
-                                        (hipStream_t)stream),
+  return check_hip(attention_bwd_launch(dtype, b, s, n_heads, n_heads, head_dim, qkv, o, lse, d_o, dqkv, workspace,
+                                        nullptr, (hipStream_t)stream),
                    "attention_bwd launch");
+}
+
+extern "C" int tps_op_rmsnorm_fwd(int dtype, int rows, int cols, const void* x, const void* gamma, float eps,
+                                  void* out, float* rstd, void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype)) return bad("rmsnorm: dtype");
+  if (rows < 0 || cols <= 0 || cols > 16384 || cols % vec_of(dtype)) return bad("rmsnorm: shape");
+  if (!(eps >= 0.f)) return bad("rmsnorm: eps");
+  if (rows == 0) return TPS_OK;
+  if (!x || !gamma || !out) return bad("rmsnorm: null pointer");
+  return check_hip(rmsnorm_fwd_launch(dtype, rows, cols, x, gamma, eps, out, rstd, (hipStream_t)stream),
+                   "rmsnorm_fwd launch");
+}
+
+extern "C" int tps_op_rmsnorm_bwd(int dtype, int rows, int cols, const void* dout, const void* x, const float* rstd,
+                                  const void* gamma, const void* resid_grad, void* dx, float* dgamma,
+                                  float* workspace, void* stream) {
+  clear_error();
+  if (!dtype_ok(dtype)) return bad("rmsnorm_bwd: dtype");
+  if (rows < 0 || cols <= 0 || cols > 16384 || cols % vec_of(dtype)) return bad("rmsnorm_bwd: shape");
+  if (rows == 0) return TPS_OK;
+  if (!dout || !x || !rstd || !gamma || !dx) return bad("rmsnorm_bwd: null pointer");
+  if (dgamma && !workspace) return bad("rmsnorm_bwd: workspace needed for dgamma");
+  return check_hip(rmsnorm_bwd_launch(dtype, rows, cols, dout, x, rstd, gamma, resid_grad, dx, dgamma, workspace,
+                                      (hipStream_t)stream),
+                   "rmsnorm_bwd launch");
+}
+
+extern "C" int tps_op_rope(void* x, int64_t ld, int rows, int s, int n_rot, int d, float base, int inverse,
+                           float* table, void* stream) {
+  clear_error();
+  if (rows < 0 || s <= 0 || n_rot < 0 || d <= 0 || d % 16 || ld % 8 || ld < (int64_t)n_rot * d)
+    return bad("rope: shape");
+  if (!(base > 1.f)) return bad("rope: base must be > 1");
+  if (rows == 0 || n_rot == 0) return TPS_OK;
+  if (!x || !table || !aligned16(x) || !aligned16(table)) return bad("rope: pointers");
+  hipError_t e = rope_table_launch(s, d, base, table, (hipStream_t)stream);
+  if (e == hipSuccess) e = rope_launch(x, ld, rows, s, n_rot, d, table, inverse, (hipStream_t)stream);
+  return check_hip(e, "rope launch");
+}
+
+extern "C" int tps_op_swiglu_fwd(int rows, int f, const void* u, void* g, void* stream) {
+  clear_error();
+  if (rows < 0 || f <= 0 || f % 8) return bad("swiglu: shape");
+  if (rows == 0) return TPS_OK;
+  if (!u || !g || !aligned16(u) || !aligned16(g)) return bad("swiglu: pointers");
+  return check_hip(swiglu_launch(rows, f, u, g, (hipStream_t)stream), "swiglu launch");
+}
+
+extern "C" int tps_op_swiglu_bwd(int rows, int f, const void* dg, const void* u, void* du, void* stream) {
+  clear_error();
+  if (rows < 0 || f <= 0 || f % 8) return bad("swiglu_bwd: shape");
+  if (rows == 0) return TPS_OK;
+  if (!dg || !u || !du || !aligned16(dg) || !aligned16(u) || !aligned16(du)) return bad("swiglu_bwd: pointers");
+  return check_hip(swiglu_bwd_launch(rows, f, dg, u, du, (hipStream_t)stream), "swiglu_bwd launch");
+}
+
+extern "C" int tps_op_attention_gqa_fwd(int b, int s, int n_heads, int n_kv, const void* qkv, void* o, float* lse,
+                                        void* stream) {
+  clear_error();
+  if (b < 0 || s < 0 || n_heads <= 0 || n_kv <= 0 || n_heads % n_kv) return bad("attention_gqa: heads");
+  if (b == 0 || s == 0) return TPS_OK;
+  if (!qkv || !o || !aligned16(qkv) || !aligned16(o)) return bad("attention_gqa: qkv/o");
+  return check_hip(attention_fwd_launch(TPS_BF16, b, s, n_heads, n_kv, 128, qkv, o, lse, (hipStream_t)stream),
+                   "attention_gqa_fwd launch");
+}
+
+extern "C" int tps_op_attention_gqa_bwd(int b, int s, int n_heads, int n_kv, const void* qkv, const void* o,
+                                        const float* lse, const void* d_o, void* dqkv, float* workspace,
+                                        void* kv_workspace, void* stream) {
+  clear_error();
+  if (b < 0 || s < 0 || n_heads <= 0 || n_kv <= 0 || n_heads % n_kv) return bad("attention_gqa_bwd: heads");
+  if (b == 0 || s == 0) return TPS_OK;
+  if (!qkv || !o || !lse || !d_o || !dqkv || !workspace) return bad("attention_gqa_bwd: null pointer");
+  if (n_kv != n_heads && (!kv_workspace || !aligned16(kv_workspace)))
+    return bad("attention_gqa_bwd: kv_workspace needed for grouped heads");
+  if (!aligned16(qkv) || !aligned16(o) || !aligned16(d_o) || !aligned16(dqkv)) return bad("attention_gqa_bwd: alignment");
+  return check_hip(attention_bwd_launch(TPS_BF16, b, s, n_heads, n_kv, 128, qkv, o, lse, d_o, dqkv, workspace,
+                                        kv_workspace, (hipStream_t)stream),
+                   "attention_gqa_bwd launch");
 }
 
 extern "C" int tps_op_colsum(int dtype, int rows, int cols, const void* x, int64_t ldx, float* out,

@@ -68,10 +68,10 @@ struct TimedSlotPool {
 double op_flops(const Plan& p, int op) {
   const double T = p.T, h = p.h, f = p.f;
   switch (op) {
-    case OP_QKV: return 2.0 * T * h * 3.0 * h;
+    case OP_QKV: return 2.0 * T * h * (double)p.qw;
     case OP_ATTN: return 2.0 * p.b * h * (double)p.s * (p.s + 1);
     case OP_OPROJ: return 2.0 * T * h * h;
-    case OP_FC1: return 2.0 * T * h * f;
+    case OP_FC1: return 2.0 * T * h * (double)p.uw;
     case OP_FC2: return 2.0 * T * f * h;
     default: return 0.0;
   }
@@ -282,6 +282,30 @@ int make_plan(const tps_config* c, Plan* out) {
   // same-device A/B of the two arrangements: inline was 2-3% faster at 4096
   // and 8192 tokens per micro-batch, 10% slower at 2048
   p.wgrad_inline = c->wgrad_stream == TPS_WGRAD_INLINE || (c->wgrad_stream == TPS_WGRAD_AUTO && p.T >= 4096);
+  if (c->arch != TPS_ARCH_GPT && c->arch != TPS_ARCH_LLAMA) return inval("arch");
+  p.llama = c->arch == TPS_ARCH_LLAMA;
+  p.nkv = c->n_kv_heads ? c->n_kv_heads : p.nh;
+  if (p.llama) {
+    if (p.dtype != TPS_BF16 || p.d != 128) return inval("LLAMA layers need bf16 storage and head dim 128");
+    if (p.nkv < 1 || p.nkv > p.nh || p.nh % p.nkv) return inval("n_kv_heads must divide n_heads");
+    p.rope_base = c->rope_base == 0.f ? 10000.f : c->rope_base;
+    if (!(p.rope_base > 1.f)) return inval("rope_base must be > 1");
+  } else if (p.nkv != p.nh) {
+    return inval("n_kv_heads applies to LLAMA layers only");
+  }
+  p.qw = (int64_t)(p.nh + 2 * p.nkv) * p.d;
+  p.uw = p.llama ? 2 * (int64_t)p.f : p.f;
+  {
+    const int64_t H = p.h, F = p.f;
+    const int64_t gpt_r[TPS_P_COUNT] = {3 * H, 1, H, 1, F, 1, H, 1, 1, 1, 1, 1};
+    const int64_t gpt_c[TPS_P_COUNT] = {H, 3 * H, H, H, H, F, F, H, H, H, H, H};
+    const int64_t lla_r[TPS_P_COUNT] = {p.qw, 0, H, 0, 2 * F, 0, H, 0, 1, 0, 1, 0};
+    const int64_t lla_c[TPS_P_COUNT] = {H, 0, H, 0, H, 0, F, 0, H, 0, H, 0};
+    for (int i = 0; i < TPS_P_COUNT; ++i) {
+      p.prow[i] = p.llama ? lla_r[i] : gpt_r[i];
+      p.pcol[i] = p.llama ? lla_c[i] : gpt_c[i];
+    }
+  }
   p.quant = c->weights_quant;
   if (p.quant != TPS_Q_NONE && p.quant != TPS_Q_FP8_ROW) return inval("weights_quant");
   if (p.quant == TPS_Q_FP8_ROW && (p.weights != TPS_W_STREAM || p.dtype != TPS_BF16))
@@ -308,12 +332,14 @@ int make_plan(const tps_config* c, Plan* out) {
   const uint64_t T = p.T, h = p.h, f = p.f, es = p.esize;
   p.tbytes[TPS_T_X] = p.tbytes[TPS_T_A] = p.tbytes[TPS_T_O] = T * h * es;
   p.tbytes[TPS_T_X1] = p.tbytes[TPS_T_C] = T * h * es;
-  p.tbytes[TPS_T_QKV] = T * 3 * h * es;
-  p.tbytes[TPS_T_U] = p.tbytes[TPS_T_G] = T * f * es;
+  p.tbytes[TPS_T_QKV] = T * (uint64_t)p.qw * es;
+  p.tbytes[TPS_T_U] = T * (uint64_t)p.uw * es;
+  p.tbytes[TPS_T_G] = T * f * es;
   p.tbytes[TPS_T_LSE] = (uint64_t)p.b * p.nh * p.s * 4;
-  p.tbytes[TPS_T_LN1] = p.tbytes[TPS_T_LN2] = 2 * T * 4;
+  p.tbytes[TPS_T_LN1] = p.tbytes[TPS_T_LN2] = (p.llama ? 1 : 2) * T * 4;
   {
-    const uint64_t elems[TPS_P_COUNT] = {3 * h * h, 3 * h, h * h, h, f * h, f, h * f, h, h, h, h, h};
+    uint64_t elems[TPS_P_COUNT];
+    for (int i = 0; i < TPS_P_COUNT; ++i) elems[i] = (uint64_t)(p.prow[i] * p.pcol[i]);
     uint64_t po = 0, go = 0;
     for (int i = 0; i < TPS_P_COUNT; ++i) {
       p.poff[i] = po; po = align256(po + elems[i] * es);
@@ -323,7 +349,8 @@ int make_plan(const tps_config* c, Plan* out) {
     // quantized block: matrices as one byte per element, their f32 row
     // scales after the vectors
     const bool is_mat[TPS_P_COUNT] = {true, false, true, false, true, false, true, false, false, false, false, false};
-    const uint64_t rows[4] = {3 * h, h, f, h};
+    const uint64_t rows[4] = {(uint64_t)p.prow[TPS_P_W_QKV], (uint64_t)p.prow[TPS_P_W_O],
+                              (uint64_t)p.prow[TPS_P_W_1], (uint64_t)p.prow[TPS_P_W_2]};
     uint64_t qo = 0;
     for (int i = 0; i < TPS_P_COUNT; ++i) {
       p.qoff[i] = qo;
@@ -430,7 +457,8 @@ int make_plan(const tps_config* c, Plan* out) {
   assign_slots(p, tF, tB, tc);
 
   // backward working buffers
-  const uint64_t hb = align256(T * h * es), fb = align256(T * f * es), qb = align256(T * 3 * h * es);
+  const uint64_t hb = align256(T * h * es), fb = align256(T * (uint64_t)p.uw * es),
+                 qb = align256(T * (uint64_t)p.qw * es);
   p.defer_join = p.weights == TPS_W_RESIDENT && (p.granularity == TPS_GRAN_SEGMENT || p.n_replay_layers == 0);
   p.replay_independent = true;
   for (int l = 1; l < p.L; ++l)
@@ -451,12 +479,21 @@ int make_plan(const tps_config* c, Plan* out) {
     }
     p.work.t1 = take(hb);
     p.work.dvec = take(align256((uint64_t)p.b * p.nh * p.s * 4));
+    p.work.dg = p.work.kvws = p.work.rope = p.work.zbias = kNone;
+    if (p.llama) {
+      p.work.dg = take(align256(T * f * es));
+      if (p.nkv != p.nh) p.work.kvws = take(align256(T * 2 * h * es));
+      p.work.rope = take(align256((uint64_t)p.s * p.d * 4));
+      p.work.zbias = take(align256(h * es));
+    }
     p.work_bytes = o;
   }
 
   {
     const int64_t H = (int64_t)h, F = (int64_t)f;
-    const int64_t widths[Plan::BP_COUNT] = {3 * H, H, F, H, H, H, H, H};
+    const int64_t gpt[Plan::BP_COUNT] = {3 * H, H, F, H, H, H, H, H};
+    const int64_t lla[Plan::BP_COUNT] = {0, 0, 0, 0, 0, H, 0, H};
+    const int64_t* widths = p.llama ? lla : gpt;
     p.bpc[0] = 0;
     for (int i = 0; i < Plan::BP_COUNT; ++i) p.bpc[i + 1] = p.bpc[i] + widths[i];
     p.bpart_segs = (int)colsum_segments(T);
@@ -469,7 +506,7 @@ int make_plan(const tps_config* c, Plan* out) {
                      ? (uint64_t)p.window * (p.pbytes + p.gbytes + (p.quant ? align256(p.qbytes) : 0))
                      : 0;
   {
-    const uint64_t mats[4] = {3 * h * h, h * h, f * h, h * f};
+    const uint64_t mats[4] = {(uint64_t)p.qw * h, h * h, (uint64_t)p.uw * h, h * f};
     uint64_t o = 0;
     for (int i = 0; i < 4; ++i) {
       p.wtoff[i] = o;

@@ -18,6 +18,14 @@ constexpr uint64_t kNone = ~0ull;
 struct Plan {
   // shape
   int L = 0, h = 0, nh = 0, d = 0, f = 0, s = 0, b = 0, M = 0, T = 0;
+  // layer kind: LLAMA (RMSNorm, rotary embedding, nkv key/value heads, SwiGLU,
+  // no biases) or GPT; qw: width of the packed qkv tensor, uw: of u
+  bool llama = false;
+  int nkv = 0;
+  float rope_base = 10000.f;
+  int64_t qw = 0, uw = 0;
+  // shape of each packed parameter ([rows][cols]; 0 x 0 when absent)
+  int64_t prow[TPS_P_COUNT] = {}, pcol[TPS_P_COUNT] = {};
   int dtype = TPS_BF16, esize = 2;
   float eps = 1e-5f;
   int weights = TPS_W_RESIDENT, window = 2, granularity = TPS_GRAN_SEGMENT, lookahead = 1;
@@ -69,8 +77,13 @@ struct Plan {
   // gradients (dx1, du, dqkv: one set per layer parity when defer_join),
   // the attention output projection's input gradient (t1) and the
   // attention backward's row dot products (dvec)
+  // (LLAMA: dg, the gradient of the SwiGLU output before its backward;
+  // kvws, the per-query-head key/value gradients of grouped attention; rope,
+  // the rotation table; zbias, a zero vector standing in for the absent
+  // biases in the residual epilogues)
   struct Work {
     uint64_t g[3], dx1[2], du[2], dqkv[2], t1, dvec;
+    uint64_t dg, kvws, rope, zbias;
   } work{};
   uint64_t work_bytes = 0;
   // the parameter-gradient kernels of a layer backward may still run while

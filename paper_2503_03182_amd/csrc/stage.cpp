@@ -229,6 +229,7 @@ struct tps_stage {
   // entry) is filled with all-ones bytes, a NaN in f32 and bf16, so a read
   // that should not happen shows in the results
   bool poison = false;
+  bool llama_tables = false;   // rotation table and zero bias written
   int poison_fill(void* ptr, uint64_t bytes, hipStream_t on) {
     if (poison && bytes) TPS_HIP(fill_bytes_launch(ptr, bytes, 0xFF, on));
     return TPS_OK;
@@ -291,6 +292,8 @@ struct tps_stage {
   }
   int fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots);
   int bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp, bool defer);
+  int bwd_layer_llama(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp,
+                      bool defer);
   // stream `on` waits for the lagging parameter-gradient kernels of layer l
   // (and all gs work before them), if any are pending
   int wait_gs_layer_on(int l, hipStream_t on) {
@@ -360,19 +363,19 @@ int tps_stage::load_params(int l, int e) {
   char* q = qstage_of(e);
   TPS_HIP(hipMemcpyAsync(q, lp[l], p.qbytes, hipMemcpyHostToDevice, ps));
   stats.h2d_bytes += p.qbytes;
-  const int64_t h = p.h, f = p.f;
   const int mats[4] = {TPS_P_W_QKV, TPS_P_W_O, TPS_P_W_1, TPS_P_W_2};
-  const int64_t rows[4] = {3 * h, h, f, h}, cols[4] = {h, h, h, f};
   for (int k = 0; k < 4; ++k) {
-    TPS_HIP(dequant_fp8_rows_launch(q + p.qoff[mats[k]], reinterpret_cast<const float*>(q + p.qsoff[k]), rows[k],
-                                    cols[k], dst + p.poff[mats[k]], ps));
+    TPS_HIP(dequant_fp8_rows_launch(q + p.qoff[mats[k]], reinterpret_cast<const float*>(q + p.qsoff[k]),
+                                    p.prow[mats[k]], p.pcol[mats[k]], dst + p.poff[mats[k]], ps));
     ++stats.kernels;
   }
   const int vecs[8] = {TPS_P_B_QKV, TPS_P_B_O, TPS_P_B_1, TPS_P_B_2, TPS_P_G1, TPS_P_BE1, TPS_P_G2, TPS_P_BE2};
-  const int64_t len[8] = {3 * h, h, f, h, h, h, h, h};
-  for (int k = 0; k < 8; ++k)
-    TPS_HIP(hipMemcpyAsync(dst + p.poff[vecs[k]], q + p.qoff[vecs[k]], (size_t)len[k] * p.esize,
-                           hipMemcpyDeviceToDevice, ps));
+  for (int k = 0; k < 8; ++k) {
+    const int64_t len = p.prow[vecs[k]] * p.pcol[vecs[k]];
+    if (len)
+      TPS_HIP(hipMemcpyAsync(dst + p.poff[vecs[k]], q + p.qoff[vecs[k]], (size_t)len * p.esize,
+                             hipMemcpyDeviceToDevice, ps));
+  }
   return TPS_OK;
 }
 
@@ -382,10 +385,10 @@ int tps_stage::refresh_wt(int l, int e) {
   int ent = e;
   const char* P = params_of(l, &ent);
   char* W = wt_of(l, e);
-  const int h = p.h, f = p.f;
-  TPS_HIP(transpose_launch(p.dtype, 3 * h, h, P + p.poff[TPS_P_W_QKV], h, W + p.wtoff[0], 3 * h, cs));
+  const int h = p.h, f = p.f, qw = (int)p.qw, uw = (int)p.uw;
+  TPS_HIP(transpose_launch(p.dtype, qw, h, P + p.poff[TPS_P_W_QKV], h, W + p.wtoff[0], qw, cs));
   TPS_HIP(transpose_launch(p.dtype, h, h, P + p.poff[TPS_P_W_O], h, W + p.wtoff[1], h, cs));
-  TPS_HIP(transpose_launch(p.dtype, f, h, P + p.poff[TPS_P_W_1], h, W + p.wtoff[2], f, cs));
+  TPS_HIP(transpose_launch(p.dtype, uw, h, P + p.poff[TPS_P_W_1], h, W + p.wtoff[2], uw, cs));
   TPS_HIP(transpose_launch(p.dtype, h, f, P + p.poff[TPS_P_W_2], f, W + p.wtoff[3], h, cs));
   stats.kernels += 4;
   return TPS_OK;
@@ -661,50 +664,80 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
   float* ln2 = static_cast<float*>(ptr(TPS_T_LN2));
 
   const double es = p.esize;
+  const int qw = (int)p.qw, uw = (int)p.uw;
+  // LLAMA layers have no biases: the residual epilogues add a zero vector
+  const void* zb = p.llama ? work(p.work.zbias) : nullptr;
+  auto bias = [&](int i) -> const void* { return p.llama ? zb : par(i); };
   const char* ln_name = tname("tps::ln_fwd_kernel<__bf16>", "tps::ln_fwd_kernel<float>");
-  if (ops & (1u << OP_LN1)) {
+  auto norm = [&](const void* in, int gi, int bi, void* out, float* st, bool keep_st) -> int {
     ++stats.kernels;
-    const int k = kbegin(ln_name, 0.0, 2.0 * T * h * es);
-    TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, x, par(TPS_P_G1), par(TPS_P_BE1), p.eps, a,
-                                 opt(TPS_T_LN1) ? ln1 : nullptr, opt(TPS_T_LN1) ? ln1 + T : nullptr, ks));
-    TPS_TRY(kend(k));
+    const int k = kbegin(p.llama ? "rmsnorm forward" : ln_name, 0.0, 2.0 * T * h * es);
+    if (p.llama)
+      TPS_HIP(rmsnorm_fwd_launch(p.dtype, T, h, in, par(gi), p.eps, out, keep_st ? st : nullptr, ks));
+    else
+      TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, in, par(gi), par(bi), p.eps, out, keep_st ? st : nullptr,
+                                   keep_st ? st + T : nullptr, ks));
+    return kend(k);
+  };
+  if (ops & (1u << OP_LN1)) TPS_TRY(norm(x, TPS_P_G1, TPS_P_BE1, a, ln1, opt(TPS_T_LN1)));
+  if (ops & (1u << OP_QKV)) {
+    if (p.llama) {
+      TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, qw, h, a, h, par(TPS_P_W_QKV), h, qkv, qw));
+      // q and k turned in place: the stored qkv is what the attention reads
+      ++stats.kernels;
+      const int k = kbegin("rope", 0.0, 4.0 * T * (p.nh + p.nkv) * p.d * es);
+      TPS_HIP(rope_launch(qkv, qw, T, p.s, p.nh + p.nkv, p.d, reinterpret_cast<const float*>(work(p.work.rope)), 0,
+                          ks));
+      TPS_TRY(kend(k));
+    } else {
+      TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS, T, 3 * h, h, a, h, par(TPS_P_W_QKV), h, qkv, 3 * h, par(TPS_P_B_QKV)));
+    }
   }
-  if (ops & (1u << OP_QKV))
-    TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS, T, 3 * h, h, a, h, par(TPS_P_W_QKV), h, qkv, 3 * h, par(TPS_P_B_QKV)));
   if (ops & (1u << OP_ATTN)) {
     ++stats.kernels;
     const int k = kbegin(p.dtype == TPS_BF16 ? (p.d == 128 ? attention_fwd_v3_name(p.b, p.s, p.nh) : "tps::attn_fwd_v2_kernel<64>")
                                              : "tps::attn_fwd_kernel<float>",
-                         2.0 * p.b * h * (double)p.s * (p.s + 1), 4.0 * T * h * es);
-    TPS_HIP(attention_fwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, opt(TPS_T_LSE) ? lse : nullptr, ks));
+                         2.0 * p.b * h * (double)p.s * (p.s + 1), ((double)qw + h) * T * es);
+    TPS_HIP(attention_fwd_launch(p.dtype, p.b, p.s, p.nh, p.nkv, p.d, qkv, o, opt(TPS_T_LSE) ? lse : nullptr, ks));
     TPS_TRY(kend(k));
   }
   if (ops & (1u << OP_OPROJ))
-    TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_RESID, T, h, h, o, h, par(TPS_P_W_O), h, x1, h, par(TPS_P_B_O), x, h));
-  if (ops & (1u << OP_LN2)) {
+    TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_RESID, T, h, h, o, h, par(TPS_P_W_O), h, x1, h, bias(TPS_P_B_O), x, h));
+  if (ops & (1u << OP_LN2)) TPS_TRY(norm(x1, TPS_P_G2, TPS_P_BE2, c, ln2, opt(TPS_T_LN2)));
+  auto swiglu = [&]() -> int {
     ++stats.kernels;
-    const int k = kbegin(ln_name, 0.0, 2.0 * T * h * es);
-    TPS_HIP(layernorm_fwd_launch(p.dtype, T, h, x1, par(TPS_P_G2), par(TPS_P_BE2), p.eps, c,
-                                 opt(TPS_T_LN2) ? ln2 : nullptr, opt(TPS_T_LN2) ? ln2 + T : nullptr, ks));
-    TPS_TRY(kend(k));
+    const int k = kbegin("swiglu", 0.0, 3.0 * T * f * es);
+    TPS_HIP(swiglu_launch(T, f, u, g, ks));
+    return kend(k);
+  };
+  if (ops & (1u << OP_FC1)) {
+    if (p.llama) {
+      // u = [gate | up] is always materialised (the SwiGLU reads it)
+      TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, uw, h, c, h, par(TPS_P_W_1), h, u, uw));
+      TPS_TRY(swiglu());
+    } else {
+      TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_GELU, T, f, h, c, h, par(TPS_P_W_1), h, g, f, par(TPS_P_B_1), nullptr, 0,
+                   opt(TPS_T_U) ? u : nullptr, f));
+    }
   }
-  if (ops & (1u << OP_FC1))
-    TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_GELU, T, f, h, c, h, par(TPS_P_W_1), h, g, f, par(TPS_P_B_1), nullptr, 0,
-                 opt(TPS_T_U) ? u : nullptr, f));
   if (ops & (1u << OP_GELU)) {
-    ++stats.kernels;
-    const int k = kbegin(tname("tps::gelu_kernel<__bf16>", "tps::gelu_kernel<float>"), 0.0, 2.0 * T * f * es);
-    TPS_HIP(gelu_launch(p.dtype, (int64_t)T * f, u, g, ks));
-    TPS_TRY(kend(k));
+    if (p.llama) {
+      TPS_TRY(swiglu());
+    } else {
+      ++stats.kernels;
+      const int k = kbegin(tname("tps::gelu_kernel<__bf16>", "tps::gelu_kernel<float>"), 0.0, 2.0 * T * f * es);
+      TPS_HIP(gelu_launch(p.dtype, (int64_t)T * f, u, g, ks));
+      TPS_TRY(kend(k));
+    }
   }
   if (ops & (1u << OP_FC2)) {
     // with resident weights the transposed copies exist from the start of
     // the iteration: a long contraction reads W2^T [f][h]
     if (nn_for(f) && p.weights == TPS_W_RESIDENT)
-      TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_BIAS_RESID, T, h, f, g, f, wt_of(l, -1) + p.wtoff[3], h, y, h, par(TPS_P_B_2),
+      TPS_TRY(gemm(TPS_GEMM_NN, TPS_EPI_BIAS_RESID, T, h, f, g, f, wt_of(l, -1) + p.wtoff[3], h, y, h, bias(TPS_P_B_2),
                    x1, h));
     else
-      TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_RESID, T, h, f, g, f, par(TPS_P_W_2), f, y, h, par(TPS_P_B_2), x1, h));
+      TPS_TRY(gemm(TPS_GEMM_NT, TPS_EPI_BIAS_RESID, T, h, f, g, f, par(TPS_P_W_2), f, y, h, bias(TPS_P_B_2), x1, h));
   }
   return TPS_OK;
 }
@@ -717,6 +750,7 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
 // the buffers of set wp are written again, and once per micro-batch)
 int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp,
                          bool defer) {
+  if (p.llama) return bwd_layer_llama(l, mb, W, WT, G, dy, dx, wp, defer);
   const int T = p.T, h = p.h, f = p.f;
   ks = cs;
   const bool fresh = grads_fresh[l] != 0;
@@ -811,7 +845,7 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   {
     ++stats.kernels;
     const int k = kbegin("attention backward", 4.0 * p.b * h * (double)p.s * (p.s + 1), 9.0 * T * h * es);
-    TPS_HIP(attention_bwd_launch(p.dtype, p.b, p.s, p.nh, p.d, qkv, o, lse, t1, dqkv, dvec, cs));
+    TPS_HIP(attention_bwd_launch(p.dtype, p.b, p.s, p.nh, p.nh, p.d, qkv, o, lse, t1, dqkv, dvec, nullptr, cs));
     TPS_TRY(kend(k));
   }
   TPS_TRY(to_gs());
@@ -823,6 +857,122 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   TPS_TRY(lnbwd(t1, x, ln1, TPS_P_G1, Plan::BP_BE1, dx1, dx));
   // finalize after both streams' column sums; cs continues at once (defer)
   // or once gs is done
+  TPS_TRY(to_gs());
+  TPS_TRY(finalize_bias_grads(l, G, fresh));
+  to_cs();
+  if (defer) {
+    TPS_HIP(hipEventRecord(ev_gs[wp], gs));
+    gs_pending[wp] = true;
+    gs_layer[wp] = l;
+  } else {
+    TPS_TRY(join_gs());
+  }
+  bpart_clean = true;
+  return TPS_OK;
+}
+
+// LLAMA-style layer backward: the same stream protocol as bwd_layer (weight
+// gradients forked to gs as their inputs appear, lazily joined), with the
+// SwiGLU and rotary backward kernels in the input-gradient chain and only the
+// two RMSNorm gains among the vector parameters.
+int tps_stage::bwd_layer_llama(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx,
+                               int wp, bool defer) {
+  const int T = p.T, h = p.h, f = p.f, qw = (int)p.qw, uw = (int)p.uw;
+  ks = cs;
+  const bool fresh = grads_fresh[l] != 0;
+  grads_fresh[l] = 0;
+  if (defer && gs_pending[wp]) {
+    TPS_HIP(hipStreamWaitEvent(cs, ev_gs[wp], 0));
+    gs_pending[wp] = false;
+  }
+  auto ptr = [&](int t) { return tensor(l, t, mb, true); };
+  auto par = [&](int i) { return W + p.poff[i]; };
+  auto grd = [&](int i) { return reinterpret_cast<float*>(reinterpret_cast<char*>(G) + p.goff[i]); };
+  void *x = ptr(TPS_T_X), *a = ptr(TPS_T_A), *qkv = ptr(TPS_T_QKV), *o = ptr(TPS_T_O);
+  void *x1 = ptr(TPS_T_X1), *c = ptr(TPS_T_C), *u = ptr(TPS_T_U), *g = ptr(TPS_T_G);
+  const float* lse = static_cast<const float*>(ptr(TPS_T_LSE));
+  const float* r1 = static_cast<const float*>(ptr(TPS_T_LN1));
+  const float* r2 = static_cast<const float*>(ptr(TPS_T_LN2));
+  void* dx1 = work(p.work.dx1[wp]);
+  void* t1 = work(p.work.t1);
+  void* du = work(p.work.du[wp]);
+  void* dqkv = work(p.work.dqkv[wp]);
+  void* dg = work(p.work.dg);
+  void* kvws = p.work.kvws == kNone ? nullptr : work(p.work.kvws);
+  const float* rope_tab = reinterpret_cast<const float*>(work(p.work.rope));
+  float* dvec = reinterpret_cast<float*>(work(p.work.dvec));
+  const double es = p.esize;
+  float* bp = bpart(l);
+  bpart_clean = false;
+  const int64_t bstride = p.bpc[Plan::BP_COUNT];
+  auto to_gs = [&]() -> int {
+    TPS_HIP(hipEventRecord(ev_fork, cs));
+    TPS_HIP(hipStreamWaitEvent(gs, ev_fork, 0));
+    ks = gs;
+    return TPS_OK;
+  };
+  auto to_cs = [&]() { ks = cs; };
+  // dst = res + RMSNorm^T(dout); the gain's per-segment sums go to its
+  // columns of the layer's partial block
+  auto rmsbwd = [&](const void* dout, const void* xin, const float* rstd, int gi, int range, const void* res,
+                    void* dst) -> int {
+    ++stats.kernels;
+    const int k = kbegin("rmsnorm backward (2 kernels)", 0.0, 5.0 * T * h * es);
+    TPS_HIP(rmsnorm_bwd_acc_launch(p.dtype, T, h, dout, xin, rstd, par(gi), res, dst, bp + p.bpc[range], bstride,
+                                   cs));
+    return kend(k);
+  };
+  auto ingrad = [&](int N, int K, const void* dY, int wi, const char* wt, void* dX) -> int {
+    if (nn_for(K)) return gemm(TPS_GEMM_NN, TPS_EPI_STORE, T, N, K, dY, K, par(wi), N, dX, N);
+    return gemm(TPS_GEMM_NT, TPS_EPI_STORE, T, N, K, dY, K, wt, K, dX, N);
+  };
+  const char* w2t = WT + p.wtoff[3];   // [f, h]
+  const char* w1t = WT + p.wtoff[2];   // [h, 2f]
+  const char* wot = WT + p.wtoff[1];   // [h, h]
+  const char* wqt = WT + p.wtoff[0];   // [h, qw]
+  // MLP: y = x1 + (SiLU(gate) * up) W2^T, [gate | up] = c W1^T
+  TPS_TRY(to_gs());
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f, nullptr, nullptr, 0, nullptr,
+               0, fresh));
+  to_cs();
+  TPS_TRY(ingrad(f, h, dy, TPS_P_W_2, w2t, dg));
+  {
+    ++stats.kernels;
+    const int k = kbegin("swiglu backward", 0.0, 5.0 * T * f * es);
+    TPS_HIP(swiglu_bwd_launch(T, f, dg, u, du, cs));
+    TPS_TRY(kend(k));
+  }
+  TPS_TRY(to_gs());
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, uw, h, T, du, uw, c, h, grd(TPS_P_W_1), h, nullptr, nullptr, 0, nullptr,
+               0, fresh));
+  to_cs();
+  TPS_TRY(ingrad(h, uw, du, TPS_P_W_1, w1t, t1));
+  TPS_TRY(rmsbwd(t1, x1, r2, TPS_P_G2, Plan::BP_G2, dy, dx1));
+  // attention block: x1 = x + o Wo^T
+  TPS_TRY(to_gs());
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h, nullptr, nullptr, 0, nullptr,
+               0, fresh));
+  to_cs();
+  TPS_TRY(ingrad(h, h, dx1, TPS_P_W_O, wot, t1));
+  {
+    ++stats.kernels;
+    const int k = kbegin("attention backward", 4.0 * p.b * h * (double)p.s * (p.s + 1), (3.0 * qw + 4.0 * h) * T * es);
+    TPS_HIP(attention_bwd_launch(p.dtype, p.b, p.s, p.nh, p.nkv, p.d, qkv, o, lse, t1, dqkv, dvec, kvws, cs));
+    TPS_TRY(kend(k));
+  }
+  {
+    // gradients of the rotated q and k turned back to those of the projections
+    ++stats.kernels;
+    const int k = kbegin("rope", 0.0, 4.0 * T * (p.nh + p.nkv) * p.d * es);
+    TPS_HIP(rope_launch(dqkv, qw, T, p.s, p.nh + p.nkv, p.d, rope_tab, 1, cs));
+    TPS_TRY(kend(k));
+  }
+  TPS_TRY(to_gs());
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, qw, h, T, dqkv, qw, a, h, grd(TPS_P_W_QKV), h, nullptr, nullptr, 0,
+               nullptr, 0, fresh));
+  to_cs();
+  TPS_TRY(ingrad(h, qw, dqkv, TPS_P_W_QKV, wqt, t1));
+  TPS_TRY(rmsbwd(t1, x, r1, TPS_P_G1, Plan::BP_G1, dx1, dx));
   TPS_TRY(to_gs());
   TPS_TRY(finalize_bias_grads(l, G, fresh));
   to_cs();
@@ -1155,6 +1305,15 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
     if (e != hipSuccess) return check_hip(e, "clear bias partials");
     ++st->stats.kernels;
     st->bpart_clean = true;
+  }
+  if (p.llama && !st->llama_tables) {
+    // the rotation table and the zero vector of the bias-free residual
+    // epilogues, once per stage
+    hipError_t e = rope_table_launch(p.s, p.d, p.rope_base, reinterpret_cast<float*>(st->work(p.work.rope)), st->cs);
+    if (e == hipSuccess) e = fill_zero_launch(st->work(p.work.zbias), (uint64_t)p.h * p.esize, st->cs);
+    if (e != hipSuccess) return check_hip(e, "rotation table");
+    st->stats.kernels += 2;
+    st->llama_tables = true;
   }
   if (p.weights == TPS_W_STREAM) {
     // host gradients of the previous iteration must be complete before reuse

@@ -15,7 +15,7 @@ from typing import Optional, Sequence
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpstage.so")
 
 # --- constants (mirror tpstage.h) ------------------------------------------
-TPS_ABI_VERSION = 3
+TPS_ABI_VERSION = 4
 TPS_OK, TPS_EINVAL, TPS_ENOMEM, TPS_EORDER, TPS_EHIP, TPS_ETIMEOUT, TPS_ESTATE = 0, -1, -2, -3, -4, -5, -6
 TPS_F32, TPS_BF16 = 0, 1
 KEEP, RECOMPUTE, OFFLOAD = 0, 1, 2
@@ -24,6 +24,7 @@ T_INDEX = {n: i for i, n in enumerate(TENSORS)}
 W_RESIDENT, W_STREAM = 0, 1
 Q_NONE, Q_FP8_ROW = 0, 1
 WGRAD_AUTO, WGRAD_SIDE, WGRAD_INLINE = 0, 1, 2
+ARCH_GPT, ARCH_LLAMA = 0, 1
 GRAN_LAYER, GRAN_SEGMENT = 0, 1
 OP_F, OP_B, OP_R = 0, 1, 2
 PARAMS = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "g1", "be1", "g2", "be2")
@@ -52,6 +53,7 @@ class Config(C.Structure):
         ("recompute_granularity", C.c_int32), ("n_ops", C.c_int32), ("ops", C.POINTER(C.c_int32)),
         ("inflight", C.c_int32), ("link_gbps_hint", C.c_float), ("tflops_hint", C.c_float),
         ("lookahead", C.c_int32), ("weights_quant", C.c_int32), ("wgrad_stream", C.c_int32),
+        ("arch", C.c_int32), ("n_kv_heads", C.c_int32), ("rope_base", C.c_float),
     ]
 
 
@@ -127,7 +129,8 @@ EXPORTED = (
     "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
     "tps_host_alloc", "tps_host_free", "tps_tpipe_schedule", "tps_op_attention_bwd_noalloc",
     "tps_op_attention_bwd_noalloc_max_rows", "tps_param_layout_q", "tps_host_adamw_layer",
-    "tps_stage_set_optimizer", "tps_op_dequant_fp8_rows",
+    "tps_stage_set_optimizer", "tps_op_dequant_fp8_rows", "tps_op_rmsnorm_fwd", "tps_op_rmsnorm_bwd", "tps_op_rope",
+    "tps_op_swiglu_fwd", "tps_op_swiglu_bwd", "tps_op_attention_gqa_fwd", "tps_op_attention_gqa_bwd",
 )
 
 
@@ -169,6 +172,13 @@ def lib() -> C.CDLL:
         L.tps_op_attention_bwd_noalloc_max_rows.restype = i64
         L.tps_op_dequant_fp8_rows.argtypes = [i64, i64, vp, vp, vp, vp]
         L.tps_op_colsum.argtypes = [i32, i32, i32, vp, i64, vp, vp, vp]
+        L.tps_op_rmsnorm_fwd.argtypes = [i32, i32, i32, vp, vp, C.c_float, vp, vp, vp]
+        L.tps_op_rmsnorm_bwd.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.tps_op_rope.argtypes = [vp, i64, i32, i32, i32, i32, C.c_float, i32, vp, vp]
+        L.tps_op_swiglu_fwd.argtypes = [i32, i32, vp, vp, vp]
+        L.tps_op_swiglu_bwd.argtypes = [i32, i32, vp, vp, vp, vp]
+        L.tps_op_attention_gqa_fwd.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp]
+        L.tps_op_attention_gqa_bwd.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
         L.tps_op_gelu.argtypes = [i32, i64, vp, vp, vp]
         L.tps_op_workspace_bytes.argtypes = [i32, i64, i64]
         L.tps_op_workspace_bytes.restype = u64
@@ -248,6 +258,9 @@ class StageConfig:
     lookahead: int = 1
     weights_quant: int = Q_NONE
     wgrad_stream: int = WGRAD_AUTO
+    arch: int = ARCH_GPT
+    n_kv_heads: int = 0                      # LLAMA: key/value heads (0: n_heads)
+    rope_base: float = 10000.0
     # drive the planned order with layer-major group calls (each run of
     # consecutive F (or B) tasks is one tps_stage_forward_group / _backward_group)
     layer_major: bool = False
@@ -303,6 +316,7 @@ class StageConfig:
         c.lookahead = self.lookahead
         c.weights_quant = self.weights_quant
         c.wgrad_stream = self.wgrad_stream
+        c.arch, c.n_kv_heads, c.rope_base = self.arch, self.n_kv_heads, self.rope_base
         return c
 
     def order(self) -> list:
@@ -582,6 +596,37 @@ def op_dequant_fp8_rows(rows, cols, q, scale, out, stream=None):
 
 def op_colsum(dtype, rows, cols, x, ldx, out, ws, stream=None):
     check(lib().tps_op_colsum(dtype, rows, cols, _ptr(x), ldx, _ptr(out), _ptr(ws), _stream(stream)))
+
+
+def op_rmsnorm_fwd(dtype, rows, cols, x, gamma, eps, out, rstd=None, stream=None):
+    check(lib().tps_op_rmsnorm_fwd(dtype, rows, cols, _ptr(x), _ptr(gamma), eps, _ptr(out), _ptr(rstd),
+                                   _stream(stream)))
+
+
+def op_rmsnorm_bwd(dtype, rows, cols, dout, x, rstd, gamma, resid, dx, dgamma, ws, stream=None):
+    check(lib().tps_op_rmsnorm_bwd(dtype, rows, cols, _ptr(dout), _ptr(x), _ptr(rstd), _ptr(gamma), _ptr(resid),
+                                   _ptr(dx), _ptr(dgamma), _ptr(ws), _stream(stream)))
+
+
+def op_rope(x, ld, rows, s, n_rot, d, base, inverse, table, stream=None):
+    check(lib().tps_op_rope(_ptr(x), ld, rows, s, n_rot, d, base, int(inverse), _ptr(table), _stream(stream)))
+
+
+def op_swiglu_fwd(rows, f, u, g, stream=None):
+    check(lib().tps_op_swiglu_fwd(rows, f, _ptr(u), _ptr(g), _stream(stream)))
+
+
+def op_swiglu_bwd(rows, f, dg, u, du, stream=None):
+    check(lib().tps_op_swiglu_bwd(rows, f, _ptr(dg), _ptr(u), _ptr(du), _stream(stream)))
+
+
+def op_attention_gqa_fwd(b, s, nh, nkv, qkv, o, lse, stream=None):
+    check(lib().tps_op_attention_gqa_fwd(b, s, nh, nkv, _ptr(qkv), _ptr(o), _ptr(lse), _stream(stream)))
+
+
+def op_attention_gqa_bwd(b, s, nh, nkv, qkv, o, lse, do, dqkv, ws, kv_ws, stream=None):
+    check(lib().tps_op_attention_gqa_bwd(b, s, nh, nkv, _ptr(qkv), _ptr(o), _ptr(lse), _ptr(do), _ptr(dqkv),
+                                         _ptr(ws), _ptr(kv_ws), _stream(stream)))
 
 
 def op_gelu(dtype, n, u, g, stream=None):

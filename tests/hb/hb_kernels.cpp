@@ -57,32 +57,44 @@ hipError_t gemm_launch(int dtype, int layout, int epi, int M, int N, int K, cons
   return hipSuccess;
 }
 
-hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, void* o, float* lse,
+hipError_t attention_fwd_launch(int dtype, int b, int s, int nh, int nkv, int d, const void* qkv, void* o, float* lse,
                                 hipStream_t st) {
-  const int64_t e = esz(dtype), T = (int64_t)b * s, h = (int64_t)nh * d;
+  const int64_t e = esz(dtype), T = (int64_t)b * s, h = (int64_t)nh * d, qw = (int64_t)(nh + 2 * nkv) * d;
   HbRanges rd, wr;
-  add1d(rd, qkv, T * 3 * h * e);
+  add1d(rd, qkv, T * qw * e);
   add1d(wr, o, T * h * e);
   add1d(wr, lse, T * nh * 4);
   hb_op(st, "attention forward", rd, wr);
   return hipSuccess;
 }
 
-hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int d, const void* qkv, const void* o, const float* lse,
-                                const void* dout, void* dqkv, float* dvec, hipStream_t st) {
-  const int64_t e = esz(dtype), T = (int64_t)b * s, h = (int64_t)nh * d;
+hipError_t attention_bwd_launch(int dtype, int b, int s, int nh, int nkv, int d, const void* qkv, const void* o,
+                                const float* lse, const void* dout, void* dqkv, float* dvec, void* kv_ws,
+                                hipStream_t st) {
+  const int64_t e = esz(dtype), T = (int64_t)b * s, h = (int64_t)nh * d, qw = (int64_t)(nh + 2 * nkv) * d;
   HbRanges rd, wr, rd2;
   add1d(rd, o, T * h * e);
   add1d(rd, dout, T * h * e);
   add1d(wr, dvec, T * nh * 4);
   hb_op(st, "attention backward row dots", rd, wr);
-  add1d(rd2, qkv, T * 3 * h * e);
+  add1d(rd2, qkv, T * qw * e);
   add1d(rd2, lse, T * nh * 4);
   add1d(rd2, dout, T * h * e);
   add1d(rd2, dvec, T * nh * 4);
   HbRanges wr2;
-  add1d(wr2, dqkv, T * 3 * h * e);
+  if (nkv == nh) {
+    add1d(wr2, dqkv, T * qw * e);
+    hb_op(st, "attention backward", rd2, wr2);
+    return hipSuccess;
+  }
+  // dQ into dqkv, per-query-head dK, dV into the workspace, then the fold
+  add2d(wr2, dqkv, T, h * e, qw * e);
+  add1d(wr2, kv_ws, T * 2 * h * e);
   hb_op(st, "attention backward", rd2, wr2);
+  HbRanges rd3, wr3;
+  add1d(rd3, kv_ws, T * 2 * h * e);
+  add2d(wr3, static_cast<const char*>(dqkv) + h * e, T, (qw - h) * e, qw * e);
+  hb_op(st, "grouped key/value gradient fold", rd3, wr3);
   return hipSuccess;
 }
 
@@ -152,6 +164,72 @@ hipError_t colsum_finalize_launch(const ColMap& m, float* part, int segs, int64_
     add1d(wr, g, n * 4);
   }
   hb_op(st, "bias gradient finalize", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t rmsnorm_fwd_launch(int dtype, int rows, int cols, const void* x, const void* gamma, float, void* out,
+                              float* rstd, hipStream_t st) {
+  const int64_t e = esz(dtype);
+  HbRanges rd, wr;
+  add1d(rd, x, (int64_t)rows * cols * e);
+  add1d(rd, gamma, cols * e);
+  add1d(wr, out, (int64_t)rows * cols * e);
+  add1d(wr, rstd, rows * 4);
+  hb_op(st, "rmsnorm forward", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t rmsnorm_bwd_acc_launch(int dtype, int rows, int cols, const void* dout, const void* x, const float* rstd,
+                                  const void* gamma, const void* resid, void* dx, float* part_dgamma,
+                                  int64_t seg_stride, hipStream_t st) {
+  const int64_t e = esz(dtype);
+  HbRanges rd, wr;
+  add1d(rd, dout, (int64_t)rows * cols * e);
+  add1d(rd, x, (int64_t)rows * cols * e);
+  add1d(rd, rstd, rows * 4);
+  add1d(rd, gamma, cols * e);
+  add1d(rd, resid, (int64_t)rows * cols * e);
+  add1d(wr, dx, (int64_t)rows * cols * e);
+  const int64_t segs = colsum_segments(rows);
+  for (int64_t sgi = 0; sgi < segs; ++sgi) {
+    add1d(rd, part_dgamma + sgi * seg_stride, cols * 4);
+    add1d(wr, part_dgamma + sgi * seg_stride, cols * 4);
+  }
+  hb_op(st, "rmsnorm backward", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t rope_table_launch(int s, int d, float, float* table, hipStream_t st) {
+  HbRanges none, wr;
+  add1d(wr, table, (int64_t)s * d * 4);
+  hb_op(st, "rotation table", none, wr);
+  return hipSuccess;
+}
+
+hipError_t rope_launch(void* x, int64_t ld, int rows, int s, int n_rot, int d, const float* table, int,
+                       hipStream_t st) {
+  HbRanges rd, wr;
+  add2d(rd, x, rows, (int64_t)n_rot * d * 2, ld * 2);
+  add2d(wr, x, rows, (int64_t)n_rot * d * 2, ld * 2);
+  add1d(rd, table, (int64_t)s * d * 4);
+  hb_op(st, "rope", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t swiglu_launch(int rows, int f, const void* u, void* g, hipStream_t st) {
+  HbRanges rd, wr;
+  add1d(rd, u, (int64_t)rows * 2 * f * 2);
+  add1d(wr, g, (int64_t)rows * f * 2);
+  hb_op(st, "swiglu", rd, wr);
+  return hipSuccess;
+}
+
+hipError_t swiglu_bwd_launch(int rows, int f, const void* dg, const void* u, void* du, hipStream_t st) {
+  HbRanges rd, wr;
+  add1d(rd, dg, (int64_t)rows * f * 2);
+  add1d(rd, u, (int64_t)rows * 2 * f * 2);
+  add1d(wr, du, (int64_t)rows * 2 * f * 2);
+  hb_op(st, "swiglu backward", rd, wr);
   return hipSuccess;
 }
 

@@ -30,6 +30,27 @@ def rel_l2(a, b) -> float:
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
 
 
+def is_llama(cfg) -> bool:
+    return cfg.arch == T.ARCH_LLAMA
+
+
+def n_kv(cfg) -> int:
+    return cfg.n_kv_heads or cfg.n_heads
+
+
+def layer_vals(cfg, l):
+    """Synthetic parameters of layer l (float32 arrays of storage values)."""
+    if is_llama(cfg):
+        return synth.llama_layer_params(l, cfg.hidden, cfg.n_heads, n_kv(cfg), cfg.mlp, cfg.dtype)
+    return synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype)
+
+
+def param_shapes(cfg) -> dict:
+    if is_llama(cfg):
+        return synth.llama_param_shapes(cfg.hidden, cfg.n_heads, n_kv(cfg), cfg.mlp)
+    return synth.param_shapes(cfg.hidden, cfg.mlp)
+
+
 def make_params(cfg):
     """Per-layer packed parameter blocks (device) and zeroed f32 gradient
     blocks, plus the float64 parameter dicts for the oracle."""
@@ -39,9 +60,11 @@ def make_params(cfg):
     blocks, grads, ora = [], [], []
     stream_host = cfg.weights == T.W_STREAM
     for l in range(cfg.n_layers):
-        vals = synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype)
+        vals = layer_vals(cfg, l)
         blk = torch.zeros(pb, dtype=torch.uint8, device="cuda")
         for i, name in enumerate(T.PARAMS):
+            if name not in vals:
+                continue
             v = to_dev(vals[name].reshape(-1), cfg.dtype)
             n = v.numel()
             blk[po[i]:po[i] + n * es].view(torch_dtype(cfg.dtype)).copy_(v)
@@ -61,12 +84,13 @@ def make_params(cfg):
 def read_grads(cfg, grads):
     import torch
     po, pb, go, gb = T.param_layout(cfg)
-    h, f = cfg.hidden, cfg.mlp
-    shapes = synth.param_shapes(h, f)
+    shapes = param_shapes(cfg)
     out = []
     for g in grads:
         d = {}
         for i, name in enumerate(T.PARAMS):
+            if name not in shapes:
+                continue
             n = int(np.prod(shapes[name]))
             d[name] = g[go[i]:go[i] + 4 * n].view(torch.float32).cpu().numpy().astype(np.float64).reshape(shapes[name])
         out.append(d)
@@ -142,13 +166,17 @@ def run_gpu(cfg, xs=None, dys=None, iterations=1, group=False, params=None, one_
 
 def run_oracle(cfg, xs=None, dys=None, ora_params=None):
     from oracle import decoder_stage as ora
+    from oracle import llama_stage as lla
     if xs is None:
         xs, dys = inputs(cfg)
     if ora_params is None:
-        ora_params = [{k: v.astype(np.float64) for k, v in synth.layer_params(l, cfg.hidden, cfg.mlp, cfg.dtype).items()}
-                      for l in range(cfg.n_layers)]
-    return ora.run_stage(ora_params, [x.astype(np.float64) for x in xs], [d.astype(np.float64) for d in dys],
-                         cfg.n_heads, cfg.micro_batch, cfg.seq, cfg.ln_eps)
+        ora_params = [{k: v.astype(np.float64) for k, v in layer_vals(cfg, l).items()} for l in range(cfg.n_layers)]
+    xs = [x.astype(np.float64) for x in xs]
+    dys = [d.astype(np.float64) for d in dys]
+    if is_llama(cfg):
+        return lla.run_stage(ora_params, xs, dys, cfg.n_heads, n_kv(cfg), cfg.micro_batch, cfg.seq, cfg.ln_eps,
+                             cfg.rope_base)
+    return ora.run_stage(ora_params, xs, dys, cfg.n_heads, cfg.micro_batch, cfg.seq, cfg.ln_eps)
 
 
 def tile_excess(a, b, tol, tile=256) -> float:

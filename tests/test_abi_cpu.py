@@ -37,12 +37,22 @@ def _align(x):
     return (x + 255) // 256 * 256
 
 
+def _widths(cfg):
+    """(qkv width, u width, LN statistics per row) of the layer kind."""
+    h, f = cfg.hidden, cfg.mlp
+    if cfg.arch == T.ARCH_LLAMA:
+        d, nkv = h // cfg.n_heads, cfg.n_kv_heads or cfg.n_heads
+        return (cfg.n_heads + 2 * nkv) * d, 2 * f, 1
+    return 3 * h, f, 2
+
+
 def _tensor_bytes(cfg):
     es = 2 if cfg.dtype == "bf16" else 4
     Tk, h, f = cfg.tokens, cfg.hidden, cfg.mlp
+    qw, uw, ns = _widths(cfg)
     b = {n: Tk * h * es for n in ("x", "a", "o", "x1", "c")}
-    b.update(qkv=Tk * 3 * h * es, u=Tk * f * es, g=Tk * f * es,
-             lse=cfg.micro_batch * cfg.n_heads * cfg.seq * 4, ln1=2 * Tk * 4, ln2=2 * Tk * 4)
+    b.update(qkv=Tk * qw * es, u=Tk * uw * es, g=Tk * f * es,
+             lse=cfg.micro_batch * cfg.n_heads * cfg.seq * 4, ln1=ns * Tk * 4, ln2=ns * Tk * 4)
     return b
 
 
@@ -63,7 +73,8 @@ def test_plan_accounting_closed_forms(name):
         assert p["n_slots"] == M
     assert p["keep_all_bytes"] == M * L * sum(_align(v) for v in tb.values())
     Tk, h, f, s, b = cfg.tokens, cfg.hidden, cfg.mlp, cfg.seq, cfg.micro_batch
-    unit = 2 * Tk * (4 * h * h + 2 * h * f) + 2 * b * h * s * (s + 1)
+    qw, uw, _ = _widths(cfg)
+    unit = 2 * Tk * (h * qw + h * h + h * uw + f * h) + 2 * b * h * s * (s + 1)
     assert p["fwd_flops"] == pytest.approx(unit * L * M, rel=1e-12)
     assert p["bwd_flops"] == pytest.approx(2 * unit * L * M, rel=1e-12)
     n_off = bin(p["offload_mb_mask"]).count("1")
@@ -96,6 +107,39 @@ def test_replay_programs_and_recompute_flops():
     full = 2 * Tk * (4 * h * h + 2 * h * f) + 2 * b * h * s * (s + 1)
     # layer 1 needs its input: layer 0 replays fully (with FC2); layer 1 replays all but FC2
     assert p["recompute_flops"] == pytest.approx((full + full - 2 * Tk * f * h) * cfg.n_micro)
+
+
+def test_llama_layout_and_validation():
+    """LLAMA-style layers: parameter blocks with the packed q | k | v and gate
+    | up matrices, the two RMSNorm gains and empty bias / shift slots; bf16
+    and head dim 128 only; n_kv_heads must divide n_heads."""
+    import dataclasses
+    cfg = W.llama4_h4096()
+    h, f, nh, nkv = cfg.hidden, cfg.mlp, cfg.n_heads, cfg.n_kv_heads
+    qw = (nh + 2 * nkv) * 128
+    po, pb, go, gb = T.param_layout(cfg)
+    elems = dict(w_qkv=qw * h, b_qkv=0, w_o=h * h, b_o=0, w_1=2 * f * h, b_1=0, w_2=h * f, b_2=0, g1=h, be1=0, g2=h,
+                 be2=0)
+    o, g = 0, 0
+    for i, n in enumerate(T.PARAMS):
+        assert po[i] == o and go[i] == g, n
+        o, g = _align(o + 2 * elems[n]), _align(g + 4 * elems[n])
+    assert pb == o and gb == g
+    with pytest.raises(T.TpsError):
+        T.plan(dataclasses.replace(cfg, n_kv_heads=5))
+    with pytest.raises(T.TpsError):
+        T.plan(dataclasses.replace(cfg, dtype="f32"))
+    with pytest.raises(T.TpsError):
+        T.plan(dataclasses.replace(cfg, n_heads=64))     # head dim 64
+    with pytest.raises(T.TpsError):
+        T.plan(dataclasses.replace(W.stage4_h2048(), n_kv_heads=4))   # GPT layers: multi-head only
+    # grouped attention needs the per-query-head key/value workspace
+    es = 2
+    Tk = cfg.tokens
+    p = T.plan(cfg)
+    p1 = T.plan(dataclasses.replace(cfg, n_kv_heads=nh))
+    assert p["work_bytes"] - p1["work_bytes"] == _align(Tk * 2 * h * es) - 2 * (
+        _align(Tk * (nh + 2 * nh) * 128 * es) - _align(Tk * qw * es))
 
 
 def test_backward_work_buffers():

@@ -37,7 +37,7 @@ def _mid(**kw):
 
 
 WORKLOADS = ["tiny", "stage4_h2048", "stage5_h5120_offload", "stage5_h5120_resident", "stage4_seq8192_recompute",
-             "stage12_h8192_stream", "stage12_h8192_stream_m20"]
+             "stage12_h8192_stream", "stage12_h8192_stream_m20", "llama4_h4096", "llama12_h8192_stream"]
 
 
 @pytest.mark.parametrize("name", WORKLOADS)
@@ -133,6 +133,29 @@ def test_poison_fills_race_free(monkeypatch):
     before = D.count_ops("fill")
     assert _run(cfgs[1][0]) == 0
     assert D.count_ops("fill") == before
+
+
+def test_llama_layers_race_free():
+    """LLAMA-style layers (rotation, grouped attention with its key/value
+    workspace, SwiGLU) under every policy kind, both call styles, streamed
+    weights and both parameter-gradient arrangements."""
+    L = 4
+    order = [("F", 0), ("F", 1), ("B", 0), ("F", 2), ("B", 1), ("B", 2)]
+    base = dict(n_layers=L, hidden=512, n_heads=4, mlp=1024, seq=200, micro_batch=2, n_micro=3, dtype="bf16",
+                arch=T.ARCH_LLAMA, n_kv_heads=2)
+    mixed = [{t: [T.KEEP, T.RECOMPUTE, T.OFFLOAD][(l + i) % 3] for i, t in enumerate(T.TENSORS)} for l in range(L)]
+    mixed[0]["x"] = T.KEEP
+    cfgs = [(T.StageConfig(**base, ops=order), False),
+            (T.StageConfig(**base, policy=W.policy_selective(L)), False),
+            (T.StageConfig(**base, ops=order, policy=mixed, offload_mb_mask=0b101), False),
+            (T.StageConfig(**base, policy=W.policy_layer_inputs(L), granularity=T.GRAN_SEGMENT), False),
+            (T.StageConfig(**base, policy=W.policy_layer_inputs(L), granularity=T.GRAN_LAYER, weights=T.W_STREAM,
+                           window=2), True),
+            (T.StageConfig(**dict(base, n_kv_heads=4), policy=W.policy_all(L, T.RECOMPUTE)), False)]
+    for i, (cfg, group) in enumerate(cfgs):
+        for mode in (T.WGRAD_SIDE, T.WGRAD_INLINE):
+            assert _run(dataclasses.replace(cfg, wgrad_stream=mode), iterations=2, group=group) == 0, \
+                (i, mode, D.report())
 
 
 def test_mixed_per_microbatch_and_group_calls_race_free():
