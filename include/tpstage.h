@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TPS_ABI_VERSION 4
+#define TPS_ABI_VERSION 5
 #define TPS_MAX_MICRO 64
 
 /* return codes */
@@ -173,6 +173,16 @@ typedef struct tps_config {
   int32_t n_kv_heads;           /* LLAMA: key/value heads, dividing n_heads (0:
                                    n_heads); GPT: 0 or n_heads                  */
   float rope_base;              /* LLAMA: rotary base (0: 10000)                */
+  int32_t group_wgrad;          /* 1: a backward group of several micro-batches
+                                   at layer granularity issues each weight-
+                                   gradient product once per layer over all of
+                                   them (K = n T tokens) instead of once per
+                                   micro-batch; the plan keeps the operands of
+                                   the group's micro-batches for the layer
+                                   (layers whose a, o, c, g are recomputed).
+                                   Outputs are bit-identical; weight gradients
+                                   equal the per-micro-batch sums up to the f32
+                                   summation order.  0: per micro-batch.        */
 } tps_config;
 
 typedef struct tps_plan_info {
@@ -202,6 +212,8 @@ typedef struct tps_plan_info {
   uint64_t h2d_bytes;           /* host-link traffic per iteration               */
   uint64_t d2h_bytes;
   int32_t wgrad_inline;         /* 1: parameter gradients on the compute stream */
+  int32_t group_wgrad_slots;    /* micro-batches a backward group can batch its
+                                   weight gradients over (0: not batched)       */
 } tps_plan_info;
 
 typedef struct tps_params {

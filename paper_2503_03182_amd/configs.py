@@ -81,11 +81,12 @@ def stage12_h8192_stream(n_micro: int = 8) -> StageConfig:
     """12 layers, hidden 8192, 64 heads, MLP 32768, causal seq 4096, micro-batch 1,
     8 micro-batches, bf16 weights and f32 grads streamed from pinned host per
     layer, run as layer-major groups (each streamed layer serves every
-    micro-batch before the next one comes in); activations recomputed from
+    micro-batch before the next one comes in, and its weight gradients are
+    one product per layer over the group); activations recomputed from
     layer inputs."""
     return StageConfig(n_layers=12, hidden=8192, n_heads=64, mlp=32768, seq=4096, micro_batch=1,
                        n_micro=n_micro, dtype="bf16", policy=policy_layer_inputs(12), granularity=GRAN_LAYER,
-                       weights=W_STREAM, window=3, layer_major=True)
+                       weights=W_STREAM, window=3, layer_major=True, group_wgrad=1)
 
 
 def stage12_h8192_stream_m20() -> StageConfig:
@@ -106,7 +107,7 @@ def llama12_h8192_stream() -> StageConfig:
     groups; activations recomputed from layer inputs."""
     return StageConfig(n_layers=12, hidden=8192, n_heads=64, mlp=28672, seq=4096, micro_batch=1, n_micro=8,
                        dtype="bf16", policy=policy_layer_inputs(12), granularity=GRAN_LAYER, weights=W_STREAM,
-                       window=3, layer_major=True, arch=ARCH_LLAMA, n_kv_heads=8)
+                       window=3, layer_major=True, arch=ARCH_LLAMA, n_kv_heads=8, group_wgrad=1)
 
 
 def llama4_h4096() -> StageConfig:

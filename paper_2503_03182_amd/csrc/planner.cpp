@@ -279,6 +279,7 @@ int make_plan(const tps_config* c, Plan* out) {
   p.lookahead = c->lookahead;
   if (p.lookahead < 1) return inval("lookahead must be >= 1");
   if (c->wgrad_stream < TPS_WGRAD_AUTO || c->wgrad_stream > TPS_WGRAD_INLINE) return inval("wgrad_stream");
+  if (c->group_wgrad != 0 && c->group_wgrad != 1) return inval("group_wgrad");
   // same-device A/B of the two arrangements: inline was 2-3% faster at 4096
   // and 8192 tokens per micro-batch, 10% slower at 2048
   p.wgrad_inline = c->wgrad_stream == TPS_WGRAD_INLINE || (c->wgrad_stream == TPS_WGRAD_AUTO && p.T >= 4096);
@@ -486,6 +487,21 @@ int make_plan(const tps_config* c, Plan* out) {
       p.work.rope = take(align256((uint64_t)p.s * p.d * 4));
       p.work.zbias = take(align256(h * es));
     }
+    p.grp_n = 0;
+    // (the slots of an operand must be consecutive rows: each slot a whole
+    // number of 256-byte units)
+    const bool rows_pack = (T * h * es) % 256 == 0 && (T * f * es) % 256 == 0 &&
+                           (T * (uint64_t)p.uw * es) % 256 == 0 && (T * (uint64_t)p.qw * es) % 256 == 0;
+    if (c->group_wgrad && p.granularity == TPS_GRAN_LAYER && p.M > 1 && rows_pack) {
+      const uint64_t n = (uint64_t)p.M;
+      p.grp_n = p.M;
+      const uint64_t w_act[4] = {h, h, h, f};   // a, o, c, g
+      for (int k = 0; k < 4; ++k) p.work.grp_act[k] = take(n * align256(T * w_act[k] * es));
+      p.work.grp_du = take(n * fb);
+      p.work.grp_dx1 = take(n * hb);
+      p.work.grp_dqkv = take(n * qb);
+      for (int k = 0; k < 2; ++k) p.work.grp_y[k] = take(n * hb);
+    }
     p.work_bytes = o;
   }
 
@@ -571,6 +587,7 @@ void fill_plan_info(const Plan& p, tps_plan_info* info) {
   info->h2d_bytes = p.h2d_bytes;
   info->d2h_bytes = p.d2h_bytes;
   info->wgrad_inline = p.wgrad_inline ? 1 : 0;
+  info->group_wgrad_slots = p.grp_n;
 }
 
 }  // namespace tps

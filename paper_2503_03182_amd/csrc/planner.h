@@ -84,7 +84,13 @@ struct Plan {
   struct Work {
     uint64_t g[3], dx1[2], du[2], dqkv[2], t1, dvec;
     uint64_t dg, kvws, rope, zbias;
+    // batched weight gradients of backward groups (group_wgrad): per
+    // micro-batch slots [grp_n][T, width] of the layer's a, o, c, g (the
+    // activation operands), du, dx1, dqkv (the gradient operands) and the
+    // running input gradient (two, alternating by layer)
+    uint64_t grp_act[4], grp_du, grp_dx1, grp_dqkv, grp_y[2];
   } work{};
+  int grp_n = 0;   // largest group the slots hold (0: no batched weight gradients)
   uint64_t work_bytes = 0;
   // the parameter-gradient kernels of a layer backward may still run while
   // the next layer's input-gradient chain starts; the two streams join once

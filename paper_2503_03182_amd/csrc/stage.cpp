@@ -210,9 +210,24 @@ struct tps_stage {
   char* oslot_base(int slot) const { return arena + p.off_oslots + (uint64_t)slot * p.oslot_bytes; }
   char* host_base(int mb) const { return host + (uint64_t)p.host_slot[mb] * p.oslot_bytes; }
 
+  // batched weight gradients of a backward group: while grp_i >= 0 the
+  // recomputed a, o, c, g of the layer live in micro-batch slot grp_i of the
+  // group's operand buffers (they are read again after the group's last
+  // micro-batch)
+  int grp_i = -1;
+  static int grp_act_index(int t) {
+    return t == TPS_T_A ? 0 : t == TPS_T_O ? 1 : t == TPS_T_C ? 2 : t == TPS_T_G ? 3 : -1;
+  }
+  char* grp_slot(uint64_t off, uint64_t slot_bytes, int i) const {
+    return arena + p.off_work + off + (uint64_t)i * ((slot_bytes + 255) & ~uint64_t(255));
+  }
   // device address of tensor t of (layer l, mb) for the phase (fwd or bwd)
   void* tensor(int l, int t, int mb, bool bwd) const {
     const size_t k = (size_t)l * TPS_T_COUNT + t;
+    if (grp_i >= 0 && bwd && p.policy[k] == TPS_RECOMPUTE) {
+      const int a = grp_act_index(t);
+      if (a >= 0) return grp_slot(p.work.grp_act[a], p.tbytes[t], grp_i);
+    }
     switch (p.policy[k]) {
       case TPS_RECOMPUTE: return arena + p.off_replay + p.replay_off[k];
       case TPS_KEEP: return kslot_base(mb) + p.kslot_off[k];
@@ -291,9 +306,19 @@ struct tps_stage {
     return p.dtype == TPS_BF16 ? bf16_name : f32_name;
   }
   int fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bool replay, bool bwd_slots);
-  int bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp, bool defer);
+  // grp >= 0: micro-batch slot of a backward group whose weight gradients
+  // are issued once per layer (batched_wgrad); the layer's gradient operands
+  // go to the group's slots and the weight-gradient GEMMs are left out
+  int bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp, bool defer,
+                int grp = -1);
   int bwd_layer_llama(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp,
-                      bool defer);
+                      bool defer, int grp);
+  bool layer_batchable(int l) const {
+    for (int t : {TPS_T_A, TPS_T_O, TPS_T_C, TPS_T_G})
+      if (p.pol(l, t) != TPS_RECOMPUTE) return false;
+    return true;
+  }
+  int batched_wgrad(int l, float* G, int n, bool fresh, int yin);
   // stream `on` waits for the lagging parameter-gradient kernels of layer l
   // (and all gs work before them), if any are pending
   int wait_gs_layer_on(int l, hipStream_t on) {
@@ -749,8 +774,8 @@ int tps_stage::fwd_layer(int l, int mb, const char* W, void* y, uint32_t ops, bo
 // parameter-gradient kernels running on gs at the end (they are joined before
 // the buffers of set wp are written again, and once per micro-batch)
 int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx, int wp,
-                         bool defer) {
-  if (p.llama) return bwd_layer_llama(l, mb, W, WT, G, dy, dx, wp, defer);
+                         bool defer, int grp) {
+  if (p.llama) return bwd_layer_llama(l, mb, W, WT, G, dy, dx, wp, defer, grp);
   const int T = p.T, h = p.h, f = p.f;
   ks = cs;
   const bool fresh = grads_fresh[l] != 0;
@@ -767,10 +792,11 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   const float* lse = static_cast<const float*>(ptr(TPS_T_LSE));
   const float* ln1 = static_cast<const float*>(ptr(TPS_T_LN1));
   const float* ln2 = static_cast<const float*>(ptr(TPS_T_LN2));
-  void* dx1 = work(p.work.dx1[wp]);
+  const bool tn = grp < 0;   // weight gradients per micro-batch
+  void* dx1 = tn ? work(p.work.dx1[wp]) : grp_slot(p.work.grp_dx1, p.tbytes[TPS_T_X], grp);
   void* t1 = work(p.work.t1);
-  void* du = work(p.work.du[wp]);
-  void* dqkv = work(p.work.dqkv[wp]);
+  void* du = tn ? work(p.work.du[wp]) : grp_slot(p.work.grp_du, p.tbytes[TPS_T_U], grp);
+  void* dqkv = tn ? work(p.work.dqkv[wp]) : grp_slot(p.work.grp_dqkv, p.tbytes[TPS_T_QKV], grp);
   float* dvec = reinterpret_cast<float*>(work(p.work.dvec));
 
   const double es = p.esize;
@@ -823,22 +849,25 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
   // read is rewritten only after a join); the bias partials of gs and of the
   // LayerNorm passes on cs are disjoint columns.
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f, nullptr, nullptr, 0, nullptr,
-               0, fresh));
+  if (tn)
+    TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f, nullptr, nullptr, 0, nullptr,
+                 0, fresh));
   TPS_TRY(colsum(dy, h, Plan::BP_2));
   to_cs();
   TPS_TRY(ingrad(TPS_EPI_GELU_GRAD, f, h, dy, TPS_P_W_2, w2t, du, u));
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h, nullptr, nullptr, 0, nullptr,
-               0, fresh));
+  if (tn)
+    TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, f, h, T, du, f, c, h, grd(TPS_P_W_1), h, nullptr, nullptr, 0, nullptr,
+                 0, fresh));
   TPS_TRY(colsum(du, f, Plan::BP_1));
   to_cs();
   TPS_TRY(ingrad(TPS_EPI_STORE, h, f, du, TPS_P_W_1, w1t, t1, nullptr));
   TPS_TRY(lnbwd(t1, x1, ln2, TPS_P_G2, Plan::BP_BE2, dy, dx1));
   // attention block: x1 = x + o Wo^T + bo
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h, nullptr, nullptr, 0, nullptr,
-               0, fresh));
+  if (tn)
+    TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h, nullptr, nullptr, 0, nullptr,
+                 0, fresh));
   TPS_TRY(colsum(dx1, h, Plan::BP_O));
   to_cs();
   TPS_TRY(ingrad(TPS_EPI_STORE, h, h, dx1, TPS_P_W_O, wot, t1, nullptr));
@@ -849,8 +878,9 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
     TPS_TRY(kend(k));
   }
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h, nullptr, nullptr, 0,
-               nullptr, 0, fresh));
+  if (tn)
+    TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, 3 * h, h, T, dqkv, 3 * h, a, h, grd(TPS_P_W_QKV), h, nullptr, nullptr,
+                 0, nullptr, 0, fresh));
   TPS_TRY(colsum(dqkv, 3 * h, Plan::BP_QKV));
   to_cs();
   TPS_TRY(ingrad(TPS_EPI_STORE, h, 3 * h, dqkv, TPS_P_W_QKV, wqt, t1, nullptr));
@@ -876,7 +906,7 @@ int tps_stage::bwd_layer(int l, int mb, const char* W, const char* WT, float* G,
 // SwiGLU and rotary backward kernels in the input-gradient chain and only the
 // two RMSNorm gains among the vector parameters.
 int tps_stage::bwd_layer_llama(int l, int mb, const char* W, const char* WT, float* G, const void* dy, void* dx,
-                               int wp, bool defer) {
+                               int wp, bool defer, int grp) {
   const int T = p.T, h = p.h, f = p.f, qw = (int)p.qw, uw = (int)p.uw;
   ks = cs;
   const bool fresh = grads_fresh[l] != 0;
@@ -893,10 +923,11 @@ int tps_stage::bwd_layer_llama(int l, int mb, const char* W, const char* WT, flo
   const float* lse = static_cast<const float*>(ptr(TPS_T_LSE));
   const float* r1 = static_cast<const float*>(ptr(TPS_T_LN1));
   const float* r2 = static_cast<const float*>(ptr(TPS_T_LN2));
-  void* dx1 = work(p.work.dx1[wp]);
+  const bool tn = grp < 0;   // weight gradients per micro-batch
+  void* dx1 = tn ? work(p.work.dx1[wp]) : grp_slot(p.work.grp_dx1, p.tbytes[TPS_T_X], grp);
   void* t1 = work(p.work.t1);
-  void* du = work(p.work.du[wp]);
-  void* dqkv = work(p.work.dqkv[wp]);
+  void* du = tn ? work(p.work.du[wp]) : grp_slot(p.work.grp_du, p.tbytes[TPS_T_U], grp);
+  void* dqkv = tn ? work(p.work.dqkv[wp]) : grp_slot(p.work.grp_dqkv, p.tbytes[TPS_T_QKV], grp);
   void* dg = work(p.work.dg);
   void* kvws = p.work.kvws == kNone ? nullptr : work(p.work.kvws);
   const float* rope_tab = reinterpret_cast<const float*>(work(p.work.rope));
@@ -932,8 +963,9 @@ int tps_stage::bwd_layer_llama(int l, int mb, const char* W, const char* WT, flo
   const char* wqt = WT + p.wtoff[0];   // [h, qw]
   // MLP: y = x1 + (SiLU(gate) * up) W2^T, [gate | up] = c W1^T
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f, nullptr, nullptr, 0, nullptr,
-               0, fresh));
+  if (tn)
+    TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, T, dy, h, g, f, grd(TPS_P_W_2), f, nullptr, nullptr, 0, nullptr,
+                 0, fresh));
   to_cs();
   TPS_TRY(ingrad(f, h, dy, TPS_P_W_2, w2t, dg));
   {
@@ -943,15 +975,17 @@ int tps_stage::bwd_layer_llama(int l, int mb, const char* W, const char* WT, flo
     TPS_TRY(kend(k));
   }
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, uw, h, T, du, uw, c, h, grd(TPS_P_W_1), h, nullptr, nullptr, 0, nullptr,
-               0, fresh));
+  if (tn)
+    TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, uw, h, T, du, uw, c, h, grd(TPS_P_W_1), h, nullptr, nullptr, 0, nullptr,
+                 0, fresh));
   to_cs();
   TPS_TRY(ingrad(h, uw, du, TPS_P_W_1, w1t, t1));
   TPS_TRY(rmsbwd(t1, x1, r2, TPS_P_G2, Plan::BP_G2, dy, dx1));
   // attention block: x1 = x + o Wo^T
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h, nullptr, nullptr, 0, nullptr,
-               0, fresh));
+  if (tn)
+    TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, T, dx1, h, o, h, grd(TPS_P_W_O), h, nullptr, nullptr, 0, nullptr,
+                 0, fresh));
   to_cs();
   TPS_TRY(ingrad(h, h, dx1, TPS_P_W_O, wot, t1));
   {
@@ -968,8 +1002,9 @@ int tps_stage::bwd_layer_llama(int l, int mb, const char* W, const char* WT, flo
     TPS_TRY(kend(k));
   }
   TPS_TRY(to_gs());
-  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, qw, h, T, dqkv, qw, a, h, grd(TPS_P_W_QKV), h, nullptr, nullptr, 0,
-               nullptr, 0, fresh));
+  if (tn)
+    TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, qw, h, T, dqkv, qw, a, h, grd(TPS_P_W_QKV), h, nullptr, nullptr, 0,
+                 nullptr, 0, fresh));
   to_cs();
   TPS_TRY(ingrad(h, qw, dqkv, TPS_P_W_QKV, wqt, t1));
   TPS_TRY(rmsbwd(t1, x, r1, TPS_P_G1, Plan::BP_G1, dx1, dx));
@@ -984,6 +1019,28 @@ int tps_stage::bwd_layer_llama(int l, int mb, const char* W, const char* WT, flo
     TPS_TRY(join_gs());
   }
   bpart_clean = true;
+  return TPS_OK;
+}
+
+// The four weight-gradient products of layer l over the n micro-batches of a
+// backward group (K = n T): the slots of each operand are consecutive, so
+// micro-batch i's rows follow micro-batch i - 1's; fresh: the first
+// contribution of the iteration (writes instead of adding).
+int tps_stage::batched_wgrad(int l, float* G, int n, bool fresh, int yin) {
+  const int h = p.h, f = p.f, qw = (int)p.qw, uw = (int)p.uw;
+  const int K = n * p.T;
+  auto grd = [&](int i) { return reinterpret_cast<float*>(reinterpret_cast<char*>(G) + p.goff[i]); };
+  auto base = [&](uint64_t off) { return static_cast<const void*>(arena + p.off_work + off); };
+  (void)l;
+  ks = cs;
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, f, K, base(p.work.grp_y[yin]), h, base(p.work.grp_act[3]), f,
+               grd(TPS_P_W_2), f, nullptr, nullptr, 0, nullptr, 0, fresh));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, uw, h, K, base(p.work.grp_du), uw, base(p.work.grp_act[2]), h,
+               grd(TPS_P_W_1), h, nullptr, nullptr, 0, nullptr, 0, fresh));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, h, h, K, base(p.work.grp_dx1), h, base(p.work.grp_act[1]), h,
+               grd(TPS_P_W_O), h, nullptr, nullptr, 0, nullptr, 0, fresh));
+  TPS_TRY(gemm(TPS_GEMM_TN, TPS_EPI_ACC_F32, qw, h, K, base(p.work.grp_dqkv), qw, base(p.work.grp_act[0]), h,
+               grd(TPS_P_W_QKV), h, nullptr, nullptr, 0, nullptr, 0, fresh));
   return TPS_OK;
 }
 
@@ -1467,6 +1524,41 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
       ++st->stats.replays;
     }
   }
+  if (p.grp_n > 0 && n > 1 && n <= p.grp_n && p.granularity == TPS_GRAN_LAYER) {
+    // Batched weight gradients: the running input gradients of the group
+    // alternate between two slot buffers by layer (layer 0 writes the
+    // caller's dx), the layer's operands stay in the group's slots, and each
+    // weight-gradient product runs once per layer over the n micro-batches.
+    int yin = 0;
+    for (int i = 0; i < n; ++i)
+      TPS_HIP(hipMemcpyAsync(st->grp_slot(p.work.grp_y[0], p.tbytes[TPS_T_X], i), dy[i], p.tbytes[TPS_T_X],
+                             hipMemcpyDeviceToDevice, st->cs));
+    for (int l = p.L - 1; l >= 0; --l) {
+      int e = -1;
+      TPS_TRY(st->ensure_layer(l, true, &e));
+      TPS_TRY(st->prefetch_layer(l - 1));
+      const char* W = st->params_of(l, &e);
+      const bool bl = st->layer_batchable(l);
+      const bool fresh = st->grads_fresh[l] != 0;   // the layer backwards below clear it
+      for (int i = 0; i < n; ++i) {
+        const int mb = mb0 + i;
+        st->grp_i = bl ? i : -1;
+        if (p.replay_ops[l]) {
+          TPS_TRY(st->fwd_layer(l, mb, W, nullptr, p.replay_ops[l], true, true));
+          ++st->stats.replays;
+        }
+        const void* in = st->grp_slot(p.work.grp_y[yin], p.tbytes[TPS_T_X], i);
+        void* out = l == 0 ? dx[i] : st->grp_slot(p.work.grp_y[yin ^ 1], p.tbytes[TPS_T_X], i);
+        const int rc = st->bwd_layer(l, mb, W, st->wt_of(l, e), st->grads_of(l, e), in, out, 0, false, bl ? i : -1);
+        st->grp_i = -1;
+        TPS_TRY(rc);
+      }
+      if (bl) TPS_TRY(st->batched_wgrad(l, st->grads_of(l, e), n, fresh, yin));
+      TPS_TRY(st->touch(e));
+      TPS_TRY(st->opt_after_backward(l, n));
+      yin ^= 1;
+    }
+  } else {
   char* gA = st->work(p.work.g[0]);
   for (int l = p.L - 1; l >= 0; --l) {
     int e = -1;
@@ -1486,6 +1578,7 @@ extern "C" int tps_stage_backward_group(tps_stage* st, int mb0, int n, const voi
     }
     TPS_TRY(st->touch(e));
     TPS_TRY(st->opt_after_backward(l, n));
+  }
   }
   for (int i = 0; i < n; ++i) {
     const int mb = mb0 + i;

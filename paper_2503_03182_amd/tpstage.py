@@ -15,7 +15,7 @@ from typing import Optional, Sequence
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpstage.so")
 
 # --- constants (mirror tpstage.h) ------------------------------------------
-TPS_ABI_VERSION = 4
+TPS_ABI_VERSION = 5
 TPS_OK, TPS_EINVAL, TPS_ENOMEM, TPS_EORDER, TPS_EHIP, TPS_ETIMEOUT, TPS_ESTATE = 0, -1, -2, -3, -4, -5, -6
 TPS_F32, TPS_BF16 = 0, 1
 KEEP, RECOMPUTE, OFFLOAD = 0, 1, 2
@@ -53,7 +53,7 @@ class Config(C.Structure):
         ("recompute_granularity", C.c_int32), ("n_ops", C.c_int32), ("ops", C.POINTER(C.c_int32)),
         ("inflight", C.c_int32), ("link_gbps_hint", C.c_float), ("tflops_hint", C.c_float),
         ("lookahead", C.c_int32), ("weights_quant", C.c_int32), ("wgrad_stream", C.c_int32),
-        ("arch", C.c_int32), ("n_kv_heads", C.c_int32), ("rope_base", C.c_float),
+        ("arch", C.c_int32), ("n_kv_heads", C.c_int32), ("rope_base", C.c_float), ("group_wgrad", C.c_int32),
     ]
 
 
@@ -70,6 +70,7 @@ class PlanInfo(C.Structure):
         ("n_offload_mbs", C.c_int32), ("n_replay_layers", C.c_int32),
         ("fwd_flops", C.c_double), ("bwd_flops", C.c_double), ("recompute_flops", C.c_double),
         ("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("wgrad_inline", C.c_int32),
+        ("group_wgrad_slots", C.c_int32),
     ]
 
     def as_dict(self) -> dict:
@@ -261,6 +262,7 @@ class StageConfig:
     arch: int = ARCH_GPT
     n_kv_heads: int = 0                      # LLAMA: key/value heads (0: n_heads)
     rope_base: float = 10000.0
+    group_wgrad: int = 0                     # 1: batch a backward group's weight gradients per layer
     # drive the planned order with layer-major group calls (each run of
     # consecutive F (or B) tasks is one tps_stage_forward_group / _backward_group)
     layer_major: bool = False
@@ -317,6 +319,7 @@ class StageConfig:
         c.weights_quant = self.weights_quant
         c.wgrad_stream = self.wgrad_stream
         c.arch, c.n_kv_heads, c.rope_base = self.arch, self.n_kv_heads, self.rope_base
+        c.group_wgrad = int(self.group_wgrad)
         return c
 
     def order(self) -> list:

@@ -153,7 +153,12 @@ def test_backward_work_buffers():
         Tk, h, f = cfg.tokens, cfg.hidden, cfg.mlp
         hb, fb, qb = _align(Tk * h * es), _align(Tk * f * es), _align(Tk * 3 * h * es)
         dvec = _align(cfg.micro_batch * cfg.n_heads * cfg.seq * 4)
-        return (3 if lag else 2) * hb + (2 if lag else 1) * (hb + fb + qb) + hb + dvec
+        base = (3 if lag else 2) * hb + (2 if lag else 1) * (hb + fb + qb) + hb + dvec
+        if cfg.group_wgrad:
+            # batched weight gradients: n slots of a, o, c, g, du, dx1, dqkv
+            # and of two running-gradient buffers
+            base += cfg.n_micro * (3 * hb + fb + fb + hb + qb + 2 * hb)
+        return base
 
     for name, lag in [("stage4_h2048", True), ("stage5_h5120_offload", True),
                       ("stage4_seq8192_recompute", True), ("stage12_h8192_stream", False)]:
@@ -330,7 +335,7 @@ def test_oversubscribed_stage_exceeds_hbm_only_when_kept():
     L = cfg.n_layers
     keep_all = info["keep_all_bytes"] + L * (info["param_bytes"] + info["grad_bytes"])
     assert keep_all > 288e9
-    assert info["predicted_peak_bytes"] < 0.2 * 288e9
+    assert info["predicted_peak_bytes"] < 0.25 * 288e9
     # the same stage at 8 micro-batches fits either way (the workload's
     # premise needs the larger in-flight count)
     info8 = T.plan(W.stage12_h8192_stream())

@@ -147,6 +147,30 @@ def test_h8192_streamed_bitexact_to_resident():
     torch.cuda.empty_cache()
 
 
+def test_h8192_batched_weight_gradients_match_per_microbatch():
+    """The hidden-8192 streamed workload (4 layers, 2 micro-batches) with the
+    weight-gradient products batched over each backward group against the
+    same stage with one product per micro-batch: outputs bit-identical,
+    gradients equal up to the f32 summation order."""
+    import torch
+    bat = dataclasses.replace(W.stage12_h8192_stream(), n_layers=4, n_micro=2)
+    bat.policy = bat.policy[:4]
+    assert bat.group_wgrad and T.plan(bat)["group_wgrad_slots"] == 2
+    per = dataclasses.replace(bat, group_wgrad=0)
+    print("hidden 8192, 4 layers, 2 micro-batches: batched vs per-micro-batch weight gradients", flush=True)
+    blocks, xs, dys = _device_params(bat, 8193)
+    a = _run(bat, blocks, xs, dys)
+    b = _run(per, blocks, xs, dys)
+    for u, v in zip(a[0] + a[1], b[0] + b[1]):
+        assert torch.equal(u, v)
+    for l, (u, v) in enumerate(zip(a[2], b[2])):
+        u32, v32 = u.view(torch.float32).double(), v.view(torch.float32).double()
+        r = ((u32 - v32).norm() / v32.norm()).item()
+        assert r <= 1e-5, (l, r)
+    del a, b
+    torch.cuda.empty_cache()
+
+
 def test_h5120_one_layer_matches_oracle():
     cfg = dataclasses.replace(W.stage5_h5120_resident(), n_layers=1, n_micro=1)
     cfg.policy = cfg.policy[:1]

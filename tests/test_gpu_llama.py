@@ -174,6 +174,21 @@ def test_llama_streamed_weights_match_oracle_and_resident():
         assert not bad, (group, bad)
 
 
+def test_llama_batched_group_weight_gradients():
+    L = 4
+    cfg = _mid(n_layers=L, policy=W.policy_layer_inputs(L), granularity=T.GRAN_LAYER, weights=T.W_STREAM, window=2)
+    per_mb = run_gpu(cfg, group=True)
+    bat = run_gpu(dataclasses.replace(cfg, group_wgrad=1), group=True)
+    from stage_harness import rel_l2
+    for mb in range(cfg.n_micro):
+        assert np.array_equal(per_mb["ys"][mb], bat["ys"][mb]) and np.array_equal(per_mb["dxs"][mb], bat["dxs"][mb])
+    for l in range(L):
+        for k, v in per_mb["grads"][l].items():
+            assert rel_l2(bat["grads"][l][k], v) <= 1e-5, (l, k)
+    worst, bad = compare(bat, run_oracle(cfg), BF16_TOL)
+    assert not bad, bad
+
+
 def _device_params(cfg, seed):
     """Seeded device parameters and inputs (for self-comparisons at full
     widths, where drawing ~10^9 values on the host would dominate)."""
@@ -238,10 +253,21 @@ def test_llama70b_width_streamed_bitexact_to_resident():
     blocks, xs, dys = _device_params(cfg, 7)
     a = _run_dev(cfg, blocks, xs, dys, group=True)
     print("resident", flush=True)
-    b = _run_dev(dataclasses.replace(cfg, weights=T.W_RESIDENT, layer_major=False), blocks, xs, dys, group=False)
+    b = _run_dev(dataclasses.replace(cfg, weights=T.W_RESIDENT), blocks, xs, dys, group=True)
     for k in ("ys", "dxs", "grads"):
         for u, v in zip(a[k], b[k]):
             assert torch.equal(u, v), k
+    # per-micro-batch weight-gradient products: same outputs, gradients up to
+    # the f32 summation order
+    print("per-micro-batch weight gradients", flush=True)
+    c = _run_dev(dataclasses.replace(cfg, group_wgrad=0), blocks, xs, dys, group=True)
+    for k in ("ys", "dxs"):
+        for u, v in zip(a[k], c[k]):
+            assert torch.equal(u, v), k
+    for l, (u, v) in enumerate(zip(a["grads"], c["grads"])):
+        u32, v32 = u.view(torch.float32).double(), v.view(torch.float32).double()
+        r = ((u32 - v32).norm() / v32.norm()).item()
+        assert r <= 1e-5, (l, r)
 
 
 @pytest.mark.timeout(1500)

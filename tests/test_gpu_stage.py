@@ -129,6 +129,50 @@ def test_poison_leaves_results_unchanged(monkeypatch):
             assert bit_equal(plain[name], out) == [], (name, mode)
 
 
+def _same_outputs_close_grads(a, b, tol=1e-5):
+    """ys and dxs bitwise equal; weight and vector gradients within tol
+    (rel-L2): only the f32 summation order of the weight gradients differs."""
+    from stage_harness import rel_l2
+    for mb in range(len(a["ys"])):
+        assert np.array_equal(a["ys"][mb], b["ys"][mb]), f"y{mb}"
+        assert np.array_equal(a["dxs"][mb], b["dxs"][mb]), f"dx{mb}"
+    for l in range(len(a["grads"])):
+        for k, v in a["grads"][l].items():
+            r = rel_l2(b["grads"][l][k], v)
+            assert r <= tol, (l, k, r)
+
+
+def test_batched_group_weight_gradients():
+    """Backward groups that issue each weight-gradient product once per layer
+    over the group's micro-batches: outputs bit-identical to per-micro-batch
+    products, weight gradients equal up to f32 summation order, and within
+    the bf16 bar of the oracle; a layer that keeps one of its operands (not
+    batchable) next to batchable ones; groups of some of the micro-batches."""
+    L = 4
+    pol = W.policy_layer_inputs(L)
+    mixed = [dict(q) for q in pol]
+    mixed[1]["c"] = T.KEEP
+    cases = {
+        "resident": _mid(n_layers=L, policy=pol, granularity=T.GRAN_LAYER),
+        "mixed": _mid(n_layers=L, policy=mixed, granularity=T.GRAN_LAYER),
+        "streamed": _mid(n_layers=L, policy=pol, granularity=T.GRAN_LAYER, weights=T.W_STREAM, window=2),
+    }
+    for name, cfg in cases.items():
+        per_mb = run_gpu(cfg, group=True)
+        for mode in (T.WGRAD_SIDE, T.WGRAD_INLINE):
+            bcfg = dataclasses.replace(cfg, group_wgrad=1, wgrad_stream=mode)
+            assert T.plan(bcfg)["group_wgrad_slots"] == cfg.n_micro
+            bat = run_gpu(bcfg, group=True)
+            _same_outputs_close_grads(per_mb, bat)
+        worst, bad = compare(bat, run_oracle(cfg), BF16_TOL)
+        assert not bad, (name, bad)
+    cfg = dataclasses.replace(cases["resident"], n_micro=4)
+    calls = [("F", [0, 1, 2, 3], True), ("B", [0, 1], True), ("B", [2], False), ("B", [3], True)]
+    per_mb = run_gpu(cfg, calls=calls)
+    bat = run_gpu(dataclasses.replace(cfg, group_wgrad=1), calls=calls, iterations=2)
+    _same_outputs_close_grads(per_mb, bat)
+
+
 def test_repeat_iterations_reproduce():
     cfg = _mid(policy=W.policy_all(3, T.OFFLOAD), offload_mb_mask=0b011, inflight=2)
     one = run_gpu(cfg, iterations=1)

@@ -135,6 +135,31 @@ def test_poison_fills_race_free(monkeypatch):
     assert D.count_ops("fill") == before
 
 
+def test_batched_group_weight_gradients_race_free():
+    """Backward groups that issue each weight-gradient product once per layer
+    over their micro-batches: resident and streamed weights, GPT and LLAMA
+    layers, both parameter-gradient arrangements, groups of all and of some
+    micro-batches, layers that cannot batch (kept activations) beside ones
+    that can."""
+    L = 4
+    pol = W.policy_layer_inputs(L)
+    mixed = [dict(p) for p in pol]
+    mixed[1]["c"] = T.KEEP            # layer 1 keeps c: its products stay per micro-batch
+    cfgs = [_mid(n_layers=L, policy=pol, granularity=T.GRAN_LAYER, group_wgrad=1),
+            _mid(n_layers=L, policy=mixed, granularity=T.GRAN_LAYER, group_wgrad=1),
+            _mid(n_layers=L, policy=pol, granularity=T.GRAN_LAYER, weights=T.W_STREAM, window=2, group_wgrad=1),
+            _mid(n_layers=L, policy=pol, granularity=T.GRAN_LAYER, weights=T.W_STREAM, window=3, group_wgrad=1,
+                 arch=T.ARCH_LLAMA, n_kv_heads=2)]
+    for i, cfg in enumerate(cfgs):
+        for mode in (T.WGRAD_SIDE, T.WGRAD_INLINE):
+            assert _run(dataclasses.replace(cfg, wgrad_stream=mode), iterations=2, group=True) == 0, \
+                (i, mode, D.report())
+    # groups of some of the micro-batches, with per-micro-batch calls between
+    cfg = _mid(n_layers=L, policy=pol, granularity=T.GRAN_LAYER, group_wgrad=1, n_micro=4)
+    calls = [("F", [0, 1, 2, 3], True), ("B", [0, 1], True), ("B", [2], False), ("B", [3], True)]
+    assert _run(cfg, iterations=2, calls=calls) == 0, D.report()
+
+
 def test_llama_layers_race_free():
     """LLAMA-style layers (rotation, grouped attention with its key/value
     workspace, SwiGLU) under every policy kind, both call styles, streamed
@@ -220,10 +245,15 @@ def test_checker_reports_left_out_waits():
     assert n > 100 and det >= 0.95 * n, (n, det)
     # (the side-stream arrangement: inline, the parameter-gradient waits are
     # on the compute stream itself and leave nothing to detect)
-    c5 = dataclasses.replace(W.stage12_h8192_stream(), n_layers=4, n_micro=4, wgrad_stream=T.WGRAD_SIDE)
+    c5 = dataclasses.replace(W.stage12_h8192_stream(), n_layers=4, n_micro=4, wgrad_stream=T.WGRAD_SIDE,
+                             group_wgrad=0)
     c5.policy = c5.policy[:4]
     n, det = _dropped_wait_detection(c5, group=True)
     assert n > 100 and det >= 0.9 * n, (n, det)
+    # batched weight gradients: every micro-batch of a group has its own
+    # operand slots, so some per-micro-batch joins guard nothing there
+    n, det = _dropped_wait_detection(dataclasses.replace(c5, group_wgrad=1), group=True)
+    assert n > 100 and det >= 0.75 * n, (n, det)
     off = _mid(policy=W.policy_all(3, T.OFFLOAD), offload_mb_mask=0b111)
     n, det = _dropped_wait_detection(off)
     # (per-layer ready events of one prefetch are recorded in order on one
