@@ -14,6 +14,7 @@ CPU oracle timed on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import statistics
@@ -125,6 +126,43 @@ def build_stage(cfg):
     ys = [torch.empty_like(x) for x in xs]
     dxs = [torch.empty_like(x) for x in xs]
     return blocks, grads, xs, dys, ys, dxs
+
+
+def t_offload_state(cfg, blocks):
+    """Host model state of T-Offload: f32 master weights (from the streamed
+    bf16 parameter blocks), zero AdamW moments, all in the gradient layout;
+    with the FP8 reload the host parameter blocks are rewritten in the
+    quantized layout from the masters.  Returns (parameter blocks, (master,
+    m, v))."""
+    import numpy as np
+    from paper_2503_03182_amd import tpstage as T
+    from paper_2503_03182_amd import synth
+    po, pb, go, gb = T.param_layout(cfg)
+    shapes = (synth.llama_param_shapes(cfg.hidden, cfg.n_heads, cfg.n_kv_heads or cfg.n_heads, cfg.mlp)
+              if cfg.arch == T.ARCH_LLAMA else synth.param_shapes(cfg.hidden, cfg.mlp))
+    masters, ms, vs = [], [], []
+    for blk in blocks:
+        src = blk.numpy()
+        mst = np.zeros(gb // 4, dtype=np.float32)
+        for i, name in enumerate(T.PARAMS):
+            if name not in shapes:
+                continue
+            n = int(np.prod(shapes[name]))
+            bits = src[po[i]:po[i] + 2 * n].view(np.uint16)
+            mst[go[i] // 4:go[i] // 4 + n] = (bits.astype(np.uint32) << 16).view(np.float32)
+        masters.append(mst)
+        ms.append(np.zeros_like(mst))
+        vs.append(np.zeros_like(mst))
+    if cfg.weights_quant == T.Q_FP8_ROW:
+        qbytes = T.param_layout_q(cfg)[2]
+        qblocks = []
+        for mst in masters:
+            hb = T.HostBuffer(qbytes)
+            T.host_adamw_layer(cfg, 0, mst, None, None, None, hb, quant=T.Q_FP8_ROW,
+                               n_threads=len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 0)
+            qblocks.append(hb)
+        blocks = qblocks
+    return blocks, (masters, ms, vs)
 
 
 def cpu_model() -> str:
@@ -272,6 +310,10 @@ def main():
                     help="run only a plain 512 MiB device-to-device copy (reference for HBM byte counters)")
     ap.add_argument("--standalone-gemms", action="store_true",
                     help="time every GEMM of one (layer, micro-batch) unit of the workload alone and exit")
+    ap.add_argument("--t-offload", choices=("bf16", "fp8"), default=None,
+                    help="streamed workloads: attach the host AdamW update of every layer (T-Offload of model "
+                         "state) and reload the updated weights as bf16 or as FP8 codes with row scales")
+    ap.add_argument("--layers", type=int, default=None, help="override the workload's layer count")
     args = ap.parse_args()
     if args.standalone_gemms:
         import torch
@@ -300,6 +342,15 @@ def main():
     from paper_2503_03182_amd import tpstage as T
 
     cfg = configs.WORKLOADS[args.workload]()
+    if args.layers is not None:
+        cfg = dataclasses.replace(cfg, n_layers=args.layers,
+                                  policy=None if cfg.policy is None else cfg.policy[:args.layers])
+    if args.t_offload is not None:
+        if cfg.weights != T.W_STREAM:
+            print("--t-offload needs a workload with streamed weights", file=sys.stderr)
+            sys.exit(2)
+        if args.t_offload == "fp8":
+            cfg = dataclasses.replace(cfg, weights_quant=T.Q_FP8_ROW)
     long_step = cfg.hidden >= 8192
     if args.steps is None:
         args.steps = 5 if long_step else 20
@@ -315,7 +366,14 @@ def main():
     log(f"[bench] workload {args.workload}: building parameters and inputs")
     blocks, grads, xs, dys, ys, dxs = build_stage(cfg)
     torch.cuda.synchronize()
+    opt_state = None
+    if args.t_offload is not None:
+        blocks, opt_state = t_offload_state(cfg, blocks)
     stage = T.Stage(cfg, blocks, grads)
+    if opt_state is not None:
+        n_threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+        stage.set_optimizer(*opt_state, first_step=1, lr=1e-5, n_threads=n_threads)
+        log(f"[bench] host AdamW on {n_threads} threads, reload as {args.t_offload}")
     assert stage.cs.cuda_stream == run_stream.cuda_stream
     order = cfg.order()
     step_flops = info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]
@@ -369,6 +427,14 @@ def main():
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     value = step_flops * args.steps / (t1 - t0) / 1e12
+    t_offload = None
+    if opt_state is not None:
+        t_offload = {"reload": args.t_offload, "optimizer": "AdamW (host, f32 master weights)",
+                     "host_updates_last_step": link["host_updates"],
+                     "host_update_ms_last_step": round(link["host_update_ms"], 1),
+                     "host_update_ms_per_layer": round(link["host_update_ms"] / max(link["host_updates"], 1), 1),
+                     "reload_wait_ms_last_step": round(link["host_wait_ms"], 1),
+                     "host_state_gb": round(3 * cfg.n_layers * info["grad_bytes"] / 1e9, 2)}
     achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
     step_ms_breakdown = sum(r["ms"] for r in breakdown)
     out = {
@@ -418,6 +484,7 @@ def main():
             "launches": dom["launches"],
             "avg_launch_us": round(dom["ms"] * 1e3 / max(dom["launches"], 1), 2),
         },
+        "t_offload": t_offload,
         "host_link": {
             "h2d_gb_per_step": round(link["h2d_bytes"] / 1e9, 3),
             "d2h_gb_per_step": round(link["d2h_bytes"] / 1e9, 3),

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TPS_ABI_VERSION 5
+#define TPS_ABI_VERSION 6
 #define TPS_MAX_MICRO 64
 
 /* return codes */
@@ -263,6 +263,11 @@ typedef struct tps_stats {
   uint64_t kernels;             /* kernel launches this iteration               */
   uint64_t replays;             /* recompute replays (layers) this iteration    */
   int32_t ops_done;             /* position in the planned order                */
+  double host_update_ms;        /* host optimizer: summed duration of the layer
+                                   updates finished since the iteration began   */
+  double host_wait_ms;          /* time the issuing thread waited for a layer's
+                                   update before reloading it, this iteration   */
+  int32_t host_updates;         /* layer updates finished since it began        */
 } tps_stats;
 
 typedef struct tps_kernel_time {

@@ -27,6 +27,9 @@ COMMON = [
 ]
 # packed-FP32 instructions are kept out of the gfx950 code
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# the host optimizer's row loops: AVX2 vectors, no contraction into FMAs (the
+# update keeps the rounding of its separate multiplies and adds)
+HOST_FLAGS = {"host_optim.cpp": ["-march=x86-64-v3", "-ffp-contract=off"]}
 
 
 def hipcc() -> str:
@@ -47,6 +50,7 @@ def _compile(src: str) -> tuple[str, int, str]:
     if src.endswith(".hip"):
         cmd[1:1] = ["-x", "hip"]
         cmd += DEVICE_FLAGS
+    cmd += HOST_FLAGS.get(os.path.basename(src), [])
     r = subprocess.run(cmd, capture_output=True, text=True)
     msg = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
                     if "packed-fp32-ops" not in l and "hip-link" not in l)

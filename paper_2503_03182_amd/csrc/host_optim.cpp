@@ -26,34 +26,32 @@ uint16_t f32_to_bf16(float x) {
   return (uint16_t)(b >> 16);
 }
 
-uint8_t e4m3_encode(float x) {
-  const uint8_t sign = std::signbit(x) ? 0x80 : 0x00;
-  const float a = std::fabs(x);
-  if (!(a < 448.f)) return sign | 0x7E;          // saturate
-  if (a < 0.015625f) {                            // below 2^-6: steps of 2^-9
-    const int q = (int)std::nearbyint(a * 512.f); // exact scaling; ties to even
-    return q == 0 ? 0 : (uint8_t)(sign | q);      // q == 8 is the smallest normal
-  }
+// Nearest E4M3 code of x (ties to an even mantissa), saturating at 448, no
+// negative zero; branch-free so that the row loops vectorise.  Normal range:
+// the f32 bit pattern rounded to 3 mantissa bits by an integer add (a carry
+// moves into the exponent), then rebiased from 127 to 7.  Below 2^-6 the code
+// is the value in steps of 2^-9, rounded by adding and subtracting 1.5 * 2^23.
+inline uint8_t e4m3_encode(float x) {
   uint32_t b;
-  memcpy(&b, &a, 4);
-  int e = (int)((b >> 23) & 0xFF) - 127;
-  uint32_t m3 = (b & 0x7FFFFFu) >> 20;
-  const uint32_t rem = b & 0xFFFFFu;
-  if (rem > 0x80000u || (rem == 0x80000u && (m3 & 1u))) ++m3;
-  if (m3 == 8) {
-    m3 = 0;
-    ++e;
-  }
-  uint32_t code = ((uint32_t)(e + 7) << 3) | m3;
-  if (code > 0x7E) code = 0x7E;
-  return (uint8_t)(sign | code);
+  memcpy(&b, &x, 4);
+  const uint32_t sign = (b >> 24) & 0x80u;
+  const uint32_t ab = b & 0x7FFFFFFFu;
+  float a;
+  memcpy(&a, &ab, 4);
+  const int32_t normal = (int32_t)((ab + 0x7FFFFu + ((ab >> 20) & 1u)) >> 20) - (120 << 3);
+  const float q = (a * 512.f + 12582912.f) - 12582912.f;
+  int32_t c = a < 0.015625f ? (int32_t)q : normal;
+  c = a < 448.f ? c : 0x7E;   // also infinities and NaN
+  c = c > 0x7E ? 0x7E : c;
+  return (uint8_t)(c == 0 ? 0u : (sign | (uint32_t)c));
 }
 
 struct Adam {
   float b1, b2, eps, lr_c, wd_c;   // lr_c = lr / (1 - b1^t) , wd_c = lr * wd
   float inv_bc2_sqrt;              // 1 / sqrt(1 - b2^t)
   bool update;
-  void apply(float* w, float* m, float* v, const float* g, int64_t n) const {
+  void apply(float* __restrict__ w, float* __restrict__ m, float* __restrict__ v, const float* __restrict__ g,
+             int64_t n) const {
     if (!update) return;
     for (int64_t i = 0; i < n; ++i) {
       const float gi = g[i];
@@ -127,11 +125,18 @@ int host_adamw(const Plan& p, const tps_adamw* opt, int32_t step, float* master,
         const int64_t o = r * per;
         A.apply(W + o, M ? M + o : nullptr, V ? V + o : nullptr, G ? G + o : nullptr, per);
         if (q8) {
+          // row maximum in 8 lanes (a max is exact, so the lane order does not matter)
+          float lane[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+          const float* wr = W + o;
+          int64_t c = 0;
+          for (; c + 8 <= per; c += 8)
+            for (int k = 0; k < 8; ++k) lane[k] = std::max(lane[k], std::fabs(wr[c + k]));
+          for (; c < per; ++c) lane[0] = std::max(lane[0], std::fabs(wr[c]));
           float amax = 0.f;
-          for (int64_t c = 0; c < per; ++c) amax = std::max(amax, std::fabs(W[o + c]));
+          for (int k = 0; k < 8; ++k) amax = std::max(amax, lane[k]);
           const float scale = amax > 0.f ? amax / 448.f : 1.f;
-          uint8_t* qd = reinterpret_cast<uint8_t*>(out + p.qoff[i]) + o;
-          for (int64_t c = 0; c < per; ++c) qd[c] = e4m3_encode(W[o + c] / scale);
+          uint8_t* __restrict__ qd = reinterpret_cast<uint8_t*>(out + p.qoff[i]) + o;
+          for (int64_t k = 0; k < per; ++k) qd[k] = e4m3_encode(wr[k] / scale);
           reinterpret_cast<float*>(out + p.qsoff[mat_slot[i]])[r] = scale;
         } else {
           const uint64_t base = quant == TPS_Q_FP8_ROW ? p.qoff[i] : p.poff[i];

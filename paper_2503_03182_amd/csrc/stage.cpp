@@ -532,8 +532,10 @@ int tps_stage::opt_after_backward(int l, int passes) {
 
 int tps_stage::wait_layer_update(int l) {
   if (!hopt.on) return TPS_OK;
+  const auto t0 = std::chrono::steady_clock::now();
   std::unique_lock<std::mutex> lock(hopt.mu);
   hopt.cv.wait(lock, [&] { return !hopt.pending[l]; });
+  stats.host_wait_ms += std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
   if (hopt.rc != TPS_OK) return set_error(hopt.rc, "host optimizer: " + hopt.err);
   return TPS_OK;
 }
@@ -568,9 +570,14 @@ void tps_stage::opt_worker() {
       rc = TPS_EHIP;
       err = std::string("waiting for the gradients of layer ") + std::to_string(l) + ": " + hipGetErrorString(he);
     } else {
+      const auto t0 = std::chrono::steady_clock::now();
       rc = host_adamw(p, &hopt.hp, hopt.step[l], hopt.master[l], hopt.m[l], hopt.v[l], lg[l], lp[l], p.quant,
                       hopt.threads);
       if (rc != TPS_OK) err = last_error();
+      const double ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+      std::lock_guard<std::mutex> lock(hopt.mu);
+      stats.host_update_ms += ms;
+      ++stats.host_updates;
     }
     {
       std::lock_guard<std::mutex> lock(hopt.mu);
@@ -1350,7 +1357,10 @@ extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
   std::fill(st->f_done.begin(), st->f_done.end(), 0);
   std::fill(st->b_done.begin(), st->b_done.end(), 0);
   std::fill(st->prefetched.begin(), st->prefetched.end(), 0);
-  st->stats = tps_stats{};
+  {
+    std::lock_guard<std::mutex> lock(st->hopt.mu);
+    st->stats = tps_stats{};
+  }
   const Plan& p = st->p;
   std::fill(st->hopt.bpass.begin(), st->hopt.bpass.end(), 0);
   // an iteration cut short may leave parameter-gradient kernels pending
@@ -1672,6 +1682,8 @@ extern "C" int tps_stage_sync_for(tps_stage* st, double timeout_ms) {
 extern "C" int tps_stage_stats(const tps_stage* st, tps_stats* out) {
   clear_error();
   if (!st || !out) return set_error(TPS_EINVAL, "null argument");
+  // the host optimizer's thread adds its timings under its lock
+  std::lock_guard<std::mutex> lock(const_cast<tps_stage*>(st)->hopt.mu);
   *out = st->stats;
   return TPS_OK;
 }

@@ -15,7 +15,7 @@ from typing import Optional, Sequence
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpstage.so")
 
 # --- constants (mirror tpstage.h) ------------------------------------------
-TPS_ABI_VERSION = 5
+TPS_ABI_VERSION = 6
 TPS_OK, TPS_EINVAL, TPS_ENOMEM, TPS_EORDER, TPS_EHIP, TPS_ETIMEOUT, TPS_ESTATE = 0, -1, -2, -3, -4, -5, -6
 TPS_F32, TPS_BF16 = 0, 1
 KEEP, RECOMPUTE, OFFLOAD = 0, 1, 2
@@ -115,7 +115,8 @@ class AdamW(C.Structure):
 
 class Stats(C.Structure):
     _fields_ = [("h2d_bytes", C.c_uint64), ("d2h_bytes", C.c_uint64), ("kernels", C.c_uint64),
-                ("replays", C.c_uint64), ("ops_done", C.c_int32)]
+                ("replays", C.c_uint64), ("ops_done", C.c_int32), ("host_update_ms", C.c_double),
+                ("host_wait_ms", C.c_double), ("host_updates", C.c_int32)]
 
 
 # --- library -----------------------------------------------------------------

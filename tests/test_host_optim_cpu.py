@@ -114,3 +114,45 @@ def test_host_adamw_argument_errors():
     f32 = T.StageConfig(**{**_cfg().__dict__, "dtype": "f32", "_keep": []})
     with pytest.raises(T.TpsError):
         T.host_adamw_layer(f32, 0, buf, None, None, None, out, quant=T.Q_FP8_ROW)
+
+
+def test_fp8_encoding_at_every_code_midpoint_and_boundary():
+    """The library's E4M3 encoder (branch-free, in the quantized block) against
+    the oracle's nearest-code search on every code value, every midpoint
+    between neighbouring codes (ties), one f32 step either side of each
+    midpoint, the subnormal/normal boundary and values beyond 448.  A row
+    whose largest magnitude is 448 has scale 1, so the encoder sees the
+    values themselves."""
+    cfg = _cfg()
+    po, pb, go, gb = T.param_layout(cfg)
+    qo, so, qb = T.param_layout_q(cfg)
+    shapes = synth.param_shapes(cfg.hidden, cfg.mlp)
+    vals = ms.e4m3_values()
+    pos = np.sort(np.array([v for v in vals[:128] if not np.isnan(v)]))
+    mids = (pos[:-1] + pos[1:]) / 2
+    f32 = lambda a: np.asarray(a, dtype=np.float32)
+    probes = np.concatenate([pos, mids, np.nextafter(f32(mids), f32(0)), np.nextafter(f32(mids), f32(1e9)),
+                             [2.0 ** -6, np.nextafter(np.float32(2.0 ** -6), np.float32(0)), 2.0 ** -9 / 2,
+                              2.0 ** -10, 1e-30, 0.0, 447.99, 464.0, 500.0, 1e6]]).astype(np.float32)
+    probes = np.concatenate([probes, -probes])
+    rows, cols = shapes["w_1"]
+    w = np.zeros((rows, cols), dtype=np.float32)
+    flat = np.concatenate([probes, np.zeros((-probes.size) % (cols - 1), dtype=np.float32)])
+    chunks = flat.reshape(-1, cols - 1)
+    assert chunks.shape[0] <= rows
+    w[:chunks.shape[0], :cols - 1] = chunks
+    w[:chunks.shape[0], cols - 1] = 448.0          # scale 1 for these rows (values above 448 saturate)
+    vals_in = {n: np.zeros(shapes[n], dtype=np.float32) for n in T.PARAMS}
+    vals_in["w_1"] = w
+    master = _block(cfg, vals_in, go, gb)
+    out = np.zeros(qb, dtype=np.uint8)
+    T.host_adamw_layer(cfg, 0, master, None, None, None, out, quant=T.Q_FP8_ROW, n_threads=2)
+    i = T.PARAMS.index("w_1")
+    codes = out[qo[i]: qo[i] + rows * cols].reshape(rows, cols)
+    scales = out[so[2]: so[2] + 4 * rows].view(np.float32)
+    n = chunks.shape[0]
+    # rows holding a value above 448 have a larger scale; compare through the oracle's own quantization
+    q_ref, s_ref = ms.quantize_rows(w[:n])
+    assert np.array_equal(scales[:n], s_ref)
+    assert np.array_equal(codes[:n], q_ref)
+    assert (scales[:n] == 1.0).sum() >= n - 2
