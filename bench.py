@@ -165,6 +165,52 @@ def t_offload_state(cfg, blocks):
     return blocks, (masters, ms, vs)
 
 
+def host_link_rates(stream, gib: float = 1.0, reps: int = 3):
+    """Copy-engine rates (GB/s) between pinned host memory and HBM, host to
+    device and device to host, timed with events on `stream`."""
+    import torch
+    n = int(gib * (1 << 30))
+    host = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    dev = torch.empty(n, dtype=torch.uint8, device="cuda")
+    rates = []
+    for h2d in (True, False):
+        with torch.cuda.stream(stream):
+            (dev.copy_(host, non_blocking=True) if h2d else host.copy_(dev, non_blocking=True))
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                (dev.copy_(host, non_blocking=True) if h2d else host.copy_(dev, non_blocking=True))
+            e1.record(stream)
+        e1.synchronize()
+        rates.append(reps * n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del host, dev
+    return rates[0], rates[1]
+
+
+def t_offload_stages(cfg, info, link, gpu_ms_per_step, h2d_gbs, d2h_gbs):
+    """The appendix "Scalability of T-Offload" applied to this stage taken as
+    one chunk: the smallest pipeline depths at which the measured host work
+    would fit T-Pipe's bubbles (tpipe_t_offload_stages).  T_unit is the
+    chunk's forward for one micro-batch, a third of its GPU time per
+    micro-batch (backward = two forwards, as in the schedule's unit-time
+    model); the chunk's offload time is its gradients over the measured
+    device-to-host rate plus its measured host updates; its upload time is
+    one load of its host parameter blocks over the host-to-device rate."""
+    from paper_2503_03182_amd import tpstage as T
+    t_unit = gpu_ms_per_step / (3 * cfg.n_micro)
+    grad_gb = cfg.n_layers * info["grad_bytes"] / 1e9
+    blk = T.param_layout_q(cfg)[2] if cfg.weights_quant == T.Q_FP8_ROW else T.param_layout(cfg)[1]
+    up_gb = cfg.n_layers * blk / 1e9
+    # the update thread lags the GPU: a step's window also sees updates of
+    # the step before, so the chunk's time is the mean per layer times L
+    t_off = grad_gb / d2h_gbs * 1e3 + cfg.n_layers * link["host_update_ms"] / max(link["host_updates"], 1)
+    t_up = up_gb / h2d_gbs * 1e3
+    p_off, p_up = T.tpipe_t_offload_stages(t_off, t_up, t_unit)
+    return {"t_unit_ms": round(t_unit, 2), "link_gbs": {"h2d": round(h2d_gbs, 1), "d2h": round(d2h_gbs, 1)},
+            "chunk_offload_ms": round(t_off, 1), "chunk_upload_ms": round(t_up, 1),
+            "min_stages_offload": p_off, "min_stages_upload": p_up}
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -370,7 +416,10 @@ def main():
     if args.t_offload is not None:
         blocks, opt_state = t_offload_state(cfg, blocks)
     stage = T.Stage(cfg, blocks, grads)
+    link_rates = None
     if opt_state is not None:
+        link_rates = host_link_rates(run_stream)
+        log(f"[bench] host link {link_rates[0]:.1f} GB/s to the device, {link_rates[1]:.1f} GB/s back")
         n_threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
         stage.set_optimizer(*opt_state, first_step=1, lr=1e-5, n_threads=n_threads)
         log(f"[bench] host AdamW on {n_threads} threads, reload as {args.t_offload}")
@@ -430,11 +479,12 @@ def main():
     t_offload = None
     if opt_state is not None:
         t_offload = {"reload": args.t_offload, "optimizer": "AdamW (host, f32 master weights)",
-                     "host_updates_last_step": link["host_updates"],
-                     "host_update_ms_last_step": round(link["host_update_ms"], 1),
                      "host_update_ms_per_layer": round(link["host_update_ms"] / max(link["host_updates"], 1), 1),
+                     "host_updates_finished_during_last_step": link["host_updates"],
                      "reload_wait_ms_last_step": round(link["host_wait_ms"], 1),
-                     "host_state_gb": round(3 * cfg.n_layers * info["grad_bytes"] / 1e9, 2)}
+                     "host_state_gb": round(3 * cfg.n_layers * info["grad_bytes"] / 1e9, 2),
+                     "tpipe_bubbles": t_offload_stages(cfg, info, link, sum(r["ms"] for r in breakdown),
+                                                       *link_rates)}
     achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
     step_ms_breakdown = sum(r["ms"] for r in breakdown)
     out = {

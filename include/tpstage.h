@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TPS_ABI_VERSION 6
+#define TPS_ABI_VERSION 7
 #define TPS_MAX_MICRO 64
 
 /* return codes */
@@ -428,6 +428,13 @@ typedef struct tps_tpipe_result {
   int32_t life_chunk1;          /* start of forward to start of backward of the
                                    middle micro-batch on the requested stage   */
   int32_t life_chunk2;
+  int32_t offload_window;       /* idle time of the requested stage from the end
+                                   of chunk 2's last backward to the start of
+                                   chunk 1's last backward (room for chunk 2's
+                                   gradient offload and host optimizer step)  */
+  int32_t upload_window;        /* idle time of the requested stage from its
+                                   first task to chunk 2's first forward (room
+                                   for the reload of chunk 2's weights)        */
 } tps_tpipe_result;
 
 /* Simulates the schedule and writes the requested stage's tasks in execution

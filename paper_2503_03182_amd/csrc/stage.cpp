@@ -495,14 +495,15 @@ int tps_stage::touch(int e) {
 // changed the host parameter blocks since the last iteration, so no layer
 // may run on parameters (or transposed copies) brought in before.  The
 // entries keep their last-use and grads-out events, which the next H2D and
-// the next gradient fill of the entry still wait for.
+// the next gradient fill of the entry still wait for, and their recency: the
+// next iteration's first loads evict the entries the backward finished with
+// first, so they overlap the end of that backward instead of waiting for it.
 int tps_stage::invalidate_window() {
   for (auto& w : win) {
     w.layer = -1;
     w.wt_valid = false;
     w.grads_live = false;
     w.param_ready.valid = false;
-    w.tick = 0;
   }
   return TPS_OK;
 }

@@ -197,6 +197,37 @@ Blocks stage_blocks(const Sim& S, int s) {
   return B;
 }
 
+// Idle time of stage s inside [a, b): the interval less the tasks of the
+// stage that run in it (tasks of one stage never overlap).
+int stage_idle(const Sim& S, int s, int a, int b) {
+  if (b <= a) return 0;
+  int busy = 0;
+  for (int i : S.order[s]) {
+    const Task& t = S.tasks[i];
+    busy += std::max(0, std::min(t.end, b) - std::max(t.start, a));
+  }
+  return (b - a) - busy;
+}
+
+// The two host-transfer windows of the appendix "Scalability of T-Offload"
+// on stage s.  Offload: idle time from the end of chunk 2's last backward to
+// the start of chunk 1's last backward (the cool-down gap that holds the
+// gradient offload and host optimizer step of chunk 2).  Upload: idle time
+// from the stage's first task to chunk 2's first forward (the warm-up gap
+// that holds the reload of chunk 2's weights).
+void stage_windows(const Sim& S, int s, int* offload, int* upload) {
+  int b2_end = 0, b1_start = 0, first = -1, f2_start = -1;
+  for (int i : S.order[s]) {
+    const Task& t = S.tasks[i];
+    if (t.kind == K_B && t.chunk == 2) b2_end = std::max(b2_end, t.end);
+    if (t.kind == K_B && t.chunk == 1) b1_start = std::max(b1_start, t.start);
+    if (first < 0 || t.start < first) first = t.start;
+    if (t.kind == K_F && t.chunk == 2 && (f2_start < 0 || t.start < f2_start)) f2_start = t.start;
+  }
+  *offload = stage_idle(S, s, b2_end, b1_start);
+  *upload = stage_idle(S, s, first, f2_start);
+}
+
 }  // namespace
 
 extern "C" int tps_tpipe_schedule(const tps_tpipe_config* cfg, int32_t stage, tps_tpipe_task* tasks,
@@ -253,6 +284,7 @@ extern "C" int tps_tpipe_schedule(const tps_tpipe_config* cfg, int32_t stage, tp
   const int jm = m / 2;
   out->life_chunk1 = S.tasks[S.idx(K_B, 1, jm, stage)].start - S.tasks[S.idx(K_F, 1, jm, stage)].start;
   out->life_chunk2 = S.tasks[S.idx(K_B, 2, jm, stage)].start - S.tasks[S.idx(K_F, 2, jm, stage)].start;
+  stage_windows(S, stage, &out->offload_window, &out->upload_window);
 
   const auto& ord = S.order[stage];
   if (n_tasks) *n_tasks = (int32_t)ord.size();

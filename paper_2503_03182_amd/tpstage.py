@@ -15,7 +15,7 @@ from typing import Optional, Sequence
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtpstage.so")
 
 # --- constants (mirror tpstage.h) ------------------------------------------
-TPS_ABI_VERSION = 6
+TPS_ABI_VERSION = 7
 TPS_OK, TPS_EINVAL, TPS_ENOMEM, TPS_EORDER, TPS_EHIP, TPS_ETIMEOUT, TPS_ESTATE = 0, -1, -2, -3, -4, -5, -6
 TPS_F32, TPS_BF16 = 0, 1
 KEEP, RECOMPUTE, OFFLOAD = 0, 1, 2
@@ -105,7 +105,8 @@ class TPipeResult(C.Structure):
     _fields_ = [("delay", C.c_int32), ("makespan", C.c_int32), ("busy", C.c_int32), ("bubble_ratio", C.c_double),
                 ("peak_blocks_chunk1", C.c_int32), ("peak_blocks_chunk2", C.c_int32),
                 ("peak_buffer_blocks", C.c_int32), ("peak_blocks", C.c_int32),
-                ("max_stage_peak_blocks", C.c_int32), ("life_chunk1", C.c_int32), ("life_chunk2", C.c_int32)]
+                ("max_stage_peak_blocks", C.c_int32), ("life_chunk1", C.c_int32), ("life_chunk2", C.c_int32),
+                ("offload_window", C.c_int32), ("upload_window", C.c_int32)]
 
 
 class AdamW(C.Structure):
@@ -413,6 +414,30 @@ def chunk_orders(tasks):
         orders[chunk].append((kind, mb))
         calls.append((chunk, kind, mb))
     return orders[1], orders[2], calls
+
+
+def tpipe_t_offload_stages(t_offload, t_upload, t_unit, micro=None, max_stages=256):
+    """Smallest pipeline depths p at which T-Offload's host transfers of one
+    chunk fit T-Pipe's bubbles (appendix "Scalability of T-Offload"): the
+    gradient offload plus host optimizer step of a chunk (`t_offload`) within
+    the cool-down window of the simulated schedule, and the reload of a
+    chunk's weights (`t_upload`) within its warm-up window.  `t_unit` is the
+    forward of one chunk for one micro-batch (a backward takes two), all three
+    in the same unit; the schedule has max(micro, 2p) micro-batches.  Returns
+    (p for the offload, p for the upload), None where no p up to max_stages
+    suffices."""
+    if not (t_unit > 0) or t_offload < 0 or t_upload < 0:
+        raise ValueError("t_unit must be positive, t_offload and t_upload non-negative")
+    p_off = p_up = None
+    for p in range(1, max_stages + 1):
+        r, _ = tpipe_schedule(p, max(micro or 0, 2 * p))
+        if p_off is None and t_offload <= r["offload_window"] * t_unit:
+            p_off = p
+        if p_up is None and t_upload <= r["upload_window"] * t_unit:
+            p_up = p
+        if p_off is not None and p_up is not None:
+            break
+    return p_off, p_up
 
 
 # --- stage ---------------------------------------------------------------------

@@ -12,7 +12,12 @@ only) pinned to the closed forms the paper derives for it:
   smallest integer with T_fwd_interval - dT_fwd_interval + 7k >= 0;
 * appendix "Theoretical Analysis of T-Recomp": chunk 2's lifespan
   3p + ceil((p-1)/2) - 2, one recompute buffer block, about 25% of m_a, and
-  total time at most 6p + 7(m - 1) T_unit.
+  total time at most 6p + 7(m - 1) T_unit;
+* appendix "Scalability of T-Offload": the cool-down window between the end
+  of chunk 2's backward and chunk 1's last backward holds
+  (p - ceil((2p-3)/6) - 1) chunk backwards (2 T_unit each), the warm-up
+  window before chunk 2's first forward (p - ceil((p-3)/6) - 1) chunk
+  forwards, growing as 2p/3 and 5p/6 for large p.
 
 None of these formulas is used by the simulator: it only orders each
 stage's tasks by the slot pattern and runs them as early as dependencies
@@ -183,3 +188,74 @@ def test_tpipe_argument_errors():
         T.tpipe_schedule(4, 4, stage=4)
     with pytest.raises(T.TpsError):
         T.tpipe_schedule(4, 4, delay=-2)
+
+
+def idle_between(tasks, a, b):
+    """Idle time of a stage's task list inside [a, b), counted from the
+    simulated start and end times."""
+    if b <= a:
+        return 0
+    busy = sum(max(0, min(e, b) - max(st, a)) for _, _, _, st, e in tasks)
+    return (b - a) - busy
+
+
+@pytest.mark.parametrize("p", list(range(1, 41)))
+def test_t_offload_windows_match_the_appendix(p):
+    """The windows equal the closed forms once the mini-batch has more
+    micro-batches than chunk 1's backward lags chunk 2's (ceil((2p-3)/6)
+    rounds) and chunk 2's forward lags chunk 1's (ceil((p-3)/6) rounds);
+    shorter mini-batches leave larger windows.  The same on every stage."""
+    lag_b, lag_f = cdiv(2 * p - 3, 6), cdiv(p - 3, 6)
+    w_off = 2 * (p - lag_b - 1)          # chunk backwards of 2 T_unit
+    w_up = p - lag_f - 1                 # chunk forwards of 1 T_unit
+    stages = sorted({0, p // 2, p - 1})
+    for m in list(range(1, lag_b + 3)) + [2 * p, 3 * p + 1]:
+        for s in stages:
+            r, _ = T.tpipe_schedule(p, m, stage=s)
+            if m >= lag_b + 1:
+                assert r["offload_window"] == w_off, (p, m, s)
+            else:
+                assert r["offload_window"] >= w_off, (p, m, s)
+            if m >= lag_f + 1:
+                assert r["upload_window"] == w_up, (p, m, s)
+            else:
+                assert r["upload_window"] >= w_up, (p, m, s)
+
+
+@pytest.mark.parametrize("t_recomp", [False, True])
+def test_t_offload_windows_recount_from_the_timeline(t_recomp):
+    for p, m in [(1, 3), (3, 5), (4, 8), (7, 9), (8, 16), (13, 30)]:
+        for s in sorted({0, p // 2, p - 1}):
+            r, tasks = T.tpipe_schedule(p, m, stage=s, t_recomp=t_recomp)
+            b2_end = max(e for k, c, _, _, e in tasks if k == "B" and c == 2)
+            b1_start = max(st for k, c, _, st, _ in tasks if k == "B" and c == 1)
+            first = min(st for _, _, _, st, _ in tasks)
+            f2_start = min(st for k, c, _, st, _ in tasks if k == "F" and c == 2)
+            assert r["offload_window"] == idle_between(tasks, b2_end, b1_start), (p, m, s)
+            assert r["upload_window"] == idle_between(tasks, first, f2_start), (p, m, s)
+
+
+def test_t_offload_windows_grow_linearly_with_stages():
+    """Large-p forms of the two conditions: T_step / T_bwd * 3 / (2p) <= 1 and
+    T_upload / T_fwd * 6 / (5p) <= 1, i.e. windows of about 2p/3 chunk
+    backwards and 5p/6 chunk forwards."""
+    for p in (24, 48, 96, 192):
+        r, _ = T.tpipe_schedule(p, 2 * p)
+        assert abs(r["offload_window"] / 2 - 2 * p / 3) <= 2
+        assert abs(r["upload_window"] - 5 * p / 6) <= 2
+
+
+def test_t_offload_stage_count():
+    # windows in T_unit at m = 2p: offload 2 (p - ceil((2p-3)/6) - 1), upload p - ceil((p-3)/6) - 1
+    def first(pred):
+        return next(p for p in range(1, 257) if pred(p))
+
+    for t_off, t_up, unit in [(0.0, 0.0, 1.0), (18.0, 3.8, 1.0), (1619.0, 345.0, 90.0), (7.0, 0.5, 0.25)]:
+        p_off, p_up = T.tpipe_t_offload_stages(t_off, t_up, unit)
+        assert p_off == first(lambda p: t_off <= 2 * (p - cdiv(2 * p - 3, 6) - 1) * unit)
+        assert p_up == first(lambda p: t_up <= (p - cdiv(p - 3, 6) - 1) * unit)
+    assert T.tpipe_t_offload_stages(18.0, 3.8, 1.0) == (15, 6)
+    assert T.tpipe_t_offload_stages(1e9, 1.0, 1.0, max_stages=16) == (None, 2)
+    for bad in [(1.0, 1.0, 0.0), (-1.0, 1.0, 1.0), (1.0, -1.0, 1.0)]:
+        with pytest.raises(ValueError):
+            T.tpipe_t_offload_stages(*bad)
