@@ -330,14 +330,22 @@ void gemm_bf16_kernel(GemmArgs g) {
   gemm_epilogue<EPI, BM, BN, WGM, WGN, TM, TN, STAGES * STAGE>(g, acc, smem, m0, n0, wm, wn, lane, wave);
 }
 
-template <int LAYOUT, int BM, int BN, int EPI>
-static hipError_t launch_pipe_epi(GemmArgs g, hipStream_t stream) {
-  constexpr V3Config c = v3_config(BM == 256);
+template <int LAYOUT, int BM, int BN, int EPI, bool LONG_K>
+static hipError_t launch_pipe_cfg(GemmArgs g, hipStream_t stream) {
+  constexpr V3Config c = v3_config(LAYOUT, BM == 256, LONG_K);
   g.tiles_m = g.M / BM;
   g.tiles_n = g.N / BN;
   hipLaunchKernelGGL((gemm_bf16_kernel<LAYOUT, BM, BN, c.wgm, c.wgn, c.bk, c.stages, EPI>), dim3(g.tiles_m * g.tiles_n),
                      dim3(64 * c.wgm * c.wgn), 0, stream, g);
   return hipGetLastError();
+}
+
+template <int LAYOUT, int BM, int BN, int EPI>
+static hipError_t launch_pipe_epi(GemmArgs g, hipStream_t stream) {
+  if constexpr (LAYOUT == TPS_GEMM_TN && BM == 256) {
+    if (g.K >= TN_LONG_K) return launch_pipe_cfg<LAYOUT, BM, BN, EPI, true>(g, stream);
+  }
+  return launch_pipe_cfg<LAYOUT, BM, BN, EPI, false>(g, stream);
 }
 
 // Epilogues each layout uses in the stage (others take the generic path).

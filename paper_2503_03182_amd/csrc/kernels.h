@@ -28,14 +28,25 @@ struct GemmTile {
 };
 GemmTile gemm_select_tile(int dtype, int layout, const GemmArgs& g);
 
-// Shape of the tile-aligned bf16 kernel per tile size, chosen by measurement
-// on MI355X: waves along M and N, K tile and LDS ring depth.  256 x 256
-// tiles run two waves per SIMD (128 x 64 per wave); 128 x 128 tiles, used
-// when 256 x 256 would leave most CUs idle, one wave per SIMD (64 x 64).
+// Shape of the tile-aligned bf16 kernel per layout and tile size, chosen by
+// measurement on MI355X: waves along M and N, K tile and LDS ring depth.
+// 256 x 256 tiles run two waves per SIMD (128 x 64 per wave, K tiles of 64,
+// a ring of 2), except the weight-gradient (TN) product with a contraction of
+// TN_LONG_K or more: both of its operands are read with 8-byte transposing LDS
+// reads, so it takes one wave per SIMD of 128 x 128 (one LDS read per MFMA
+// instead of 1.5) with K tiles of 32 in a ring of 4 (3-7% faster at
+// K = 32768, 1% at 4096; at 2048, where the product runs beside the input-
+// gradient chain, the stage lost 0.5%).  128 x 128 tiles, used when 256 x 256
+// would leave most CUs idle: one wave per SIMD (64 x 64), K tiles of 64, a
+// ring of 4.
 struct V3Config {
   int wgm, wgn, bk, stages;
 };
-constexpr V3Config v3_config(bool big) { return big ? V3Config{2, 4, 64, 2} : V3Config{2, 2, 64, 4}; }
+constexpr int TN_LONG_K = 4096;
+constexpr V3Config v3_config(int layout, bool big, bool long_k) {
+  return !big ? V3Config{2, 2, 64, 4}
+              : (layout == TPS_GEMM_TN && long_k) ? V3Config{2, 2, 32, 4} : V3Config{2, 4, 64, 2};
+}
 // Demangled name of the kernel instantiation a launch uses (as profilers
 // print it), e.g. "tps::gemm_bf16_kernel<0, 256, 256, 2, 4, 64, 2, 1>".
 const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g);

@@ -256,23 +256,23 @@ const char* gemm_kernel_name(int dtype, int layout, const GemmArgs& g) {
         "tps::gemm_kernel<__bf16, 128, 128, 64, 2>"},
        {"tps::gemm_kernel<__bf16, 256, 128, 64, 0>", "tps::gemm_kernel<__bf16, 256, 128, 64, 1>",
         "tps::gemm_kernel<__bf16, 256, 128, 64, 2>"}}};
-  // [tile][layout][epilogue]
-  static char v3[2][3][6][64];
+  // [long K][tile][layout][epilogue]
+  static char v3[2][2][3][6][64];
   static bool init = false;
   if (!init) {
-    for (int t = 0; t < 2; ++t)
-      for (int l = 0; l < 3; ++l)
-        for (int e = 0; e < 6; ++e)
-        {
-          const V3Config c = v3_config(t == 1);
-          const int tile = t ? 256 : 128;
-          snprintf(v3[t][l][e], sizeof(v3[t][l][e]), "tps::gemm_bf16_kernel<%d, %d, %d, %d, %d, %d, %d, %d>", l,
-                   tile, tile, c.wgm, c.wgn, c.bk, c.stages, e);
-        }
+    for (int k = 0; k < 2; ++k)
+      for (int t = 0; t < 2; ++t)
+        for (int l = 0; l < 3; ++l)
+          for (int e = 0; e < 6; ++e) {
+            const V3Config c = v3_config(l, t == 1, k == 1);
+            const int tile = t ? 256 : 128;
+            snprintf(v3[k][t][l][e], sizeof(v3[k][t][l][e]), "tps::gemm_bf16_kernel<%d, %d, %d, %d, %d, %d, %d, %d>",
+                     l, tile, tile, c.wgm, c.wgn, c.bk, c.stages, e);
+          }
     init = true;
   }
   const GemmTile t = gemm_select_tile(dtype, layout, g);
-  if (t.aligned) return v3[t.bm == 256][layout][g.epi];
+  if (t.aligned) return v3[g.K >= TN_LONG_K][t.bm == 256][layout][g.epi];
   return v1[dtype == TPS_BF16][t.bm == 256][layout];
 }
 
