@@ -423,14 +423,15 @@ def tpipe_t_offload_stages(t_offload, t_upload, t_unit, micro=None, max_stages=2
     the cool-down window of the simulated schedule, and the reload of a
     chunk's weights (`t_upload`) within its warm-up window.  `t_unit` is the
     forward of one chunk for one micro-batch (a backward takes two), all three
-    in the same unit; the schedule has max(micro, 2p) micro-batches.  Returns
-    (p for the offload, p for the upload), None where no p up to max_stages
-    suffices."""
+    in the same unit; the windows are those of stage 0 of the plain schedule
+    (no T-Recomp, no delay) with max(micro, 2p) micro-batches, where every
+    stage has the same windows.  Returns (p for the offload, p for the
+    upload), None where no p up to max_stages suffices."""
     if not (t_unit > 0) or t_offload < 0 or t_upload < 0:
         raise ValueError("t_unit must be positive, t_offload and t_upload non-negative")
     p_off = p_up = None
     for p in range(1, max_stages + 1):
-        r, _ = tpipe_schedule(p, max(micro or 0, 2 * p))
+        r, _ = tpipe_schedule(p, max(micro or 0, 2 * p), delay=0)
         if p_off is None and t_offload <= r["offload_window"] * t_unit:
             p_off = p
         if p_up is None and t_upload <= r["upload_window"] * t_unit:
