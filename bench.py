@@ -128,12 +128,14 @@ def build_stage(cfg):
     return blocks, grads, xs, dys, ys, dxs
 
 
-def t_offload_state(cfg, blocks):
-    """Host model state of T-Offload: f32 master weights (from the streamed
-    bf16 parameter blocks), zero AdamW moments, all in the gradient layout;
-    with the FP8 reload the host parameter blocks are rewritten in the
-    quantized layout from the masters.  Returns (parameter blocks, (master,
-    m, v))."""
+def t_offload_state(cfg, blocks, n_device=0):
+    """Model state of T-Offload: f32 master weights (from the streamed bf16
+    parameter blocks), zero AdamW moments, all in the gradient layout; with
+    the FP8 reload the host parameter blocks are rewritten in the quantized
+    layout from the masters.  The first n_device layers keep their state on
+    the GPU: device master, moments and a device copy of their bf16
+    parameter block.  Returns (parameter blocks, (master, m, v), device
+    parameter blocks)."""
     import numpy as np
     from paper_2503_03182_amd import tpstage as T
     from paper_2503_03182_amd import synth
@@ -153,6 +155,8 @@ def t_offload_state(cfg, blocks):
         masters.append(mst)
         ms.append(np.zeros_like(mst))
         vs.append(np.zeros_like(mst))
+    import torch
+    dparams = [torch.from_numpy(blocks[l].numpy()).cuda() for l in range(n_device)]
     if cfg.weights_quant == T.Q_FP8_ROW:
         qbytes = T.param_layout_q(cfg)[2]
         qblocks = []
@@ -162,7 +166,9 @@ def t_offload_state(cfg, blocks):
                                n_threads=len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 0)
             qblocks.append(hb)
         blocks = qblocks
-    return blocks, (masters, ms, vs)
+    for l in range(n_device):
+        masters[l], ms[l], vs[l] = (torch.from_numpy(a).cuda() for a in (masters[l], ms[l], vs[l]))
+    return blocks, (masters, ms, vs), dparams
 
 
 def host_link_rates(stream, gib: float = 1.0, reps: int = 3):
@@ -187,23 +193,25 @@ def host_link_rates(stream, gib: float = 1.0, reps: int = 3):
     return rates[0], rates[1]
 
 
-def t_offload_stages(cfg, info, link, gpu_ms_per_step, h2d_gbs, d2h_gbs):
+def t_offload_stages(cfg, info, link, gpu_ms_per_step, h2d_gbs, d2h_gbs, n_device=0):
     """The appendix "Scalability of T-Offload" applied to this stage taken as
     one chunk: the smallest pipeline depths at which the measured host work
     would fit T-Pipe's bubbles (tpipe_t_offload_stages).  T_unit is the
     chunk's forward for one micro-batch, a third of its GPU time per
     micro-batch (backward = two forwards, as in the schedule's unit-time
-    model); the chunk's offload time is its gradients over the measured
-    device-to-host rate plus its measured host updates; its upload time is
-    one load of its host parameter blocks over the host-to-device rate."""
+    model); the chunk's offload time is the gradients of its host-updated
+    layers over the measured device-to-host rate plus their measured host
+    updates; its upload time is one load of their host parameter blocks over
+    the host-to-device rate."""
     from paper_2503_03182_amd import tpstage as T
     t_unit = gpu_ms_per_step / (3 * cfg.n_micro)
-    grad_gb = cfg.n_layers * info["grad_bytes"] / 1e9
+    n_host = cfg.n_layers - n_device
+    grad_gb = n_host * info["grad_bytes"] / 1e9
     blk = T.param_layout_q(cfg)[2] if cfg.weights_quant == T.Q_FP8_ROW else T.param_layout(cfg)[1]
-    up_gb = cfg.n_layers * blk / 1e9
+    up_gb = n_host * blk / 1e9
     # the update thread lags the GPU: a step's window also sees updates of
-    # the step before, so the chunk's time is the mean per layer times L
-    t_off = grad_gb / d2h_gbs * 1e3 + cfg.n_layers * link["host_update_ms"] / max(link["host_updates"], 1)
+    # the step before, so the chunk's time is the mean per layer times the layers
+    t_off = grad_gb / d2h_gbs * 1e3 + n_host * link["host_update_ms"] / max(link["host_updates"], 1)
     t_up = up_gb / h2d_gbs * 1e3
     p_off, p_up = T.tpipe_t_offload_stages(t_off, t_up, t_unit)
     return {"t_unit_ms": round(t_unit, 2), "link_gbs": {"h2d": round(h2d_gbs, 1), "d2h": round(d2h_gbs, 1)},
@@ -359,6 +367,8 @@ def main():
     ap.add_argument("--t-offload", choices=("bf16", "fp8"), default=None,
                     help="streamed workloads: attach the host AdamW update of every layer (T-Offload of model "
                          "state) and reload the updated weights as bf16 or as FP8 codes with row scales")
+    ap.add_argument("--device-layers", type=int, default=2,
+                    help="with --t-offload: the shallowest layers whose model state and AdamW step stay on the GPU")
     ap.add_argument("--layers", type=int, default=None, help="override the workload's layer count")
     args = ap.parse_args()
     if args.standalone_gemms:
@@ -397,6 +407,9 @@ def main():
             sys.exit(2)
         if args.t_offload == "fp8":
             cfg = dataclasses.replace(cfg, weights_quant=T.Q_FP8_ROW)
+        if not 0 <= args.device_layers <= cfg.n_layers:
+            print("--device-layers must be in 0..layers", file=sys.stderr)
+            sys.exit(2)
     long_step = cfg.hidden >= 8192
     if args.steps is None:
         args.steps = 5 if long_step else 20
@@ -413,16 +426,18 @@ def main():
     blocks, grads, xs, dys, ys, dxs = build_stage(cfg)
     torch.cuda.synchronize()
     opt_state = None
+    dparams = []
     if args.t_offload is not None:
-        blocks, opt_state = t_offload_state(cfg, blocks)
+        blocks, opt_state, dparams = t_offload_state(cfg, blocks, args.device_layers)
     stage = T.Stage(cfg, blocks, grads)
     link_rates = None
     if opt_state is not None:
         link_rates = host_link_rates(run_stream)
         log(f"[bench] host link {link_rates[0]:.1f} GB/s to the device, {link_rates[1]:.1f} GB/s back")
         n_threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
-        stage.set_optimizer(*opt_state, first_step=1, lr=1e-5, n_threads=n_threads)
-        log(f"[bench] host AdamW on {n_threads} threads, reload as {args.t_offload}")
+        stage.set_optimizer(*opt_state, first_step=1, lr=1e-5, n_threads=n_threads, dparams=dparams)
+        log(f"[bench] AdamW of layers 0..{args.device_layers - 1} on the GPU, of the others on {n_threads} host "
+            f"threads, reload as {args.t_offload}")
     assert stage.cs.cuda_stream == run_stream.cuda_stream
     order = cfg.order()
     step_flops = info["fwd_flops"] + info["bwd_flops"] + info["recompute_flops"]
@@ -478,13 +493,16 @@ def main():
     value = step_flops * args.steps / (t1 - t0) / 1e12
     t_offload = None
     if opt_state is not None:
-        t_offload = {"reload": args.t_offload, "optimizer": "AdamW (host, f32 master weights)",
+        t_offload = {"reload": args.t_offload, "optimizer": "AdamW (f32 master weights)",
+                     "device_layers": args.device_layers,
                      "host_update_ms_per_layer": round(link["host_update_ms"] / max(link["host_updates"], 1), 1),
                      "host_updates_finished_during_last_step": link["host_updates"],
                      "reload_wait_ms_last_step": round(link["host_wait_ms"], 1),
-                     "host_state_gb": round(3 * cfg.n_layers * info["grad_bytes"] / 1e9, 2),
+                     "host_state_gb": round(3 * (cfg.n_layers - args.device_layers) * info["grad_bytes"] / 1e9, 2),
+                     "device_state_gb": round(args.device_layers * (3 * info["grad_bytes"] + info["param_bytes"]) / 1e9,
+                                              2),
                      "tpipe_bubbles": t_offload_stages(cfg, info, link, sum(r["ms"] for r in breakdown),
-                                                       *link_rates)}
+                                                       *link_rates, n_device=args.device_layers)}
     achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
     step_ms_breakdown = sum(r["ms"] for r in breakdown)
     out = {

@@ -491,6 +491,27 @@ int tps_host_adamw_layer(const tps_config* cfg, const tps_adamw* opt, int32_t st
 int tps_stage_set_optimizer(tps_stage* st, const tps_adamw* opt, float* const* master, float* const* m,
                             float* const* v, int32_t first_step, int32_t n_threads);
 
+/* As tps_stage_set_optimizer, with the model state of the shallowest
+ * n_device layers (0 .. n_device - 1) kept on the GPU (paper, Section 5 and
+ * the T-Offload scalability appendix: the shallow chunk's states stay on the
+ * device where no bubble hides their offload; on one GPU layer 0's update
+ * would otherwise sit between two iterations).  For those layers master[l],
+ * m[l] and v[l] are device f32 blocks (gradient-block layout, 16-byte
+ * aligned) and dparams[l] a device parameter block in the storage dtype
+ * (tps_param_layout) holding the layer's current parameters, all owned by the
+ * caller.  Once every backward of an iteration has passed such a layer, its
+ * AdamW step runs on the compute stream with the host update's arithmetic
+ * (the same f32 operations, hence the same bits), writing master, m, v and
+ * dparams[l]; its gradient block is consumed on the device and not written
+ * to the host, and its loads copy dparams[l] (its pinned host block is no
+ * longer read, and with weights_quant its parameters are not quantized).
+ * Iterations must start with zero_grads set.  n_device in 0 .. n_layers
+ * (dparams may be NULL when 0); TPS_EINVAL otherwise, or for a null or
+ * misaligned device block. */
+int tps_stage_set_optimizer_split(tps_stage* st, const tps_adamw* opt, float* const* master, float* const* m,
+                                  float* const* v, void* const* dparams, int32_t n_device, int32_t first_step,
+                                  int32_t n_threads);
+
 /* Thread-local message of the last failing call ("" if none). */
 const char* tps_last_error(void);
 

@@ -50,6 +50,8 @@ struct Adam {
   float b1, b2, eps, lr_c, wd_c;   // lr_c = lr / (1 - b1^t) , wd_c = lr * wd
   float inv_bc2_sqrt;              // 1 / sqrt(1 - b2^t)
   bool update;
+  // the element update; the device update (optim.hip) performs the same f32
+  // operations in the same order
   void apply(float* __restrict__ w, float* __restrict__ m, float* __restrict__ v, const float* __restrict__ g,
              int64_t n) const {
     if (!update) return;
@@ -85,6 +87,18 @@ void parallel_for(int64_t n, int threads, F&& f) {
 
 namespace tps {
 
+AdamwCoef adamw_coef(const tps_adamw& opt, int32_t step) {
+  AdamwCoef c{};
+  c.b1 = opt.beta1;
+  c.b2 = opt.beta2;
+  c.eps = opt.eps;
+  const double bc1 = 1.0 - std::pow((double)opt.beta1, step), bc2 = 1.0 - std::pow((double)opt.beta2, step);
+  c.lr_c = (float)(opt.lr / bc1);
+  c.inv_bc2_sqrt = (float)(1.0 / std::sqrt(bc2));
+  c.wd_c = opt.lr * opt.weight_decay;
+  return c;
+}
+
 int host_adamw(const Plan& p, const tps_adamw* opt, int32_t step, float* master, float* m, float* v,
                const float* grad, void* params_out, int32_t quant, int32_t n_threads) {
   if (!master || !params_out) return tps::set_error(TPS_EINVAL, "tps_host_adamw_layer: null argument");
@@ -99,13 +113,13 @@ int host_adamw(const Plan& p, const tps_adamw* opt, int32_t step, float* master,
   Adam A{};
   A.update = step > 0;
   if (A.update) {
-    A.b1 = opt->beta1;
-    A.b2 = opt->beta2;
-    A.eps = opt->eps;
-    const double bc1 = 1.0 - std::pow((double)opt->beta1, step), bc2 = 1.0 - std::pow((double)opt->beta2, step);
-    A.lr_c = (float)(opt->lr / bc1);
-    A.inv_bc2_sqrt = (float)(1.0 / std::sqrt(bc2));
-    A.wd_c = opt->lr * opt->weight_decay;
+    const AdamwCoef c = adamw_coef(*opt, step);
+    A.b1 = c.b1;
+    A.b2 = c.b2;
+    A.eps = c.eps;
+    A.lr_c = c.lr_c;
+    A.inv_bc2_sqrt = c.inv_bc2_sqrt;
+    A.wd_c = c.wd_c;
   }
   const int threads = n_threads > 0 ? n_threads : std::max(1u, std::thread::hardware_concurrency());
   const int mat_slot[TPS_P_COUNT] = {0, -1, 1, -1, 2, -1, 3, -1, -1, -1, -1, -1};

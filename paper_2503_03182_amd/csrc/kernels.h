@@ -151,6 +151,14 @@ hipError_t gqa_fold_launch(const void* ws, void* dqkv, int rows, int nh, int nkv
 hipError_t fill_bytes_launch(void* p, uint64_t bytes, uint8_t value, hipStream_t st);
 // out (bf16) [rows][cols] = bf16(decode_e4m3(q[r][c]) * scale[r]); cols % 8 == 0,
 // q 8-byte and out 16-byte aligned
+// One AdamW step of n contiguous parameters on the device (f32 master w and
+// moments m, v updated in place from the f32 gradient g; out receives w in the
+// storage dtype, round to nearest even): the host update's f32 operations in
+// its order, so both give the same bits.  c: b1, b2, eps, lr_c, inv_bc2_sqrt,
+// wd_c as in AdamwCoef (planner.h).
+hipError_t adamw_launch(int dtype, int64_t n, float* w, float* m, float* v, const float* g, void* out,
+                        const float c[6], hipStream_t st);
+
 hipError_t dequant_fp8_rows_launch(const void* q, const float* scale, int64_t rows, int64_t cols, void* out,
                                    hipStream_t st);
 // out[c][r] = in[r][c] for in [rows, cols]; rows and cols multiples of 8

@@ -145,6 +145,15 @@ double op_flops(const Plan& p, int op);
 
 void fill_plan_info(const Plan& p, tps_plan_info* info);
 
+// f32 coefficients of one AdamW step (step >= 1), computed once per layer
+// update in double and rounded to f32: lr_c = lr / (1 - b1^step),
+// inv_bc2_sqrt = 1 / sqrt(1 - b2^step), wd_c = lr wd.  The host update and the
+// device update take the same values.
+struct AdamwCoef {
+  float b1, b2, eps, lr_c, inv_bc2_sqrt, wd_c;
+};
+AdamwCoef adamw_coef(const tps_adamw& opt, int32_t step);
+
 // One host AdamW step of a layer and its parameter block for the device
 // (tps_host_adamw_layer, on an existing plan).
 int host_adamw(const Plan& p, const tps_adamw* opt, int32_t step, float* master, float* m, float* v,

@@ -171,6 +171,13 @@ struct tps_stage {
     std::vector<int> bpass;          // layer backwards this iteration
     std::vector<hipEvent_t> final_ev;   // final gradient flush of the layer (copy stream)
     std::vector<char> pending;       // update queued or running
+    // layers 0 .. n_dev - 1 are updated on the device: master, m, v are device
+    // blocks, dparams[l] the layer's device parameter block (loads copy it),
+    // dev_ev[l] the end of its last update (compute stream)
+    int n_dev = 0;
+    std::vector<void*> dparams;
+    std::vector<hipEvent_t> dev_ev;
+    std::vector<char> dev_ev_valid;
     std::deque<int> queue;
     std::mutex mu;
     std::condition_variable cv;
@@ -380,6 +387,19 @@ char* tps_stage::qstage_of(int entry) {
 int tps_stage::load_params(int l, int e) {
   int ent = e;
   char* dst = const_cast<char*>(params_of(l, &ent));
+  if (hopt.on && l < hopt.n_dev) {
+    // a layer updated on the device: its parameters in the storage dtype,
+    // after its last update, or before the first one after the caller's
+    // writes (which every call orders before the compute stream's work)
+    if (hopt.dev_ev_valid[l]) {
+      TPS_HIP(hipStreamWaitEvent(ps, hopt.dev_ev[l], 0));
+    } else {
+      TPS_HIP(hipEventRecord(ev_tmp, cs));
+      TPS_HIP(hipStreamWaitEvent(ps, ev_tmp, 0));
+    }
+    TPS_HIP(hipMemcpyAsync(dst, hopt.dparams[l], p.pbytes, hipMemcpyDeviceToDevice, ps));
+    return TPS_OK;
+  }
   if (p.quant != TPS_Q_FP8_ROW) {
     TPS_HIP(hipMemcpyAsync(dst, lp[l], p.pbytes, hipMemcpyHostToDevice, ps));
     stats.h2d_bytes += p.pbytes;
@@ -519,6 +539,30 @@ int tps_stage::opt_after_backward(int l, int passes) {
   if (!hopt.on) return TPS_OK;
   hopt.bpass[l] += passes;
   if (hopt.bpass[l] < p.M) return TPS_OK;
+  if (l < hopt.n_dev) {
+    // on the device, in compute-stream order after the layer's last
+    // backward: its gradients stay in the window entry and are consumed
+    // there (not copied to the host)
+    int e = 0;
+    while (e < (int)win.size() && win[e].layer != l) ++e;
+    if (e == (int)win.size()) return set_error(TPS_ESTATE, "device optimizer: layer not resident");
+    const AdamwCoef c = adamw_coef(hopt.hp, hopt.step[l]);
+    const float cf[6] = {c.b1, c.b2, c.eps, c.lr_c, c.inv_bc2_sqrt, c.wd_c};
+    const float* G = grads_of(l, e);
+    char* out = static_cast<char*>(hopt.dparams[l]);
+    for (int i = 0; i < TPS_P_COUNT; ++i) {
+      if (p.prow[i] == 0) continue;
+      const int64_t n = p.prow[i] * p.pcol[i], o = (int64_t)(p.goff[i] / 4);
+      TPS_HIP(adamw_launch(p.dtype, n, hopt.master[l] + o, hopt.m[l] + o, hopt.v[l] + o, G + o, out + p.poff[i], cf,
+                           cs));
+      ++stats.kernels;
+    }
+    TPS_HIP(hipEventRecord(hopt.dev_ev[l], cs));
+    hopt.dev_ev_valid[l] = 1;
+    ++hopt.step[l];
+    win[e].grads_live = false;
+    return touch(e);
+  }
   for (size_t e = 0; e < win.size(); ++e)
     if (win[e].layer == l) TPS_TRY(flush_grads((int)e));
   TPS_HIP(hipEventRecord(hopt.final_ev[l], xs));
@@ -1352,6 +1396,8 @@ extern "C" int tps_stage_init(const tps_config* cfg, const tps_params* params, c
 extern "C" int tps_stage_begin_iteration(tps_stage* st, int zero_grads) {
   clear_error();
   if (!st) return set_error(TPS_EINVAL, "null stage");
+  if (st->hopt.on && st->hopt.n_dev > 0 && !zero_grads)
+    return set_error(TPS_EINVAL, "tps_stage_begin_iteration: layers updated on the device need zero_grads");
   if (st->in_iteration && st->cursor != 0 && st->cursor < (int)st->p.op_kind.size())
     return set_error(TPS_ESTATE, "previous iteration has unfinished ops");
   st->cursor = 0;
@@ -1616,8 +1662,22 @@ extern "C" int tps_stage_sync(tps_stage* st) {
 
 extern "C" int tps_stage_set_optimizer(tps_stage* st, const tps_adamw* opt, float* const* master, float* const* m,
                                        float* const* v, int32_t first_step, int32_t n_threads) {
+  return tps_stage_set_optimizer_split(st, opt, master, m, v, nullptr, 0, first_step, n_threads);
+}
+
+extern "C" int tps_stage_set_optimizer_split(tps_stage* st, const tps_adamw* opt, float* const* master,
+                                             float* const* m, float* const* v, void* const* dparams, int32_t n_device,
+                                             int32_t first_step, int32_t n_threads) {
   clear_error();
   if (!st || !opt || !master || !m || !v) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: null argument");
+  if (n_device < 0 || n_device > st->p.L) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: n_device out of range");
+  if (n_device > 0 && !dparams) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: null device parameter blocks");
+  for (int l = 0; l < n_device; ++l) {
+    if (!dparams[l]) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: null device parameter block");
+    // the device update reads and writes 16-byte groups of the f32 blocks
+    if (((uintptr_t)master[l] | (uintptr_t)m[l] | (uintptr_t)v[l]) & 15u)
+      return set_error(TPS_EINVAL, "tps_stage_set_optimizer: device blocks must be 16-byte aligned");
+  }
   const Plan& p = st->p;
   if (p.weights != TPS_W_STREAM) return set_error(TPS_EINVAL, "tps_stage_set_optimizer: needs streamed weights");
   if (st->hopt.on) return set_error(TPS_ESTATE, "tps_stage_set_optimizer: already set");
@@ -1640,6 +1700,13 @@ extern "C" int tps_stage_set_optimizer(tps_stage* st, const tps_adamw* opt, floa
   h.pending.assign(p.L, 0);
   h.final_ev.assign(p.L, nullptr);
   for (auto& e : h.final_ev) TPS_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  h.n_dev = n_device;
+  h.dparams.assign(p.L, nullptr);
+  for (int l = 0; l < n_device; ++l) h.dparams[l] = dparams[l];
+  h.dev_ev.assign(p.L, nullptr);
+  h.dev_ev_valid.assign(p.L, 0);
+  for (int l = 0; l < n_device; ++l)
+    TPS_HIP(hipEventCreateWithFlags(&h.dev_ev[l], hipEventDisableTiming | hipEventDisableSystemFence));
   h.on = true;
   h.worker = std::thread([st] { st->opt_worker(); });
   return TPS_OK;
@@ -1726,6 +1793,8 @@ extern "C" int tps_stage_destroy(tps_stage* st) {
     st->hopt.worker.join();
   }
   for (auto e : st->hopt.final_ev)
+    if (e) (void)hipEventDestroy(e);
+  for (auto e : st->hopt.dev_ev)
     if (e) (void)hipEventDestroy(e);
   if (st->cs) (void)hipStreamSynchronize(st->cs);
   if (st->xs) (void)hipStreamSynchronize(st->xs);

@@ -132,7 +132,8 @@ EXPORTED = (
     "tps_op_workspace_bytes", "tps_stage_time_kernels", "tps_stage_kernel_times",
     "tps_host_alloc", "tps_host_free", "tps_tpipe_schedule", "tps_op_attention_bwd_noalloc",
     "tps_op_attention_bwd_noalloc_max_rows", "tps_param_layout_q", "tps_host_adamw_layer",
-    "tps_stage_set_optimizer", "tps_op_dequant_fp8_rows", "tps_op_rmsnorm_fwd", "tps_op_rmsnorm_bwd", "tps_op_rope",
+    "tps_stage_set_optimizer", "tps_stage_set_optimizer_split", "tps_op_dequant_fp8_rows", "tps_op_rmsnorm_fwd",
+    "tps_op_rmsnorm_bwd", "tps_op_rope",
     "tps_op_swiglu_fwd", "tps_op_swiglu_bwd", "tps_op_attention_gqa_fwd", "tps_op_attention_gqa_bwd",
 )
 
@@ -192,6 +193,8 @@ def lib() -> C.CDLL:
         L.tps_host_adamw_layer.argtypes = [C.POINTER(Config), C.POINTER(AdamW), i32, vp, vp, vp, vp, vp, i32, i32]
         L.tps_stage_set_optimizer.argtypes = [vp, C.POINTER(AdamW), C.POINTER(vp), C.POINTER(vp), C.POINTER(vp),
                                               i32, i32]
+        L.tps_stage_set_optimizer_split.argtypes = [vp, C.POINTER(AdamW), C.POINTER(vp), C.POINTER(vp), C.POINTER(vp),
+                                                   C.POINTER(vp), i32, i32, i32]
         L.tps_tpipe_schedule.argtypes = [C.POINTER(TPipeConfig), i32, C.POINTER(TPipeTask), i32,
                                          C.POINTER(C.c_int32), C.POINTER(TPipeResult)]
         _lib = L
@@ -527,19 +530,23 @@ class Stage:
         check(lib().tps_stage_sync(self.handle))
 
     def set_optimizer(self, master, m, v, first_step: int = 1, lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8,
-                      weight_decay=0.0, n_threads: int = 0) -> None:
-        """tps_stage_set_optimizer: host AdamW of every streamed layer once its
-        gradients of the iteration are final (master, m, v: per-layer host f32
-        blocks in the gradient layout, each with data_ptr() or a numpy array)."""
+                      weight_decay=0.0, n_threads: int = 0, dparams=None) -> None:
+        """tps_stage_set_optimizer(_split): AdamW of every streamed layer once
+        its gradients of the iteration are final (master, m, v: per-layer f32
+        blocks in the gradient layout, each with data_ptr() or a numpy array).
+        With dparams (device parameter blocks of the first len(dparams)
+        layers), those layers' master, m and v are device tensors and their
+        update runs on the GPU; the other layers' blocks are host memory."""
         def ptrs(blocks):
             return (C.c_void_p * len(blocks))(*[b.data_ptr() if hasattr(b, "data_ptr") else b.ctypes.data
                                                 for b in blocks])
-        self._opt_keep = (ptrs(master), ptrs(m), ptrs(v), master, m, v)
+        dparams = list(dparams or [])
+        self._opt_keep = (ptrs(master), ptrs(m), ptrs(v), ptrs(dparams) if dparams else None, master, m, v, dparams)
         opt = AdamW(lr, beta1, beta2, eps, weight_decay)
-        check(lib().tps_stage_set_optimizer(self.handle, C.byref(opt),
-                                            C.cast(self._opt_keep[0], C.POINTER(C.c_void_p)),
-                                            C.cast(self._opt_keep[1], C.POINTER(C.c_void_p)),
-                                            C.cast(self._opt_keep[2], C.POINTER(C.c_void_p)), first_step, n_threads))
+        cast = lambda a: C.cast(a, C.POINTER(C.c_void_p)) if a is not None else None
+        check(lib().tps_stage_set_optimizer_split(self.handle, C.byref(opt), cast(self._opt_keep[0]),
+                                                  cast(self._opt_keep[1]), cast(self._opt_keep[2]),
+                                                  cast(self._opt_keep[3]), len(dparams), first_step, n_threads))
 
     def sync_for(self, timeout_ms: float) -> int:
         """Bounded wait: TPS_OK when every stream of the stage is idle,

@@ -186,6 +186,27 @@ class FakeStage:
         for l in range(self.cfg.n_layers):
             L.tps_hb_host_access(self.grads[l], self.gbytes, 0)
 
+    def set_device_optimizer(self, tag: int = 0):
+        """Every layer's AdamW on the device (tps_stage_set_optimizer_split
+        with n_device = n_layers): fake device master, moment and parameter
+        blocks, written by the caller on the compute stream beforehand."""
+        L = lib()
+        n = self.cfg.n_layers
+        base = (tag + 1) * 64 * TiB + 9 * TiB
+        blocks = {k: [base + i * TiB + l * 16 * GiB for l in range(n)] for i, k in enumerate(("m", "mo", "v", "p"))}
+        for k, arr in blocks.items():
+            for l, a in enumerate(arr):
+                nb = self.pbytes if k == "p" else self.gbytes
+                L.tps_hb_name_region(a, nb, f"opt-{k}[{tag}][{l}]".encode())
+                L.tps_hb_stream_access(self.cs, a, nb, 1)
+        self.opt_blocks = blocks
+        arr = {k: (C.c_void_p * n)(*v) for k, v in blocks.items()}
+        self._opt_keep = arr
+        opt = T.AdamW(1e-3, 0.9, 0.95, 1e-8, 0.0)
+        cast = lambda a: C.cast(a, C.POINTER(C.c_void_p))
+        check(L.tps_stage_set_optimizer_split(C.c_void_p(self.h.value), C.byref(opt), cast(arr["m"]), cast(arr["mo"]),
+                                              cast(arr["v"]), cast(arr["p"]), n, 1, 1))
+
     def close(self):
         if self.h:
             lib().tps_stage_destroy(self.h)

@@ -250,6 +250,16 @@ hipError_t fill_bytes_launch(void* p, uint64_t bytes, uint8_t value, hipStream_t
 
 hipError_t fill_zero_launch(void* p, uint64_t bytes, hipStream_t st) { return fill_bytes_launch(p, bytes, 0, st); }
 
+hipError_t adamw_launch(int dtype, int64_t n, float* w, float* m, float* v, const float* g, void* out,
+                        const float* /*c*/, hipStream_t st) {
+  HbRanges rd, wr;
+  for (const float* p : {(const float*)w, (const float*)m, (const float*)v, g}) add1d(rd, p, n * 4);
+  for (float* p : {w, m, v}) add1d(wr, p, n * 4);
+  add1d(wr, out, n * esz(dtype));
+  hb_op(st, "adamw", rd, wr);
+  return hipSuccess;
+}
+
 hipError_t dequant_fp8_rows_launch(const void* q, const float* scale, int64_t rows, int64_t cols, void* out,
                                    hipStream_t st) {
   HbRanges rd, wr;

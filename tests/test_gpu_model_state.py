@@ -174,3 +174,134 @@ def test_host_optimizer_iterations_match_oracle(quant, group):
             # (the k part of the qkv bias has an exactly zero true gradient,
             # so its rounding noise is all relative error)
             assert rel < 5e-2, (quant, group, l, n, rel)
+
+
+def _run_split(cfg, n_dev, group, iterations=3, hp=HP):
+    """`iterations` iterations with the AdamW of layers < n_dev on the GPU
+    (device master, moments and parameter blocks) and of the others on the
+    host; returns the per-iteration outputs and input gradients, the host
+    gradient blocks of the last iteration and the final master weights and
+    moments of every layer (numpy)."""
+    import torch
+    L = cfg.n_layers
+    masters = _master_blocks(cfg)
+    m0 = [np.zeros_like(b) for b in masters]
+    v0 = [np.zeros_like(b) for b in masters]
+    blocks = _host_param_blocks(cfg, masters)
+    gb = T.param_layout(cfg)[3]
+    grads = [torch.zeros(gb, dtype=torch.uint8, pin_memory=True) for _ in range(L)]
+    xs, dys = inputs(cfg)
+    st = T.Stage(cfg, blocks, grads)
+    dev = [[torch.from_numpy(b[l]).cuda() for l in range(n_dev)] for b in (masters, m0, v0)]
+    # the device parameter blocks start as the host blocks (storage dtype)
+    pb = T.param_layout(cfg)[1]
+    dpar = [_host_param_blocks(dataclasses_replace_quant(cfg), [masters[l]])[0][:pb].cuda() for l in range(n_dev)]
+    pick = lambda d, h: [d[l] if l < n_dev else h[l] for l in range(L)]
+    st.set_optimizer(pick(dev[0], masters), pick(dev[1], m0), pick(dev[2], v0), first_step=1, n_threads=4,
+                     dparams=dpar, **hp)
+    X = [to_dev(x, cfg.dtype) for x in xs]
+    DY = [to_dev(d, cfg.dtype) for d in dys]
+    Y = [torch.empty_like(x) for x in X]
+    DX = [torch.empty_like(x) for x in X]
+    outs = []
+    for _ in range(iterations):
+        drive_iteration(st, cfg, X, DY, Y, DX, group=group)
+        outs.append(results(cfg, st, Y, DX, grads))
+    st.close()
+    state = [[(d[l].cpu().numpy() if l < n_dev else h[l]) for l in range(L)] for d, h in zip(dev, (masters, m0, v0))]
+    return outs, state
+
+
+def dataclasses_replace_quant(cfg):
+    import dataclasses
+    return dataclasses.replace(cfg, weights_quant=T.Q_NONE)
+
+
+@pytest.mark.parametrize("group", [False, True])
+def test_device_updated_layers_bitexact_to_host_updates(group):
+    """The AdamW of the shallowest layers on the GPU
+    (tps_stage_set_optimizer_split) gives the bits of the host update: over
+    three iterations with layer 0, then layers 0 and 1, updated on the
+    device, the outputs and input gradients of every iteration, the host
+    layers' gradient blocks and every layer's master weights and moments
+    equal those of the run with every layer updated on the host."""
+    cfg = _cfg(T.Q_NONE)
+    ref_outs, ref_state = _run_split(cfg, 0, group)
+    for n_dev in (1, 2):
+        outs, state = _run_split(cfg, n_dev, group)
+        for it, (a, b) in enumerate(zip(outs, ref_outs)):
+            for mb in range(cfg.n_micro):
+                assert np.array_equal(a["ys"][mb], b["ys"][mb]), (n_dev, it, mb)
+                assert np.array_equal(a["dxs"][mb], b["dxs"][mb]), (n_dev, it, mb)
+        for l in range(n_dev, cfg.n_layers):
+            for n in a["grads"][l]:
+                assert np.array_equal(outs[-1]["grads"][l][n], ref_outs[-1]["grads"][l][n]), (n_dev, l, n)
+        for k, (got, ref) in enumerate(zip(state, ref_state)):
+            for l in range(cfg.n_layers):
+                assert np.array_equal(got[l], ref[l]), (n_dev, k, l)
+        # the updates reached the device
+        assert not np.array_equal(outs[1]["ys"][0], outs[0]["ys"][0])
+
+
+def test_device_updated_layer_with_quantized_reload_matches_oracle():
+    """FP8 reload of the host-updated layers with layer 0 updated on the GPU:
+    layer 0 computes with bf16 of its master weights, the others with the
+    decoded FP8 codes of theirs; the second iteration and the master weights
+    match the oracle's."""
+    cfg = _cfg(T.Q_FP8_ROW)
+    L = cfg.n_layers
+    outs, state = _run_split(cfg, 1, True, iterations=2)
+    start = [_unpack(cfg, b) for b in _master_blocks(cfg)]
+    xs, dys = inputs(cfg)
+    w = [{n: v.copy() for n, v in s.items()} for s in start]
+    mo = [{n: np.zeros_like(v) for n, v in s.items()} for s in start]
+    vo = [{n: np.zeros_like(v) for n, v in s.items()} for s in start]
+    bf16_cfg = dataclasses_replace_quant(cfg)
+    for step in (1, 2):
+        ora_params = [_device_weights(bf16_cfg if l == 0 else cfg, {n: v.astype(np.float32) for n, v in wl.items()})
+                      for l, wl in enumerate(w)]
+        ref = run_oracle(cfg, xs, dys, ora_params=ora_params)
+        got = dict(outs[step - 1])
+        # layer 0's gradient block stays on the device
+        got["grads"] = [ref["grads"][0]] + got["grads"][1:]
+        worst, bad = compare(got, ref, BF16_TOL)
+        assert not bad, (step, bad)
+        for l in range(L):
+            for n in T.PARAMS:
+                w[l][n], mo[l][n], vo[l][n] = ms.adamw_step(w[l][n], mo[l][n], vo[l][n], ref["grads"][l][n], step, **HP)
+    rels = {}
+    for l in range(L):
+        got = _unpack(cfg, state[0][l])
+        for n in T.PARAMS:
+            du, dr = got[n] - start[l][n], w[l][n] - start[l][n]
+            rels[(l, n)] = np.linalg.norm(du - dr) / max(np.linalg.norm(dr), 1e-30)
+    # with eps far above sqrt(v) the update error is the gradient error; the
+    # LayerNorm parameters' gradients are column sums over the 400 tokens of
+    # bf16-rounded products, the noisiest (0.03-0.06 here, the matrices and
+    # biases 0.006-0.03)
+    for (l, n), rel in rels.items():
+        assert rel < (8e-2 if n in ("g1", "be1", "g2", "be2") else 5e-2), (l, n, rel, rels)
+
+
+def test_device_optimizer_argument_errors():
+    import torch
+    cfg = _cfg(T.Q_NONE)
+    L = cfg.n_layers
+    masters = _master_blocks(cfg)
+    blocks = _host_param_blocks(cfg, masters)
+    gb = T.param_layout(cfg)[3]
+    grads = [torch.zeros(gb, dtype=torch.uint8, pin_memory=True) for _ in range(L)]
+    st = T.Stage(cfg, blocks, grads)
+    zeros = [np.zeros_like(b) for b in masters]
+    try:
+        with pytest.raises(T.TpsError):   # more device layers than layers
+            st.set_optimizer(masters, zeros, zeros, dparams=[blocks[0].cuda()] * (L + 1))
+        dm = torch.from_numpy(masters[0]).cuda()
+        dz = torch.zeros_like(dm)
+        st.set_optimizer([dm] + masters[1:], [dz] + zeros[1:], [dz.clone()] + zeros[1:],
+                         dparams=[blocks[0][:T.param_layout(cfg)[1]].cuda()])
+        with pytest.raises(T.TpsError) as e:   # device layers need zero_grads
+            st.begin_iteration(zero_grads=False)
+        assert e.value.code == T.TPS_EINVAL
+    finally:
+        st.close()

@@ -285,3 +285,40 @@ def test_host_access_needs_sync():
     st.read_results(sync=True)
     assert D.races() == 0, D.report()
     st.close()
+
+
+def test_device_optimizer_race_free():
+    """Every layer's AdamW on the device: the update reads the gradients the
+    layer's last backward wrote and rewrites the device parameter block that
+    the next iteration's loads copy into the window; per-micro-batch and
+    group calls, bf16 and quantized reload configs, windows of 2 and 3."""
+    for window in (2, 3):
+        for quant in (T.Q_NONE, T.Q_FP8_ROW):
+            cfg = _mid(n_layers=4, policy=W.policy_layer_inputs(4), granularity=T.GRAN_LAYER, weights=T.W_STREAM,
+                       window=window, weights_quant=quant)
+            for group in (False, True):
+                D.reset()
+                st = D.FakeStage(cfg)
+                st.write_inputs()
+                st.set_device_optimizer()
+                for _ in range(3):
+                    st.iteration(group=group)
+                st.read_results()
+                st.close()
+                assert D.races() == 0, (window, quant, group, D.report())
+    # one update per parameter tensor of every layer per iteration, and the
+    # host link carries no gradient block of a device-updated layer
+    cfg = _mid(n_layers=4, policy=W.policy_layer_inputs(4), granularity=T.GRAN_LAYER, weights=T.W_STREAM, window=4)
+    D.reset()
+    st = D.FakeStage(cfg)
+    st.write_inputs()
+    st.set_device_optimizer()
+    updates0 = D.count_ops("adamw")
+    d2h0 = D.count_ops("copy device->host") + D.count_ops("pitched copy device->host")
+    for it in range(2):
+        st.iteration(group=True)
+        assert D.count_ops("adamw") - updates0 == (it + 1) * 4 * len(T.PARAMS)
+    st.read_results()
+    st.close()
+    assert D.races() == 0, D.report()
+    assert D.count_ops("copy device->host") + D.count_ops("pitched copy device->host") == d2h0
