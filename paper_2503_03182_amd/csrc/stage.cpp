@@ -134,7 +134,8 @@ struct tps_stage {
   int gs_layer[2] = {-1, -1};
   int bstep = 0;
   // grads_fresh[l]: layer l's gradient block counts as zero (requested by
-  // begin_iteration and not yet written): its next layer backward writes the
+  // begin_iteration, or a streamed layer's first load for a backward of the
+  // iteration, and not yet written): its next layer backward writes the
   // gradients instead of adding to them, so no zero fill is needed
   std::vector<char> grads_fresh;
   // rs: replays of all but the first replayed layer of a segment run here,
@@ -663,8 +664,9 @@ int tps_stage::ensure_layer(int l, bool for_backward, int* entry) {
       TPS_HIP(hipEventRecord(ev_tmp, ps));
       TPS_HIP(hipStreamWaitEvent(cs, ev_tmp, 0));
     } else {
-      TPS_HIP(fill_zero_launch(grads_of(l, e), p.gbytes, cs));
-      ++stats.kernels;
+      // the layer's first backward of the iteration writes every gradient
+      // tensor instead of adding to it, so the block needs no zero fill
+      grads_fresh[l] = 1;
       grads_touched[l] = 1;
     }
     w.grads_live = true;
