@@ -425,18 +425,32 @@ int tps_stage::load_params(int l, int e) {
   return TPS_OK;
 }
 
-// Transposed copies of the four weight matrices (operands of the input-
-// gradient GEMMs, which then read both operands K-contiguous).
+// Transposed copies of the weight matrices that an NT product reads: the
+// input-gradient GEMMs whose contraction is shorter than the NN threshold
+// (QKV over qw, output projection over h, up projection over uw, down
+// projection over h), and with resident weights the forward down projection
+// when its contraction f takes the NN form against W2^T.
 int tps_stage::refresh_wt(int l, int e) {
   int ent = e;
   const char* P = params_of(l, &ent);
   char* W = wt_of(l, e);
   const int h = p.h, f = p.f, qw = (int)p.qw, uw = (int)p.uw;
-  TPS_HIP(transpose_launch(p.dtype, qw, h, P + p.poff[TPS_P_W_QKV], h, W + p.wtoff[0], qw, cs));
-  TPS_HIP(transpose_launch(p.dtype, h, h, P + p.poff[TPS_P_W_O], h, W + p.wtoff[1], h, cs));
-  TPS_HIP(transpose_launch(p.dtype, uw, h, P + p.poff[TPS_P_W_1], h, W + p.wtoff[2], uw, cs));
-  TPS_HIP(transpose_launch(p.dtype, h, f, P + p.poff[TPS_P_W_2], f, W + p.wtoff[3], h, cs));
-  stats.kernels += 4;
+  if (!nn_for(qw)) {
+    TPS_HIP(transpose_launch(p.dtype, qw, h, P + p.poff[TPS_P_W_QKV], h, W + p.wtoff[0], qw, cs));
+    ++stats.kernels;
+  }
+  if (!nn_for(h)) {
+    TPS_HIP(transpose_launch(p.dtype, h, h, P + p.poff[TPS_P_W_O], h, W + p.wtoff[1], h, cs));
+    ++stats.kernels;
+  }
+  if (!nn_for(uw)) {
+    TPS_HIP(transpose_launch(p.dtype, uw, h, P + p.poff[TPS_P_W_1], h, W + p.wtoff[2], uw, cs));
+    ++stats.kernels;
+  }
+  if (!nn_for(h) || (nn_for(f) && p.weights == TPS_W_RESIDENT)) {
+    TPS_HIP(transpose_launch(p.dtype, h, f, P + p.poff[TPS_P_W_2], f, W + p.wtoff[3], h, cs));
+    ++stats.kernels;
+  }
   return TPS_OK;
 }
 
