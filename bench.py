@@ -367,8 +367,9 @@ def main():
     ap.add_argument("--t-offload", choices=("bf16", "fp8"), default=None,
                     help="streamed workloads: attach the host AdamW update of every layer (T-Offload of model "
                          "state) and reload the updated weights as bf16 or as FP8 codes with row scales")
-    ap.add_argument("--device-layers", type=int, default=2,
-                    help="with --t-offload: the shallowest layers whose model state and AdamW step stay on the GPU")
+    ap.add_argument("--device-layers", type=int, default=None,
+                    help="with --t-offload: the shallowest layers whose model state and AdamW step stay on the GPU "
+                         "(default: 2, at most the layer count)")
     ap.add_argument("--layers", type=int, default=None, help="override the workload's layer count")
     args = ap.parse_args()
     if args.standalone_gemms:
@@ -407,6 +408,8 @@ def main():
             sys.exit(2)
         if args.t_offload == "fp8":
             cfg = dataclasses.replace(cfg, weights_quant=T.Q_FP8_ROW)
+        if args.device_layers is None:
+            args.device_layers = min(2, cfg.n_layers)
         if not 0 <= args.device_layers <= cfg.n_layers:
             print("--device-layers must be in 0..layers", file=sys.stderr)
             sys.exit(2)

@@ -502,9 +502,11 @@ int tps_stage_set_optimizer(tps_stage* st, const tps_adamw* opt, float* const* m
  * caller.  Once every backward of an iteration has passed such a layer, its
  * AdamW step runs on the compute stream with the host update's arithmetic
  * (the same f32 operations, hence the same bits), writing master, m, v and
- * dparams[l]; its gradient block is consumed on the device and not written
- * to the host, and its loads copy dparams[l] (its pinned host block is no
- * longer read, and with weights_quant its parameters are not quantized).
+ * dparams[l]; its final gradients are consumed on the device (its host
+ * gradient block is no result: it holds at most partial sums from times the
+ * layer left the window during the iteration), and its loads copy dparams[l]
+ * (its pinned host parameter block is no longer read, and with weights_quant
+ * its parameters are not quantized).
  * Iterations must start with zero_grads set.  n_device in 0 .. n_layers
  * (dparams may be NULL when 0); TPS_EINVAL otherwise, or for a null or
  * misaligned device block. */
