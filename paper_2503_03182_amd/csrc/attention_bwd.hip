@@ -122,17 +122,50 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
   // c = 32 qb + 8 (j / 4) + j % 4 the query offset of accumulator j of block qb
   const int kthr = key - 4 * g;
 
-  // One 64-query tile, as two 32-query halves each taken through the whole
-  // chain (S, dP -> P, dS -> dV, dK): only one half's scores, probabilities
-  // and per-row vectors are live at a time, which keeps the K/V fragments and
-  // the dK/dV accumulators resident in registers.
+  // One 64-query tile, as two 32-query halves each taken through the chain
+  // S, dP -> P, dS -> dV, dK.  The two chains are staggered so that the
+  // elementwise work of one half runs while the MFMAs of the other issue
+  // (independent registers: the vector ALU and the MFMA pipe overlap):
+  //   S, dP of half 0
+  //   S, dP of half 1          beside  P, dS of half 0
+  //   dV, dK from half 0       beside  P, dS of half 1
+  //   dV, dK from half 1
+  // Only one half's row vectors (lse, D) are live at a time.
   auto tile = [&](int t, int st, auto diag_c) {
     constexpr bool DIAG = decltype(diag_c)::value;
     const uint32_t qs = lds0 + st * STAGE, ds = qs + TILE, ls = ds + TILE, vs = ls + VEC;
-    static_for<2>([&](auto qc) {
+    // lse and D of the rows this lane holds in half qb: 32 qb + 8 (j / 4) + 4 g + (j % 4)
+    f32x4 lv[4], dvv[4];
+    auto read_vec = [&](int qb) {
+#pragma unroll
+      for (int j4 = 0; j4 < 4; ++j4) {
+        const uint32_t o = (uint32_t)((32 * qb + 8 * j4 + 4 * g) * 4);
+        asm volatile("ds_read_b128 %0, %1" : "=v"(lv[j4]) : "v"(ls + o));
+        asm volatile("ds_read_b128 %0, %1" : "=v"(dvv[j4]) : "v"(vs + o));
+      }
+    };
+    auto pin_vec = [&] {
+#pragma unroll
+      for (int j4 = 0; j4 < 4; ++j4) {
+        pin(lv[j4]);
+        pin(dvv[j4]);
+      }
+    };
+    // P and dS of accumulator element j of half qb
+    auto elem = [&](auto qc, auto jc, const f32x16& sacc, const f32x16& pacc, float* p, float* d) {
+      constexpr int qb = decltype(qc)::value, j = decltype(jc)::value;
+      float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[j], sl2, -lv[j / 4][j % 4] * kLog2e));
+      if constexpr (DIAG) {
+        if (32 * qb + 8 * (j / 4) + (j % 4) < kthr - t * BT) pv = 0.f;
+      }
+      p[j] = pv;
+      d[j] = pv * (pacc[j] - dvv[j / 4][j % 4]);
+    };
+    // S = Q K^T and dP = dO V^T of half qb: 8 d-steps each; first() runs
+    // after the first wait (every LDS read issued before the phase has
+    // landed), mid(i) after MFMA i
+    auto sdp = [&](auto qc, f32x16& sacc, f32x16& pacc, auto&& first, auto&& mid) {
       constexpr int qb = decltype(qc)::value;
-      // ---- S = Q K^T and dP = dO V^T for queries 32 qb .. +32: 8 d-steps each
-      f32x16 sacc, pacc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) sacc[r] = pacc[r] = 0.f;
       bf16x8 fr[16];
@@ -147,43 +180,18 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
         constexpr int i = decltype(ic)::value, w = i % 2, ks = i / 2;
         constexpr int issued = (i + WF < 16) ? i + WF : 16;
         wait_lgkm<issued - i - 1>();
+        if constexpr (i == 0) first();
         pin(fr[i]);
         if constexpr (w == 0) sacc = Mma<bf16>::run(fr[i], kf[ks], sacc);
         else pacc = Mma<bf16>::run(fr[i], vf[ks], pacc);
         if constexpr (i + WF < 16) read_f(std::integral_constant<int, i + WF>{});
+        mid(ic);
       });
-      // ---- lse and D of the rows this lane holds: 32 qb + 8 (j / 4) + 4 g + (j % 4)
-      f32x4 lv[4], dvv[4];
-#pragma unroll
-      for (int j4 = 0; j4 < 4; ++j4) {
-        const uint32_t o = (uint32_t)((32 * qb + 8 * j4 + 4 * g) * 4);
-        asm volatile("ds_read_b128 %0, %1" : "=v"(lv[j4]) : "v"(ls + o));
-        asm volatile("ds_read_b128 %0, %1" : "=v"(dvv[j4]) : "v"(vs + o));
-      }
-      wait_lgkm<0>();
-#pragma unroll
-      for (int j4 = 0; j4 < 4; ++j4) {
-        pin(lv[j4]);
-        pin(dvv[j4]);
-      }
-      // ---- P, dS
-      float p[16], d[16];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[j], sl2, -lv[j / 4][j % 4] * kLog2e));
-        if constexpr (DIAG) {
-          if (32 * qb + 8 * (j / 4) + (j % 4) < kthr - t * BT) pv = 0.f;
-        }
-        p[j] = pv;
-        d[j] = pv * (pacc[j] - dvv[j / 4][j % 4]);
-      }
-      bf16x8 pb[2], sb[2];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        pb[u] = to_frag(&p[8 * u]);
-        sb[u] = to_frag(&d[8 * u]);
-      }
-      // ---- dV^T += dO^T P, dK^T += Q^T dS: 2 query steps x 4 d tiles each
+    };
+    // dV^T += dO^T P, dK^T += Q^T dS of half qb: 2 query steps x 4 d tiles
+    // each; first() and mid(i) as for sdp
+    auto dvdk = [&](auto qc, const bf16x8* pb, const bf16x8* sb, auto&& first, auto&& mid) {
+      constexpr int qb = decltype(qc)::value;
       s16x4 lo[16], hi[16];
       // issue order i: operand (dO^T, Q^T) = i % 2, d tile = (i / 2) % 4, query step u = i / 8
       auto read_t = [&](auto ic) {
@@ -199,14 +207,43 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
         constexpr int i = decltype(ic)::value, w = i % 2, mt = (i / 2) % 4, u = i / 8;
         constexpr int issued = (i + WT < 16) ? i + WT : 16;
         wait_lgkm<2 * (issued - i - 1)>();
+        if constexpr (i == 0) first();
         s16x8 v8 = {lo[i][0], lo[i][1], lo[i][2], lo[i][3], hi[i][0], hi[i][1], hi[i][2], hi[i][3]};
         bf16x8 f = *reinterpret_cast<bf16x8*>(&v8);
         pin(f);
         if constexpr (w == 0) dv[mt] = Mma<bf16>::run(f, pb[u], dv[mt]);
         else dk[mt] = Mma<bf16>::run(f, sb[u], dk[mt]);
         if constexpr (i + WT < 16) read_t(std::integral_constant<int, i + WT>{});
+        mid(ic);
       });
+    };
+    auto none = [](auto...) {};
+    using Q0 = std::integral_constant<int, 0>;
+    using Q1 = std::integral_constant<int, 1>;
+
+    f32x16 sacc0, pacc0, sacc1, pacc1;
+    read_vec(0);
+    sdp(Q0{}, sacc0, pacc0, pin_vec, none);
+    float p[16], d[16];
+    bf16x8 pb0[2], sb0[2], pb1[2], sb1[2];
+    sdp(Q1{}, sacc1, pacc1, none, [&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      elem(Q0{}, ic, sacc0, pacc0, p, d);
+      if constexpr (i % 8 == 7) {
+        pb0[i / 8] = to_frag(&p[i - 7]);
+        sb0[i / 8] = to_frag(&d[i - 7]);
+      }
     });
+    read_vec(1);
+    dvdk(Q0{}, pb0, sb0, pin_vec, [&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      elem(Q1{}, ic, sacc1, pacc1, p, d);
+      if constexpr (i % 8 == 7) {
+        pb1[i / 8] = to_frag(&p[i - 7]);
+        sb1[i / 8] = to_frag(&d[i - 7]);
+      }
+    });
+    dvdk(Q1{}, pb1, sb1, none, none);
   };
 
   // the i-th tile lives in stage i & 1
@@ -338,47 +375,62 @@ __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf1
   const float sl2 = scale * kLog2e;
   const int qthr = q - 4 * g;
 
+  // One 64-key tile as two 32-key blocks.  The elementwise work of block 0
+  // runs while the S^T, dP^T MFMAs of block 1 issue, and that of block 1
+  // while the first half of the dQ MFMAs (block 0's key steps) issue.
   auto tile = [&](int t, int st, auto diag_c) {
     constexpr bool DIAG = decltype(diag_c)::value;
     const uint32_t ks_ = lds0 + st * STAGE, vs = ks_ + TILE;
-    // ---- S^T = K Q^T and dP^T = V dO^T: 2 key blocks x 8 d-steps each
-    f32x16 sacc[2], pacc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = pacc[kb][r] = 0.f;
-    bf16x8 fr[32];
-    auto read_f = [&](auto ic) {
-      constexpr int i = decltype(ic)::value, w = i % 2, kb = (i / 2) % 2, ks = i / 4;
-      fr[i] = ds_b128<kb * 32 * ROWB>((w ? vs : ks_) + fo.row[ks]);
-    };
-    constexpr int WF = 10;   // fragments in flight
-    static_for<WF>([&](auto ic) { read_f(ic); });
-    static_for<32>([&](auto ic) {
-      constexpr int i = decltype(ic)::value, w = i % 2, kb = (i / 2) % 2, ks = i / 4;
-      constexpr int issued = (i + WF < 32) ? i + WF : 32;
-      wait_lgkm<issued - i - 1>();
-      pin(fr[i]);
-      if constexpr (w == 0) sacc[kb] = Mma<bf16>::run(fr[i], qf[ks], sacc[kb]);
-      else pacc[kb] = Mma<bf16>::run(fr[i], df[ks], pacc[kb]);
-      if constexpr (i + WF < 32) read_f(std::integral_constant<int, i + WF>{});
-    });
-    // ---- dS^T = P^T (dP^T - D), P^T = exp2(S^T s log2e - lse log2e)
-    float d[2][16];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], sl2, -lse2));
-        if constexpr (DIAG) {
-          if (32 * kb + 8 * (j / 4) + (j % 4) > qthr - t * BT) pv = 0.f;
-        }
-        d[kb][j] = pv * (pacc[kb][j] - dq_dot);
+    // dS^T of accumulator element j of key block kb:
+    // dS^T = P^T (dP^T - D), P^T = exp2(S^T s log2e - lse log2e)
+    auto elem = [&](auto kc, auto jc, const f32x16& sacc, const f32x16& pacc, float* d) {
+      constexpr int kb = decltype(kc)::value, j = decltype(jc)::value;
+      float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[j], sl2, -lse2));
+      if constexpr (DIAG) {
+        if (32 * kb + 8 * (j / 4) + (j % 4) > qthr - t * BT) pv = 0.f;
       }
-    bf16x8 sb[4];
+      d[j] = pv * (pacc[j] - dq_dot);
+    };
+    // S^T = K Q^T and dP^T = V dO^T of key block kb: 8 d-steps each; mid(i)
+    // runs after MFMA i
+    auto sdp = [&](auto kc, f32x16& sacc, f32x16& pacc, auto&& mid) {
+      constexpr int kb = decltype(kc)::value;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) sb[u] = to_frag(&d[u / 2][8 * (u % 2)]);
-    // ---- dQ^T += K^T dS^T: 4 key steps x 4 d tiles
+      for (int r = 0; r < 16; ++r) sacc[r] = pacc[r] = 0.f;
+      bf16x8 fr[16];
+      // issue order i: operand (K, V) = i % 2, d-step = i / 2
+      auto read_f = [&](auto ic) {
+        constexpr int i = decltype(ic)::value, w = i % 2, ks = i / 2;
+        fr[i] = ds_b128<kb * 32 * ROWB>((w ? vs : ks_) + fo.row[ks]);
+      };
+      constexpr int WF = 8;   // fragments in flight
+      static_for<WF>([&](auto ic) { read_f(ic); });
+      static_for<16>([&](auto ic) {
+        constexpr int i = decltype(ic)::value, w = i % 2, ks = i / 2;
+        constexpr int issued = (i + WF < 16) ? i + WF : 16;
+        wait_lgkm<issued - i - 1>();
+        pin(fr[i]);
+        if constexpr (w == 0) sacc = Mma<bf16>::run(fr[i], qf[ks], sacc);
+        else pacc = Mma<bf16>::run(fr[i], df[ks], pacc);
+        if constexpr (i + WF < 16) read_f(std::integral_constant<int, i + WF>{});
+        mid(ic);
+      });
+    };
+    auto none = [](auto...) {};
+    using K0 = std::integral_constant<int, 0>;
+    using K1 = std::integral_constant<int, 1>;
+
+    f32x16 sacc0, pacc0, sacc1, pacc1;
+    sdp(K0{}, sacc0, pacc0, none);
+    float d[16];
+    bf16x8 sb[4];
+    sdp(K1{}, sacc1, pacc1, [&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      elem(K0{}, ic, sacc0, pacc0, d);
+      if constexpr (i % 8 == 7) sb[i / 8] = to_frag(&d[i - 7]);
+    });
+    // ---- dQ^T += K^T dS^T: 4 key steps x 4 d tiles; key steps 0, 1 come
+    // from block 0, whose MFMAs carry block 1's elementwise work
     s16x4 lo[16], hi[16];
     auto read_t = [&](auto ic) {
       constexpr int i = decltype(ic)::value, mt = i % 4, u = i / 4;
@@ -397,6 +449,11 @@ __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf1
       pin(f);
       dq[mt] = Mma<bf16>::run(f, sb[u], dq[mt]);
       if constexpr (i + WT < 16) read_t(std::integral_constant<int, i + WT>{});
+      if constexpr (i < 8) {
+        elem(K1{}, std::integral_constant<int, 2 * i>{}, sacc1, pacc1, d);
+        elem(K1{}, std::integral_constant<int, 2 * i + 1>{}, sacc1, pacc1, d);
+        if constexpr (i % 4 == 3) sb[2 + i / 4] = to_frag(&d[2 * i - 6]);
+      }
     });
   };
 
