@@ -138,14 +138,29 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const T* __restrict__ dout,
 
 // Wave-per-row LayerNorm for rows of NV * 512 bf16 (lane l holds the 8-column
 // chunks l, l + 64, ...): reductions are wave butterflies only, four rows per
-// 256-thread workgroup.
+// 256-thread workgroup.  Rows of 4096 columns and more stay in registers as
+// packed bf16 and each pass converts them again: settle() between passes
+// keeps the compiler from holding the f32 values of one pass for the next,
+// which at 8192 columns took every register of the SIMD and left one or two
+// waves per SIMD to hide the HBM latency.  The operations are those of the
+// source either way; only the compiler's pairing of multiplies and adds into
+// FMAs may differ (one bf16 ulp in one element of 33.5M seen in the RMS
+// backward at 4096 x 8192).
+template <int NV>
+__device__ __forceinline__ void settle(Vec16<bf16> (&v)[NV]) {
+#pragma unroll
+  for (int c = 0; c < NV; ++c) asm volatile("" : "+v"(v[c].raw));
+}
+// rows this wide keep only the packed row live across passes
+template <int NV> constexpr bool kWideRow = NV >= 8;
+
 template <int NV, bool RMS = false>
 __global__ __launch_bounds__(256) void ln_fwd_wave_kernel(const bf16* __restrict__ x, const bf16* __restrict__ gamma,
                                                           const bf16* __restrict__ beta, float eps,
                                                           bf16* __restrict__ out, float* __restrict__ mean,
                                                           float* __restrict__ rstd, int rows, int cols) {
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int row = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   if (row >= rows) return;
   const bf16* xr = x + (int64_t)row * cols;
   Vec16<bf16> xv[NV];
@@ -159,6 +174,7 @@ __global__ __launch_bounds__(256) void ln_fwd_wave_kernel(const bf16* __restrict
       for (int i = 0; i < 8; ++i) s += to_f32(xv[c].get(i));
   }
   const float mu = RMS ? 0.f : wave_sum(s) / (float)cols;
+  if constexpr (kWideRow<NV>) settle(xv);
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < NV; ++c)
@@ -168,6 +184,7 @@ __global__ __launch_bounds__(256) void ln_fwd_wave_kernel(const bf16* __restrict
       ss += d * d;
     }
   const float rs = 1.0f / sqrtf(wave_sum(ss) / (float)cols + eps);
+  if constexpr (kWideRow<NV>) settle(xv);
   bf16* orow = out + (int64_t)row * cols;
 #pragma unroll
   for (int c = 0; c < NV; ++c) {
@@ -197,18 +214,23 @@ __global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict
                                                           const bf16* __restrict__ resid, bf16* __restrict__ dx,
                                                           int rows, int cols) {
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int row = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   if (row >= rows) return;
   const float mu = RMS ? 0.f : mean[row], rs = rstd[row];
   const bf16* xr = x + (int64_t)row * cols;
   const bf16* dr = dout + (int64_t)row * cols;
-  Vec16<bf16> xv[NV], dv[NV], rv[NV];
+  // narrower rows load the residual gradient with the row; wide rows load it
+  // chunk by chunk in the output pass
+  constexpr bool WIDE = kWideRow<NV>;
+  Vec16<bf16> xv[NV], dv[NV], rv[WIDE ? 1 : NV];
 #pragma unroll
   for (int c = 0; c < NV; ++c) {
     const int col = (c * 64 + lane) * 8;
     xv[c] = load16(xr + col);
     dv[c] = load16(dr + col);
-    if (resid) rv[c] = load16(resid + (int64_t)row * cols + col);
+    if constexpr (!WIDE) {
+      if (resid) rv[c] = load16(resid + (int64_t)row * cols + col);
+    }
   }
   float s1 = 0.f, s2 = 0.f;
 #pragma unroll
@@ -223,18 +245,24 @@ __global__ __launch_bounds__(256) void ln_bwd_wave_kernel(const bf16* __restrict
   }
   const float m1 = RMS ? 0.f : wave_sum(s1) / (float)cols;
   const float m2 = wave_sum(s2) / (float)cols;
+  if constexpr (WIDE) {
+    settle(xv);
+    settle(dv);
+  }
   bf16* o = dx + (int64_t)row * cols;
 #pragma unroll
   for (int c = 0; c < NV; ++c) {
     const int col = (c * 64 + lane) * 8;
     const Vec16<bf16> g = load16(gamma + col);
+    if constexpr (WIDE) rv[0] = resid ? load16(resid + (int64_t)row * cols + col) : zero16<bf16>();
+    const Vec16<bf16>& r = rv[WIDE ? 0 : c];
     Vec16<bf16> w;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const float gv = to_f32(dv[c].get(i)) * to_f32(g.get(i));
       const float zh = (to_f32(xv[c].get(i)) - mu) * rs;
       float val = rs * (gv - m1 - zh * m2);
-      if (resid) val += to_f32(rv[c].get(i));
+      if (resid) val += to_f32(r.get(i));
       w.set(i, from_f32<bf16>(val));
     }
     store16(o + col, w);
