@@ -43,6 +43,14 @@ constexpr int kDkdvLds = 2 * (2 * TILE + 2 * kVecBytes);
 // LDS of a dQ block: a ring of two stages of K, V
 constexpr int kDqLds = 2 * (2 * TILE);
 
+// 16-byte LDS read of four f32 at byte address a + OFF.
+template <int OFF>
+__device__ __forceinline__ f32x4 ds_f32x4(uint32_t a) {
+  f32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(OFF));
+  return v;
+}
+
 // Where dK/dV blocks write: with one key/value head per query head into
 // dqkv's k and v blocks; with grouped heads (nkv < nh) into a workspace
 // [T][2 nh d] of per-query-head gradients (dK of head n at column n d, dV at
@@ -108,9 +116,21 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
   };
   // load instructions per tile: the tiles' share, plus the vectors for slice 0
   constexpr int LPT = 2 * TileSrcN<KW>::IPW;
+  // Every LDS read below is a loop-invariant base register plus an immediate
+  // offset (stage, operand, row block): the ring's address is folded into the
+  // per-lane fragment offsets and the stage is a compile-time argument of the
+  // tile, so no address arithmetic runs per read.
   FragOff fo;
   fo.init(lane);
   const uint32_t lds0 = lds_u32(ring);
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) fo.row[ks] += lds0;
+#pragma unroll
+  for (int mt = 0; mt < D / 32; ++mt) {
+    fo.lo[mt] += lds0;
+    fo.hi[mt] += lds0;
+  }
+  const uint32_t vbase = lds0 + 2 * TILE + 16 * g;   // lse of row 4 g of the stage-0 tile
 
   f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -131,18 +151,20 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
   //   dV, dK from half 0       beside  P, dS of half 1
   //   dV, dK from half 1
   // Only one half's row vectors (lse, D) are live at a time.
-  auto tile = [&](int t, int st, auto diag_c) {
+  // stage ST of the ring: Q at ST * STAGE, dO at + TILE, lse at + 2 TILE, D at + 2 TILE + VEC
+  auto tile = [&](auto st_c, int t, auto diag_c) {
+    constexpr int ST = decltype(st_c)::value;
+    constexpr int QO = ST * STAGE, DO = QO + TILE;   // immediate offsets of Q and dO
     constexpr bool DIAG = decltype(diag_c)::value;
-    const uint32_t qs = lds0 + st * STAGE, ds = qs + TILE, ls = ds + TILE, vs = ls + VEC;
     // lse and D of the rows this lane holds in half qb: 32 qb + 8 (j / 4) + 4 g + (j % 4)
     f32x4 lv[4], dvv[4];
-    auto read_vec = [&](int qb) {
-#pragma unroll
-      for (int j4 = 0; j4 < 4; ++j4) {
-        const uint32_t o = (uint32_t)((32 * qb + 8 * j4 + 4 * g) * 4);
-        asm volatile("ds_read_b128 %0, %1" : "=v"(lv[j4]) : "v"(ls + o));
-        asm volatile("ds_read_b128 %0, %1" : "=v"(dvv[j4]) : "v"(vs + o));
-      }
+    auto read_vec = [&](auto qc) {
+      constexpr int qb = decltype(qc)::value;
+      static_for<4>([&](auto jc) {
+        constexpr int j4 = decltype(jc)::value, o = ST * STAGE + (32 * qb + 8 * j4) * 4;
+        lv[j4] = ds_f32x4<o>(vbase);
+        dvv[j4] = ds_f32x4<o + VEC>(vbase);
+      });
     };
     auto pin_vec = [&] {
 #pragma unroll
@@ -172,7 +194,7 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
       // issue order i: operand (Q, dO) = i % 2, d-step = i / 2
       auto read_f = [&](auto ic) {
         constexpr int i = decltype(ic)::value, w = i % 2, ks = i / 2;
-        fr[i] = ds_b128<qb * 32 * ROWB>((w ? ds : qs) + fo.row[ks]);
+        fr[i] = ds_b128<qb * 32 * ROWB + (w ? DO : QO)>(fo.row[ks]);
       };
       constexpr int WF = 8;   // fragments in flight
       static_for<WF>([&](auto ic) { read_f(ic); });
@@ -196,10 +218,9 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
       // issue order i: operand (dO^T, Q^T) = i % 2, d tile = (i / 2) % 4, query step u = i / 8
       auto read_t = [&](auto ic) {
         constexpr int i = decltype(ic)::value, w = i % 2, mt = (i / 2) % 4, u = i / 8;
-        constexpr int roff = 16 * (2 * qb + u) * ROWB;
-        const uint32_t src = w ? qs : ds;
-        lo[i] = ds_tr16<roff>(src + fo.lo[mt]);
-        hi[i] = ds_tr16<roff>(src + fo.hi[mt]);
+        constexpr int roff = 16 * (2 * qb + u) * ROWB + (w ? QO : DO);
+        lo[i] = ds_tr16<roff>(fo.lo[mt]);
+        hi[i] = ds_tr16<roff>(fo.hi[mt]);
       };
       constexpr int WT = 7;   // transposed fragments in flight
       static_for<WT>([&](auto ic) { read_t(ic); });
@@ -222,7 +243,7 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
     using Q1 = std::integral_constant<int, 1>;
 
     f32x16 sacc0, pacc0, sacc1, pacc1;
-    read_vec(0);
+    read_vec(Q0{});
     sdp(Q0{}, sacc0, pacc0, pin_vec, none);
     float p[16], d[16];
     bf16x8 pb0[2], sb0[2], pb1[2], sb1[2];
@@ -234,7 +255,7 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
         sb0[i / 8] = to_frag(&d[i - 7]);
       }
     });
-    read_vec(1);
+    read_vec(Q1{});
     dvdk(Q0{}, pb0, sb0, pin_vec, [&](auto ic) {
       constexpr int i = decltype(ic)::value;
       elem(Q1{}, ic, sacc1, pacc1, p, d);
@@ -270,14 +291,30 @@ __device__ __forceinline__ void dkdv_block(const bf16* __restrict__ qkv, const b
   const int n_diag = min(max((k0 + 30) / BT + 1 - tb, n_skip), np);
   int it = 0;
   for (; it < n_skip; ++it) trip_end(it);
-  for (; it < n_diag; ++it) {
-    tile(tb + it, it & 1, std::true_type{});
-    trip_end(it);
-  }
-  for (; it < np; ++it) {
-    tile(tb + it, it & 1, std::false_type{});
-    trip_end(it);
-  }
+  // tiles it .. end - 1 of one kind, in pairs (stage 0, stage 1) so that the
+  // loop body is straight-line code with both stages' offsets as immediates
+  auto run = [&](int end, auto diag_c) {
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    if ((it & 1) && it < end) {
+      tile(S1{}, tb + it, diag_c);
+      trip_end(it);
+      ++it;
+    }
+    for (; it + 1 < end; it += 2) {
+      tile(S0{}, tb + it, diag_c);
+      trip_end(it);
+      tile(S1{}, tb + it + 1, diag_c);
+      trip_end(it + 1);
+    }
+    if (it < end) {
+      tile(S0{}, tb + it, diag_c);
+      trip_end(it);
+      ++it;
+    }
+  };
+  run(n_diag, std::true_type{});
+  run(np, std::false_type{});
 
   // ---- store: lane holds dK^T / dV^T [32 mt + acc_row(j, l)][key]
   if (key < s) {
@@ -363,9 +400,17 @@ __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf1
     vsrc.load(t * BT, ring + st * STAGE + TILE);
   };
   constexpr int LPT = 2 * TileSrcN<QW>::IPW;   // load instructions per wave per tile
+  // LDS reads as base register + immediate, as in dkdv_block
   FragOff fo;
   fo.init(lane);
   const uint32_t lds0 = lds_u32(ring);
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) fo.row[ks] += lds0;
+#pragma unroll
+  for (int mt = 0; mt < D / 32; ++mt) {
+    fo.lo[mt] += lds0;
+    fo.hi[mt] += lds0;
+  }
 
   f32x16 dq[D / 32];
 #pragma unroll
@@ -378,9 +423,11 @@ __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf1
   // One 64-key tile as two 32-key blocks.  The elementwise work of block 0
   // runs while the S^T, dP^T MFMAs of block 1 issue, and that of block 1
   // while the first half of the dQ MFMAs (block 0's key steps) issue.
-  auto tile = [&](int t, int st, auto diag_c) {
+  // stage ST of the ring: K at ST * STAGE, V at + TILE
+  auto tile = [&](auto st_c, int t, auto diag_c) {
+    constexpr int ST = decltype(st_c)::value;
+    constexpr int KO = ST * STAGE, VO = KO + TILE;   // immediate offsets of K and V
     constexpr bool DIAG = decltype(diag_c)::value;
-    const uint32_t ks_ = lds0 + st * STAGE, vs = ks_ + TILE;
     // dS^T of accumulator element j of key block kb:
     // dS^T = P^T (dP^T - D), P^T = exp2(S^T s log2e - lse log2e)
     auto elem = [&](auto kc, auto jc, const f32x16& sacc, const f32x16& pacc, float* d) {
@@ -401,7 +448,7 @@ __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf1
       // issue order i: operand (K, V) = i % 2, d-step = i / 2
       auto read_f = [&](auto ic) {
         constexpr int i = decltype(ic)::value, w = i % 2, ks = i / 2;
-        fr[i] = ds_b128<kb * 32 * ROWB>((w ? vs : ks_) + fo.row[ks]);
+        fr[i] = ds_b128<kb * 32 * ROWB + (w ? VO : KO)>(fo.row[ks]);
       };
       constexpr int WF = 8;   // fragments in flight
       static_for<WF>([&](auto ic) { read_f(ic); });
@@ -434,9 +481,9 @@ __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf1
     s16x4 lo[16], hi[16];
     auto read_t = [&](auto ic) {
       constexpr int i = decltype(ic)::value, mt = i % 4, u = i / 4;
-      constexpr int roff = 16 * u * ROWB;
-      lo[i] = ds_tr16<roff>(ks_ + fo.lo[mt]);
-      hi[i] = ds_tr16<roff>(ks_ + fo.hi[mt]);
+      constexpr int roff = 16 * u * ROWB + KO;
+      lo[i] = ds_tr16<roff>(fo.lo[mt]);
+      hi[i] = ds_tr16<roff>(fo.hi[mt]);
     };
     constexpr int WT = 7;   // transposed fragments in flight
     static_for<WT>([&](auto ic) { read_t(ic); });
@@ -476,14 +523,29 @@ __device__ __forceinline__ void dq_block(const bf16* __restrict__ qkv, const bf1
   const int n_comp = max(0, min(np, wave_last + 1 - tb));
   const int n_plain = max(0, min(n_comp, (q0 + 1) / BT - tb));   // tiles whose last key <= q0
   int it = 0;
-  for (; it < n_plain; ++it) {
-    tile(tb + it, it & 1, std::false_type{});
-    trip_end(it);
-  }
-  for (; it < n_comp; ++it) {
-    tile(tb + it, it & 1, std::true_type{});
-    trip_end(it);
-  }
+  // tiles it .. end - 1 of one kind in (stage 0, stage 1) pairs, as for dK/dV
+  auto run = [&](int end, auto diag_c) {
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    if ((it & 1) && it < end) {
+      tile(S1{}, tb + it, diag_c);
+      trip_end(it);
+      ++it;
+    }
+    for (; it + 1 < end; it += 2) {
+      tile(S0{}, tb + it, diag_c);
+      trip_end(it);
+      tile(S1{}, tb + it + 1, diag_c);
+      trip_end(it + 1);
+    }
+    if (it < end) {
+      tile(S0{}, tb + it, diag_c);
+      trip_end(it);
+      ++it;
+    }
+  };
+  run(n_plain, std::false_type{});
+  run(n_comp, std::true_type{});
   for (; it < np; ++it) trip_end(it);
 
   if (q < s) {
