@@ -371,6 +371,9 @@ def main():
                     help="with --t-offload: the shallowest layers whose model state and AdamW step stay on the GPU "
                          "(default: 2, at most the layer count)")
     ap.add_argument("--layers", type=int, default=None, help="override the workload's layer count")
+    ap.add_argument("--wgrad", choices=("auto", "side", "inline"), default="auto",
+                    help="where the parameter-gradient kernels run: the plan's choice (auto), a stream "
+                         "of their own beside the input-gradient chain (side) or the compute stream (inline)")
     args = ap.parse_args()
     if args.standalone_gemms:
         import torch
@@ -402,6 +405,8 @@ def main():
     if args.layers is not None:
         cfg = dataclasses.replace(cfg, n_layers=args.layers,
                                   policy=None if cfg.policy is None else cfg.policy[:args.layers])
+    if args.wgrad != "auto":
+        cfg = dataclasses.replace(cfg, wgrad_stream=T.WGRAD_SIDE if args.wgrad == "side" else T.WGRAD_INLINE)
     if args.t_offload is not None:
         if cfg.weights != T.W_STREAM:
             print("--t-offload needs a workload with streamed weights", file=sys.stderr)
